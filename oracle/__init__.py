@@ -1,0 +1,30 @@
+"""CPU oracle for the PARD speculative-decode step.
+
+TEST INFRASTRUCTURE.  This package is the slow, plain float64 reference that
+the GPU path is checked against.  Only ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py`` may import it; the product path
+(the HIP library ``libpard.so`` and its Python binding) never routes through
+it, and it shares no code with that path.  Inputs come from ``pard_inputs``.
+
+Modules:
+* ``oracle.model`` -- the decoder (forward with and without a KV cache).
+* ``oracle.pard``  -- greedy decoding (eq. 2) and the PARD draft / verify /
+  accept loop (Sec. 2.2, Sec. 3.1 eq. 7).
+
+Pins (tests marked "not gpu"): the decoder against the independent
+Hugging Face Llama/Qwen2 implementations and torch's attention/normalisation
+routines; cached vs. uncached forward position by position; the one-pass draft
+against K separate uncached passes (eq. 7); lossless greedy speculative
+decoding against plain greedy decoding (eq. 2) for K in {1, 2, 4, 8, 12};
+forced-candidate acceptance; the draft-equals-target special case.
+"""
+from .model import (KVCache, Model, attention, forward_cached, forward_full, linear,
+                    rms_norm, rope, silu)
+from .pard import (PardTrace, accept_prefix, argmax_rows, draft_step, greedy_ar,
+                   pard_generate, prefill, verify_step)
+
+
+def build_model(spec, layers=None) -> Model:
+    """Oracle model with weights generated from ``spec`` by ``pard_inputs``."""
+    import pard_inputs
+    return Model(spec, pard_inputs.gen_model_weights(spec, layers=layers))

@@ -1,0 +1,204 @@
+#!/usr/bin/env python3
+"""Benchmark of the PARD decode step on one MI355X.
+
+A step is one pass of the whole hot path: one draft forward over the pending
+tokens plus K-1 mask tokens, one target verify forward over K+1 rows, argmax,
+greedy acceptance and KV rollback, all on the device (fused loop,
+``pard_generate``).  The workload is the LLaMA3.1-8B-shaped target with the
+LLaMA3.2-1B-shaped draft, bf16, batch 1, K = 8, 512-token prompt, seeded
+random weights (synthetic data).  Prints one JSON line.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import pard_inputs as pi  # noqa: E402
+from paper_2504_18583_amd import bytes_model as bm  # noqa: E402
+
+METRIC = "tokens/sec batch-1 PARD decode, 1B draft/8B target K=8; step HBM GB/s vs peak"
+PEAK_HBM_GBPS = 8000.0
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, tokens_per_step: float, context: int) -> dict:
+    """The oracle, as it is, timed on the host for one step at this workload's shapes.
+
+    Bounded sample: the target and draft run with 1 and with 2 of their layers
+    (embedding and lm_head in full) against a synthetic KV cache of `context`
+    positions; the per-layer cost is extrapolated linearly to all layers."""
+    import oracle
+    from dataclasses import replace
+    threads = len(os.sched_getaffinity(0))
+    k = wl.k
+    rng = np.random.default_rng(0)
+    t_full = 0.0
+    for spec, is_target in ((wl.target, True), (wl.draft, False)):
+        full = oracle.build_model(replace(spec, n_layers=2))
+        times = {}
+        for n_layers in (1, 2):
+            layers = {l: full.weights["layers"][l] for l in range(n_layers)}
+            model = oracle.Model(replace(spec, n_layers=n_layers), dict(full.weights, layers=layers))
+            samples = []
+            for _ in range(2):
+                cache = oracle.KVCache(model)
+                for l in range(n_layers):
+                    cache.k[l] = rng.standard_normal((context, spec.n_kv_heads, spec.head_dim))
+                    cache.v[l] = rng.standard_normal((context, spec.n_kv_heads, spec.head_dim))
+                t0 = time.perf_counter()
+                if is_target:
+                    oracle.verify_step(model, cache, 1, list(range(2, 2 + k)))
+                else:
+                    oracle.draft_step(model, cache, [1], k, wl.mask_id)
+                samples.append(time.perf_counter() - t0)
+            times[n_layers] = min(samples)
+        per_layer = max(times[2] - times[1], 0.0)
+        fixed = max(times[1] - per_layer, 0.0)
+        t_full += fixed + per_layer * spec.n_layers
+        log(f"cpu_baseline: {'target' if is_target else 'draft'} 1 layer {times[1]:.2f}s, "
+            f"2 layers {times[2]:.2f}s")
+    return {"value": round(tokens_per_step / t_full, 4), "unit": "tokens/s", "cores": threads,
+            "kind": "oracle",
+            "sample": (f"one step (draft pass over 1 pending + {k - 1} mask rows, verify pass over "
+                       f"{k + 1} rows) at these shapes, context {context}, float64 numpy; target and "
+                       f"draft timed with 1 and 2 layers (full embedding/lm_head), per-layer time "
+                       f"extrapolated to {wl.target.n_layers}/{wl.draft.n_layers} layers; "
+                       f"{tokens_per_step:.3f} tokens/step as measured on the GPU; "
+                       f"step {t_full:.2f} s")}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--workload", default="llama8b_1b")
+    ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        log("bench.py measures one GPU: the decode step of one batch-1 sequence does not shard "
+            "(see the design notes); run with --gpus 1")
+        return 2
+
+    import torch
+    from paper_2504_18583_amd import binding as B
+
+    wl = pi.WORKLOADS[args.workload]
+    if wl.batch != 1:
+        log(f"workload {wl.name} is batched; this build benchmarks batch 1")
+        return 2
+    k = args.k if args.k is not None else wl.k
+    t_spec, d_spec = pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0]]
+    max_ctx = len(prompt) + (args.warmup + args.steps + 2) * (k + 1) + 2 * k + 8
+
+    t0 = time.perf_counter()
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=max_ctx, max_k=max(k, 1))
+    torch.cuda.synchronize()
+    log(f"load + weight generation: {time.perf_counter() - t0:.2f}s")
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    eng.prefill(prompt)
+    torch.cuda.synchronize()
+    ttft_ms = (time.perf_counter() - t0) * 1e3
+    log(f"prefill ({len(prompt)} tokens, both models): {ttft_ms:.1f} ms")
+
+    big = max_ctx  # n_tokens bound; max_steps decides
+    if args.warmup:
+        eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2, max_steps=args.warmup)
+    l_t0 = eng.kv_len(B.PARD_TARGET)
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, stats = eng.generate(k, big - l_t0 - 2 * k - 2, max_steps=args.steps)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    steps = int(stats.steps)
+    hist = list(stats.accept_hist)
+    emitted = sum((a + 1) * n for a, n in enumerate(hist))
+    assert steps == args.steps, (steps, args.steps)
+    tokens_per_step = emitted / steps
+    step_s = wall / steps
+    l_t1 = eng.kv_len(B.PARD_TARGET)
+
+    # algorithmic bytes of the timed steps (context grows by a+1 per step)
+    mean_acc = tokens_per_step - 1.0
+    tot_bytes = 0.0
+    for i in range(steps):
+        lt = l_t0 + i * tokens_per_step
+        tot_bytes += bm.step_bytes(t_spec, d_spec, k, round(mean_acc), int(lt), int(lt) + 1)
+    step_gbps = tot_bytes / wall / 1e9
+
+    # dominant kernel: the target's gate/up GEMM, timed with HIP events around
+    # each launch on the engine's stream over a second run of the same steps
+    kclass = B.PARD_TARGET * 8 + B.OP_GATEUP
+    n_launch = steps * t_spec.n_layers
+    eng.timer_enable(kclass, min(n_launch, 1 << 16))
+    eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2,
+                 max_steps=max(1, min(steps, (max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2) // (k + 1))))
+    launches, total_ms = eng.timer_read()
+    eng.timer_enable(-1, 1)
+    avg_s = total_ms / 1e3 / max(launches, 1)
+    f_pad = (t_spec.ffn_dim + 31) // 32 * 32
+    # bf16 weights [2*F, d] once, bf16 activations in, bf16 h = silu(gate)*up out
+    gu_bytes = 2 * (2 * f_pad * t_spec.d_model) + (k + 1) * t_spec.d_model * 2 + (k + 1) * f_pad * 2
+    achieved = gu_bytes / avg_s / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                "kernel": "k_gemm<MT=1,S=2,EPI_SWIGLU> (target gate/up, 8B shape)",
+                "launches": launches, "avg_us": round(avg_s * 1e6, 2),
+                "bytes_per_launch": gu_bytes}
+
+    result = {
+        "metric": METRIC,
+        "value": round(emitted / wall, 3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(step_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {wl.target.n_layers}-layer d{wl.target.d_model} target / "
+                               f"{wl.draft.n_layers}-layer d{wl.draft.d_model} draft, batch 1, "
+                               f"prompt {len(prompt)}, K={k}, seed {wl.seed}",
+                   "batch": 1, "prompt_len": len(prompt), "k": k, "seed": wl.seed},
+        "tokens_per_step": round(tokens_per_step, 4),
+        "accept_hist": hist[:k + 1],
+        "step_hbm_gbps": round(step_gbps, 1),
+        "step_hbm_frac": round(step_gbps / PEAK_HBM_GBPS, 4),
+        "bytes_per_step": round(tot_bytes / steps),
+        "context": [l_t0, l_t1],
+        "ttft_ms": round(ttft_ms, 2),
+        "device_ms_per_step": round(stats.elapsed_ms / steps, 4),
+        "roofline": roofline,
+    }
+    eng.close()
+    del eng
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, tokens_per_step, len(prompt))
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,193 @@
+/*
+ * pard.h -- C ABI of the PARD parallel-draft speculative-decode engine
+ * (hand-written HIP kernels for AMD Instinct MI355X, gfx950).
+ *
+ * The engine runs one speculative-decoding step as the paper states it:
+ *   - drafting stage (Sec. 2.2; Sec. 3.1 eq. 7): the draft model makes ONE
+ *     forward pass over the tokens it has not yet seen followed by K-1 copies of
+ *     a shared mask token (Sec. 4.3, shared mask id) and proposes K candidates;
+ *   - verification stage (Sec. 2.2): the target model scores the pending token
+ *     and the K candidates in one forward pass; greedy decoding (Sec. 2.1 eq. 2)
+ *     keeps the longest prefix of candidates that equals the target's argmax,
+ *     plus one bonus token, and rolls the KV caches back to the accepted length.
+ * Weights are generated on the device from a seed (no checkpoints); see
+ * pard_model_load.
+ *
+ * Conventions for every call
+ *   - Return value: PARD_OK (0) or a negative pard_status.  On error nothing in
+ *     the context has changed and pard_last_error() describes the problem.
+ *     Validation of arguments, state and capacity happens on the host before
+ *     any device work.  Nothing aborts, prints or allocates device memory.
+ *   - Host pointers (prompt, prefix, cand, outputs) are owned by the caller and
+ *     are only accessed during the call.  Granular calls return after their
+ *     outputs are valid (one device->host copy and a stream synchronisation).
+ *   - Device memory: the caller provides one arena (pard_arena_bytes bytes,
+ *     256-byte aligned) that must outlive the context; the library carves
+ *     weights, KV caches, activations and workspaces out of it and never
+ *     frees it.  All device work is enqueued on the caller's HIP stream.
+ *   - Token ids must lie in [0, vocab).  0 <= K <= max_k <= 32.
+ *   - A context is not thread-safe.
+ */
+#ifndef PARD_H
+#define PARD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PARD_OK = 0,
+  PARD_ERR_ARG = -1,         /* bad argument (null pointer, id out of range, bad shape) */
+  PARD_ERR_STATE = -2,       /* call not valid in the current state (e.g. before prefill) */
+  PARD_ERR_CAPACITY = -3,    /* would exceed max_ctx / max_k / max_batch */
+  PARD_ERR_NOMEM = -4,       /* arena smaller than pard_arena_bytes() */
+  PARD_ERR_DEVICE = -5,      /* a HIP runtime call failed */
+  PARD_ERR_UNSUPPORTED = -6  /* valid request this build does not implement */
+} pard_status;
+
+enum { PARD_F32 = 0, PARD_BF16 = 1 };
+enum { PARD_TARGET = 0, PARD_DRAFT = 1 };
+
+/* Shape and initialisation of one Llama-family decoder (Sec. 4.1 names
+ * LLaMA3 and Qwen2.5 members).  Weights are drawn N(0, init_std^2) with the
+ * counter-based generator below and stored in bf16; RMSNorm gains are 1.
+ * Constraints: d_model % 32 == 0, head_dim in {64, 128},
+ * n_heads % n_kv_heads == 0, vocab % 16 == 0, dtype == PARD_BF16.
+ *
+ * Generator (both this library and the test inputs implement it):
+ * SplitMix64 (Steele, Lea, Flood 2014) stream with state
+ * mix64(seed * 2^20 + weight_stream * 2^16 + tensor), i-th output
+ * mix64(state + (i + 1) * 0x9E3779B97F4A7C15); element i of a tensor in
+ * canonical row-major [out, in] order takes the basic Box-Muller transform of
+ * outputs 2*(i/2) and 2*(i/2)+1 (u1 = ((z0>>11)+1)*2^-53, u2 = (z1>>11)*2^-53,
+ * cosine branch for even i, sine for odd i), times init_std, rounded to float32
+ * then to bf16 (nearest, ties to even).  Tensor ordinals: embedding 0,
+ * lm_head 1 (untied only), layer l: 16*(l+1) + {wq 0, wk 1, wv 2, wo 3,
+ * w_gate 4, w_up 5, w_down 6, bq 7, bk 8, bv 9}. */
+typedef struct {
+  int32_t n_layers, d_model, n_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps, rope_theta, init_std;
+  int32_t qkv_bias;          /* 1: Q/K/V projections carry a bias (Qwen2.5 family) */
+  int32_t tied_embeddings;   /* 1: lm_head is the embedding matrix */
+  int32_t dtype;             /* PARD_BF16 */
+  uint32_t weight_stream;    /* generator stream id (target 0, draft 1 by convention) */
+  uint64_t seed;
+} pard_model_spec;
+
+typedef struct pard_ctx pard_ctx;
+
+typedef struct {
+  int64_t steps;             /* draft+verify steps executed */
+  int64_t tokens;            /* tokens written to out_tokens */
+  double elapsed_ms;         /* device time between the first and last step */
+  int64_t accept_hist[33];   /* accept_hist[a] = steps that accepted a candidates */
+} pard_stats;
+
+/* Bytes of device arena needed for a target/draft pair with the given
+ * capacities; 0 if the specs or capacities are invalid.  Host-only. */
+size_t pard_arena_bytes(const pard_model_spec *target, const pard_model_spec *draft,
+                        int32_t max_batch, int32_t max_ctx, int32_t max_k);
+
+/* Create a context: carve the arena, generate both models' weights on the
+ * device, build rotary tables.  target->vocab must equal draft->vocab;
+ * mask_id in [0, vocab) is the shared mask token of the draft (Sec. 4.3).
+ * max_ctx bounds every sequence's KV length (prompt + generated + 2*max_k).
+ * hip_stream is a hipStream_t (NULL = the default stream).
+ * Errors: ARG (bad spec/pointer), UNSUPPORTED (constraint above),
+ * NOMEM (arena_bytes too small), DEVICE. */
+pard_status pard_model_load(const pard_model_spec *target, const pard_model_spec *draft,
+                            int32_t mask_id, int32_t max_batch, int32_t max_ctx, int32_t max_k,
+                            void *dev_arena, size_t arena_bytes, void *hip_stream,
+                            pard_ctx **out);
+
+/* Prefill sequence slot `seq` (Sec. 2.1): both models ingest the n prompt
+ * tokens (their KV lengths become n) and the target's greedy argmax after the
+ * prompt is returned in *first_token.  That token is "pending": it is in
+ * neither cache and is the first row of the next draft and verify passes.
+ * Re-prefilling a slot discards its previous contents.
+ * Errors: ARG, CAPACITY (n + 2*max_k + 1 > max_ctx, seq >= max_batch), DEVICE. */
+pard_status pard_prefill(pard_ctx *ctx, int32_t seq, const int32_t *prompt, int32_t n,
+                         int32_t *first_token);
+
+/* Drafting stage, Sec. 3.1 eq. 7.  `prefix` is the whole committed sequence
+ * (prompt and every generated token, ending with the latest pending token).
+ * The draft ingests prefix[L_d : n_prefix] followed by K-1 mask tokens in one
+ * forward pass (if L_d >= n_prefix it first truncates to n_prefix-1, so at
+ * least the last token is re-read) and writes cand[k] = argmax of the row
+ * that reads the last real token (k = 0) or mask k-1 (k >= 1), k < K.
+ * Afterwards L_d = n_prefix: mask rows are never committed.  K = 1 is an
+ * ordinary draft decode step.  Errors: ARG (1 <= K <= max_k, ids), STATE
+ * (slot not prefilled), CAPACITY, DEVICE. */
+pard_status pard_draft(pard_ctx *ctx, int32_t seq, const int32_t *prefix, int32_t n_prefix,
+                       int32_t K, int32_t *cand);
+
+/* Verification stage, Sec. 2.2 with greedy acceptance (eq. 2).  The target
+ * runs [pending, cand[0..K-1]] at positions L_t .. L_t+K; with t_j its
+ * argmax at row j, *n_accepted = a = the largest j with cand[i] == t_i for all
+ * i < j, *bonus = t_a.  The target cache keeps a+1 rows (L_t += a+1), the
+ * bonus becomes the pending token.  K = 0 is a plain greedy target step.
+ * Errors: ARG, STATE, CAPACITY, DEVICE. */
+pard_status pard_verify(pard_ctx *ctx, int32_t seq, const int32_t *cand, int32_t K,
+                        int32_t *n_accepted, int32_t *bonus);
+
+/* Roll the KV cache of `which` (PARD_TARGET / PARD_DRAFT) back to new_len
+ * (0 <= new_len <= current length).  O(1): a length update.
+ * Errors: ARG, STATE. */
+pard_status pard_kv_truncate(pard_ctx *ctx, int32_t seq, int32_t which, int32_t new_len);
+
+/* Current committed KV length of `which` for slot `seq`. */
+pard_status pard_kv_len(const pard_ctx *ctx, int32_t seq, int32_t which, int32_t *len);
+
+/* Fused device-resident loop for slot seqs[0] (n_seq must be 1 in this build):
+ * repeated draft (one pass) -> verify -> accept steps with no host round trip
+ * per step.  out_tokens[0] is the current pending token; every step appends
+ * its accepted candidates and bonus; exactly n_tokens tokens are written
+ * (surplus tokens of the last step are dropped).  max_steps > 0 caps the
+ * number of steps (then fewer tokens may be written; stats->tokens says how
+ * many).  K = 0 runs plain greedy target steps.  stats may be NULL.
+ * Errors: ARG, STATE, CAPACITY (the KV would exceed max_ctx), UNSUPPORTED
+ * (n_seq != 1), DEVICE. */
+pard_status pard_generate(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, int32_t K,
+                          int32_t n_tokens, int32_t max_steps, int32_t *out_tokens,
+                          pard_stats *stats);
+
+/* Copy the fp32 logits of the last lm_head pass of `which` (rows x vocab,
+ * row-major; draft rows are the K candidate rows, target rows the verify
+ * rows, prefill the single last-prompt row).  rows must not exceed the rows of
+ * that pass.  Parity/debug.  Errors: ARG, STATE, DEVICE. */
+pard_status pard_read_logits(const pard_ctx *ctx, int32_t which, int32_t seq, float *out,
+                             int32_t rows, int32_t vocab);
+
+/* Read n consecutive canonical weight elements [row, col0 .. col0+n) of one
+ * tensor (ordinal as in the generator comment; layer tensors use their layer's
+ * ordinal) of model `which`, as float.  Debug/parity of the generator and the
+ * on-device weight layout.  Errors: ARG, DEVICE. */
+pard_status pard_read_weight(const pard_ctx *ctx, int32_t which, int32_t tensor, int32_t row,
+                             int32_t col0, int32_t n, float *out);
+
+/* Per-kernel timer: HIP events around each launch of one kernel class
+ * (class = which * 8 + op, op: 0 embed, 1 qkv, 2 attention, 3 o-proj,
+ * 4 gate/up, 5 down, 6 lm_head) on the context's stream, for up to
+ * max_launches launches after enabling.  pard_timer_read synchronises the
+ * stream and returns the number of timed launches and their summed duration.
+ * kernel_class < 0 disables.  Errors: ARG, DEVICE. */
+pard_status pard_timer_enable(pard_ctx *ctx, int32_t kernel_class, int32_t max_launches);
+pard_status pard_timer_read(pard_ctx *ctx, int32_t *launches, double *total_ms);
+
+/* Message of the last error on this context (never NULL; "" if none). */
+const char *pard_last_error(const pard_ctx *ctx);
+
+/* Static name of a status code. */
+const char *pard_status_string(pard_status status);
+
+/* Destroy a context (the arena stays owned by the caller).  NULL is allowed. */
+void pard_free(pard_ctx *ctx);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PARD_H */

@@ -1,0 +1,1040 @@
+// Host side of the PARD engine: arena layout, model generation, the forward
+// pass launch sequence, the speculative-decoding step and the C ABI.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/pard.h"
+#include "device_init.h"
+#include "pard_internal.h"
+
+using namespace pard;
+
+namespace {
+
+constexpr int kTargetWorkgroups = 512;   // per GEMM launch: ~2 per CU on 256 CUs
+constexpr int kPrefillRows = kMaxRows;
+constexpr int kDescRing = 512;
+constexpr int kGatherMax = 4096;
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+uint64_t stream_key(uint64_t seed, uint32_t stream, uint32_t tensor) {
+  return mix64((seed << 20) + ((uint64_t)stream << 16) + tensor);
+}
+int layer_tensor(int l, int j) { return 16 * (l + 1) + j; }
+
+struct Bump {
+  char* base = nullptr;
+  size_t off = 0;
+  template <class T>
+  T* take(size_t count) {
+    off = align256(off);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// Tile plan of one skinny GEMM.  The input-dimension split G depends only on
+// the weight shape, so per-element summation order is the same for any row count.
+struct GemmPlan {
+  int n_strips = 0, kb_total = 0, G = 1;
+};
+
+int pick_S(int epi, int n_strips, int mt) {
+  int s = 2;
+  if (epi == EPI_LOGITS) s = (mt == 1) ? 8 : (mt == 2 ? 4 : 2);
+  while (s > 1 && n_strips % s) s >>= 1;
+  if (epi == EPI_SWIGLU && s < 2) s = 2;
+  return s;
+}
+
+GemmPlan plan_gemm(int epi, int n_pad, int k_pad) {
+  GemmPlan p;
+  p.n_strips = n_pad / 16;
+  p.kb_total = k_pad / 32;
+  const int tiles_ref = p.n_strips / pick_S(epi, p.n_strips, 1);
+  if (epi != EPI_LOGITS) {
+    while (tiles_ref * p.G < kTargetWorkgroups && p.kb_total >= 4 * (2 * p.G) * 2) p.G *= 2;
+  }
+  return p;
+}
+
+struct Layer {
+  uint16_t *wqkv = nullptr, *wo = nullptr, *wgu = nullptr, *wd = nullptr;
+  float *bqkv = nullptr, *g_attn = nullptr, *g_mlp = nullptr;
+};
+
+struct ModelDev {
+  pard_model_spec spec{};
+  int d = 0, q_dim = 0, kv_dim = 0, nqkv = 0, f_pad = 0, group = 0;
+  GemmPlan p_qkv, p_o, p_gu, p_d, p_lm;
+  int attn_chunk = 64, attn_chunks = 1;
+  std::vector<Layer> layers;
+  uint16_t *embed = nullptr, *lm_head = nullptr;
+  float* g_final = nullptr;
+  uint16_t *kcache = nullptr, *vcache = nullptr;
+  float2* rope = nullptr;
+  float* x = nullptr;                 // residual stream, fp32 [kMaxRows][d]
+  uint16_t* xg = nullptr;             // bf16(x * g) of the next normalised GEMM
+  float* ss = nullptr;                // per-tile row sums of squares of x [tiles][kMaxRows]
+  int ss_tiles_resid = 1;             // tiles of the residual GEMMs (producers of ss)
+  uint16_t *q = nullptr, *attn = nullptr, *h = nullptr;
+  float* logits = nullptr;
+  int* result = nullptr;
+  FwdDesc* desc = nullptr;
+  int last_lm_rows = 0;
+};
+
+}  // namespace
+
+struct pard_ctx {
+  ModelDev m[2];
+  int mask_id = 0, max_batch = 0, max_ctx = 0, max_k = 0;
+  hipStream_t stream = nullptr;
+  char* arena = nullptr;
+  size_t arena_bytes = 0;
+  // shared device workspaces
+  float* gemm_part = nullptr;
+  int* gemm_cnt = nullptr;
+  int* lm_cnt = nullptr;
+  float* amax_val = nullptr;
+  int* amax_idx = nullptr;
+  float* attn_part = nullptr;
+  int* attn_cnt = nullptr;
+  SeqState* seq_dev = nullptr;
+  int* out_dev = nullptr;
+  size_t* gather_idx_dev = nullptr;
+  float* gather_out_dev = nullptr;
+  // pinned host staging
+  FwdDesc* h_desc = nullptr;
+  int desc_slot = 0;
+  SeqState* h_seq = nullptr;
+  size_t* h_gather_idx = nullptr;
+  float* h_gather_out = nullptr;
+  int* h_out = nullptr;
+  hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+  // host mirrors
+  std::vector<std::vector<int>> hist;   // committed tokens + pending token
+  std::vector<char> prefilled;
+  // per-kernel timer
+  int timer_class = -1, timer_max = 0, timer_used = 0;
+  std::vector<hipEvent_t> timer_ev;
+  std::string err;
+  size_t kv_seq_stride[2] = {0, 0};
+};
+
+namespace {
+
+pard_status fail(pard_ctx* c, pard_status s, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return s;
+}
+
+#define HIP_TRY(ctx, expr)                                                                  \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail((ctx), PARD_ERR_DEVICE, "%s failed: %s", #expr, hipGetErrorString(e_));   \
+  } while (0)
+
+pard_status check_spec(const pard_model_spec* s, const char* who, std::string* why) {
+  char buf[256];
+  auto bad = [&](pard_status st, const char* msg) {
+    snprintf(buf, sizeof buf, "%s spec: %s", who, msg);
+    *why = buf;
+    return st;
+  };
+  if (!s) return bad(PARD_ERR_ARG, "null");
+  if (s->n_layers < 1 || s->n_layers > 4000) return bad(PARD_ERR_ARG, "n_layers out of range");
+  if (s->d_model < 32 || s->n_heads < 1 || s->n_kv_heads < 1 || s->ffn_dim < 1 || s->vocab < 16)
+    return bad(PARD_ERR_ARG, "non-positive dimension");
+  if (s->n_heads % s->n_kv_heads) return bad(PARD_ERR_ARG, "n_heads not a multiple of n_kv_heads");
+  if (!(s->rms_eps > 0.f) || !(s->rope_theta > 1.f) || !(s->init_std > 0.f))
+    return bad(PARD_ERR_ARG, "rms_eps, rope_theta or init_std out of range");
+  if (s->seed >= (1ull << 44) || s->weight_stream >= 16) return bad(PARD_ERR_ARG, "seed or weight_stream out of range");
+  if (s->dtype != PARD_BF16) return bad(PARD_ERR_UNSUPPORTED, "only bf16 weights are supported");
+  if (s->head_dim != 64 && s->head_dim != 128) return bad(PARD_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (s->d_model % 32) return bad(PARD_ERR_UNSUPPORTED, "d_model must be a multiple of 32");
+  if (s->vocab % 16) return bad(PARD_ERR_UNSUPPORTED, "vocab must be a multiple of 16");
+  if ((int64_t)s->vocab * s->d_model >= (1ll << 40)) return bad(PARD_ERR_ARG, "vocab too large");
+  return PARD_OK;
+}
+
+pard_status check_all(const pard_model_spec* t, const pard_model_spec* d, int mask_id, int max_batch,
+                      int max_ctx, int max_k, std::string* why) {
+  pard_status st = check_spec(t, "target", why);
+  if (st != PARD_OK) return st;
+  st = check_spec(d, "draft", why);
+  if (st != PARD_OK) return st;
+  if (t->vocab != d->vocab) { *why = "target and draft vocab differ"; return PARD_ERR_ARG; }
+  if (mask_id < 0 || mask_id >= t->vocab) { *why = "mask_id out of range"; return PARD_ERR_ARG; }
+  if (max_k < 1 || max_k > kMaxK) { *why = "max_k must be in [1, 32]"; return PARD_ERR_ARG; }
+  if (max_batch < 1 || max_batch > 4096) { *why = "max_batch out of range"; return PARD_ERR_ARG; }
+  if (max_ctx < 2 * max_k + 2 || max_ctx > (1 << 24)) { *why = "max_ctx out of range"; return PARD_ERR_ARG; }
+  return PARD_OK;
+}
+
+void derive(ModelDev& M, const pard_model_spec& s, int max_ctx) {
+  M.spec = s;
+  M.d = s.d_model;
+  M.q_dim = s.n_heads * s.head_dim;
+  M.kv_dim = s.n_kv_heads * s.head_dim;
+  M.nqkv = M.q_dim + 2 * M.kv_dim;
+  M.f_pad = ceil_div(s.ffn_dim, 32) * 32;
+  M.group = s.n_heads / s.n_kv_heads;
+  M.p_qkv = plan_gemm(EPI_QKV, M.nqkv, M.d);
+  M.p_o = plan_gemm(EPI_RESID, M.d, M.q_dim);
+  M.p_gu = plan_gemm(EPI_SWIGLU, 2 * M.f_pad, M.d);
+  M.p_d = plan_gemm(EPI_RESID, M.d, M.f_pad);
+  M.p_lm = plan_gemm(EPI_LOGITS, s.vocab, M.d);
+  M.ss_tiles_resid = M.p_o.n_strips / pick_S(EPI_RESID, M.p_o.n_strips, 1);
+  M.attn_chunk = kAttnSub * std::max(1, ceil_div(max_ctx, kAttnSub * 64));
+  M.attn_chunks = ceil_div(max_ctx, M.attn_chunk);
+}
+
+size_t part_floats(const GemmPlan& p, int epi) {
+  size_t worst = 0;
+  for (int mt = 1; mt <= 4; ++mt) {
+    const int S = pick_S(epi, p.n_strips, mt);
+    const size_t tiles = p.n_strips / S;
+    if (p.G > 1) worst = std::max(worst, tiles * p.G * (size_t)(S * mt * 256 + mt * 16));
+  }
+  return worst;
+}
+
+// Lays out (base == nullptr: sizes) every device region of a context.
+size_t layout(pard_ctx* c, char* base) {
+  Bump b;
+  b.base = base;
+  size_t part = 0;
+  int max_tiles = 1, max_lm_tiles = 1, max_attn_cnt = 1;
+  size_t attn_part = 1;
+  for (int w = 0; w < 2; ++w) {
+    ModelDev& M = c->m[w];
+    const pard_model_spec& s = M.spec;
+    M.layers.assign(s.n_layers, Layer{});
+    for (int l = 0; l < s.n_layers; ++l) {
+      Layer& L = M.layers[l];
+      L.wqkv = b.take<uint16_t>((size_t)M.nqkv * M.d);
+      L.wo = b.take<uint16_t>((size_t)M.d * M.q_dim);
+      L.wgu = b.take<uint16_t>((size_t)2 * M.f_pad * M.d);
+      L.wd = b.take<uint16_t>((size_t)M.d * M.f_pad);
+      L.bqkv = s.qkv_bias ? b.take<float>(M.nqkv) : nullptr;
+      L.g_attn = b.take<float>(M.d);
+      L.g_mlp = b.take<float>(M.d);
+    }
+    M.embed = b.take<uint16_t>((size_t)s.vocab * M.d);
+    M.lm_head = s.tied_embeddings ? M.embed : b.take<uint16_t>((size_t)s.vocab * M.d);
+    M.g_final = b.take<float>(M.d);
+    const size_t kv = (size_t)c->max_batch * s.n_layers * s.n_kv_heads * c->max_ctx * s.head_dim;
+    c->kv_seq_stride[w] = (size_t)s.n_layers * s.n_kv_heads * c->max_ctx * s.head_dim;
+    M.kcache = b.take<uint16_t>(kv);
+    M.vcache = b.take<uint16_t>(kv);
+    M.rope = b.take<float2>((size_t)c->max_ctx * s.head_dim / 2);
+    M.x = b.take<float>((size_t)kMaxRows * M.d);
+    M.xg = b.take<uint16_t>((size_t)kMaxRows * M.d);
+    M.ss = b.take<float>((size_t)std::max(1, M.ss_tiles_resid) * kMaxRows);
+    M.q = b.take<uint16_t>((size_t)kMaxRows * M.q_dim);
+    M.attn = b.take<uint16_t>((size_t)kMaxRows * M.q_dim);
+    M.h = b.take<uint16_t>((size_t)kMaxRows * M.f_pad);
+    M.logits = b.take<float>((size_t)kMaxLmRows * s.vocab);
+    M.result = b.take<int>(kMaxLmRows);
+    M.desc = b.take<FwdDesc>(1);
+    part = std::max({part, part_floats(M.p_qkv, EPI_QKV), part_floats(M.p_o, EPI_RESID),
+                     part_floats(M.p_gu, EPI_SWIGLU), part_floats(M.p_d, EPI_RESID)});
+    max_tiles = std::max({max_tiles, M.p_qkv.n_strips, M.p_o.n_strips, M.p_gu.n_strips, M.p_d.n_strips});
+    max_lm_tiles = std::max(max_lm_tiles, M.p_lm.n_strips);
+    const int qblocks = ceil_div(kMaxRows * M.group, kAttnQB);
+    max_attn_cnt = std::max(max_attn_cnt, s.n_kv_heads * qblocks);
+    attn_part = std::max(attn_part, (size_t)s.n_kv_heads * qblocks * M.attn_chunks * attn_part_floats(s.head_dim));
+  }
+  c->gemm_part = b.take<float>(std::max<size_t>(part, 1));
+  c->gemm_cnt = b.take<int>(max_tiles);
+  c->lm_cnt = b.take<int>(64);
+  c->amax_val = b.take<float>((size_t)max_lm_tiles * kMaxLmRows);
+  c->amax_idx = b.take<int>((size_t)max_lm_tiles * kMaxLmRows);
+  c->attn_part = b.take<float>(attn_part);
+  c->attn_cnt = b.take<int>(max_attn_cnt);
+  c->seq_dev = b.take<SeqState>(c->max_batch);
+  c->out_dev = b.take<int>((size_t)c->max_batch * c->max_ctx);
+  c->gather_idx_dev = b.take<size_t>(kGatherMax);
+  c->gather_out_dev = b.take<float>(kGatherMax);
+  return align256(b.off);
+}
+
+// ----------------------------------------------------------------------------
+// weight generation
+// ----------------------------------------------------------------------------
+
+pard_status generate(pard_ctx* c, int w) {
+  ModelDev& M = c->m[w];
+  const pard_model_spec& s = M.spec;
+  const double stdv = s.init_std;
+  auto key = [&](int tensor) { return stream_key(s.seed, s.weight_stream, (uint32_t)tensor); };
+  auto gen = [&](uint16_t* dst, int n_pad, int k_pad, int rows, int cols, int map, uint64_t k0, uint64_t k1,
+                 uint64_t k2) -> hipError_t {
+    GenArgs a{};
+    a.dst = dst;
+    a.n_strips = n_pad / 16;
+    a.kb_total = k_pad / 32;
+    a.rows = rows;
+    a.cols = cols;
+    a.map = map;
+    a.q_dim = M.q_dim;
+    a.kv_dim = M.kv_dim;
+    a.hd = s.head_dim;
+    a.key0 = k0;
+    a.key1 = k1;
+    a.key2 = k2;
+    a.stdv = stdv;
+    return launch_gen_packed(a, c->stream);
+  };
+  for (int l = 0; l < s.n_layers; ++l) {
+    Layer& L = M.layers[l];
+    HIP_TRY(c, gen(L.wqkv, M.nqkv, M.d, 0, M.d, MAP_QKV, key(layer_tensor(l, 0)), key(layer_tensor(l, 1)),
+                   key(layer_tensor(l, 2))));
+    HIP_TRY(c, gen(L.wo, M.d, M.q_dim, M.d, M.q_dim, MAP_IDENTITY, key(layer_tensor(l, 3)), 0, 0));
+    HIP_TRY(c, gen(L.wgu, 2 * M.f_pad, M.d, s.ffn_dim, M.d, MAP_GATEUP, key(layer_tensor(l, 4)),
+                   key(layer_tensor(l, 5)), 0));
+    HIP_TRY(c, gen(L.wd, M.d, M.f_pad, M.d, s.ffn_dim, MAP_IDENTITY, key(layer_tensor(l, 6)), 0, 0));
+    if (L.bqkv) {
+      GenArgs a{};
+      a.map = MAP_QKV;
+      a.q_dim = M.q_dim;
+      a.kv_dim = M.kv_dim;
+      a.hd = s.head_dim;
+      a.key0 = key(layer_tensor(l, 7));
+      a.key1 = key(layer_tensor(l, 8));
+      a.key2 = key(layer_tensor(l, 9));
+      a.stdv = stdv;
+      HIP_TRY(c, launch_gen_bias(a, L.bqkv, M.nqkv, c->stream));
+    }
+    HIP_TRY(c, launch_fill_f32(L.g_attn, M.d, 1.0f, c->stream));
+    HIP_TRY(c, launch_fill_f32(L.g_mlp, M.d, 1.0f, c->stream));
+  }
+  HIP_TRY(c, gen(M.embed, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(0), 0, 0));
+  if (!s.tied_embeddings) HIP_TRY(c, gen(M.lm_head, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(1), 0, 0));
+  HIP_TRY(c, launch_fill_f32(M.g_final, M.d, 1.0f, c->stream));
+  HIP_TRY(c, launch_rope_table(M.rope, c->max_ctx, s.head_dim, (double)s.rope_theta, c->stream));
+  return PARD_OK;
+}
+
+// ----------------------------------------------------------------------------
+// forward pass
+// ----------------------------------------------------------------------------
+
+struct Timed {
+  pard_ctx* c;
+  bool on;
+  Timed(pard_ctx* ctx, int cls) : c(ctx), on(false) {
+    if (c->timer_class == cls && c->timer_used < c->timer_max) {
+      on = hipEventRecord(c->timer_ev[2 * c->timer_used], c->stream) == hipSuccess;
+    }
+  }
+  ~Timed() {
+    if (on) {
+      (void)hipEventRecord(c->timer_ev[2 * c->timer_used + 1], c->stream);
+      ++c->timer_used;
+    }
+  }
+};
+
+GemmArgs gemm_base(const ModelDev& M, const GemmPlan& p, int S, const uint16_t* W) {
+  GemmArgs a{};
+  a.W = W;
+  a.kb_total = p.kb_total;
+  a.G = p.G;
+  a.n_tiles = p.n_strips / S;
+  a.desc = M.desc;
+  a.eps = M.spec.rms_eps;
+  a.inv_k = 1.0f / (float)M.d;
+  return a;
+}
+
+hipError_t run_gemm(pard_ctx* c, int cls, int epi, int mt, GemmArgs a, const GemmPlan& p) {
+  const int S = pick_S(epi, p.n_strips, mt);
+  a.n_tiles = p.n_strips / S;
+  a.part = c->gemm_part;
+  a.counters = c->gemm_cnt;
+  Timed t(c, cls);
+  return launch_gemm(epi, mt, S, a, c->stream);
+}
+
+struct PassSpec {
+  int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
+  int max_lm_rows = 0;    // 0: no lm_head
+  int tail = TAIL_NONE;
+  FwdDesc* next_desc = nullptr;
+  bool emit = false;
+};
+
+pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
+  ModelDev& M = c->m[w];
+  const pard_model_spec& s = M.spec;
+  const int mt = ceil_div(ps.max_rows, 16);
+  const int cls0 = w * 8;
+  {
+    Timed t(c, cls0 + 0);
+    HIP_TRY(c, launch_embed(M.embed, M.p_lm.kb_total, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, M.ss,
+                            ps.max_rows, c->stream));
+  }
+  const size_t layer_kv = (size_t)s.n_kv_heads * c->max_ctx * s.head_dim;
+  uint16_t* kc_seq = M.kcache + c->kv_seq_stride[w] * seq;
+  uint16_t* vc_seq = M.vcache + c->kv_seq_stride[w] * seq;
+  for (int l = 0; l < s.n_layers; ++l) {
+    const Layer& L = M.layers[l];
+    uint16_t* kc = kc_seq + layer_kv * l;
+    uint16_t* vc = vc_seq + layer_kv * l;
+    {  // norm + QKV + bias + RoPE + KV append
+      GemmArgs a = gemm_base(M, M.p_qkv, 1, L.wqkv);
+      a.A = M.xg;
+      a.lda = M.d;
+      a.ss_in = M.ss;
+      a.ss_tiles = l == 0 ? 1 : M.ss_tiles_resid;
+      a.out = M.q;
+      a.ld_out = M.q_dim;
+      a.kc = kc;
+      a.vc = vc;
+      a.cap = c->max_ctx;
+      a.bias = L.bqkv;
+      a.rope = M.rope;
+      a.q_dim = M.q_dim;
+      a.kv_dim = M.kv_dim;
+      a.hd = s.head_dim;
+      HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, mt, a, M.p_qkv));
+    }
+    {  // attention
+      AttnArgs a{};
+      a.q = M.q;
+      a.ldq = M.q_dim;
+      a.kc = kc;
+      a.vc = vc;
+      a.cap = c->max_ctx;
+      a.out = M.attn;
+      a.ldo = M.q_dim;
+      a.desc = M.desc;
+      a.n_heads = s.n_heads;
+      a.n_kv = s.n_kv_heads;
+      a.chunk = M.attn_chunk;
+      a.n_chunks = M.attn_chunks;
+      a.n_qblocks = ceil_div(ps.max_rows * M.group, kAttnQB);
+      a.scale = 1.0f / std::sqrt((float)s.head_dim);
+      a.part = c->attn_part;
+      a.counters = c->attn_cnt;
+      Timed t(c, cls0 + 2);
+      HIP_TRY(c, launch_attention(s.head_dim, a, c->stream));
+    }
+    {  // O-projection + residual
+      GemmArgs a = gemm_base(M, M.p_o, 1, L.wo);
+      a.A = M.attn;
+      a.lda = M.q_dim;
+      a.x = M.x;
+      a.ldx = M.d;
+      a.g_next = L.g_mlp;
+      a.xg = M.xg;
+      a.ss_out = M.ss;
+      HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, mt, a, M.p_o));
+    }
+    {  // norm + gate/up + SiLU * up
+      GemmArgs a = gemm_base(M, M.p_gu, 2, L.wgu);
+      a.A = M.xg;
+      a.lda = M.d;
+      a.ss_in = M.ss;
+      a.ss_tiles = M.ss_tiles_resid;
+      a.out = M.h;
+      a.ld_out = M.f_pad;
+      HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, mt, a, M.p_gu));
+    }
+    {  // down + residual
+      GemmArgs a = gemm_base(M, M.p_d, 1, L.wd);
+      a.A = M.h;
+      a.lda = M.f_pad;
+      a.x = M.x;
+      a.ldx = M.d;
+      a.g_next = (l + 1 < s.n_layers) ? M.layers[l + 1].g_attn : M.g_final;
+      a.xg = M.xg;
+      a.ss_out = M.ss;
+      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, mt, a, M.p_d));
+    }
+  }
+  if (ps.max_lm_rows > 0) {
+    GemmArgs a = gemm_base(M, M.p_lm, 1, M.lm_head);
+    a.A = M.xg;
+    a.lda = M.d;
+    a.ss_in = M.ss;
+    a.ss_tiles = M.ss_tiles_resid;
+    a.lm_mode = 1;
+    a.logits = M.logits;
+    a.vocab = s.vocab;
+    a.amax_val = c->amax_val;
+    a.amax_idx = c->amax_idx;
+    a.lm_counter = c->lm_cnt;
+    a.result = M.result;
+    a.tail = ps.tail;
+    a.seq = c->seq_dev + seq;
+    a.next_desc = ps.next_desc;
+    a.out_tokens = ps.emit ? c->out_dev + (size_t)seq * c->max_ctx : nullptr;
+    a.out_cap = c->max_ctx;
+    HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, ceil_div(ps.max_lm_rows, 16), a, M.p_lm));
+  }
+  return PARD_OK;
+}
+
+// Copies a host-built pass description into model w's device descriptor.
+pard_status stage_desc(pard_ctx* c, int w, const FwdDesc& d) {
+  if (c->desc_slot == kDescRing) {
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    c->desc_slot = 0;
+  }
+  FwdDesc* h = c->h_desc + c->desc_slot++;
+  *h = d;
+  HIP_TRY(c, hipMemcpyAsync(c->m[w].desc, h, sizeof(FwdDesc), hipMemcpyHostToDevice, c->stream));
+  return PARD_OK;
+}
+
+pard_status push_seq(pard_ctx* c, int seq) {
+  HIP_TRY(c, hipMemcpyAsync(c->seq_dev + seq, c->h_seq + seq, sizeof(SeqState), hipMemcpyHostToDevice, c->stream));
+  return PARD_OK;
+}
+
+pard_status pull_seq_sync(pard_ctx* c, int seq) {
+  HIP_TRY(c, hipMemcpyAsync(c->h_seq + seq, c->seq_dev + seq, sizeof(SeqState), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->desc_slot = 0;
+  return PARD_OK;
+}
+
+FwdDesc make_desc(const int* ids, int n_ids, int n_masks, int mask_id, int pos0, int n_real, int lm_row0,
+                  int lm_rows) {
+  FwdDesc d{};
+  int n = 0;
+  for (int i = 0; i < n_ids; ++i) d.ids[n++] = ids[i];
+  for (int i = 0; i < n_masks; ++i) d.ids[n++] = mask_id;
+  d.n_rows = n;
+  d.n_real = n_real;
+  d.pos0 = pos0;
+  d.lm_row0 = lm_row0;
+  d.lm_rows = lm_rows;
+  return d;
+}
+
+// Ingest tokens[0..n) at positions pos0.. into model w's cache (no lm_head).
+pard_status ingest(pard_ctx* c, int w, int seq, const int* tokens, int n, int pos0) {
+  for (int off = 0; off < n; off += kPrefillRows) {
+    const int rows = std::min(kPrefillRows, n - off);
+    pard_status st = stage_desc(c, w, make_desc(tokens + off, rows, 0, 0, pos0 + off, rows, rows - 1, 1));
+    if (st != PARD_OK) return st;
+    PassSpec ps;
+    ps.max_rows = rows;
+    st = forward(c, w, seq, ps);
+    if (st != PARD_OK) return st;
+  }
+  return PARD_OK;
+}
+
+bool ids_ok(const int* ids, int n, int vocab) {
+  for (int i = 0; i < n; ++i)
+    if (ids[i] < 0 || ids[i] >= vocab) return false;
+  return true;
+}
+
+pard_status check_seq(pard_ctx* c, int seq, bool need_prefill) {
+  if (seq < 0 || seq >= c->max_batch) return fail(c, PARD_ERR_CAPACITY, "seq %d outside [0, max_batch=%d)", seq, c->max_batch);
+  if (need_prefill && !c->prefilled[seq]) return fail(c, PARD_ERR_STATE, "sequence slot %d is not prefilled", seq);
+  return PARD_OK;
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+
+extern "C" {
+
+const char* pard_status_string(pard_status s) {
+  switch (s) {
+    case PARD_OK: return "PARD_OK";
+    case PARD_ERR_ARG: return "PARD_ERR_ARG";
+    case PARD_ERR_STATE: return "PARD_ERR_STATE";
+    case PARD_ERR_CAPACITY: return "PARD_ERR_CAPACITY";
+    case PARD_ERR_NOMEM: return "PARD_ERR_NOMEM";
+    case PARD_ERR_DEVICE: return "PARD_ERR_DEVICE";
+    case PARD_ERR_UNSUPPORTED: return "PARD_ERR_UNSUPPORTED";
+  }
+  return "PARD_UNKNOWN";
+}
+
+size_t pard_arena_bytes(const pard_model_spec* target, const pard_model_spec* draft, int32_t max_batch,
+                        int32_t max_ctx, int32_t max_k) {
+  std::string why;
+  const int mask = target ? target->vocab - 1 : 0;
+  if (check_all(target, draft, mask, max_batch, max_ctx, max_k, &why) != PARD_OK) return 0;
+  pard_ctx tmp;
+  tmp.max_batch = max_batch;
+  tmp.max_ctx = max_ctx;
+  tmp.max_k = max_k;
+  derive(tmp.m[0], *target, max_ctx);
+  derive(tmp.m[1], *draft, max_ctx);
+  return layout(&tmp, nullptr);
+}
+
+pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec* draft, int32_t mask_id,
+                            int32_t max_batch, int32_t max_ctx, int32_t max_k, void* dev_arena,
+                            size_t arena_bytes, void* hip_stream, pard_ctx** out) {
+  if (!out) return PARD_ERR_ARG;
+  *out = nullptr;
+  std::string why;
+  pard_status st = check_all(target, draft, mask_id, max_batch, max_ctx, max_k, &why);
+  if (st != PARD_OK) return st;
+  if (!dev_arena || (reinterpret_cast<uintptr_t>(dev_arena) & 255)) return PARD_ERR_ARG;
+  const size_t need = pard_arena_bytes(target, draft, max_batch, max_ctx, max_k);
+  if (arena_bytes < need) return PARD_ERR_NOMEM;
+
+  pard_ctx* c = new (std::nothrow) pard_ctx();
+  if (!c) return PARD_ERR_NOMEM;
+  c->mask_id = mask_id;
+  c->max_batch = max_batch;
+  c->max_ctx = max_ctx;
+  c->max_k = max_k;
+  c->stream = reinterpret_cast<hipStream_t>(hip_stream);
+  c->arena = static_cast<char*>(dev_arena);
+  c->arena_bytes = arena_bytes;
+  derive(c->m[0], *target, max_ctx);
+  derive(c->m[1], *draft, max_ctx);
+  layout(c, c->arena);
+  c->hist.assign(max_batch, {});
+  c->prefilled.assign(max_batch, 0);
+
+  auto bail = [&](pard_status s) {
+    pard_free(c);
+    return s;
+  };
+  if (hipHostMalloc((void**)&c->h_desc, sizeof(FwdDesc) * kDescRing, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_seq, sizeof(SeqState) * max_batch, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_gather_idx, sizeof(size_t) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_gather_out, sizeof(float) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_out, sizeof(int) * max_ctx, hipHostMallocDefault) != hipSuccess)
+    return bail(PARD_ERR_DEVICE);
+  memset(c->h_seq, 0, sizeof(SeqState) * max_batch);
+  if (hipEventCreate(&c->ev_start) != hipSuccess || hipEventCreate(&c->ev_stop) != hipSuccess)
+    return bail(PARD_ERR_DEVICE);
+
+  for (int w = 0; w < 2; ++w)
+    if (generate(c, w) != PARD_OK) return bail(PARD_ERR_DEVICE);
+  int max_tiles = 1;
+  for (int w = 0; w < 2; ++w) {
+    const ModelDev& M = c->m[w];
+    max_tiles = std::max({max_tiles, M.p_qkv.n_strips, M.p_o.n_strips, M.p_gu.n_strips, M.p_d.n_strips});
+  }
+  if (launch_fill_u32(reinterpret_cast<uint32_t*>(c->gemm_cnt), max_tiles, 0, c->stream) != hipSuccess ||
+      launch_fill_u32(reinterpret_cast<uint32_t*>(c->lm_cnt), 64, 0, c->stream) != hipSuccess)
+    return bail(PARD_ERR_DEVICE);
+  size_t attn_cnt = 1;
+  for (int w = 0; w < 2; ++w) {
+    const ModelDev& M = c->m[w];
+    attn_cnt = std::max(attn_cnt, (size_t)M.spec.n_kv_heads * ceil_div(kMaxRows * M.group, kAttnQB));
+  }
+  if (launch_fill_u32(reinterpret_cast<uint32_t*>(c->attn_cnt), attn_cnt, 0, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
+      hipStreamSynchronize(c->stream) != hipSuccess)
+    return bail(PARD_ERR_DEVICE);
+  *out = c;
+  return PARD_OK;
+}
+
+void pard_free(pard_ctx* c) {
+  if (!c) return;
+  (void)hipStreamSynchronize(c->stream);
+  if (c->h_desc) (void)hipHostFree(c->h_desc);
+  if (c->h_seq) (void)hipHostFree(c->h_seq);
+  if (c->h_gather_idx) (void)hipHostFree(c->h_gather_idx);
+  if (c->h_gather_out) (void)hipHostFree(c->h_gather_out);
+  if (c->h_out) (void)hipHostFree(c->h_out);
+  if (c->ev_start) (void)hipEventDestroy(c->ev_start);
+  if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
+  for (hipEvent_t e : c->timer_ev) (void)hipEventDestroy(e);
+  delete c;
+}
+
+const char* pard_last_error(const pard_ctx* c) { return c ? c->err.c_str() : "null context"; }
+
+pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_t n, int32_t* first_token) {
+  if (!c) return PARD_ERR_ARG;
+  pard_status st = check_seq(c, seq, false);
+  if (st != PARD_OK) return st;
+  if (!prompt || !first_token || n < 1) return fail(c, PARD_ERR_ARG, "prefill: null pointer or empty prompt");
+  if (!ids_ok(prompt, n, c->m[0].spec.vocab)) return fail(c, PARD_ERR_ARG, "prefill: token id out of range");
+  if ((int64_t)n + 2 * c->max_k + 1 > c->max_ctx)
+    return fail(c, PARD_ERR_CAPACITY, "prefill: prompt of %d does not fit max_ctx=%d", n, c->max_ctx);
+  SeqState& S = c->h_seq[seq];
+  memset(&S, 0, sizeof S);
+  S.L[0] = n;
+  S.L[1] = n;
+  S.mask_id = c->mask_id;
+  if ((st = push_seq(c, seq)) != PARD_OK) return st;
+  for (int w = 1; w >= 0; --w) {   // draft first, the target's last chunk sets the first token
+    for (int off = 0; off < n; off += kPrefillRows) {
+      const int rows = std::min(kPrefillRows, n - off);
+      const bool last = (off + rows == n) && w == PARD_TARGET;
+      st = stage_desc(c, w, make_desc(prompt + off, rows, 0, 0, off, rows, rows - 1, 1));
+      if (st != PARD_OK) return st;
+      PassSpec ps;
+      ps.max_rows = rows;
+      if (last) {
+        ps.max_lm_rows = 1;
+        ps.tail = TAIL_PREFILL;
+      }
+      if ((st = forward(c, w, seq, ps)) != PARD_OK) return st;
+    }
+  }
+  if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
+  c->m[PARD_TARGET].last_lm_rows = 1;
+  *first_token = S.bonus;
+  c->hist[seq].assign(prompt, prompt + n);
+  c->hist[seq].push_back(S.bonus);
+  c->prefilled[seq] = 1;
+  return PARD_OK;
+}
+
+pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t n_prefix, int32_t K,
+                       int32_t* cand) {
+  if (!c) return PARD_ERR_ARG;
+  pard_status st = check_seq(c, seq, true);
+  if (st != PARD_OK) return st;
+  if (!prefix || !cand || n_prefix < 1) return fail(c, PARD_ERR_ARG, "draft: null pointer or empty prefix");
+  if (K < 1 || K > c->max_k) return fail(c, PARD_ERR_ARG, "draft: K=%d outside [1, max_k=%d]", K, c->max_k);
+  if (!ids_ok(prefix, n_prefix, c->m[1].spec.vocab)) return fail(c, PARD_ERR_ARG, "draft: token id out of range");
+  if ((int64_t)n_prefix + K - 1 > c->max_ctx)
+    return fail(c, PARD_ERR_CAPACITY, "draft: %d rows past position %d exceed max_ctx", K - 1, n_prefix);
+  SeqState& S = c->h_seq[seq];
+  const SeqState saved = S;
+  int Ld = std::min(S.L[1], n_prefix - 1);
+  // a long unseen tail is ingested first so that the draft pass fits kMaxRows rows
+  const int max_real = kMaxRows - (K - 1);
+  if (n_prefix - Ld > max_real) {
+    const int extra = n_prefix - Ld - max_real;
+    if ((st = ingest(c, PARD_DRAFT, seq, prefix + Ld, extra, Ld)) != PARD_OK) { S = saved; return st; }
+    Ld += extra;
+  }
+  const int n_new = n_prefix - Ld;
+  S.k = K;
+  S.L[1] = Ld;
+  if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
+  const FwdDesc d = make_desc(prefix + Ld, n_new, K - 1, c->mask_id, Ld, n_new, n_new - 1, K);
+  if ((st = stage_desc(c, PARD_DRAFT, d)) != PARD_OK) { S = saved; return st; }
+  PassSpec ps;
+  ps.max_rows = d.n_rows;
+  ps.max_lm_rows = K;
+  ps.tail = TAIL_DRAFT;
+  ps.next_desc = c->m[PARD_TARGET].desc;
+  if ((st = forward(c, PARD_DRAFT, seq, ps)) != PARD_OK) { S = saved; return st; }
+  if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
+  c->m[PARD_DRAFT].last_lm_rows = K;
+  for (int i = 0; i < K; ++i) cand[i] = S.cand[i];
+  return PARD_OK;
+}
+
+pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K, int32_t* n_accepted,
+                        int32_t* bonus) {
+  if (!c) return PARD_ERR_ARG;
+  pard_status st = check_seq(c, seq, true);
+  if (st != PARD_OK) return st;
+  if (!n_accepted || !bonus || (K > 0 && !cand)) return fail(c, PARD_ERR_ARG, "verify: null pointer");
+  if (K < 0 || K > c->max_k) return fail(c, PARD_ERR_ARG, "verify: K=%d outside [0, max_k=%d]", K, c->max_k);
+  if (K > 0 && !ids_ok(cand, K, c->m[0].spec.vocab)) return fail(c, PARD_ERR_ARG, "verify: token id out of range");
+  SeqState& S = c->h_seq[seq];
+  if ((int64_t)S.L[0] + K + 1 > c->max_ctx)
+    return fail(c, PARD_ERR_CAPACITY, "verify: %d rows at position %d exceed max_ctx", K + 1, S.L[0]);
+  const SeqState saved = S;
+  const int Lt = S.L[0];
+  int ids[kMaxK + 1];
+  ids[0] = S.bonus;
+  for (int i = 0; i < K; ++i) {
+    ids[1 + i] = cand[i];
+    S.cand[i] = cand[i];
+  }
+  S.k = K;
+  if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
+  if ((st = stage_desc(c, PARD_TARGET, make_desc(ids, K + 1, 0, 0, Lt, K + 1, 0, K + 1))) != PARD_OK) {
+    S = saved;
+    return st;
+  }
+  PassSpec ps;
+  ps.max_rows = K + 1;
+  ps.max_lm_rows = K + 1;
+  ps.tail = TAIL_VERIFY;
+  ps.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
+  if ((st = forward(c, PARD_TARGET, seq, ps)) != PARD_OK) { S = saved; return st; }
+  if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
+  c->m[PARD_TARGET].last_lm_rows = K + 1;
+  *n_accepted = S.a;
+  *bonus = S.bonus;
+  std::vector<int>& h = c->hist[seq];
+  h.resize(Lt + 1);
+  for (int i = 0; i < S.a; ++i) h.push_back(cand[i]);
+  h.push_back(S.bonus);
+  return PARD_OK;
+}
+
+pard_status pard_kv_truncate(pard_ctx* c, int32_t seq, int32_t which, int32_t new_len) {
+  if (!c) return PARD_ERR_ARG;
+  pard_status st = check_seq(c, seq, true);
+  if (st != PARD_OK) return st;
+  if (which != PARD_TARGET && which != PARD_DRAFT) return fail(c, PARD_ERR_ARG, "truncate: bad model id");
+  SeqState& S = c->h_seq[seq];
+  if (new_len < 0 || new_len > S.L[which])
+    return fail(c, PARD_ERR_ARG, "truncate: new_len %d outside [0, %d]", new_len, S.L[which]);
+  const SeqState saved = S;
+  S.L[which] = new_len;
+  if ((st = push_seq(c, seq)) != PARD_OK || (st = pull_seq_sync(c, seq)) != PARD_OK) {
+    S = saved;
+    return st;
+  }
+  if (which == PARD_TARGET) {
+    std::vector<int>& h = c->hist[seq];
+    const int pending = h.back();
+    h.resize(new_len);
+    h.push_back(pending);
+  }
+  return PARD_OK;
+}
+
+pard_status pard_kv_len(const pard_ctx* c, int32_t seq, int32_t which, int32_t* len) {
+  if (!c || !len || (which != PARD_TARGET && which != PARD_DRAFT)) return PARD_ERR_ARG;
+  if (seq < 0 || seq >= c->max_batch) return PARD_ERR_CAPACITY;
+  *len = c->h_seq[seq].L[which];
+  return PARD_OK;
+}
+
+pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32_t K, int32_t n_tokens,
+                          int32_t max_steps, int32_t* out_tokens, pard_stats* stats) {
+  if (!c) return PARD_ERR_ARG;
+  if (!seqs || !out_tokens || n_tokens < 1) return fail(c, PARD_ERR_ARG, "generate: null pointer or n_tokens < 1");
+  if (n_seq != 1) return fail(c, PARD_ERR_UNSUPPORTED, "generate: only one sequence per call in this build");
+  const int seq = seqs[0];
+  pard_status st = check_seq(c, seq, true);
+  if (st != PARD_OK) return st;
+  if (K < 0 || K > c->max_k) return fail(c, PARD_ERR_ARG, "generate: K=%d outside [0, max_k=%d]", K, c->max_k);
+  SeqState& S = c->h_seq[seq];
+  std::vector<int>& hist = c->hist[seq];
+  const int Lt = S.L[0];
+  if ((int64_t)Lt + n_tokens + 2 * K + 1 > c->max_ctx)
+    return fail(c, PARD_ERR_CAPACITY, "generate: %d tokens from length %d may exceed max_ctx=%d", n_tokens, Lt,
+                c->max_ctx);
+  const SeqState saved = S;
+  auto restore = [&](pard_status s) {
+    S = saved;
+    return s;
+  };
+  // the draft catches up with every committed token it has not seen
+  int Ld = std::min(S.L[1], Lt);
+  if (K > 0) {
+    const int total = Lt + 1;                  // committed tokens + pending
+    const int max_first = kMaxRows - (K - 1);
+    if (total - Ld > max_first) {
+      const int extra = total - Ld - max_first;
+      if ((st = ingest(c, PARD_DRAFT, seq, hist.data() + Ld, extra, Ld)) != PARD_OK) return restore(st);
+      Ld += extra;
+    }
+    S.n_pending = total - Ld;
+    for (int i = 0; i < S.n_pending; ++i) S.pending[i] = hist[Ld + i];
+  }
+  S.L[1] = Ld;
+  S.k = K;
+  S.n_out = 1;
+  S.n_target = n_tokens;
+  S.steps = 0;
+  S.mask_id = c->mask_id;
+  memset(S.accept_hist, 0, sizeof S.accept_hist);
+  if ((st = push_seq(c, seq)) != PARD_OK) return restore(st);
+  int first_rows;
+  if (K > 0) {
+    const FwdDesc d = make_desc(S.pending, S.n_pending, K - 1, c->mask_id, Ld, S.n_pending, S.n_pending - 1, K);
+    first_rows = d.n_rows;
+    if ((st = stage_desc(c, PARD_DRAFT, d)) != PARD_OK) return restore(st);
+  } else {
+    const int b = S.bonus;
+    if ((st = stage_desc(c, PARD_TARGET, make_desc(&b, 1, 0, 0, Lt, 1, 0, 1))) != PARD_OK) return restore(st);
+    first_rows = 1;
+  }
+  HIP_TRY(c, hipEventRecord(c->ev_start, c->stream));
+  int produced = 1, steps = 0;
+  bool first = true;
+  while (produced < n_tokens && (max_steps <= 0 || steps < max_steps)) {
+    int batch = ceil_div(n_tokens - produced, K + 1);
+    if (max_steps > 0) batch = std::min(batch, max_steps - steps);
+    for (int i = 0; i < batch; ++i) {
+      if (K > 0) {
+        PassSpec pd;
+        pd.max_rows = first ? std::max(first_rows, 2 * K) : 2 * K;
+        pd.max_lm_rows = K;
+        pd.tail = TAIL_DRAFT;
+        pd.next_desc = c->m[PARD_TARGET].desc;
+        if ((st = forward(c, PARD_DRAFT, seq, pd)) != PARD_OK) return st;
+      }
+      PassSpec pv;
+      pv.max_rows = K + 1;
+      pv.max_lm_rows = K + 1;
+      pv.tail = TAIL_VERIFY;
+      pv.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
+      pv.emit = true;
+      if ((st = forward(c, PARD_TARGET, seq, pv)) != PARD_OK) return st;
+      first = false;
+    }
+    HIP_TRY(c, hipEventRecord(c->ev_stop, c->stream));
+    if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
+    produced = S.n_out;
+    steps = S.steps;
+  }
+  float ms = 0.f;
+  if (steps > 0) HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_start, c->ev_stop));
+  const int n_new = produced - 1;   // tokens appended after the pending one
+  if (n_new > 0) {
+    HIP_TRY(c, hipMemcpyAsync(c->h_out, c->out_dev + (size_t)seq * c->max_ctx + 1, sizeof(int) * n_new,
+                              hipMemcpyDeviceToHost, c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+  }
+  const int written = std::min(produced, n_tokens);
+  out_tokens[0] = hist.back();
+  for (int i = 1; i < written; ++i) out_tokens[i] = c->h_out[i - 1];
+  for (int i = 0; i < n_new; ++i) hist.push_back(c->h_out[i]);
+  if (K > 0) c->m[PARD_DRAFT].last_lm_rows = K;
+  c->m[PARD_TARGET].last_lm_rows = K + 1;
+  if (stats) {
+    memset(stats, 0, sizeof *stats);
+    stats->steps = steps;
+    stats->tokens = written;
+    stats->elapsed_ms = ms;
+    for (int i = 0; i <= kMaxK; ++i) stats->accept_hist[i] = S.accept_hist[i];
+  }
+  return PARD_OK;
+}
+
+pard_status pard_read_logits(const pard_ctx* cc, int32_t which, int32_t seq, float* out, int32_t rows,
+                             int32_t vocab) {
+  pard_ctx* c = const_cast<pard_ctx*>(cc);
+  if (!c || !out || (which != PARD_TARGET && which != PARD_DRAFT)) return PARD_ERR_ARG;
+  if (seq < 0 || seq >= c->max_batch) return fail(c, PARD_ERR_ARG, "read_logits: bad seq");
+  const ModelDev& M = c->m[which];
+  if (vocab != M.spec.vocab) return fail(c, PARD_ERR_ARG, "read_logits: vocab mismatch");
+  if (M.last_lm_rows == 0) return fail(c, PARD_ERR_STATE, "read_logits: no lm_head pass yet");
+  if (rows < 1 || rows > M.last_lm_rows)
+    return fail(c, PARD_ERR_ARG, "read_logits: rows %d outside [1, %d]", rows, M.last_lm_rows);
+  HIP_TRY(c, hipMemcpyAsync(out, M.logits, sizeof(float) * rows * vocab, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return PARD_OK;
+}
+
+pard_status pard_read_weight(const pard_ctx* cc, int32_t which, int32_t tensor, int32_t row, int32_t col0,
+                             int32_t n, float* out) {
+  pard_ctx* c = const_cast<pard_ctx*>(cc);
+  if (!c || !out || (which != PARD_TARGET && which != PARD_DRAFT)) return PARD_ERR_ARG;
+  if (n < 1 || n > kGatherMax || row < 0 || col0 < 0) return fail(c, PARD_ERR_ARG, "read_weight: bad range");
+  const ModelDev& M = c->m[which];
+  const pard_model_spec& s = M.spec;
+  const int hd = s.head_dim;
+  const uint16_t* buf = nullptr;
+  int prow = 0, rows = 0, cols = 0, kpad = 0;
+  const float* fbuf = nullptr;
+  auto qk_row = [&](int r) { const int head = r / hd, dim = r % hd; return head * hd + (dim < hd / 2 ? 2 * dim : 2 * (dim - hd / 2) + 1); };
+  if (tensor == 0 || (tensor == 1 && !s.tied_embeddings)) {
+    buf = tensor == 0 ? M.embed : M.lm_head;
+    rows = s.vocab; cols = M.d; kpad = M.d; prow = row;
+  } else if (tensor >= 16 && tensor / 16 - 1 < s.n_layers) {
+    const int l = tensor / 16 - 1, j = tensor % 16;
+    const Layer& L = M.layers[l];
+    switch (j) {
+      case 0: buf = L.wqkv; rows = M.q_dim; cols = M.d; kpad = M.d; prow = qk_row(row); break;
+      case 1: buf = L.wqkv; rows = M.kv_dim; cols = M.d; kpad = M.d; prow = M.q_dim + qk_row(row); break;
+      case 2: buf = L.wqkv; rows = M.kv_dim; cols = M.d; kpad = M.d; prow = M.q_dim + M.kv_dim + row; break;
+      case 3: buf = L.wo; rows = M.d; cols = M.q_dim; kpad = M.q_dim; prow = row; break;
+      case 4: buf = L.wgu; rows = s.ffn_dim; cols = M.d; kpad = M.d; prow = (row / 16) * 32 + row % 16; break;
+      case 5: buf = L.wgu; rows = s.ffn_dim; cols = M.d; kpad = M.d; prow = (row / 16) * 32 + 16 + row % 16; break;
+      case 6: buf = L.wd; rows = M.d; cols = s.ffn_dim; kpad = M.f_pad; prow = row; break;
+      case 7: case 8: case 9:
+        if (!L.bqkv) return fail(c, PARD_ERR_ARG, "read_weight: model has no bias");
+        fbuf = L.bqkv; cols = 1;
+        rows = j == 7 ? M.q_dim : M.kv_dim;
+        prow = j == 7 ? qk_row(row) : (j == 8 ? M.q_dim + qk_row(row) : M.q_dim + M.kv_dim + row);
+        break;
+      default: return fail(c, PARD_ERR_ARG, "read_weight: bad tensor ordinal");
+    }
+  } else {
+    return fail(c, PARD_ERR_ARG, "read_weight: bad tensor ordinal");
+  }
+  if (row >= rows || col0 + n > cols) return fail(c, PARD_ERR_ARG, "read_weight: range outside the tensor");
+  if (fbuf) {
+    HIP_TRY(c, hipMemcpy(out, fbuf + prow, sizeof(float), hipMemcpyDeviceToHost));
+    return PARD_OK;
+  }
+  const int kb_total = kpad / 32;
+  for (int i = 0; i < n; ++i) {
+    const int col = col0 + i;
+    const size_t strip = prow / 16, kb = col / 32;
+    const int lane = (prow % 16) + 16 * ((col % 32) / 8);
+    c->h_gather_idx[i] = ((strip * kb_total + kb) * 64 + lane) * 8 + (col % 8);
+  }
+  HIP_TRY(c, hipMemcpyAsync(c->gather_idx_dev, c->h_gather_idx, sizeof(size_t) * n, hipMemcpyHostToDevice, c->stream));
+  HIP_TRY(c, launch_gather_u16(buf, c->gather_idx_dev, n, c->gather_out_dev, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(out, c->gather_out_dev, sizeof(float) * n, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  return PARD_OK;
+}
+
+pard_status pard_timer_enable(pard_ctx* c, int32_t kernel_class, int32_t max_launches) {
+  if (!c) return PARD_ERR_ARG;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  c->timer_class = -1;
+  c->timer_used = 0;
+  c->timer_max = 0;
+  if (kernel_class < 0) return PARD_OK;
+  if (kernel_class >= 16 || max_launches < 1 || max_launches > 1 << 16)
+    return fail(c, PARD_ERR_ARG, "timer: bad class or launch count");
+  while ((int)c->timer_ev.size() < 2 * max_launches) {
+    hipEvent_t e;
+    HIP_TRY(c, hipEventCreate(&e));
+    c->timer_ev.push_back(e);
+  }
+  c->timer_class = kernel_class;
+  c->timer_max = max_launches;
+  return PARD_OK;
+}
+
+pard_status pard_timer_read(pard_ctx* c, int32_t* launches, double* total_ms) {
+  if (!c || !launches || !total_ms) return PARD_ERR_ARG;
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  double sum = 0;
+  for (int i = 0; i < c->timer_used; ++i) {
+    float ms = 0;
+    HIP_TRY(c, hipEventElapsedTime(&ms, c->timer_ev[2 * i], c->timer_ev[2 * i + 1]));
+    sum += ms;
+  }
+  *launches = c->timer_used;
+  *total_ms = sum;
+  return PARD_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,110 @@
+// Internal structures shared by the engine (host) and the HIP kernels.
+//
+// Device data layout (all carved from the caller's arena):
+//   * every weight matrix W [out, in] is stored bf16 in "strip" order: 16 output
+//     rows x 32 input columns form a 1 KiB block laid out in the lane order of
+//     the v_mfma_f32_16x16x32_bf16 B operand (lane l holds row l%16, columns
+//     8*(l/16) .. +7); the blocks of one strip are contiguous along the input
+//     dimension, so a wavefront streaming a strip reads contiguous memory.
+//   * Q/K rows are stored pair-interleaved per head (packed row 2j = dim j,
+//     2j+1 = dim j + head_dim/2) so the rotate-half rotary pairs sit in
+//     neighbouring lanes; K is cached in that order and attention's q.k is
+//     invariant to it.  Gate/up rows are interleaved by strips (gate strip,
+//     up strip, ...) so one tile holds matching gate and up columns.
+//   * KV cache: K and V bf16 [batch][layer][kv_head][max_ctx][head_dim].
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pard {
+
+constexpr int kMaxK = 32;
+constexpr int kMaxRows = 64;      // rows of one forward pass (prefill chunk, 2*max_k)
+constexpr int kMaxLmRows = kMaxK + 1;
+constexpr int kBlock = 256;
+
+// Rows of the next forward pass of one model.  Written by the host (granular
+// calls) or by the tail of the previous pass (fused loop).
+struct FwdDesc {
+  int n_rows;     // rows in the pass
+  int n_real;     // leading rows that carry real tokens (committed afterwards)
+  int pos0;       // absolute position of row 0 (= committed KV length)
+  int lm_row0;    // first row fed to the lm_head
+  int lm_rows;    // rows fed to the lm_head
+  int pad[3];
+  int ids[kMaxRows];
+};
+
+// Decode state of one sequence slot.
+struct SeqState {
+  int L[2];                  // committed KV length: [0] target, [1] draft
+  int k;                     // draft length of the current step
+  int n_pending;             // tokens produced but not yet in the draft cache
+  int pending[kMaxK + 1];
+  int cand[kMaxK];           // draft candidates of the current step
+  int t[kMaxK + 1];          // target argmax of the last verify pass
+  int a, bonus;              // accepted count, bonus (= pending token for the target)
+  int n_out, n_target;       // tokens written to the output buffer / requested
+  int steps;
+  int mask_id;
+  int accept_hist[kMaxK + 1];
+};
+
+enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
+enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3 };
+
+struct GemmArgs {
+  const uint16_t* W;      // strip-packed bf16 weight
+  int kb_total;           // padded input dim / 32
+  int G;                  // input-dim splits across workgroups
+  int n_tiles;            // output tiles (S strips each)
+  const uint16_t* A;      // bf16 activations [kMaxRows][lda]
+  int lda;
+  const FwdDesc* desc;
+  int lm_mode;            // 0: rows [0, n_rows)   1: rows [lm_row0, lm_row0 + lm_rows)
+  float* part;            // split partials [tile][G][S*MT*256]
+  int* counters;          // per tile, self-resetting
+  // RMSNorm of the A operand (QKV, SWIGLU, LOGITS): A already holds x*g in
+  // bf16; 1/rms comes from the producer's per-tile sums of squares.
+  const float* ss_in; int ss_tiles;
+  float eps, inv_k;
+  // EPI_RESID: x += Y, and for the next consumer xg = bf16(x * g_next) and
+  // per-tile sums of squares of x.
+  float* x; int ldx;
+  const float* g_next; uint16_t* xg; float* ss_out;
+  // EPI_QKV / EPI_SWIGLU
+  uint16_t* out; int ld_out;
+  uint16_t* kc; uint16_t* vc; int cap;
+  const float* bias; const float2* rope;
+  int q_dim, kv_dim, hd;
+  // EPI_LOGITS
+  float* logits; int vocab;
+  float* amax_val; int* amax_idx; int* lm_counter;
+  int* result;            // argmax per lm row
+  int tail;
+  SeqState* seq;
+  FwdDesc* next_desc;     // staged by the tail
+  int* out_tokens;        // emitted tokens of the fused loop (verify tail)
+  int out_cap;
+};
+
+struct AttnArgs {
+  const uint16_t* q; int ldq;
+  const uint16_t* kc; const uint16_t* vc; int cap;
+  uint16_t* out; int ldo;
+  const FwdDesc* desc;
+  int n_heads, n_kv, chunk, n_chunks, n_qblocks;
+  float scale;
+  float* part; int* counters;
+};
+
+constexpr int kAttnQB = 16;   // query (row, head) pairs per workgroup
+constexpr int kAttnSub = 64;  // keys per LDS sub-chunk
+
+// Launchers (return hipSuccess or the launch error).
+hipError_t launch_gemm(int epi, int mt, int S, const GemmArgs& a, hipStream_t st);
+hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
+size_t attn_part_floats(int head_dim);
+
+}  // namespace pard

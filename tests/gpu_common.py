@@ -1,0 +1,94 @@
+"""Shared helpers of the GPU parity tests (lock-step comparison against the oracle)."""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+
+import oracle
+
+ATOL, RTOL = 3e-2, 1e-2      # logits: |gpu - oracle| <= ATOL + RTOL * |oracle|
+MARGIN = 0.1                 # token decisions are compared where top1 - top2 > MARGIN
+
+
+def say(msg: str) -> None:
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def require_gpu():
+    import pytest
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+
+
+def margins(logits: np.ndarray) -> np.ndarray:
+    part = np.partition(logits, -2, axis=-1)
+    return part[..., -1] - part[..., -2]
+
+
+def assert_logits_close(gpu: np.ndarray, ref: np.ndarray, what: str) -> float:
+    err = np.abs(gpu.astype(np.float64) - ref)
+    bound = ATOL + RTOL * np.abs(ref)
+    bad = err > bound
+    worst = float(err.max())
+    assert not bad.any(), (f"{what}: {int(bad.sum())} of {err.size} logits outside tolerance; "
+                           f"max abs err {worst:.4g} (ref scale {np.abs(ref).max():.3g})")
+    return worst
+
+
+def assert_tokens_match(gpu_tokens, ref_logits: np.ndarray, what: str) -> None:
+    """GPU argmax must equal the oracle's wherever the oracle's margin exceeds MARGIN."""
+    ref = np.argmax(ref_logits, axis=-1)
+    m = margins(ref_logits)
+    for i, (g, r) in enumerate(zip(gpu_tokens, ref)):
+        if m[i] > MARGIN:
+            assert int(g) == int(r), f"{what}: row {i} gpu {g} oracle {r} (margin {m[i]:.3f})"
+
+
+def lockstep(eng, target, draft, prompt, k, steps, mask_id, seq=0, tag=""):
+    """Run `steps` PARD steps on the GPU and the oracle with identical inputs.
+
+    Returns the max logit error seen.  The oracle is re-synchronised to the
+    GPU's decisions, which may differ from its own only at near-ties."""
+    from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
+    worst = 0.0
+    first = eng.prefill(prompt, seq=seq)
+    cache_t, cache_d, first_o, lg = oracle.prefill(target, draft, prompt)
+    worst = max(worst, assert_logits_close(eng.read_logits(PARD_TARGET, 1, seq=seq), lg,
+                                           f"{tag} prefill logits"))
+    assert_tokens_match([first], lg, f"{tag} first token")
+    if first != first_o:                       # near-tie: follow the GPU
+        pass
+    hist = list(prompt) + [first]
+    pending = [first]
+    for step in range(steps):
+        if k > 0:
+            cands = eng.draft(hist, k, seq=seq)
+            g_dl = eng.read_logits(PARD_DRAFT, k, seq=seq)
+            _, o_dl = oracle.draft_step(draft, cache_d, pending, k, mask_id)
+            worst = max(worst, assert_logits_close(g_dl, o_dl, f"{tag} step {step} draft logits"))
+            assert_tokens_match(cands, o_dl, f"{tag} step {step} candidates")
+            assert eng.kv_len(PARD_DRAFT, seq=seq) == cache_d.length == len(hist)
+        else:
+            cands = []
+        lt = cache_t.length
+        a, bonus = eng.verify(cands, seq=seq)
+        g_vl = eng.read_logits(PARD_TARGET, k + 1, seq=seq)
+        o_a, o_bonus, o_t, o_vl = oracle.verify_step(target, cache_t, pending[-1], cands)
+        worst = max(worst, assert_logits_close(g_vl, o_vl, f"{tag} step {step} verify logits"))
+        # the GPU's decision is consistent with its own argmax ...
+        g_t = np.argmax(g_vl, axis=-1)
+        assert (a, bonus) == oracle.accept_prefix(cands, g_t), f"{tag} step {step} accept rule"
+        # ... and equals the oracle's wherever the inspected rows are not near-ties
+        inspected = o_vl[:min(o_a, a) + 1]
+        if (margins(inspected) > MARGIN).all():
+            assert (a, bonus) == (o_a, o_bonus), f"{tag} step {step}: gpu {(a, bonus)} oracle {(o_a, o_bonus)}"
+        if a != o_a:
+            cache_t.truncate(lt)
+            oracle.forward_cached(target, cache_t, [pending[-1]] + list(cands[:a]), logits_rows=[])
+        assert eng.kv_len(PARD_TARGET, seq=seq) == cache_t.length == lt + a + 1
+        pending = list(cands[:a]) + [bonus]
+        hist += pending
+    return worst

@@ -1,0 +1,111 @@
+"""Host-side checks of the C ABI: symbols, arena sizing and argument validation.
+
+None of these calls reaches the GPU: validation precedes all device work.
+"""
+import ctypes as C
+import os
+import re
+
+import pytest
+
+import pard_inputs as pi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pard.h")
+LIB = os.path.join(ROOT, "paper_2504_18583_amd", "libpard.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="libpard.so not built")
+
+
+@pytest.fixture(scope="module")
+def b():
+    from paper_2504_18583_amd import binding
+    return binding
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pard_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_function_is_exported(b):
+    names = declared_functions()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(b.lib, n), n
+    assert set(names) == set(b.EXPORTED)
+
+
+def _pair(name="llama8b_1b"):
+    wl = pi.WORKLOADS[name]
+    return wl, pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")
+
+
+def test_arena_bytes_covers_weights_and_cache(b):
+    wl, t, d = _pair()
+    n = b.pard_arena_bytes(b.spec_from(t), b.spec_from(d), 1, 1100, 8)
+    weights = 2 * (t.n_params() + d.n_params())
+    kv = 1100 * (131072 + 32768)
+    assert weights + kv < n < weights + kv + 2.0e9
+    n2 = b.pard_arena_bytes(b.spec_from(t), b.spec_from(d), 2, 1100, 8)
+    assert n2 - n >= kv
+
+
+@pytest.mark.parametrize("field,value", [("head_dim", 96), ("dtype", 0), ("vocab", 1000),
+                                         ("d_model", 100), ("n_kv_heads", 3), ("n_layers", 0),
+                                         ("rms_eps", 0.0)])
+def test_arena_bytes_rejects_bad_spec(b, field, value):
+    _, t, d = _pair("tiny")
+    ts = b.spec_from(t)
+    setattr(ts, field, value)
+    assert b.pard_arena_bytes(ts, b.spec_from(d), 1, 256, 4) == 0
+
+
+def test_arena_bytes_rejects_bad_capacity(b):
+    _, t, d = _pair("tiny")
+    ts, ds = b.spec_from(t), b.spec_from(d)
+    assert b.pard_arena_bytes(ts, ds, 1, 256, 0) == 0
+    assert b.pard_arena_bytes(ts, ds, 1, 256, 33) == 0
+    assert b.pard_arena_bytes(ts, ds, 0, 256, 4) == 0
+    assert b.pard_arena_bytes(ts, ds, 1, 9, 4) == 0
+    ds.vocab = 2048
+    assert b.pard_arena_bytes(ts, ds, 1, 256, 4) == 0
+
+
+def _load(b, t, d, mask, arena, nbytes, max_k=4):
+    ctx = b._CTX()
+    st = b.lib.pard_model_load(C.byref(t), C.byref(d), mask, 1, 256, max_k, C.c_void_p(arena),
+                               nbytes, None, C.byref(ctx))
+    return st, ctx.value
+
+
+def test_model_load_validates_before_device_work(b):
+    _, t, d = _pair("tiny")
+    ts, ds = b.spec_from(t), b.spec_from(d)
+    need = b.pard_arena_bytes(ts, ds, 1, 256, 4)
+    assert _load(b, ts, ds, 1023, 0, need)[0] == b.PARD_ERR_ARG            # null arena
+    assert _load(b, ts, ds, 1023, 0x1000 + 8, need)[0] == b.PARD_ERR_ARG   # misaligned
+    assert _load(b, ts, ds, 1023, 0x1000, need - 1)[0] == b.PARD_ERR_NOMEM
+    assert _load(b, ts, ds, 1024, 0x1000, need)[0] == b.PARD_ERR_ARG       # mask id
+    assert _load(b, ts, ds, 1023, 0x1000, need, max_k=0)[0] == b.PARD_ERR_ARG
+    bad = b.spec_from(t)
+    bad.head_dim = 96
+    assert _load(b, bad, ds, 1023, 0x1000, need)[0] == b.PARD_ERR_UNSUPPORTED
+    bad = b.spec_from(t)
+    bad.dtype = b.PARD_F32
+    assert _load(b, bad, ds, 1023, 0x1000, need)[0] == b.PARD_ERR_UNSUPPORTED
+
+
+def test_null_context_calls_return_arg(b):
+    one = (C.c_int32 * 4)(1, 2, 3, 4)
+    out = C.c_int32()
+    assert b.lib.pard_prefill(None, 0, one, 4, C.byref(out)) == b.PARD_ERR_ARG
+    assert b.lib.pard_draft(None, 0, one, 4, 2, one) == b.PARD_ERR_ARG
+    assert b.lib.pard_verify(None, 0, one, 2, C.byref(out), C.byref(out)) == b.PARD_ERR_ARG
+    assert b.lib.pard_kv_truncate(None, 0, 0, 0) == b.PARD_ERR_ARG
+    assert b.lib.pard_kv_len(None, 0, 0, C.byref(out)) == b.PARD_ERR_ARG
+    assert b.lib.pard_generate(None, 1, one, 2, 4, 0, one, None) == b.PARD_ERR_ARG
+    assert b.lib.pard_last_error(None) == b"null context"
+    b.lib.pard_free(None)
+    assert b.lib.pard_status_string(b.PARD_ERR_CAPACITY) == b"PARD_ERR_CAPACITY"

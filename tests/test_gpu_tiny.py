@@ -1,0 +1,216 @@
+"""GPU parity on the tiny pair (2-layer target, 1-layer tied draft, vocab 1024).
+
+Every call goes through the C ABI; the oracle runs on the same bf16-rounded
+weights and the same prompt.  Logits must agree within 3e-2 + 1e-2*|ref|,
+token decisions wherever the oracle's top-1/top-2 margin exceeds 0.1, accept
+counts and KV lengths exactly.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import pard_inputs as pi
+from gpu_common import (assert_logits_close, assert_tokens_match, lockstep, margins, require_gpu,
+                        say, MARGIN)
+
+pytestmark = pytest.mark.gpu
+
+WL = pi.WORKLOADS["tiny"]
+T_SPEC = pi.with_dtype(WL.target, "bf16")
+D_SPEC = pi.with_dtype(WL.draft, "bf16")
+PROMPT = [int(x) for x in pi.workload_prompts(WL)[0]]
+
+
+@pytest.fixture(scope="module")
+def models():
+    return oracle.build_model(T_SPEC), oracle.build_model(D_SPEC)
+
+
+@pytest.fixture(scope="module")
+def B():
+    require_gpu()
+    from paper_2504_18583_amd import binding
+    return binding
+
+
+@pytest.fixture(scope="module")
+def eng(B):
+    say("[gpu] tiny engine: load")
+    e = B.Engine(T_SPEC, D_SPEC, WL.mask_id, max_ctx=512, max_k=16, max_batch=2)
+    yield e
+    e.close()
+
+
+def test_weights_match_generator_bitwise(eng, models, B):
+    say("[gpu] tiny: weight readback")
+    rng = np.random.default_rng(0)
+    for which, model in ((B.PARD_TARGET, models[0]), (B.PARD_DRAFT, models[1])):
+        w = model.weights
+        spec = model.spec
+        cases = [(0, w["embed"])]
+        if not spec.tied:
+            cases.append((1, w["lm_head"]))
+        for l, lw in w["layers"].items():
+            for j, name in enumerate(["wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"]):
+                cases.append((pi.layer_tensor(l, j), lw[name]))
+        for tensor, ref in cases:
+            for row in rng.choice(ref.shape[0], size=6, replace=False):
+                got = eng.read_weight(which, tensor, int(row), 0, ref.shape[1])
+                assert np.array_equal(got, ref[row]), (which, tensor, row)
+
+
+def test_prefill_logits_and_first_token(eng, models, B):
+    say("[gpu] tiny: prefill")
+    target, draft = models
+    first = eng.prefill(PROMPT)
+    _, _, first_o, lg = oracle.prefill(target, draft, PROMPT)
+    assert_logits_close(eng.read_logits(B.PARD_TARGET, 1), lg, "prefill")
+    assert_tokens_match([first], lg, "first token")
+    assert eng.kv_len(B.PARD_TARGET) == eng.kv_len(B.PARD_DRAFT) == len(PROMPT)
+
+
+@pytest.mark.parametrize("k", [WL.k, 1, 8, 12, 0])
+def test_lockstep_draft_verify(eng, models, k):
+    say(f"[gpu] tiny: lock-step K={k}")
+    target, draft = models
+    worst = lockstep(eng, target, draft, PROMPT, k, steps=12, mask_id=WL.mask_id, tag=f"K={k}")
+    say(f"    max |logit err| {worst:.3g}")
+
+
+def test_generate_matches_greedy(eng, models, B):
+    say("[gpu] tiny: fused generate vs greedy")
+    target, _ = models
+    eng.prefill(PROMPT)
+    toks, stats = eng.generate(WL.k, WL.n_tokens)
+    assert len(toks) == WL.n_tokens == stats.tokens
+    assert sum(stats.accept_hist) == stats.steps
+    assert sum((a + 1) * n for a, n in enumerate(stats.accept_hist)) >= WL.n_tokens - 1
+    # oracle greedy with the margin of every decision
+    cache = oracle.KVCache(target)
+    lg = oracle.forward_cached(target, cache, PROMPT, logits_rows=[len(PROMPT) - 1])[0]
+    ref, marg = [], []
+    for i in range(WL.n_tokens):
+        ref.append(int(np.argmax(lg)))
+        marg.append(float(margins(lg)))
+        if toks[i] != ref[i]:
+            assert marg[i] <= MARGIN, f"token {i}: gpu {toks[i]} oracle {ref[i]} margin {marg[i]:.3f}"
+            break                                   # a genuine near-tie: sequences fork here
+        lg = oracle.forward_cached(target, cache, [toks[i]])[0]
+    committed = sum((a + 1) * n for a, n in enumerate(stats.accept_hist))
+    assert eng.kv_len(B.PARD_TARGET) == len(PROMPT) + committed
+
+
+def test_k1_draft_is_plain_draft_decode(eng, models, B):
+    say("[gpu] tiny: K=1 draft")
+    target, draft = models
+    first = eng.prefill(PROMPT)
+    prefix = PROMPT + [first]
+    cand = eng.draft(prefix, 1)
+    cache = oracle.KVCache(draft)
+    lg = oracle.forward_cached(draft, cache, prefix, logits_rows=[len(prefix) - 1])
+    assert_logits_close(eng.read_logits(B.PARD_DRAFT, 1), lg, "K=1 draft logits")
+    assert_tokens_match(cand, lg, "K=1 candidate")
+
+
+@pytest.mark.parametrize("k", [4, 8])
+def test_forced_candidates_accept_exact_prefix(eng, models, k):
+    say(f"[gpu] tiny: forced candidates K={k}")
+    target, _ = models
+    cache = oracle.KVCache(target)
+    lg = oracle.forward_cached(target, cache, PROMPT, logits_rows=[len(PROMPT) - 1])
+    greedy, marg = [int(np.argmax(lg[0]))], [float(margins(lg[0]))]
+    for _ in range(k + 1):
+        lg = oracle.forward_cached(target, cache, [greedy[-1]])
+        greedy.append(int(np.argmax(lg[0])))
+        marg.append(float(margins(lg[0])))
+    if min(marg) <= MARGIN:
+        pytest.skip("greedy continuation has a near-tie; forced acceptance is not decidable")
+    for j in range(k + 1):
+        first = eng.prefill(PROMPT)
+        assert first == greedy[0]
+        cands = list(greedy[1:1 + k])
+        if j < k:
+            cands[j] = (cands[j] + 1) % WL.mask_id
+        a, bonus = eng.verify(cands)
+        assert a == j and bonus == greedy[1 + j], (j, a, bonus)
+
+
+def test_rewind_reproduces_draft_logits(eng, B):
+    say("[gpu] tiny: truncate and re-draft")
+    first = eng.prefill(PROMPT)
+    hist = PROMPT + [first]
+    for _ in range(3):
+        cands = eng.draft(hist, 4)
+        a, bonus = eng.verify(cands)
+        hist += cands[:a] + [bonus]
+    c1 = eng.draft(hist, 6)
+    l1 = eng.read_logits(B.PARD_DRAFT, 6)
+    eng.kv_truncate(B.PARD_DRAFT, len(hist) - 4)
+    assert eng.kv_len(B.PARD_DRAFT) == len(hist) - 4
+    c2 = eng.draft(hist, 6)
+    l2 = eng.read_logits(B.PARD_DRAFT, 6)
+    assert c1 == c2 and np.array_equal(l1, l2)
+
+
+def test_runs_are_bitwise_deterministic(eng, B):
+    say("[gpu] tiny: determinism")
+    outs = []
+    for _ in range(2):
+        eng.prefill(PROMPT)
+        toks, _ = eng.generate(WL.k, 24)
+        outs.append((toks, eng.read_logits(B.PARD_TARGET, WL.k + 1).copy()))
+    assert outs[0][0] == outs[1][0] and np.array_equal(outs[0][1], outs[1][1])
+
+
+def test_errors_leave_state_unchanged(eng, B):
+    say("[gpu] tiny: error paths")
+    with pytest.raises(B.PardError) as e:
+        eng.verify([1, 2], seq=1)                       # slot 1 never prefilled
+    assert e.value.status == B.PARD_ERR_STATE
+    eng.prefill(PROMPT)
+    lt, ld = eng.kv_len(B.PARD_TARGET), eng.kv_len(B.PARD_DRAFT)
+    for call, code in [(lambda: eng.draft(PROMPT, 17), B.PARD_ERR_ARG),
+                       (lambda: eng.verify([1] * 17), B.PARD_ERR_ARG),
+                       (lambda: eng.verify([5000]), B.PARD_ERR_ARG),
+                       (lambda: eng.kv_truncate(B.PARD_TARGET, lt + 1), B.PARD_ERR_ARG),
+                       (lambda: eng.prefill(list(range(500))), B.PARD_ERR_CAPACITY),
+                       (lambda: eng.generate(4, 600), B.PARD_ERR_CAPACITY),
+                       (lambda: eng.prefill(PROMPT, seq=2), B.PARD_ERR_CAPACITY)]:
+        with pytest.raises(B.PardError) as e:
+            call()
+        assert e.value.status == code
+        assert (eng.kv_len(B.PARD_TARGET), eng.kv_len(B.PARD_DRAFT)) == (lt, ld)
+
+
+def test_self_draft_accepts_every_step(B):
+    say("[gpu] tiny: draft == target")
+    eng = B.Engine(T_SPEC, T_SPEC, WL.mask_id, max_ctx=256, max_k=8)
+    try:
+        for k in (1, 3):
+            eng.prefill(PROMPT)
+            toks, stats = eng.generate(k, 40)
+            assert stats.accept_hist[0] == 0, list(stats.accept_hist)[:k + 1]
+            if k == 1:
+                assert stats.accept_hist[1] == stats.steps
+    finally:
+        eng.close()
+
+
+QWEN_T = pi.ModelSpec(n_layers=2, d_model=448, n_heads=7, n_kv_heads=1, head_dim=64, ffn_dim=320,
+                      vocab=512, rms_eps=1e-6, rope_theta=1e6, qkv_bias=True, tied=False,
+                      dtype="bf16", seed=5, stream=0)
+QWEN_D = pi.ModelSpec(n_layers=1, d_model=256, n_heads=2, n_kv_heads=1, head_dim=128, ffn_dim=200,
+                      vocab=512, rms_eps=1e-6, rope_theta=1e6, qkv_bias=True, tied=True,
+                      dtype="bf16", seed=5, stream=1)
+
+
+def test_qwen_shaped_bias_group7_lockstep(B):
+    say("[gpu] qwen-shaped tiny: lock-step with QKV bias, GQA group 7")
+    target, draft = oracle.build_model(QWEN_T), oracle.build_model(QWEN_D)
+    eng = B.Engine(QWEN_T, QWEN_D, 511, max_ctx=256, max_k=12)
+    try:
+        prompt = [int(x) for x in pi.gen_prompt(5, 512, 40)]
+        for k in (4, 12):
+            lockstep(eng, target, draft, prompt, k, steps=6, mask_id=511, tag=f"qwen K={k}")
+    finally:
+        eng.close()

@@ -141,9 +141,9 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta) {
 
 // x[r, :] = E[ids[r], :] (fp32) from the strip-packed embedding, plus the
 // first normalised GEMM's operand xg = bf16(x * g) and the row's sum of squares.
-__global__ __launch_bounds__(128) void k_embed(const uint16_t* E, int kb_total, int d, const FwdDesc* desc,
+__global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int kb_total, int d, const FwdDesc* desc,
                                                float* x, const float* g, uint16_t* xg, float* ss) {
-  __shared__ float wsum[2];
+  __shared__ float wsum[4];
   const int r = blockIdx.x;
   if (r >= desc->n_rows) return;
   const int id = desc->ids[r];
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(128) void k_embed(const uint16_t* E, int kb_total, 
   for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
   __syncthreads();
-  if (threadIdx.x == 0) ss[r] = wsum[0] + wsum[1];
+  if (threadIdx.x == 0) ss[r] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
 __global__ void k_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out) {
@@ -216,7 +216,7 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStre
 
 hipError_t launch_embed(const uint16_t* E, int kb_total, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, float* ss, int max_rows, hipStream_t st) {
-  k_embed<<<max_rows, 128, 0, st>>>(E, kb_total, d, desc, x, g, xg, ss);
+  k_embed<<<max_rows, 256, 0, st>>>(E, kb_total, d, desc, x, g, xg, ss);
   return hipGetLastError();
 }
 

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <string>
@@ -19,7 +20,7 @@ using namespace pard;
 
 namespace {
 
-constexpr int kTargetWorkgroups = 512;   // per GEMM launch: ~2 per CU on 256 CUs
+constexpr int kTargetWaves = 2048;       // per GEMM launch: 2 per SIMD on 256 CUs
 constexpr int kPrefillRows = kMaxRows;
 constexpr int kDescRing = 512;
 constexpr int kGatherMax = 4096;
@@ -49,15 +50,18 @@ struct Bump {
   }
 };
 
-// Tile plan of one skinny GEMM.  The input-dimension split G depends only on
-// the weight shape, so per-element summation order is the same for any row count.
+// Tile plan of one skinny GEMM: S strips per workgroup, nw wavefronts splitting
+// the input dimension.  nw depends only on the weight shape (for the row
+// counts of decode passes), so per-element summation order does not depend on
+// how many rows a pass has.
 struct GemmPlan {
-  int n_strips = 0, kb_total = 0, G = 1;
+  int n_strips = 0, kb_total = 0, nw = 4;
 };
 
 int pick_S(int epi, int n_strips, int mt) {
-  int s = 2;
-  if (epi == EPI_LOGITS) s = (mt == 1) ? 8 : (mt == 2 ? 4 : 2);
+  int s = 1;
+  if (epi == EPI_SWIGLU) s = 2;
+  if (epi == EPI_LOGITS) s = (mt == 1) ? 4 : 2;
   while (s > 1 && n_strips % s) s >>= 1;
   if (epi == EPI_SWIGLU && s < 2) s = 2;
   return s;
@@ -67,11 +71,16 @@ GemmPlan plan_gemm(int epi, int n_pad, int k_pad) {
   GemmPlan p;
   p.n_strips = n_pad / 16;
   p.kb_total = k_pad / 32;
-  const int tiles_ref = p.n_strips / pick_S(epi, p.n_strips, 1);
-  if (epi != EPI_LOGITS) {
-    while (tiles_ref * p.G < kTargetWorkgroups && p.kb_total >= 4 * (2 * p.G) * 2) p.G *= 2;
-  }
+  const int wgs = p.n_strips / pick_S(epi, p.n_strips, 1);
+  while (wgs * p.nw < kTargetWaves && p.nw < 16 && p.kb_total / (2 * p.nw) >= 4) p.nw *= 2;
   return p;
+}
+
+// Wavefronts per workgroup for a pass of mt row tiles (LDS <= 32 KiB).
+int plan_nw(const GemmPlan& p, int S, int mt) {
+  int nw = p.nw;
+  while (nw > 4 && (nw * S * mt > 32 || (mt >= 3 && nw > 8))) nw >>= 1;
+  return nw;
 }
 
 struct Layer {
@@ -83,7 +92,6 @@ struct ModelDev {
   pard_model_spec spec{};
   int d = 0, q_dim = 0, kv_dim = 0, nqkv = 0, f_pad = 0, group = 0;
   GemmPlan p_qkv, p_o, p_gu, p_d, p_lm;
-  int attn_chunk = 64, attn_chunks = 1;
   std::vector<Layer> layers;
   uint16_t *embed = nullptr, *lm_head = nullptr;
   float* g_final = nullptr;
@@ -109,13 +117,9 @@ struct pard_ctx {
   char* arena = nullptr;
   size_t arena_bytes = 0;
   // shared device workspaces
-  float* gemm_part = nullptr;
-  int* gemm_cnt = nullptr;
-  int* lm_cnt = nullptr;
   float* amax_val = nullptr;
   int* amax_idx = nullptr;
   float* attn_part = nullptr;
-  int* attn_cnt = nullptr;
   SeqState* seq_dev = nullptr;
   int* out_dev = nullptr;
   size_t* gather_idx_dev = nullptr;
@@ -128,6 +132,11 @@ struct pard_ctx {
   float* h_gather_out = nullptr;
   int* h_out = nullptr;
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+  // captured fused steps (draft pass + verify pass), replayed on `stream`
+  struct StepGraph { int seq, k, l_class; hipGraphExec_t exec; };
+  std::vector<StepGraph> graphs;
+  hipStream_t cap_stream = nullptr;     // private stream used only for capture
+  bool use_graphs = true;
   // host mirrors
   std::vector<std::vector<int>> hist;   // committed tokens + pending token
   std::vector<char> prefilled;
@@ -136,6 +145,8 @@ struct pard_ctx {
   std::vector<hipEvent_t> timer_ev;
   std::string err;
   size_t kv_seq_stride[2] = {0, 0};
+  size_t kv_elems[2] = {0, 0};
+  int kv_cap = 0;                       // KV capacity per sequence, max_ctx rounded up to 32
 };
 
 namespace {
@@ -210,27 +221,15 @@ void derive(ModelDev& M, const pard_model_spec& s, int max_ctx) {
   M.p_d = plan_gemm(EPI_RESID, M.d, M.f_pad);
   M.p_lm = plan_gemm(EPI_LOGITS, s.vocab, M.d);
   M.ss_tiles_resid = M.p_o.n_strips / pick_S(EPI_RESID, M.p_o.n_strips, 1);
-  M.attn_chunk = kAttnSub * std::max(1, ceil_div(max_ctx, kAttnSub * 64));
-  M.attn_chunks = ceil_div(max_ctx, M.attn_chunk);
-}
-
-size_t part_floats(const GemmPlan& p, int epi) {
-  size_t worst = 0;
-  for (int mt = 1; mt <= 4; ++mt) {
-    const int S = pick_S(epi, p.n_strips, mt);
-    const size_t tiles = p.n_strips / S;
-    if (p.G > 1) worst = std::max(worst, tiles * p.G * (size_t)(S * mt * 256 + mt * 16));
-  }
-  return worst;
 }
 
 // Lays out (base == nullptr: sizes) every device region of a context.
 size_t layout(pard_ctx* c, char* base) {
   Bump b;
   b.base = base;
-  size_t part = 0;
-  int max_tiles = 1, max_lm_tiles = 1, max_attn_cnt = 1;
+  int max_lm_tiles = 1;
   size_t attn_part = 1;
+  const int cap = c->kv_cap;
   for (int w = 0; w < 2; ++w) {
     ModelDev& M = c->m[w];
     const pard_model_spec& s = M.spec;
@@ -248,11 +247,12 @@ size_t layout(pard_ctx* c, char* base) {
     M.embed = b.take<uint16_t>((size_t)s.vocab * M.d);
     M.lm_head = s.tied_embeddings ? M.embed : b.take<uint16_t>((size_t)s.vocab * M.d);
     M.g_final = b.take<float>(M.d);
-    const size_t kv = (size_t)c->max_batch * s.n_layers * s.n_kv_heads * c->max_ctx * s.head_dim;
-    c->kv_seq_stride[w] = (size_t)s.n_layers * s.n_kv_heads * c->max_ctx * s.head_dim;
+    const size_t kv = (size_t)c->max_batch * s.n_layers * s.n_kv_heads * cap * s.head_dim;
+    c->kv_seq_stride[w] = (size_t)s.n_layers * s.n_kv_heads * cap * s.head_dim;
+    c->kv_elems[w] = kv;
     M.kcache = b.take<uint16_t>(kv);
     M.vcache = b.take<uint16_t>(kv);
-    M.rope = b.take<float2>((size_t)c->max_ctx * s.head_dim / 2);
+    M.rope = b.take<float2>((size_t)cap * s.head_dim / 2);
     M.x = b.take<float>((size_t)kMaxRows * M.d);
     M.xg = b.take<uint16_t>((size_t)kMaxRows * M.d);
     M.ss = b.take<float>((size_t)std::max(1, M.ss_tiles_resid) * kMaxRows);
@@ -262,21 +262,13 @@ size_t layout(pard_ctx* c, char* base) {
     M.logits = b.take<float>((size_t)kMaxLmRows * s.vocab);
     M.result = b.take<int>(kMaxLmRows);
     M.desc = b.take<FwdDesc>(1);
-    part = std::max({part, part_floats(M.p_qkv, EPI_QKV), part_floats(M.p_o, EPI_RESID),
-                     part_floats(M.p_gu, EPI_SWIGLU), part_floats(M.p_d, EPI_RESID)});
-    max_tiles = std::max({max_tiles, M.p_qkv.n_strips, M.p_o.n_strips, M.p_gu.n_strips, M.p_d.n_strips});
     max_lm_tiles = std::max(max_lm_tiles, M.p_lm.n_strips);
-    const int qblocks = ceil_div(kMaxRows * M.group, kAttnQB);
-    max_attn_cnt = std::max(max_attn_cnt, s.n_kv_heads * qblocks);
-    attn_part = std::max(attn_part, (size_t)s.n_kv_heads * qblocks * M.attn_chunks * attn_part_floats(s.head_dim));
+    attn_part = std::max(attn_part, (size_t)s.n_kv_heads * kAttnRecords *
+                                        attn_part_floats(s.head_dim, s.head_dim == 128 ? 1 : 2));
   }
-  c->gemm_part = b.take<float>(std::max<size_t>(part, 1));
-  c->gemm_cnt = b.take<int>(max_tiles);
-  c->lm_cnt = b.take<int>(64);
   c->amax_val = b.take<float>((size_t)max_lm_tiles * kMaxLmRows);
   c->amax_idx = b.take<int>((size_t)max_lm_tiles * kMaxLmRows);
   c->attn_part = b.take<float>(attn_part);
-  c->attn_cnt = b.take<int>(max_attn_cnt);
   c->seq_dev = b.take<SeqState>(c->max_batch);
   c->out_dev = b.take<int>((size_t)c->max_batch * c->max_ctx);
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
@@ -337,7 +329,10 @@ pard_status generate(pard_ctx* c, int w) {
   HIP_TRY(c, gen(M.embed, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(0), 0, 0));
   if (!s.tied_embeddings) HIP_TRY(c, gen(M.lm_head, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(1), 0, 0));
   HIP_TRY(c, launch_fill_f32(M.g_final, M.d, 1.0f, c->stream));
-  HIP_TRY(c, launch_rope_table(M.rope, c->max_ctx, s.head_dim, (double)s.rope_theta, c->stream));
+  HIP_TRY(c, launch_rope_table(M.rope, c->kv_cap, s.head_dim, (double)s.rope_theta, c->stream));
+  // zero KV caches: padded key tiles read stale slots, which must hold finite values
+  HIP_TRY(c, launch_fill_u32(reinterpret_cast<uint32_t*>(M.kcache), c->kv_elems[w] / 2, 0u, c->stream));
+  HIP_TRY(c, launch_fill_u32(reinterpret_cast<uint32_t*>(M.vcache), c->kv_elems[w] / 2, 0u, c->stream));
   return PARD_OK;
 }
 
@@ -361,12 +356,9 @@ struct Timed {
   }
 };
 
-GemmArgs gemm_base(const ModelDev& M, const GemmPlan& p, int S, const uint16_t* W) {
+GemmArgs gemm_base(const ModelDev& M, const uint16_t* W) {
   GemmArgs a{};
   a.W = W;
-  a.kb_total = p.kb_total;
-  a.G = p.G;
-  a.n_tiles = p.n_strips / S;
   a.desc = M.desc;
   a.eps = M.spec.rms_eps;
   a.inv_k = 1.0f / (float)M.d;
@@ -375,16 +367,16 @@ GemmArgs gemm_base(const ModelDev& M, const GemmPlan& p, int S, const uint16_t* 
 
 hipError_t run_gemm(pard_ctx* c, int cls, int epi, int mt, GemmArgs a, const GemmPlan& p) {
   const int S = pick_S(epi, p.n_strips, mt);
+  a.kb_total = p.kb_total;
   a.n_tiles = p.n_strips / S;
-  a.part = c->gemm_part;
-  a.counters = c->gemm_cnt;
   Timed t(c, cls);
-  return launch_gemm(epi, mt, S, a, c->stream);
+  return launch_gemm(epi, mt, S, plan_nw(p, S, mt), a, c->stream);
 }
 
 struct PassSpec {
   int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
   int max_lm_rows = 0;    // 0: no lm_head
+  int l_bound = 0;        // upper bound of pos0 + n_rows (attention split plan)
   int tail = TAIL_NONE;
   FwdDesc* next_desc = nullptr;
   bool emit = false;
@@ -400,7 +392,24 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
     HIP_TRY(c, launch_embed(M.embed, M.p_lm.kb_total, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, M.ss,
                             ps.max_rows, c->stream));
   }
-  const size_t layer_kv = (size_t)s.n_kv_heads * c->max_ctx * s.head_dim;
+  const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
+  // attention plan: query blocks of up to 48/64 (row, head) pairs; keys split
+  // over workgroups of ~kAttnSplit keys (merged by a second kernel), with at
+  // most kAttnRecords (query block, split) records per KV head
+  const int qpairs = ps.max_rows * M.group;
+  const int nqt = std::min(s.head_dim == 128 ? 1 : 2, ceil_div(qpairs, 16));
+  const int n_qblocks = ceil_div(qpairs, 16 * nqt);
+  const int l_bound = std::min(std::max(ps.l_bound, 1), c->kv_cap);
+  // one workgroup per (KV head, query block) up to 2*kAttnSplit keys; beyond,
+  // split boundaries sit at multiples of kAttnSplit whatever the pass length,
+  // so a query's result does not depend on the other rows of its pass (only
+  // very long prefill chunks, with many query blocks, use longer splits)
+  int n_splits = l_bound <= 2 * kAttnSplit ? 1 : ceil_div(l_bound, kAttnSplit);
+  int split_len = n_splits == 1 ? c->kv_cap : kAttnSplit;
+  if (n_splits * n_qblocks > kAttnRecords) {
+    n_splits = std::max(1, kAttnRecords / n_qblocks);
+    split_len = ceil_div(ceil_div(l_bound, n_splits), 32) * 32;
+  }
   uint16_t* kc_seq = M.kcache + c->kv_seq_stride[w] * seq;
   uint16_t* vc_seq = M.vcache + c->kv_seq_stride[w] * seq;
   for (int l = 0; l < s.n_layers; ++l) {
@@ -408,7 +417,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
     uint16_t* kc = kc_seq + layer_kv * l;
     uint16_t* vc = vc_seq + layer_kv * l;
     {  // norm + QKV + bias + RoPE + KV append
-      GemmArgs a = gemm_base(M, M.p_qkv, 1, L.wqkv);
+      GemmArgs a = gemm_base(M, L.wqkv);
       a.A = M.xg;
       a.lda = M.d;
       a.ss_in = M.ss;
@@ -417,7 +426,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.ld_out = M.q_dim;
       a.kc = kc;
       a.vc = vc;
-      a.cap = c->max_ctx;
+      a.cap = c->kv_cap;
       a.bias = L.bqkv;
       a.rope = M.rope;
       a.q_dim = M.q_dim;
@@ -431,23 +440,23 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.ldq = M.q_dim;
       a.kc = kc;
       a.vc = vc;
-      a.cap = c->max_ctx;
+      a.cap = c->kv_cap;
       a.out = M.attn;
       a.ldo = M.q_dim;
       a.desc = M.desc;
       a.n_heads = s.n_heads;
       a.n_kv = s.n_kv_heads;
-      a.chunk = M.attn_chunk;
-      a.n_chunks = M.attn_chunks;
-      a.n_qblocks = ceil_div(ps.max_rows * M.group, kAttnQB);
+      a.nqt = nqt;
+      a.n_qblocks = n_qblocks;
+      a.split_len = split_len;
+      a.n_splits = n_splits;
       a.scale = 1.0f / std::sqrt((float)s.head_dim);
       a.part = c->attn_part;
-      a.counters = c->attn_cnt;
       Timed t(c, cls0 + 2);
       HIP_TRY(c, launch_attention(s.head_dim, a, c->stream));
     }
     {  // O-projection + residual
-      GemmArgs a = gemm_base(M, M.p_o, 1, L.wo);
+      GemmArgs a = gemm_base(M, L.wo);
       a.A = M.attn;
       a.lda = M.q_dim;
       a.x = M.x;
@@ -458,7 +467,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, mt, a, M.p_o));
     }
     {  // norm + gate/up + SiLU * up
-      GemmArgs a = gemm_base(M, M.p_gu, 2, L.wgu);
+      GemmArgs a = gemm_base(M, L.wgu);
       a.A = M.xg;
       a.lda = M.d;
       a.ss_in = M.ss;
@@ -468,7 +477,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, mt, a, M.p_gu));
     }
     {  // down + residual
-      GemmArgs a = gemm_base(M, M.p_d, 1, L.wd);
+      GemmArgs a = gemm_base(M, L.wd);
       a.A = M.h;
       a.lda = M.f_pad;
       a.x = M.x;
@@ -480,7 +489,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
     }
   }
   if (ps.max_lm_rows > 0) {
-    GemmArgs a = gemm_base(M, M.p_lm, 1, M.lm_head);
+    GemmArgs a = gemm_base(M, M.lm_head);
     a.A = M.xg;
     a.lda = M.d;
     a.ss_in = M.ss;
@@ -490,14 +499,22 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
     a.vocab = s.vocab;
     a.amax_val = c->amax_val;
     a.amax_idx = c->amax_idx;
-    a.lm_counter = c->lm_cnt;
-    a.result = M.result;
-    a.tail = ps.tail;
-    a.seq = c->seq_dev + seq;
-    a.next_desc = ps.next_desc;
-    a.out_tokens = ps.emit ? c->out_dev + (size_t)seq * c->max_ctx : nullptr;
-    a.out_cap = c->max_ctx;
-    HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, ceil_div(ps.max_lm_rows, 16), a, M.p_lm));
+    const int mt_lm = ceil_div(ps.max_lm_rows, 16);
+    HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, mt_lm, a, M.p_lm));
+    TailArgs ta{};
+    ta.desc = M.desc;
+    ta.amax_val = c->amax_val;
+    ta.amax_idx = c->amax_idx;
+    ta.n_tiles = M.p_lm.n_strips / pick_S(EPI_LOGITS, M.p_lm.n_strips, mt_lm);
+    ta.vocab = s.vocab;
+    ta.result = M.result;
+    ta.tail = ps.tail;
+    ta.seq = c->seq_dev + seq;
+    ta.next_desc = ps.next_desc;
+    ta.out_tokens = ps.emit ? c->out_dev + (size_t)seq * c->max_ctx : nullptr;
+    ta.out_cap = c->max_ctx;
+    Timed t(c, cls0 + 7);
+    HIP_TRY(c, launch_tail(ta, c->stream));
   }
   return PARD_OK;
 }
@@ -548,6 +565,7 @@ pard_status ingest(pard_ctx* c, int w, int seq, const int* tokens, int n, int po
     if (st != PARD_OK) return st;
     PassSpec ps;
     ps.max_rows = rows;
+    ps.l_bound = pos0 + off + rows;
     st = forward(c, w, seq, ps);
     if (st != PARD_OK) return st;
   }
@@ -563,6 +581,69 @@ bool ids_ok(const int* ids, int n, int vocab) {
 pard_status check_seq(pard_ctx* c, int seq, bool need_prefill) {
   if (seq < 0 || seq >= c->max_batch) return fail(c, PARD_ERR_CAPACITY, "seq %d outside [0, max_batch=%d)", seq, c->max_batch);
   if (need_prefill && !c->prefilled[seq]) return fail(c, PARD_ERR_STATE, "sequence slot %d is not prefilled", seq);
+  return PARD_OK;
+}
+
+// Upper bound of the context length used to plan attention for a batch of
+// steps: one class up to two splits' worth, then multiples of 4 splits.
+int attn_l_class(int l) {
+  return l <= 2 * kAttnSplit ? 2 * kAttnSplit : ceil_div(l, 4 * kAttnSplit) * 4 * kAttnSplit;
+}
+
+// One fused step: draft pass (pending + K-1 masks) then verify pass, each
+// followed by its argmax tail; K = 0 runs the verify pass only.
+pard_status step_passes(pard_ctx* c, int seq, int K, int draft_rows, int l_class) {
+  pard_status st;
+  if (K > 0) {
+    PassSpec pd;
+    pd.max_rows = draft_rows;
+    pd.max_lm_rows = K;
+    pd.l_bound = l_class;
+    pd.tail = TAIL_DRAFT;
+    pd.next_desc = c->m[PARD_TARGET].desc;
+    if ((st = forward(c, PARD_DRAFT, seq, pd)) != PARD_OK) return st;
+  }
+  PassSpec pv;
+  pv.max_rows = K + 1;
+  pv.max_lm_rows = K + 1;
+  pv.l_bound = l_class;
+  pv.tail = TAIL_VERIFY;
+  pv.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
+  pv.emit = true;
+  return forward(c, PARD_TARGET, seq, pv);
+}
+
+// Replays the captured step for (seq, K, l_class), capturing it on first use.
+// A capture failure switches the context to eager launches.
+pard_status launch_step_graph(pard_ctx* c, int seq, int K, int l_class) {
+  for (const auto& g : c->graphs)
+    if (g.seq == seq && g.k == K && g.l_class == l_class) {
+      HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
+      return PARD_OK;
+    }
+  if (!c->cap_stream && hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess) {
+    c->use_graphs = false;
+    return step_passes(c, seq, K, 2 * K, l_class);
+  }
+  hipStream_t user = c->stream;
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+  bool ok = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal) == hipSuccess;
+  if (ok) {
+    c->stream = c->cap_stream;
+    const pard_status st = step_passes(c, seq, K, 2 * K, l_class);
+    c->stream = user;
+    ok = hipStreamEndCapture(c->cap_stream, &graph) == hipSuccess && st == PARD_OK && graph;
+  }
+  ok = ok && hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0) == hipSuccess;
+  if (graph) (void)hipGraphDestroy(graph);
+  (void)hipGetLastError();
+  if (!ok) {
+    c->use_graphs = false;
+    return step_passes(c, seq, K, 2 * K, l_class);
+  }
+  c->graphs.push_back({seq, K, l_class, exec});
+  HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return PARD_OK;
 }
 
@@ -596,6 +677,7 @@ size_t pard_arena_bytes(const pard_model_spec* target, const pard_model_spec* dr
   tmp.max_batch = max_batch;
   tmp.max_ctx = max_ctx;
   tmp.max_k = max_k;
+  tmp.kv_cap = ceil_div(max_ctx, 32) * 32;
   derive(tmp.m[0], *target, max_ctx);
   derive(tmp.m[1], *draft, max_ctx);
   return layout(&tmp, nullptr);
@@ -619,6 +701,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   c->max_batch = max_batch;
   c->max_ctx = max_ctx;
   c->max_k = max_k;
+  c->kv_cap = ceil_div(max_ctx, 32) * 32;
   c->stream = reinterpret_cast<hipStream_t>(hip_stream);
   c->arena = static_cast<char*>(dev_arena);
   c->arena_bytes = arena_bytes;
@@ -626,6 +709,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   derive(c->m[1], *draft, max_ctx);
   layout(c, c->arena);
   c->hist.assign(max_batch, {});
+  if (const char* e = getenv("PARD_NO_GRAPH")) c->use_graphs = e[0] == '0';
   c->prefilled.assign(max_batch, 0);
 
   auto bail = [&](pard_status s) {
@@ -644,21 +728,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
 
   for (int w = 0; w < 2; ++w)
     if (generate(c, w) != PARD_OK) return bail(PARD_ERR_DEVICE);
-  int max_tiles = 1;
-  for (int w = 0; w < 2; ++w) {
-    const ModelDev& M = c->m[w];
-    max_tiles = std::max({max_tiles, M.p_qkv.n_strips, M.p_o.n_strips, M.p_gu.n_strips, M.p_d.n_strips});
-  }
-  if (launch_fill_u32(reinterpret_cast<uint32_t*>(c->gemm_cnt), max_tiles, 0, c->stream) != hipSuccess ||
-      launch_fill_u32(reinterpret_cast<uint32_t*>(c->lm_cnt), 64, 0, c->stream) != hipSuccess)
-    return bail(PARD_ERR_DEVICE);
-  size_t attn_cnt = 1;
-  for (int w = 0; w < 2; ++w) {
-    const ModelDev& M = c->m[w];
-    attn_cnt = std::max(attn_cnt, (size_t)M.spec.n_kv_heads * ceil_div(kMaxRows * M.group, kAttnQB));
-  }
-  if (launch_fill_u32(reinterpret_cast<uint32_t*>(c->attn_cnt), attn_cnt, 0, c->stream) != hipSuccess ||
-      hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
+  if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   *out = c;
@@ -676,6 +746,8 @@ void pard_free(pard_ctx* c) {
   if (c->ev_start) (void)hipEventDestroy(c->ev_start);
   if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
   for (hipEvent_t e : c->timer_ev) (void)hipEventDestroy(e);
+  for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
   delete c;
 }
 
@@ -703,6 +775,7 @@ pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_
       if (st != PARD_OK) return st;
       PassSpec ps;
       ps.max_rows = rows;
+      ps.l_bound = off + rows;
       if (last) {
         ps.max_lm_rows = 1;
         ps.tail = TAIL_PREFILL;
@@ -747,6 +820,7 @@ pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t 
   if ((st = stage_desc(c, PARD_DRAFT, d)) != PARD_OK) { S = saved; return st; }
   PassSpec ps;
   ps.max_rows = d.n_rows;
+  ps.l_bound = Ld + d.n_rows;
   ps.max_lm_rows = K;
   ps.tail = TAIL_DRAFT;
   ps.next_desc = c->m[PARD_TARGET].desc;
@@ -784,6 +858,7 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
   }
   PassSpec ps;
   ps.max_rows = K + 1;
+  ps.l_bound = Lt + K + 1;
   ps.max_lm_rows = K + 1;
   ps.tail = TAIL_VERIFY;
   ps.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
@@ -886,22 +961,15 @@ pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32
   while (produced < n_tokens && (max_steps <= 0 || steps < max_steps)) {
     int batch = ceil_div(n_tokens - produced, K + 1);
     if (max_steps > 0) batch = std::min(batch, max_steps - steps);
+    // L_t grows by at most K+1 per step: one attention plan covers the batch
+    const int l_class = attn_l_class(S.L[0] + batch * (K + 1) + K + 1);
     for (int i = 0; i < batch; ++i) {
-      if (K > 0) {
-        PassSpec pd;
-        pd.max_rows = first ? std::max(first_rows, 2 * K) : 2 * K;
-        pd.max_lm_rows = K;
-        pd.tail = TAIL_DRAFT;
-        pd.next_desc = c->m[PARD_TARGET].desc;
-        if ((st = forward(c, PARD_DRAFT, seq, pd)) != PARD_OK) return st;
+      if (first || !c->use_graphs || c->timer_class >= 0) {
+        if ((st = step_passes(c, seq, K, first ? std::max(first_rows, 2 * K) : 2 * K, l_class)) != PARD_OK)
+          return st;
+      } else {
+        if ((st = launch_step_graph(c, seq, K, l_class)) != PARD_OK) return st;
       }
-      PassSpec pv;
-      pv.max_rows = K + 1;
-      pv.max_lm_rows = K + 1;
-      pv.tail = TAIL_VERIFY;
-      pv.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
-      pv.emit = true;
-      if ((st = forward(c, PARD_TARGET, seq, pv)) != PARD_OK) return st;
       first = false;
     }
     HIP_TRY(c, hipEventRecord(c->ev_stop, c->stream));

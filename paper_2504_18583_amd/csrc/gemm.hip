@@ -4,30 +4,30 @@
 //
 // Decode streams every weight once per forward (Sec. 2.1: decoding is bound by
 // reloading the weights), so the kernel is organised around the weight
-// stream: a workgroup owns S strips (16 output columns each) and a slice of the
-// input dimension; its four wavefronts split that slice again, each one
-// streaming its strips' 1 KiB blocks (one 16-byte load per lane, directly in
-// the v_mfma_f32_16x16x32_bf16 B-operand layout) and accumulating MT 16x16
-// fp32 tiles.  Activation rows (<= 16*MT) are the A operand.
+// stream.  A workgroup owns S strips (16 output columns each) over the whole
+// input dimension; its NW wavefronts split the input dimension, each one
+// streaming its slice of the strips' 1 KiB blocks (one 16-byte load per lane,
+// directly in the v_mfma_f32_16x16x32_bf16 B-operand layout) through a
+// double-buffered register pipeline and accumulating MT 16x16 fp32 tiles.
+// Activation rows (<= 16*MT) are the A operand.
 //
-// Reductions are deterministic: wavefront partials are summed in LDS in wave
-// order; when the input dimension is also split across workgroups (G > 1) each
-// workgroup writes its partial tile, and the workgroup that finishes last for a
-// tile (device-scope counter, self-resetting) sums the G partials in split
-// order and runs the epilogue.  The split only depends on the weight shape, so
-// a row's result does not depend on how many other rows are in the pass.
+// The wavefront partials are summed in LDS in wave order, so results are
+// deterministic; the split depends only on the weight shape, so a row's result
+// does not depend on how many other rows are in the pass.  No workgroup ever
+// waits for another one.
 //
 // Epilogues fuse the surrounding element-wise work of a Llama block:
-//   EPI_QKV     RMSNorm row scale (the gain is applied to A, the 1/rms factor
-//               after the sum), bias, rotate-half RoPE on Q/K, Q to a bf16
-//               buffer, K/V appended to the bf16 cache at their positions.
-//   EPI_RESID   x += Y (O-projection and down-projection).
+//   EPI_QKV     RMSNorm row scale (A holds x*g in bf16, written by the
+//               producer; 1/rms comes from the producer's per-tile sums of
+//               squares), bias, rotate-half RoPE on Q/K, Q to a bf16 buffer,
+//               K (row-major) and V (key-blocked, transposed) to the cache.
+//   EPI_RESID   x += Y (O-projection, down-projection), plus bf16(x * g_next)
+//               and per-tile row sums of squares for the next normalised GEMM.
 //   EPI_SWIGLU  RMSNorm row scale, h = silu(gate) * up, bf16.
-//   EPI_LOGITS  final RMSNorm scale, fp32 logits, per-tile (max, argmax), then
-//               the last tile of the launch reduces the tiles per row (lowest
-//               id on ties) and runs the step tail: candidates for a draft
-//               pass, greedy prefix acceptance + KV rollback + next-pass
-//               staging for a verify pass.
+//   EPI_LOGITS  final RMSNorm scale, fp32 logits and per-tile (max, argmax).
+// k_lm_tail then reduces the tiles per row (lowest id on ties) and runs the
+// step tail: candidates for a draft pass; greedy prefix acceptance, KV
+// rollback and next-pass staging for a verify pass.
 #include "pard_internal.h"
 
 #include <climits>
@@ -48,8 +48,266 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
+// Slot of key (pos % 32) inside its 32-key block of the transposed V cache:
+// attention's P^T fragment holds keys {4g..4g+3, 16+4g..16+4g+3} in lane
+// group g, so those eight keys are stored contiguously at 8g..8g+7.
+__device__ __forceinline__ int v_slot(int k) {
+  return (k & 16) ? ((k & 12) << 1) + 4 + (k & 3) : ((k & 12) << 1) + (k & 3);
+}
+
+template <int MT, int S, int EPI>
+__global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p) {
+  constexpr int NE = S * MT * 256;   // elements of one workgroup tile
+  constexpr int NJ = S * MT;         // elements per thread in the epilogue (first 256 threads)
+  constexpr int U = (4 / S) > 0 ? 4 / S : 1;   // k-blocks per pipeline stage (4 KiB of W per wave)
+  extern __shared__ float red[];     // [NW][NE]
+  __shared__ float rs_s[MT * 16];
+
+  const int tile = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int nw = blockDim.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wavefront
+  const FwdDesc d = *p.desc;
+  const int row_begin = p.lm_mode ? d.lm_row0 : 0;
+  const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
+
+  // wave w streams k-blocks w, w + nw, w + 2*nw, ...: at any time the
+  // workgroup reads nw consecutive 1 KiB blocks of each strip
+  const int n_it = (p.kb_total - wave + nw - 1) / nw;
+
+  f32x4 acc[S][MT];
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) acc[s][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const u32x4* Wt = reinterpret_cast<const u32x4*>(p.W) + (size_t)tile * S * p.kb_total * 64 + lane;
+  // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at 8*(lane/16)
+  const u32x4* Ar[MT];
+  bool a_ok[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    const int r = mt * 16 + (lane & 15);
+    a_ok[mt] = r < row_count;
+    const int row = min(row_begin + r, kMaxRows - 1);
+    Ar[mt] = reinterpret_cast<const u32x4*>(p.A + (size_t)row * p.lda + (lane >> 4) * 8);
+  }
+
+  // Two register stages of U k-blocks each: loads of stage i+1 are in flight
+  // while stage i feeds the MFMAs.  Iterations past the wave's range are
+  // clamped (cache hits) and their A fragment is zeroed.
+  u32x4 w0[U][S], a0[U][MT], w1[U][S], a1[U][MT];
+  auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int its) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = wave + min(its + u, n_it - 1) * nw;
+#pragma unroll
+      for (int s = 0; s < S; ++s) w[u][s] = __builtin_nontemporal_load(Wt + ((size_t)s * p.kb_total + kb) * 64);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) a[u][mt] = Ar[mt][kb * 4];
+    }
+  };
+  auto compute = [&](const u32x4 (&w)[U][S], const u32x4 (&a)[U][MT], int its) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool live = its + u < n_it;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const u32x4 av = (live && a_ok[mt]) ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int s = 0; s < S; ++s)
+          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
+                                                               __builtin_bit_cast(bf16x8, w[u][s]),
+                                                               acc[s][mt], 0, 0, 0);
+      }
+    }
+  };
+  // 1/rms per row from the producer's per-tile sums of squares: 16 threads per
+  // row, 16 independent loads each in flight together, fixed summation order
+  auto row_scales = [&]() {
+    if (tid < 256) {
+      for (int r = tid >> 4; r < MT * 16; r += 16) {
+        const int row = min(row_begin + r, kMaxRows - 1);
+        float t = 0.f;
+        for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 256) {
+          float part[16];
+#pragma unroll
+          for (int u = 0; u < 16; ++u) {
+            const int q = q0 + 16 * u;
+            part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxRows + row] : 0.f;
+          }
+#pragma unroll
+          for (int u = 0; u < 16; ++u) t += part[u];
+        }
+        t += __shfl_xor(t, 8);
+        t += __shfl_xor(t, 4);
+        t += __shfl_xor(t, 2);
+        t += __shfl_xor(t, 1);
+        if ((tid & 15) == 0) rs_s[r] = 1.0f / sqrtf(t * p.inv_k + p.eps);
+      }
+    }
+  };
+
+  // sched_barrier keeps the compiler from sinking the prefetch next to its use
+  if (n_it > 0) {
+    int its = 0;
+    load(w0, a0, its);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (EPI != EPI_RESID) row_scales();   // overlaps the first weight loads
+    while (true) {
+      load(w1, a1, its + U);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(w0, a0, its);
+      __builtin_amdgcn_sched_barrier(0);
+      its += U;
+      if (its >= n_it) break;
+      load(w0, a0, its + U);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(w1, a1, its);
+      __builtin_amdgcn_sched_barrier(0);
+      its += U;
+      if (its >= n_it) break;
+    }
+  } else if constexpr (EPI != EPI_RESID) {
+    row_scales();
+  }
+
+  // ---- workgroup reduction over the NW input-dimension slices (wave order) ----
+#pragma unroll
+  for (int s = 0; s < S; ++s)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave * NE + ((s * MT + mt) * 4 + i) * 64 + lane] = acc[s][mt][i];
+
+  __syncthreads();
+
+  // the first four wavefronts run the epilogue; all waves stay until the end
+  // so that every barrier below is reached by the whole workgroup
+  const bool epi = tid < 256;
+  float v[NJ];
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const int e = j * 256 + (tid & 255);
+    float t = red[e];
+    for (int w = 1; w < nw; ++w) t += red[w * NE + e];
+    v[j] = t;
+  }
+
+  // thread tid (< 256) holds, for j = s*MT + mt, element (row, col) below
+  const int ew = tid >> 6;
+  const int rsub = (lane >> 4) * 4 + ew;
+  const int csub = lane & 15;
+
+  if constexpr (EPI == EPI_QKV) {
+    if (!epi) return;   // no barrier follows in this epilogue
+    const int pos0 = d.pos0;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int s = j / MT, mt = j % MT;
+      const int row = mt * 16 + rsub;
+      const int n = (tile * S + s) * 16 + csub;
+      float y = v[j] * rs_s[row];
+      if (p.bias) y += p.bias[n];
+      const float partner = __shfl_xor(y, 1);
+      if (row < row_count) {
+        const int pos = pos0 + row;
+        if (n < p.q_dim + p.kv_dim) {
+          const int pp = n % p.hd;
+          const float2 cs = p.rope[(size_t)pos * (p.hd / 2) + (pp >> 1)];
+          y = (pp & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
+        }
+        const uint16_t b = (uint16_t)f2bf_bits(y);
+        if (n < p.q_dim) {
+          p.out[(size_t)row * p.ld_out + n] = b;
+        } else if (n < p.q_dim + p.kv_dim) {
+          const int c = n - p.q_dim;
+          p.kc[((size_t)(c / p.hd) * p.cap + pos) * p.hd + (c % p.hd)] = b;
+        } else {
+          const int c = n - p.q_dim - p.kv_dim;
+          const size_t blk = (size_t)(c / p.hd) * (p.cap / 32) + (pos >> 5);
+          p.vc[(blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31)] = b;
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    if (!epi) return;   // no barrier follows in this epilogue
+    float sq[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int s = j / MT, mt = j % MT;
+      const int row = mt * 16 + rsub;
+      const int n = (tile * S + s) * 16 + csub;
+      if (row < row_count) {
+        const size_t o = (size_t)(row_begin + row) * p.ldx + n;
+        const float xn = p.x[o] + v[j];
+        p.x[o] = xn;
+        p.xg[o] = (uint16_t)f2bf_bits(xn * p.g_next[n]);
+        sq[mt] += xn * xn;
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+      float t = sq[mt];
+      t += __shfl_xor(t, 1);
+      t += __shfl_xor(t, 2);
+      t += __shfl_xor(t, 4);
+      t += __shfl_xor(t, 8);
+      if (csub == 0) p.ss_out[(size_t)tile * kMaxRows + mt * 16 + rsub] = t;
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+    if (!epi) return;   // no barrier follows in this epilogue
+#pragma unroll
+    for (int q = 0; q < S / 2; ++q)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const int row = mt * 16 + rsub;
+        const float gt = v[(2 * q) * MT + mt] * rs_s[row];
+        const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
+        const float h = gt / (1.0f + expf(-gt)) * up;
+        const int f = (tile * (S / 2) + q) * 16 + csub;
+        if (row < row_count) p.out[(size_t)row * p.ld_out + f] = (uint16_t)f2bf_bits(h);
+      }
+  } else {  // EPI_LOGITS
+    constexpr int TW = S * 16;
+    __syncthreads();   // everyone is done reading red; it becomes the [row][col] tile
+    if (epi) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j) {
+        const int s = j / MT, mt = j % MT;
+        const int row = mt * 16 + rsub;
+        const int c = s * 16 + csub;
+        const float val = v[j] * rs_s[row];
+        red[row * TW + c] = val;
+        if (row < row_count) p.logits[(size_t)row * p.vocab + tile * TW + c] = val;
+      }
+    }
+    __syncthreads();
+    if (!epi) return;
+    for (int r = ew; r < row_count; r += 4) {
+      float bv = -INFINITY;
+      int bi = INT_MAX;
+      for (int c = lane; c < TW; c += 64) {
+        const float x = red[r * TW + c];
+        if (better(x, c, bv, bi)) { bv = x; bi = c; }
+      }
+      for (int off = 32; off > 0; off >>= 1) {
+        const float ov = __shfl_xor(bv, off);
+        const int oi = __shfl_xor(bi, off);
+        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+      }
+      if (lane == 0) {
+        p.amax_val[(size_t)r * p.n_tiles + tile] = bv;
+        p.amax_idx[(size_t)r * p.n_tiles + tile] = (bi == INT_MAX) ? INT_MAX : tile * TW + bi;
+      }
+    }
+  }
+}
+
 // Step tail, run by one thread once every argmax of the pass is known.
-__device__ void run_tail(const GemmArgs& p, const FwdDesc& d, const int* res) {
+__device__ void run_tail(const TailArgs& p, const FwdDesc& d, const int* res) {
   SeqState* s = p.seq;
   if (p.tail == TAIL_PREFILL) {
     s->bonus = res[0];
@@ -109,312 +367,89 @@ __device__ void run_tail(const GemmArgs& p, const FwdDesc& d, const int* res) {
   }
 }
 
-template <int MT, int S, int EPI>
-__global__ __launch_bounds__(kBlock) void k_gemm(const GemmArgs p) {
-  constexpr bool kNorm = (EPI != EPI_RESID);   // A is a normalised residual
-  constexpr int NE = S * MT * 256;   // elements of one workgroup tile
-  constexpr int NJ = S * MT;         // elements per thread
-  constexpr int U = (8 / S) > 0 ? 8 / S : 1;   // k-blocks per pipeline stage (8 KiB of W per wave)
-  __shared__ float red[4 * NE];
-  __shared__ float rs_s[MT * 16];
+// One workgroup of 1024 threads: wave w reduces lm rows w, w+16, ... over
+// tiles, 16 independent loads per lane in flight at a time.
+__global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
   __shared__ int res_s[kMaxLmRows];
-  __shared__ int last_s;
-
-  const int tile = blockIdx.x, g = blockIdx.y;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wavefront
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const FwdDesc d = *p.desc;
-  const int row_begin = p.lm_mode ? d.lm_row0 : 0;
-  const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
-
-  const int nparts = p.G * 4, part = g * 4 + wave;
-  const int kb0 = (p.kb_total * part) / nparts;
-  const int kb1 = (p.kb_total * (part + 1)) / nparts;
-
-  f32x4 acc[S][MT];
+  const int rows = d.lm_rows;
+  for (int r = wave; r < rows; r += 16) {
+    float bv = -INFINITY;
+    int bi = INT_MAX;
+    const float* vals = p.amax_val + (size_t)r * p.n_tiles;
+    const int* idxs = p.amax_idx + (size_t)r * p.n_tiles;
+    for (int t0 = lane; t0 < p.n_tiles; t0 += 64 * 16) {
+      float xv[16];
+      int xi[16];
 #pragma unroll
-  for (int s = 0; s < S; ++s)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) acc[s][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  const u32x4* Wt = reinterpret_cast<const u32x4*>(p.W) + (size_t)tile * S * p.kb_total * 64 + lane;
-  // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at 8*(lane/16)
-  const u32x4* Ar[MT];
-  bool a_ok[MT];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt) {
-    const int r = mt * 16 + (lane & 15);
-    a_ok[mt] = r < row_count;
-    const int row = min(row_begin + r, kMaxRows - 1);
-    Ar[mt] = reinterpret_cast<const u32x4*>(p.A + (size_t)row * p.lda + (lane >> 4) * 8);
-  }
-
-  // Two register stages of U k-blocks each: loads of stage i+1 are in flight
-  // while stage i feeds the MFMAs.  Indices past the wave's range are clamped
-  // (cache hits) and their A fragment is zeroed.
-  u32x4 w0[U][S], a0[U][MT], w1[U][S], a1[U][MT];
-  auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int kbs) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kb = min(kbs + u, kb1 - 1);
-#pragma unroll
-      for (int s = 0; s < S; ++s) w[u][s] = __builtin_nontemporal_load(Wt + ((size_t)s * p.kb_total + kb) * 64);
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) a[u][mt] = Ar[mt][kb * 4];
-    }
-  };
-  auto compute = [&](const u32x4 (&w)[U][S], const u32x4 (&a)[U][MT], int kbs) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const bool live = kbs + u < kb1;
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const u32x4 av = (live && a_ok[mt]) ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-        for (int s = 0; s < S; ++s)
-          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
-                                                               __builtin_bit_cast(bf16x8, w[u][s]),
-                                                               acc[s][mt], 0, 0, 0);
+      for (int u = 0; u < 16; ++u) {
+        const int t = t0 + 64 * u;
+        xv[u] = t < p.n_tiles ? vals[t] : -INFINITY;
+        xi[u] = t < p.n_tiles ? idxs[t] : INT_MAX;
       }
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (better(xv[u], xi[u], bv, bi)) { bv = xv[u]; bi = xi[u]; }
     }
-  };
-  // sched_barrier keeps the compiler from sinking the prefetch next to its use
-  if (kb0 < kb1) {
-    int kbs = kb0;
-    load(w0, a0, kbs);
-    while (true) {
-      load(w1, a1, kbs + U);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(w0, a0, kbs);
-      __builtin_amdgcn_sched_barrier(0);
-      kbs += U;
-      if (kbs >= kb1) break;
-      load(w0, a0, kbs + U);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(w1, a1, kbs);
-      __builtin_amdgcn_sched_barrier(0);
-      kbs += U;
-      if (kbs >= kb1) break;
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ov = __shfl_xor(bv, off);
+      const int oi = __shfl_xor(bi, off);
+      if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
     }
+    if (lane == 0) res_s[r] = (bi >= 0 && bi < p.vocab) ? bi : 0;
   }
-
-  // ---- workgroup reduction (wave order) ----
-#pragma unroll
-  for (int s = 0; s < S; ++s)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) red[wave * NE + ((s * MT + mt) * 4 + i) * 64 + lane] = acc[s][mt][i];
   __syncthreads();
-
-  float v[NJ];
-#pragma unroll
-  for (int j = 0; j < NJ; ++j) {
-    const int e = j * 256 + tid;
-    v[j] = ((red[e] + red[NE + e]) + red[2 * NE + e]) + red[3 * NE + e];
-  }
-
-  // ---- split fixup across workgroups ----
-  if (p.G > 1) {
-    float* mine = p.part + ((size_t)tile * p.G + g) * NE;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) mine[j * 256 + tid] = v[j];
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) last_s = (atomicAdd(&p.counters[tile], 1) == p.G - 1);
-    __syncthreads();
-    if (!last_s) return;
-    __threadfence();
-    const float* all = p.part + (size_t)tile * p.G * NE;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      float t = all[j * 256 + tid];
-      for (int gg = 1; gg < p.G; ++gg) t += all[(size_t)gg * NE + j * 256 + tid];
-      v[j] = t;
-    }
-    if (tid == 0) p.counters[tile] = 0;
-  }
-
-  // ---- 1/rms per row from the producer's per-tile sums of squares ----
-  if constexpr (kNorm) {
-    for (int r = tid >> 4; r < MT * 16; r += 16) {
-      const int row = min(row_begin + r, kMaxRows - 1);
-      float t = 0.f;
-      for (int q = tid & 15; q < p.ss_tiles; q += 16) t += p.ss_in[(size_t)q * kMaxRows + row];
-      t += __shfl_xor(t, 8);
-      t += __shfl_xor(t, 4);
-      t += __shfl_xor(t, 2);
-      t += __shfl_xor(t, 1);
-      if ((tid & 15) == 0) rs_s[r] = 1.0f / sqrtf(t * p.inv_k + p.eps);
-    }
-    __syncthreads();
-  }
-
-  // thread tid holds, for j = s*MT + mt, element (row, col) below
-  const int rsub = (lane >> 4) * 4 + wave;
-  const int csub = lane & 15;
-
-  if constexpr (EPI == EPI_QKV) {
-    const int pos0 = d.pos0;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int s = j / MT, mt = j % MT;
-      const int row = mt * 16 + rsub;
-      const int n = (tile * S + s) * 16 + csub;
-      float y = v[j] * rs_s[row];
-      if (p.bias) y += p.bias[n];
-      const float partner = __shfl_xor(y, 1);
-      if (row < row_count) {
-        const int pos = pos0 + row;
-        if (n < p.q_dim + p.kv_dim) {
-          const int pp = n % p.hd;
-          const float2 cs = p.rope[(size_t)pos * (p.hd / 2) + (pp >> 1)];
-          y = (pp & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
-        }
-        const uint16_t b = (uint16_t)f2bf_bits(y);
-        if (n < p.q_dim) {
-          p.out[(size_t)row * p.ld_out + n] = b;
-        } else if (n < p.q_dim + p.kv_dim) {
-          const int c = n - p.q_dim;
-          p.kc[((size_t)(c / p.hd) * p.cap + pos) * p.hd + (c % p.hd)] = b;
-        } else {
-          const int c = n - p.q_dim - p.kv_dim;
-          p.vc[((size_t)(c / p.hd) * p.cap + pos) * p.hd + (c % p.hd)] = b;
-        }
-      }
-    }
-  } else if constexpr (EPI == EPI_RESID) {
-    // x += Y; xg = bf16(x * g_next); per-row sum of squares over this tile
-    float sq[MT];
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) sq[mt] = 0.f;
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int s = j / MT, mt = j % MT;
-      const int row = mt * 16 + rsub;
-      const int n = (tile * S + s) * 16 + csub;
-      if (row < row_count) {
-        const size_t o = (size_t)(row_begin + row) * p.ldx + n;
-        const float xn = p.x[o] + v[j];
-        p.x[o] = xn;
-        p.xg[o] = (uint16_t)f2bf_bits(xn * p.g_next[n]);
-        sq[mt] += xn * xn;
-      }
-    }
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-      float t = sq[mt];
-      t += __shfl_xor(t, 1);
-      t += __shfl_xor(t, 2);
-      t += __shfl_xor(t, 4);
-      t += __shfl_xor(t, 8);
-      if (csub == 0) p.ss_out[(size_t)tile * kMaxRows + mt * 16 + rsub] = t;
-    }
-  } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int q = 0; q < S / 2; ++q)
-#pragma unroll
-      for (int mt = 0; mt < MT; ++mt) {
-        const int row = mt * 16 + rsub;
-        const float gt = v[(2 * q) * MT + mt] * rs_s[row];
-        const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
-        const float h = gt / (1.0f + expf(-gt)) * up;
-        const int f = (tile * (S / 2) + q) * 16 + csub;
-        if (row < row_count) p.out[(size_t)row * p.ld_out + f] = (uint16_t)f2bf_bits(h);
-      }
-  } else {  // EPI_LOGITS
-    constexpr int TW = S * 16;
-    __syncthreads();   // red is reused as the [row][col] tile
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const int s = j / MT, mt = j % MT;
-      const int row = mt * 16 + rsub;
-      const int c = s * 16 + csub;
-      const float val = v[j] * rs_s[row];
-      red[row * TW + c] = val;
-      if (row < row_count) p.logits[(size_t)row * p.vocab + tile * TW + c] = val;
-    }
-    __syncthreads();
-    for (int r = wave; r < row_count; r += 4) {
-      float bv = -INFINITY;
-      int bi = INT_MAX;
-      for (int c = lane; c < TW; c += 64) {
-        const float x = red[r * TW + c];
-        if (better(x, c, bv, bi)) { bv = x; bi = c; }
-      }
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bv, off);
-        const int oi = __shfl_xor(bi, off);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-      }
-      if (lane == 0) {
-        p.amax_val[(size_t)tile * kMaxLmRows + r] = bv;
-        p.amax_idx[(size_t)tile * kMaxLmRows + r] = (bi == INT_MAX) ? INT_MAX : tile * TW + bi;
-      }
-    }
-    __threadfence();
-    __syncthreads();
-    if (tid == 0) last_s = (atomicAdd(p.lm_counter, 1) == p.n_tiles - 1);
-    __syncthreads();
-    if (!last_s) return;
-    __threadfence();
-    for (int r = wave; r < row_count; r += 4) {
-      float bv = -INFINITY;
-      int bi = INT_MAX;
-      for (int t = lane; t < p.n_tiles; t += 64) {
-        const float x = p.amax_val[(size_t)t * kMaxLmRows + r];
-        const int xi = p.amax_idx[(size_t)t * kMaxLmRows + r];
-        if (better(x, xi, bv, bi)) { bv = x; bi = xi; }
-      }
-      for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(bv, off);
-        const int oi = __shfl_xor(bi, off);
-        if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
-      }
-      if (lane == 0) res_s[r] = (bi >= 0 && bi < p.vocab) ? bi : 0;
-    }
-    __syncthreads();
-    if (tid == 0) {
-      *p.lm_counter = 0;
-      for (int r = 0; r < row_count; ++r) p.result[r] = res_s[r];
-      run_tail(p, d, res_s);
-    }
+  if (tid == 0) {
+    for (int r = 0; r < rows; ++r) p.result[r] = res_s[r];
+    run_tail(p, d, res_s);
   }
 }
 
+template <int EPI, int MT, int S>
+hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st) {
+  const size_t lds = (size_t)nw * S * MT * 256 * sizeof(float);
+  k_gemm<MT, S, EPI><<<dim3(a.n_tiles), dim3(64 * nw), lds, st>>>(a);
+  return hipGetLastError();
+}
+
 template <int EPI, int MT>
-hipError_t launch_s(int S, const GemmArgs& a, hipStream_t st) {
-  const dim3 grid(a.n_tiles, a.G), block(kBlock);
+hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st) {
   switch (S) {
-    case 1: if constexpr (EPI != EPI_SWIGLU) { k_gemm<MT, 1, EPI><<<grid, block, 0, st>>>(a); return hipGetLastError(); } break;
-    case 2: k_gemm<MT, 2, EPI><<<grid, block, 0, st>>>(a); return hipGetLastError();
-    case 4: if constexpr (MT <= 2) { k_gemm<MT, 4, EPI><<<grid, block, 0, st>>>(a); return hipGetLastError(); } break;
-    case 8: if constexpr (MT == 1 && (EPI == EPI_LOGITS || EPI == EPI_SWIGLU)) { k_gemm<MT, 8, EPI><<<grid, block, 0, st>>>(a); return hipGetLastError(); } break;
+    case 1: if constexpr (EPI != EPI_SWIGLU) return launch_one<EPI, MT, 1>(nw, a, st); break;
+    case 2: return launch_one<EPI, MT, 2>(nw, a, st);
+    case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st); break;
   }
   return hipErrorInvalidValue;
 }
 
 template <int EPI>
-hipError_t launch_mt(int mt, int S, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
   switch (mt) {
-    case 1: return launch_s<EPI, 1>(S, a, st);
-    case 2: return launch_s<EPI, 2>(S, a, st);
-    case 3: return launch_s<EPI, 3>(S, a, st);
-    case 4: return launch_s<EPI, 4>(S, a, st);
+    case 1: return launch_s<EPI, 1>(S, nw, a, st);
+    case 2: return launch_s<EPI, 2>(S, nw, a, st);
+    case 3: return launch_s<EPI, 3>(S, nw, a, st);
+    case 4: return launch_s<EPI, 4>(S, nw, a, st);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int epi, int mt, int S, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
+  if (nw < 4 || nw > (mt >= 3 ? 8 : 16) || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, a, st);
-    case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, a, st);
-    case EPI_SWIGLU: return launch_mt<EPI_SWIGLU>(mt, S, a, st);
-    case EPI_LOGITS: return launch_mt<EPI_LOGITS>(mt, S, a, st);
+    case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, nw, a, st);
+    case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, nw, a, st);
+    case EPI_SWIGLU: return launch_mt<EPI_SWIGLU>(mt, S, nw, a, st);
+    case EPI_LOGITS: return launch_mt<EPI_LOGITS>(mt, S, nw, a, st);
   }
   return hipErrorInvalidValue;
+}
+
+hipError_t launch_tail(const TailArgs& a, hipStream_t st) {
+  k_lm_tail<<<1, 1024, 0, st>>>(a);
+  return hipGetLastError();
 }
 
 }  // namespace pard

@@ -23,6 +23,9 @@ constexpr int kMaxK = 32;
 constexpr int kMaxRows = 64;      // rows of one forward pass (prefill chunk, 2*max_k)
 constexpr int kMaxLmRows = kMaxK + 1;
 constexpr int kBlock = 256;
+constexpr int kAttnWaves = 8;      // wavefronts per attention workgroup
+constexpr int kAttnSplit = 1024;   // keys per workgroup once a context is split (> 2 splits' worth)
+constexpr int kAttnRecords = 512;  // max (query block, key split) partial records per KV head
 
 // Rows of the next forward pass of one model.  Written by the host (granular
 // calls) or by the tail of the previous pass (fused loop).
@@ -57,14 +60,11 @@ enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3 };
 struct GemmArgs {
   const uint16_t* W;      // strip-packed bf16 weight
   int kb_total;           // padded input dim / 32
-  int G;                  // input-dim splits across workgroups
-  int n_tiles;            // output tiles (S strips each)
+  int n_tiles;            // output tiles (S strips each) = grid size
   const uint16_t* A;      // bf16 activations [kMaxRows][lda]
   int lda;
   const FwdDesc* desc;
   int lm_mode;            // 0: rows [0, n_rows)   1: rows [lm_row0, lm_row0 + lm_rows)
-  float* part;            // split partials [tile][G][S*MT*256]
-  int* counters;          // per tile, self-resetting
   // RMSNorm of the A operand (QKV, SWIGLU, LOGITS): A already holds x*g in
   // bf16; 1/rms comes from the producer's per-tile sums of squares.
   const float* ss_in; int ss_tiles;
@@ -78,9 +78,16 @@ struct GemmArgs {
   uint16_t* kc; uint16_t* vc; int cap;
   const float* bias; const float2* rope;
   int q_dim, kv_dim, hd;
-  // EPI_LOGITS
+  // EPI_LOGITS: fp32 logits and the per-tile (max, argmax) of every lm row
   float* logits; int vocab;
-  float* amax_val; int* amax_idx; int* lm_counter;
+  float* amax_val; int* amax_idx;
+};
+
+// Second argmax pass over the lm_head tiles and the step tail (one workgroup).
+struct TailArgs {
+  const FwdDesc* desc;
+  const float* amax_val; const int* amax_idx;
+  int n_tiles, vocab;
   int* result;            // argmax per lm row
   int tail;
   SeqState* seq;
@@ -90,21 +97,22 @@ struct GemmArgs {
 };
 
 struct AttnArgs {
-  const uint16_t* q; int ldq;
-  const uint16_t* kc; const uint16_t* vc; int cap;
-  uint16_t* out; int ldo;
+  const uint16_t* q; int ldq;                 // [rows][H_q*hd] bf16, pair-interleaved dims
+  const uint16_t* kc; const uint16_t* vc;     // this layer's cache of one sequence
+  int cap;                                    // KV capacity (multiple of 32)
+  uint16_t* out; int ldo;                     // [rows][H_q*hd] bf16
   const FwdDesc* desc;
-  int n_heads, n_kv, chunk, n_chunks, n_qblocks;
+  int n_heads, n_kv;
+  int nqt, n_qblocks;                         // 16*nqt query pairs per block
+  int split_len, n_splits;                    // keys per split (multiple of 32)
   float scale;
-  float* part; int* counters;
+  float* part;                                // split partials when n_splits > 1
 };
 
-constexpr int kAttnQB = 16;   // query (row, head) pairs per workgroup
-constexpr int kAttnSub = 64;  // keys per LDS sub-chunk
-
 // Launchers (return hipSuccess or the launch error).
-hipError_t launch_gemm(int epi, int mt, int S, const GemmArgs& a, hipStream_t st);
+hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st);
+hipError_t launch_tail(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
-size_t attn_part_floats(int head_dim);
+size_t attn_part_floats(int head_dim, int nqt);
 
 }  // namespace pard

@@ -112,21 +112,30 @@ def test_k1_draft_is_plain_draft_decode(eng, models, B):
     assert_tokens_match(cand, lg, "K=1 candidate")
 
 
+def _decisive_prompt(target, n_follow):
+    """First seeded prompt whose greedy continuation has no near-tie for n_follow tokens."""
+    for seed in range(100, 400):
+        prompt = [int(x) for x in pi.gen_prompt(seed, WL.target.vocab, 32)]
+        cache = oracle.KVCache(target)
+        lg = oracle.forward_cached(target, cache, prompt, logits_rows=[len(prompt) - 1])[0]
+        greedy = []
+        for _ in range(n_follow):
+            if margins(lg) <= MARGIN:
+                break
+            greedy.append(int(np.argmax(lg)))
+            lg = oracle.forward_cached(target, cache, [greedy[-1]])[0]
+        if len(greedy) == n_follow:
+            return prompt, greedy
+    pytest.skip("no decisive prompt found")
+
+
 @pytest.mark.parametrize("k", [4, 8])
 def test_forced_candidates_accept_exact_prefix(eng, models, k):
     say(f"[gpu] tiny: forced candidates K={k}")
     target, _ = models
-    cache = oracle.KVCache(target)
-    lg = oracle.forward_cached(target, cache, PROMPT, logits_rows=[len(PROMPT) - 1])
-    greedy, marg = [int(np.argmax(lg[0]))], [float(margins(lg[0]))]
-    for _ in range(k + 1):
-        lg = oracle.forward_cached(target, cache, [greedy[-1]])
-        greedy.append(int(np.argmax(lg[0])))
-        marg.append(float(margins(lg[0])))
-    if min(marg) <= MARGIN:
-        pytest.skip("greedy continuation has a near-tie; forced acceptance is not decidable")
+    prompt, greedy = _decisive_prompt(target, k + 2)
     for j in range(k + 1):
-        first = eng.prefill(PROMPT)
+        first = eng.prefill(prompt)
         assert first == greedy[0]
         cands = list(greedy[1:1 + k])
         if j < k:
@@ -212,5 +221,20 @@ def test_qwen_shaped_bias_group7_lockstep(B):
         prompt = [int(x) for x in pi.gen_prompt(5, 512, 40)]
         for k in (4, 12):
             lockstep(eng, target, draft, prompt, k, steps=6, mask_id=511, tag=f"qwen K={k}")
+    finally:
+        eng.close()
+
+
+def test_long_prompt_split_attention_lockstep(models, B):
+    say("[gpu] tiny: 2300-token prompt (attention split over 3 key ranges + merge)")
+    target, draft = models
+    eng = B.Engine(T_SPEC, D_SPEC, WL.mask_id, max_ctx=2400, max_k=8)
+    try:
+        prompt = [int(x) for x in pi.gen_prompt(11, WL.target.vocab, 2300)]
+        worst = lockstep(eng, target, draft, prompt, 6, steps=3, mask_id=WL.mask_id, tag="long")
+        say(f"    max |logit err| {worst:.3g}")
+        first = eng.prefill(prompt)
+        toks, stats = eng.generate(6, 24)
+        assert toks[0] == first and len(toks) == 24
     finally:
         eng.close()

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
       if (qh < n_qh) {
         const int row = qh / group, head = kvh * group + qh % group;
         // same arithmetic as k_attn_merge with a single split
-        p.out[(size_t)row * p.ldo + head * HD + dim] = (uint16_t)f2bf_bits(ob[q][dim] * (1.0f / fin_l[q]));
+        p.out[act_index(row, head * HD + dim)] = (uint16_t)f2bf_bits(ob[q][dim] * (1.0f / fin_l[q]));
       }
     }
   } else {
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
         if (s0 + u < n_act && mv[u] != -INFINITY) O += ov[u] * expf(mv[u] - M);
     }
     const int row = qh / group, head = kvh * group + qh % group;
-    p.out[(size_t)row * p.ldo + head * HD + dim] = (uint16_t)f2bf_bits(O * Linv[q]);
+    p.out[act_index(row, head * HD + dim)] = (uint16_t)f2bf_bits(O * Linv[q]);
   }
 }
 

@@ -76,8 +76,8 @@ __global__ void k_gen_packed(const GenArgs a) {
        t += (size_t)gridDim.x * blockDim.x) {
     const int lane = (int)(t & 63);
     const size_t blk = t >> 6;
-    const int kb = (int)(blk % a.kb_total);
-    const int strip = (int)(blk / a.kb_total);
+    const int strip = (int)(blk % a.n_strips);   // k-block-major: (kb, strip) blocks
+    const int kb = (int)(blk / a.n_strips);
     const int n = strip * 16 + (lane & 15);
     const int k0 = kb * 32 + (lane >> 4) * 8;
     uint16_t out[8] = {0, 0, 0, 0, 0, 0, 0, 0};
@@ -141,7 +141,7 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta) {
 
 // x[r, :] = E[ids[r], :] (fp32) from the strip-packed embedding, plus the
 // first normalised GEMM's operand xg = bf16(x * g) and the row's sum of squares.
-__global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int kb_total, int d, const FwdDesc* desc,
+__global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc,
                                                float* x, const float* g, uint16_t* xg, float* ss) {
   __shared__ float wsum[4];
   const int r = blockIdx.x;
@@ -152,7 +152,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int kb_total, 
   for (int c8 = threadIdx.x; c8 < d / 8; c8 += blockDim.x) {
     const int k0 = c8 * 8, kb = k0 >> 5;
     const int lane = (id & 15) + 16 * ((k0 & 31) >> 3);
-    const uint4 w = *reinterpret_cast<const uint4*>(E + ((strip * kb_total + kb) * 64 + lane) * 8);
+    const uint4 w = *reinterpret_cast<const uint4*>(E + (((size_t)kb * n_strips + strip) * 64 + lane) * 8);
     const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
     float v[8];
     for (int i = 0; i < 4; ++i) {
@@ -167,7 +167,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int kb_total, 
       o[i] = (uint32_t)f2bf(v[2 * i] * g[k0 + 2 * i]) | ((uint32_t)f2bf(v[2 * i + 1] * g[k0 + 2 * i + 1]) << 16);
       sq += v[2 * i] * v[2 * i] + v[2 * i + 1] * v[2 * i + 1];
     }
-    *reinterpret_cast<uint4*>(xg + (size_t)r * d + k0) = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint4*>(xg + act_index(r, k0)) = make_uint4(o[0], o[1], o[2], o[3]);
   }
   for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
@@ -214,9 +214,9 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_embed(const uint16_t* E, int kb_total, int d, const FwdDesc* desc, float* x, const float* g,
+hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, float* ss, int max_rows, hipStream_t st) {
-  k_embed<<<max_rows, 256, 0, st>>>(E, kb_total, d, desc, x, g, xg, ss);
+  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, ss);
   return hipGetLastError();
 }
 

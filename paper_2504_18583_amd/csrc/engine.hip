@@ -72,14 +72,14 @@ GemmPlan plan_gemm(int epi, int n_pad, int k_pad) {
   p.n_strips = n_pad / 16;
   p.kb_total = k_pad / 32;
   const int wgs = p.n_strips / pick_S(epi, p.n_strips, 1);
-  while (wgs * p.nw < kTargetWaves && p.nw < 16 && p.kb_total / (2 * p.nw) >= 4) p.nw *= 2;
+  while (wgs * p.nw < kTargetWaves && p.nw < 8 && p.kb_total / (2 * p.nw) >= 4) p.nw *= 2;
   return p;
 }
 
 // Wavefronts per workgroup for a pass of mt row tiles (LDS <= 32 KiB).
 int plan_nw(const GemmPlan& p, int S, int mt) {
   int nw = p.nw;
-  while (nw > 4 && (nw * S * mt > 32 || (mt >= 3 && nw > 8))) nw >>= 1;
+  while (nw > 4 && nw * S * mt > 32) nw >>= 1;
   return nw;
 }
 
@@ -389,7 +389,7 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
   const int cls0 = w * 8;
   {
     Timed t(c, cls0 + 0);
-    HIP_TRY(c, launch_embed(M.embed, M.p_lm.kb_total, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, M.ss,
+    HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, M.ss,
                             ps.max_rows, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
@@ -442,7 +442,6 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.vc = vc;
       a.cap = c->kv_cap;
       a.out = M.attn;
-      a.ldo = M.q_dim;
       a.desc = M.desc;
       a.n_heads = s.n_heads;
       a.n_kv = s.n_kv_heads;
@@ -473,7 +472,6 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.ss_in = M.ss;
       a.ss_tiles = M.ss_tiles_resid;
       a.out = M.h;
-      a.ld_out = M.f_pad;
       HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, mt, a, M.p_gu));
     }
     {  // down + residual
@@ -1025,23 +1023,23 @@ pard_status pard_read_weight(const pard_ctx* cc, int32_t which, int32_t tensor, 
   const pard_model_spec& s = M.spec;
   const int hd = s.head_dim;
   const uint16_t* buf = nullptr;
-  int prow = 0, rows = 0, cols = 0, kpad = 0;
+  int prow = 0, rows = 0, cols = 0, npad = 0;   // npad: packed rows of the buffer
   const float* fbuf = nullptr;
   auto qk_row = [&](int r) { const int head = r / hd, dim = r % hd; return head * hd + (dim < hd / 2 ? 2 * dim : 2 * (dim - hd / 2) + 1); };
   if (tensor == 0 || (tensor == 1 && !s.tied_embeddings)) {
     buf = tensor == 0 ? M.embed : M.lm_head;
-    rows = s.vocab; cols = M.d; kpad = M.d; prow = row;
+    rows = s.vocab; cols = M.d; npad = s.vocab; prow = row;
   } else if (tensor >= 16 && tensor / 16 - 1 < s.n_layers) {
     const int l = tensor / 16 - 1, j = tensor % 16;
     const Layer& L = M.layers[l];
     switch (j) {
-      case 0: buf = L.wqkv; rows = M.q_dim; cols = M.d; kpad = M.d; prow = qk_row(row); break;
-      case 1: buf = L.wqkv; rows = M.kv_dim; cols = M.d; kpad = M.d; prow = M.q_dim + qk_row(row); break;
-      case 2: buf = L.wqkv; rows = M.kv_dim; cols = M.d; kpad = M.d; prow = M.q_dim + M.kv_dim + row; break;
-      case 3: buf = L.wo; rows = M.d; cols = M.q_dim; kpad = M.q_dim; prow = row; break;
-      case 4: buf = L.wgu; rows = s.ffn_dim; cols = M.d; kpad = M.d; prow = (row / 16) * 32 + row % 16; break;
-      case 5: buf = L.wgu; rows = s.ffn_dim; cols = M.d; kpad = M.d; prow = (row / 16) * 32 + 16 + row % 16; break;
-      case 6: buf = L.wd; rows = M.d; cols = s.ffn_dim; kpad = M.f_pad; prow = row; break;
+      case 0: buf = L.wqkv; rows = M.q_dim; cols = M.d; npad = M.nqkv; prow = qk_row(row); break;
+      case 1: buf = L.wqkv; rows = M.kv_dim; cols = M.d; npad = M.nqkv; prow = M.q_dim + qk_row(row); break;
+      case 2: buf = L.wqkv; rows = M.kv_dim; cols = M.d; npad = M.nqkv; prow = M.q_dim + M.kv_dim + row; break;
+      case 3: buf = L.wo; rows = M.d; cols = M.q_dim; npad = M.d; prow = row; break;
+      case 4: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 16) * 32 + row % 16; break;
+      case 5: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 16) * 32 + 16 + row % 16; break;
+      case 6: buf = L.wd; rows = M.d; cols = s.ffn_dim; npad = M.d; prow = row; break;
       case 7: case 8: case 9:
         if (!L.bqkv) return fail(c, PARD_ERR_ARG, "read_weight: model has no bias");
         fbuf = L.bqkv; cols = 1;
@@ -1058,12 +1056,12 @@ pard_status pard_read_weight(const pard_ctx* cc, int32_t which, int32_t tensor, 
     HIP_TRY(c, hipMemcpy(out, fbuf + prow, sizeof(float), hipMemcpyDeviceToHost));
     return PARD_OK;
   }
-  const int kb_total = kpad / 32;
+  const size_t n_strips = (size_t)npad / 16;
   for (int i = 0; i < n; ++i) {
     const int col = col0 + i;
     const size_t strip = prow / 16, kb = col / 32;
     const int lane = (prow % 16) + 16 * ((col % 32) / 8);
-    c->h_gather_idx[i] = ((strip * kb_total + kb) * 64 + lane) * 8 + (col % 8);
+    c->h_gather_idx[i] = ((kb * n_strips + strip) * 64 + lane) * 8 + (col % 8);
   }
   HIP_TRY(c, hipMemcpyAsync(c->gather_idx_dev, c->h_gather_idx, sizeof(size_t) * n, hipMemcpyHostToDevice, c->stream));
   HIP_TRY(c, launch_gather_u16(buf, c->gather_idx_dev, n, c->gather_out_dev, c->stream));

@@ -1,6 +1,6 @@
 // Skinny bf16 GEMM for decode-sized row counts, on gfx950 MFMA.
 //
-//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W strip-packed, bf16)
+//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W block-packed, bf16)
 //
 // Decode streams every weight once per forward (Sec. 2.1: decoding is bound by
 // reloading the weights), so the kernel is organised around the weight
@@ -44,6 +44,9 @@ __device__ __forceinline__ uint32_t f2bf_bits(float f) {
   return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;   // round to nearest, ties to even
 }
 
+constexpr int kRsrcWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-family raw buffers
+constexpr int kCachePolicyNT = 2;        // non-temporal: weights are streamed once
+
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
@@ -56,10 +59,11 @@ __device__ __forceinline__ int v_slot(int k) {
 }
 
 template <int MT, int S, int EPI>
-__global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p) {
+__global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
   constexpr int NJ = S * MT;         // elements per thread in the epilogue (first 256 threads)
-  constexpr int U = (4 / S) > 0 ? 4 / S : 1;   // k-blocks per pipeline stage (4 KiB of W per wave)
+  // k-blocks per pipeline stage: 8 KiB of W per wave (smaller for prefill-sized row counts)
+  constexpr int U = MT >= 3 ? 2 : ((8 / S) > 0 ? 8 / S : 1);
   extern __shared__ float red[];     // [NW][NE]
   __shared__ float rs_s[MT * 16];
 
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
   const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
 
   // wave w streams k-blocks w, w + nw, w + 2*nw, ...: at any time the
-  // workgroup reads nw consecutive 1 KiB blocks of each strip
+  // workgroup reads nw consecutive k-blocks of each strip
   const int n_it = (p.kb_total - wave + nw - 1) / nw;
 
   f32x4 acc[S][MT];
@@ -81,16 +85,27 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) acc[s][mt] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const u32x4* Wt = reinterpret_cast<const u32x4*>(p.W) + (size_t)tile * S * p.kb_total * 64 + lane;
-  // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at 8*(lane/16)
-  const u32x4* Ar[MT];
-  bool a_ok[MT];
+  // Raw buffer loads: a per-matrix descriptor, a constant per-lane VGPR offset
+  // and a scalar per-iteration offset, so the prefetch needs no VGPR address
+  // arithmetic (which would otherwise force waits on in-flight loads), and
+  // every access is bounds-checked by the hardware.
+  // W is k-block-major: block (kb, strip) sits at (kb * n_strips + strip) KiB.
+  const int n_strips = p.n_tiles * S;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.W), 0, (int)min((size_t)n_strips * p.kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
+  const int w_voff = (tile * S * 64 + lane) * 16;
+  // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at
+  // 8*(lane/16); A is k-blocked, so k-block kb of all rows is one contiguous
+  // run at kb * kMaxRows * 64 bytes.  Rows past the pass get an offset beyond
+  // the buffer: the hardware returns zeros for them without a memory access.
+  const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.A), 0, kMaxRows * p.lda * 2, kRsrcWord3);
+  constexpr int kOutOfRange = 0x7FFFFFF0;
+  int a_voff[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int r = mt * 16 + (lane & 15);
-    a_ok[mt] = r < row_count;
-    const int row = min(row_begin + r, kMaxRows - 1);
-    Ar[mt] = reinterpret_cast<const u32x4*>(p.A + (size_t)row * p.lda + (lane >> 4) * 8);
+    a_voff[mt] = r < row_count ? ((row_begin + r) * 32 + (lane >> 4) * 8) * 2 : kOutOfRange;
   }
 
   // Two register stages of U k-blocks each: loads of stage i+1 are in flight
@@ -102,9 +117,11 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
     for (int u = 0; u < U; ++u) {
       const int kb = wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
-      for (int s = 0; s < S; ++s) w[u][s] = __builtin_nontemporal_load(Wt + ((size_t)s * p.kb_total + kb) * 64);
+      for (int s = 0; s < S; ++s)
+        w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
 #pragma unroll
-      for (int mt = 0; mt < MT; ++mt) a[u][mt] = Ar[mt][kb * 4];
+      for (int mt = 0; mt < MT; ++mt)
+        a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (kMaxRows * 64), 0);
     }
   };
   auto compute = [&](const u32x4 (&w)[U][S], const u32x4 (&a)[U][MT], int its) {
@@ -113,7 +130,7 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
       const bool live = its + u < n_it;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const u32x4 av = (live && a_ok[mt]) ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
+        const u32x4 av = live ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int s = 0; s < S; ++s)
           acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
@@ -122,6 +139,7 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
       }
     }
   };
+
   // 1/rms per row from the producer's per-tile sums of squares: 16 threads per
   // row, 16 independent loads each in flight together, fixed summation order
   auto row_scales = [&]() {
@@ -244,7 +262,7 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
         const size_t o = (size_t)(row_begin + row) * p.ldx + n;
         const float xn = p.x[o] + v[j];
         p.x[o] = xn;
-        p.xg[o] = (uint16_t)f2bf_bits(xn * p.g_next[n]);
+        p.xg[act_index(row_begin + row, n)] = (uint16_t)f2bf_bits(xn * p.g_next[n]);
         sq[mt] += xn * xn;
       }
     }
@@ -268,7 +286,7 @@ __global__ __launch_bounds__(MT >= 3 ? 512 : 1024) void k_gemm(const GemmArgs p)
         const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * (S / 2) + q) * 16 + csub;
-        if (row < row_count) p.out[(size_t)row * p.ld_out + f] = (uint16_t)f2bf_bits(h);
+        if (row < row_count) p.out[act_index(row, f)] = (uint16_t)f2bf_bits(h);
       }
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;
@@ -409,6 +427,7 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
 template <int EPI, int MT, int S>
 hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st) {
   const size_t lds = (size_t)nw * S * MT * 256 * sizeof(float);
+  if (nw > 8) return hipErrorInvalidValue;
   k_gemm<MT, S, EPI><<<dim3(a.n_tiles), dim3(64 * nw), lds, st>>>(a);
   return hipGetLastError();
 }
@@ -437,7 +456,7 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
-  if (nw < 4 || nw > (mt >= 3 ? 8 : 16) || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
+  if (nw < 4 || nw > 8 || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
   switch (epi) {
     case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, nw, a, st);
     case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, nw, a, st);

@@ -1,17 +1,24 @@
 // Internal structures shared by the engine (host) and the HIP kernels.
 //
 // Device data layout (all carved from the caller's arena):
-//   * every weight matrix W [out, in] is stored bf16 in "strip" order: 16 output
-//     rows x 32 input columns form a 1 KiB block laid out in the lane order of
-//     the v_mfma_f32_16x16x32_bf16 B operand (lane l holds row l%16, columns
-//     8*(l/16) .. +7); the blocks of one strip are contiguous along the input
-//     dimension, so a wavefront streaming a strip reads contiguous memory.
+//   * every weight matrix W [out, in] is stored bf16 in 1 KiB blocks of 16
+//     output rows ("strip") x 32 input columns ("k-block"), each laid out in
+//     the lane order of the v_mfma_f32_16x16x32_bf16 B operand (lane l holds
+//     row l%16, columns 8*(l/16) .. +7).  Blocks are k-block-major: block
+//     (kb, strip) sits at (kb * n_strips + strip) KiB, so while every
+//     workgroup streams its strips, the grid as a whole sweeps contiguous
+//     memory (spreading the reads over all HBM channels).
 //   * Q/K rows are stored pair-interleaved per head (packed row 2j = dim j,
 //     2j+1 = dim j + head_dim/2) so the rotate-half rotary pairs sit in
 //     neighbouring lanes; K is cached in that order and attention's q.k is
 //     invariant to it.  Gate/up rows are interleaved by strips (gate strip,
 //     up strip, ...) so one tile holds matching gate and up columns.
 //   * KV cache: K and V bf16 [batch][layer][kv_head][max_ctx][head_dim].
+//   * activations that feed a GEMM (x*g, attention output, silu(gate)*up) are
+//     k-blocked bf16: element (row, k) sits at act_index(row, k), i.e. the 64
+//     row slots of one 32-column block are contiguous (64 bytes per row), so
+//     the MFMA A fragment of one k-block is one contiguous run of rows * 64
+//     bytes instead of one 64-byte piece per row.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,6 +33,11 @@ constexpr int kBlock = 256;
 constexpr int kAttnWaves = 8;      // wavefronts per attention workgroup
 constexpr int kAttnSplit = 1024;   // keys per workgroup once a context is split (> 2 splits' worth)
 constexpr int kAttnRecords = 512;  // max (query block, key split) partial records per KV head
+
+// Position of activation element (row, k) in a k-blocked [kMaxRows x K] buffer.
+__host__ __device__ inline size_t act_index(int row, int k) {
+  return ((size_t)(k >> 5) * kMaxRows + row) * 32 + (k & 31);
+}
 
 // Rows of the next forward pass of one model.  Written by the host (granular
 // calls) or by the tail of the previous pass (fused loop).
@@ -61,7 +73,7 @@ struct GemmArgs {
   const uint16_t* W;      // strip-packed bf16 weight
   int kb_total;           // padded input dim / 32
   int n_tiles;            // output tiles (S strips each) = grid size
-  const uint16_t* A;      // bf16 activations [kMaxRows][lda]
+  const uint16_t* A;      // bf16 activations, k-blocked (act_index), lda columns
   int lda;
   const FwdDesc* desc;
   int lm_mode;            // 0: rows [0, n_rows)   1: rows [lm_row0, lm_row0 + lm_rows)
@@ -100,7 +112,7 @@ struct AttnArgs {
   const uint16_t* q; int ldq;                 // [rows][H_q*hd] bf16, pair-interleaved dims
   const uint16_t* kc; const uint16_t* vc;     // this layer's cache of one sequence
   int cap;                                    // KV capacity (multiple of 32)
-  uint16_t* out; int ldo;                     // [rows][H_q*hd] bf16
+  uint16_t* out;                              // k-blocked (act_index), H_q*hd columns, bf16
   const FwdDesc* desc;
   int n_heads, n_kv;
   int nqt, n_qblocks;                         // 16*nqt query pairs per block

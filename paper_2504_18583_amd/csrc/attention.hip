@@ -2,26 +2,33 @@
 // bf16 KV cache (the draft pass with its mask rows, the verify pass, prefill
 // chunks), on gfx950 MFMA.
 //
-// A workgroup serves one KV head, one block of 16*NQT (row, head-in-group)
-// query pairs and one range of keys.  Per 32-key tile a wavefront computes
-//   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_bf16, K rows as A,
+// A workgroup serves one KV head, one group of 16*NQ (row, head-in-group)
+// query pairs -- for decode passes every pair of the KV head, so each key is
+// read once per pass -- and one chunk of split_len keys.  Its four wavefronts
+// take the chunk's 32-key tiles round-robin; per tile a wavefront computes
+//   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_bf16, K as A,
 //                                          Q as B, accumulated over head_dim)
 //   O^T[dim][q] += V^T[dim][key] P^T[key][q]
-// with an online softmax (running max m, sum l, fp32) in between.  The S^T
-// accumulator of lane l holds keys 4g..4g+3 (and 16+4g..) for query l%16,
+// with an online softmax (running max m, sum l, fp32, base 2) in between.  The
+// S^T accumulator of lane l holds keys 4g..4g+3 (and 16+4g..) for query l%16,
 // g = l/16, which is exactly the B-operand fragment P^T needs once packed to
 // bf16; the V cache stores each 32-key block transposed ([dim][key]) with those
-// eight keys of group g contiguous, so V^T fragments are single 16-byte loads.
-// K is cached row-major, so K fragments are 16-byte loads too.  Scores are
-// causal by absolute position: key j is visible to the query at position
-// pos0 + row iff j <= pos0 + row (mask rows of the draft pass are ordinary
-// causal rows; Sec. 3.1 eq. 7 conditions candidate k on x_<n, m_0..m_{k-1}).
+// eight keys of group g contiguous, and the K cache stores each 16-key block as
+// ready A fragments, so every K or V fragment is one contiguous 1 KiB
+// wavefront load.  Q fragments are staged once in LDS.
 //
-// The kAttnWaves wavefronts of a workgroup take its 32-key tiles round-robin
-// and are merged in LDS in wave order.  With several key splits (long contexts) each workgroup writes
-// (o, m, l) and k_attn_merge combines the splits in split order.  All
-// reductions have a fixed order: results are deterministic and a query's
-// result does not depend on the other rows of the pass.
+// Scores are causal by absolute position: key j is visible to the query at
+// position pos0 + row iff j <= pos0 + row.  Mask rows of the draft pass are
+// ordinary causal rows (Sec. 3.1, eq. 7: candidate k is conditioned on the
+// prefix and the k-1 mask tokens before it).
+//
+// The wavefronts are merged in LDS in wave order.  With several chunks each
+// workgroup writes (o, m, l) and k_attn_merge combines them in chunk order.
+// All reductions have a fixed order, chunk boundaries sit at fixed multiples
+// of split_len and a query's arithmetic does not depend on which other pairs
+// share its workgroup: results are deterministic and a query's result does
+// not depend on the other rows of the pass.  Chunks past a query's position
+// contribute exact zeros.
 #include "pard_internal.h"
 
 namespace pard {
@@ -31,32 +38,39 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t f2bf_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// two floats to packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
 
-template <int HD, int NQT>
+constexpr float kLog2e = 1.4426950408889634f;
+
+template <int HD, int NQ>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   constexpr int NWA = kAttnWaves;
-  constexpr int QB = 16 * NQT;   // query pairs per block
-  constexpr int KS = HD / 32;    // 32-dim steps of Q.K
-  constexpr int DB = HD / 16;    // 16-dim blocks of the output
-  __shared__ float mw[NWA][QB], lw[NWA][QB], fin_m[QB], fin_l[QB];
-  __shared__ float ob[QB][HD + 1];
+  constexpr int QP = 16 * NQ;        // query pairs per workgroup
+  constexpr int KS = HD / 32;        // 32-dim steps of Q.K
+  constexpr int DB = HD / 16;        // 16-dim blocks of the output
+  constexpr int OS = HD + 4;         // row stride of the per-wave output tiles in LDS
+  __shared__ u32x4 q_lds[NQ * KS * 64];   // Q fragments in B-operand lane order
+  __shared__ __attribute__((aligned(16))) float o_lds[NWA][QP][OS];
+  __shared__ float m_lds[NWA][QP], l_lds[NWA][QP], sc_lds[NWA][QP], linv_lds[QP];
 
-  const int kvh = blockIdx.x, z = blockIdx.y, sp = blockIdx.z;
+  const int kvh = blockIdx.x, qg = blockIdx.y, ch = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int group = p.n_heads / p.n_kv;
   const FwdDesc d = *p.desc;
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
-  if (z * QB >= n_qh) return;                      // uniform: the whole block leaves
-  const int k_begin = sp * p.split_len;            // multiple of 32
-  if (k_begin >= L_end) return;                    // uniform: split beyond the context
+  if (qg * QP >= n_qh) return;                     // uniform: the whole block leaves
+  const int k_begin = ch * p.split_len;            // multiple of 128
+  if (k_begin >= L_end) return;                    // uniform: chunk beyond the context
   const int k_end = min(L_end, k_begin + p.split_len);
-  // wave w takes tiles w, w+NWA, ... of the split: the assignment does not
+  // wave w takes tiles w, w+NWA, ... of the chunk: the assignment does not
   // depend on where the pass ends, so tiles beyond a query's position add
   // exact zeros
   const int n_t = (k_end - k_begin + 31) / 32;
@@ -66,249 +80,290 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   const uint16_t* vbase = p.vc + (size_t)kvh * p.cap * HD;
   const int g4 = lane >> 4, c16 = lane & 15;
 
-  // Q fragments (B operand): query c16 of tile t, dims 32*ks + 8*g4 .. +7
-  u32x4 qf[NQT][KS];
-  int qpos[NQT];
-#pragma unroll
-  for (int t = 0; t < NQT; ++t) {
-    const int qh = z * QB + t * 16 + c16;
-    const bool ok = qh < n_qh;
-    const int row = ok ? qh / group : 0;
-    const int head = kvh * group + (ok ? qh % group : 0);
-    qpos[t] = ok ? d.pos0 + row : -1;
-    const uint16_t* qp = p.q + (size_t)row * p.ldq + head * HD + g4 * 8;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[t][ks] = ok ? *reinterpret_cast<const u32x4*>(qp + ks * 32) : u32x4{0u, 0u, 0u, 0u};
-  }
-
-  float m[NQT], l[NQT];
-  f32x4 o[DB][NQT];
-#pragma unroll
-  for (int t = 0; t < NQT; ++t) {
-    m[t] = -INFINITY;
-    l[t] = 0.f;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) o[db][t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  // two register stages of K and V fragments (tile i+1 loads while tile i computes)
-  u32x4 kf0[2][KS], vf0[DB], kf1[2][KS], vf1[DB];
-  auto load = [&](u32x4 (&kf)[2][KS], u32x4 (&vf)[DB], int it) {
+  // K and V fragments of two tiles (a pair of tiles shares one softmax max)
+  u32x4 kf[2][2][KS], vf[2][DB];
+  auto load = [&](int tt, int it) {
     const int key0 = k_begin + (wave + NWA * min(it, n_my - 1)) * 32;   // in bounds: key0 + 31 < cap
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      const uint16_t* kp = kbase + (size_t)(key0 + kb * 16 + c16) * HD + g4 * 8;
+      const uint16_t* kp = kbase + ((size_t)((key0 >> 4) + kb) * KS * 64 + lane) * 8;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) kf[kb][ks] = *reinterpret_cast<const u32x4*>(kp + ks * 32);
+      for (int ks = 0; ks < KS; ++ks) kf[tt][kb][ks] = *reinterpret_cast<const u32x4*>(kp + ks * 64 * 8);
     }
     const uint16_t* vp = vbase + ((size_t)(key0 >> 5) * HD + c16) * 32 + g4 * 8;
 #pragma unroll
-    for (int db = 0; db < DB; ++db) vf[db] = *reinterpret_cast<const u32x4*>(vp + db * 16 * 32);
+    for (int db = 0; db < DB; ++db) vf[tt][db] = *reinterpret_cast<const u32x4*>(vp + db * 16 * 32);
   };
-  auto compute = [&](const u32x4 (&kf)[2][KS], const u32x4 (&vf)[DB], int it) {
-    const int key0 = k_begin + (wave + NWA * it) * 32;
+  if (n_my > 0) {
+    load(0, 0);
+    load(1, 1);
+  }
+
+  // stage the Q fragments: entry (t, ks, l) = pair t*16 + l%16, dims ks*32 + 8*(l/16) .. +7
+  for (int e = tid; e < NQ * KS * 64; e += 64 * NWA) {
+    const int t = e / (KS * 64), ks = (e / 64) % KS, l = e & 63;
+    const int qh = qg * QP + t * 16 + (l & 15);
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (qh < n_qh) {
+      const int row = qh / group, head = kvh * group + qh % group;
+      v = *reinterpret_cast<const u32x4*>(p.q + (size_t)row * p.ldq + head * HD + ks * 32 + (l >> 4) * 8);
+    }
+    q_lds[e] = v;
+  }
+  int qpos[NQ];
 #pragma unroll
-    for (int t = 0; t < NQT; ++t) {
-      f32x4 s[2];
+  for (int t = 0; t < NQ; ++t) {
+    const int qh = qg * QP + t * 16 + c16;
+    qpos[t] = qh < n_qh ? d.pos0 + qh / group : -1;
+  }
+  __syncthreads();
+
+  float m[NQ], l[NQ];
+  f32x4 o[NQ][DB];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int t = 0; t < NQ; ++t) {
+    m[t] = -INFINITY;
+    l[t] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks)
-          s[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kf[kb][ks]),
-                                                          __builtin_bit_cast(bf16x8, qf[t][ks]), s[kb], 0, 0, 0);
+    for (int db = 0; db < DB; ++db) o[t][db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const float scale2 = p.scale * kLog2e;   // scores in base 2
+
+  for (int it0 = 0; it0 < n_my; it0 += 2) {
+    if (it0 > 0) {
+      load(0, it0);
+      load(1, it0 + 1);
+    }
+    const int nt = min(2, n_my - it0);     // tiles in this pair (uniform)
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      f32x4 s[2][2];
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb) {
+          s[tt][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks)
+            s[tt][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf16x8, kf[tt][kb][ks]), __builtin_bit_cast(bf16x8, q_lds[(t * KS + ks) * 64 + lane]),
+                s[tt][kb], 0, 0, 0);
+        }
+      // causal / range mask; only tiles that reach past the context end or the
+      // first query's position need it
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt) {
+        const int key0 = k_begin + (wave + NWA * (it0 + tt)) * 32;
+        if (tt >= nt || key0 + 31 >= k_end || key0 + 31 > d.pos0) {
+#pragma unroll
+          for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int key = key0 + kb * 16 + g4 * 4 + i;
+              if (tt >= nt || key >= k_end || key > qpos[t]) s[tt][kb][i] = -INFINITY;
+            }
+        }
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = key0 + kb * 16 + g4 * 4 + i;
-          const bool vis = key < k_end && key <= qpos[t];
-          s[kb][i] = vis ? s[kb][i] * p.scale : -INFINITY;
-          mx = fmaxf(mx, s[kb][i]);
-        }
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[tt][kb][i]);
       mx = fmaxf(mx, __shfl_xor(mx, 16));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m[t], mx);
-      const float corr = (m[t] == -INFINITY) ? 0.f : expf(m[t] - m_new);
-      float pv[8];
+      const float m_new = fmaxf(m[t], mx * scale2);
+      const float m_use = m_new == -INFINITY ? 0.f : m_new;   // keeps 2^(-inf - m) = 0 well defined
+      const float corr = __builtin_amdgcn_exp2f(m[t] - m_use);
       float rs = 0.f;
+      u32x4 pf[2];
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int tt = 0; tt < 2; ++tt) {
+        float pv[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = (s[kb][i] == -INFINITY) ? 0.f : expf(s[kb][i] - m_new);
-          pv[kb * 4 + i] = e;
-          rs += e;
-        }
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pv[kb * 4 + i] = __builtin_amdgcn_exp2f(fmaf(s[tt][kb][i], scale2, -m_use));
+            rs += pv[kb * 4 + i];
+          }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) pf[tt][i] = pack_bf16x2(pv[2 * i], pv[2 * i + 1]);
+      }
       rs += __shfl_xor(rs, 16);
       rs += __shfl_xor(rs, 32);
       l[t] = l[t] * corr + rs;
       m[t] = m_new;
-      u32x4 pf;
+      if (it0 > 0) {                       // uniform; o is still zero for the first pair
 #pragma unroll
-      for (int i = 0; i < 4; ++i) pf[i] = f2bf_bits(pv[2 * i]) | (f2bf_bits(pv[2 * i + 1]) << 16);
-#pragma unroll
-      for (int db = 0; db < DB; ++db) {
-        o[db][t] *= corr;
-        o[db][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[db]),
-                                                           __builtin_bit_cast(bf16x8, pf), o[db][t], 0, 0, 0);
+        for (int db = 0; db < DB; ++db) o[t][db] *= corr;
       }
-    }
-  };
-  if (n_my > 0) {
-    int it = 0;
-    load(kf0, vf0, it);
-    while (true) {
-      load(kf1, vf1, it + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(kf0, vf0, it);
-      __builtin_amdgcn_sched_barrier(0);
-      if (++it >= n_my) break;
-      load(kf0, vf0, it + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      compute(kf1, vf1, it);
-      __builtin_amdgcn_sched_barrier(0);
-      if (++it >= n_my) break;
+#pragma unroll
+      for (int tt = 0; tt < 2; ++tt)
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[tt][db]),
+                                                             __builtin_bit_cast(bf16x8, pf[tt]), o[t][db], 0, 0, 0);
     }
   }
 
   // ---- merge the wavefronts in wave order ----
   if (g4 == 0) {
 #pragma unroll
-    for (int t = 0; t < NQT; ++t) {
-      mw[wave][t * 16 + c16] = m[t];
-      lw[wave][t * 16 + c16] = l[t];
+    for (int t = 0; t < NQ; ++t) {
+      m_lds[wave][t * 16 + c16] = m[t];
+      l_lds[wave][t * 16 + c16] = l[t];
     }
   }
+  // lane (c16, g4) holds dims db*16 + 4*g4 .. +3 of pair t*16 + c16
+#pragma unroll
+  for (int t = 0; t < NQ; ++t)
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+      *reinterpret_cast<f32x4*>(&o_lds[wave][t * 16 + c16][db * 16 + g4 * 4]) = o[t][db];
   __syncthreads();
-  if (tid < QB) {
-    float M = mw[0][tid];
-    for (int w = 1; w < NWA; ++w) M = fmaxf(M, mw[w][tid]);
+  if (tid < QP) {
+    float M = m_lds[0][tid];
+    for (int w = 1; w < NWA; ++w) M = fmaxf(M, m_lds[w][tid]);
+    const float M_use = M == -INFINITY ? 0.f : M;
     float L = 0.f;
-    for (int w = 0; w < NWA; ++w) L += (mw[w][tid] == -INFINITY) ? 0.f : lw[w][tid] * expf(mw[w][tid] - M);
-    fin_m[tid] = M;
-    fin_l[tid] = L;
+    for (int w = 0; w < NWA; ++w) {
+      const float sc = __builtin_amdgcn_exp2f(m_lds[w][tid] - M_use);
+      sc_lds[w][tid] = sc;
+      L += l_lds[w][tid] * sc;
+    }
+    if (p.n_splits == 1) {
+      linv_lds[tid] = 1.0f / L;            // same arithmetic as k_attn_merge with one chunk
+    } else {
+      float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * (QP * HD + 2 * QP);
+      rec[QP * HD + tid] = M;
+      rec[QP * HD + QP + tid] = L;
+    }
   }
   __syncthreads();
-  for (int w = 0; w < NWA; ++w) {
-    if (wave == w) {
+  // each thread finishes 8 consecutive dims of one pair: one 16-byte bf16
+  // store (or two 16-byte fp32 stores of the chunk record)
+  for (int e = tid; e < QP * HD / 8; e += 64 * NWA) {
+    const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, b = a;
 #pragma unroll
-      for (int t = 0; t < NQT; ++t) {
-        const int q = t * 16 + c16;
-        const float f = (m[t] == -INFINITY) ? 0.f : expf(m[t] - fin_m[q]);
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            float& dst = ob[q][db * 16 + g4 * 4 + i];
-            dst = (w == 0 ? 0.f : dst) + o[db][t][i] * f;
-          }
-      }
+    for (int w = 0; w < NWA; ++w) {
+      const float sc = sc_lds[w][q];
+      a += *reinterpret_cast<const f32x4*>(&o_lds[w][q][d0]) * sc;
+      b += *reinterpret_cast<const f32x4*>(&o_lds[w][q][d0 + 4]) * sc;
     }
-    __syncthreads();
-  }
-
-  if (p.n_splits == 1) {
-    for (int e = tid; e < QB * HD; e += 64 * NWA) {
-      const int q = e / HD, dim = e % HD;
-      const int qh = z * QB + q;
+    if (p.n_splits == 1) {
+      const int qh = qg * QP + q;
       if (qh < n_qh) {
         const int row = qh / group, head = kvh * group + qh % group;
-        // same arithmetic as k_attn_merge with a single split
-        p.out[act_index(row, head * HD + dim)] = (uint16_t)f2bf_bits(ob[q][dim] * (1.0f / fin_l[q]));
+        const float li = linv_lds[q];
+        const u32x4 v = u32x4{pack_bf16x2(a[0] * li, a[1] * li), pack_bf16x2(a[2] * li, a[3] * li),
+                              pack_bf16x2(b[0] * li, b[1] * li), pack_bf16x2(b[2] * li, b[3] * li)};
+        *reinterpret_cast<u32x4*>(p.out + act_index(row, head * HD + d0)) = v;
       }
-    }
-  } else {
-    float* rec = p.part + ((size_t)(kvh * p.n_qblocks + z) * p.n_splits + sp) * (QB * HD + 2 * QB);
-    for (int e = tid; e < QB * HD; e += 64 * NWA) rec[e] = ob[e / HD][e % HD];
-    if (tid < QB) {
-      rec[QB * HD + tid] = fin_m[tid];
-      rec[QB * HD + QB + tid] = fin_l[tid];
+    } else {
+      float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * (QP * HD + 2 * QP);
+      *reinterpret_cast<f32x4*>(rec + q * HD + d0) = a;
+      *reinterpret_cast<f32x4*>(rec + q * HD + d0 + 4) = b;
     }
   }
 }
 
-// Combine the key splits of k_attn in split order.  Grid (kv head, query
-// block, kMergeParts): per-query (max, sum) first, then each workgroup merges
-// a slice of the (query, dim) outputs with 8 split loads in flight at a time.
+// Combine the key chunks of k_attn in chunk order.  Grid (kv head, query
+// group, kMergeParts): per-query (max, sum) first, then each thread merges 8
+// consecutive dims of one pair with the loads of 4 chunks in flight at a time.
 constexpr int kMergeParts = 8;
 
-template <int HD, int NQT>
+template <int HD, int NQ>
 __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
-  constexpr int QB = 16 * NQT;
-  constexpr int REC = QB * HD + 2 * QB;
-  __shared__ float Ms[QB], Linv[QB];
-  const int kvh = blockIdx.x, z = blockIdx.y, part = blockIdx.z, tid = threadIdx.x;
+  constexpr int QP = 16 * NQ;
+  constexpr int REC = QP * HD + 2 * QP;
+  __shared__ float Ms[QP], Linv[QP];
+  const int kvh = blockIdx.x, qg = blockIdx.y, part = blockIdx.z, tid = threadIdx.x;
   const int group = p.n_heads / p.n_kv;
   const FwdDesc d = *p.desc;
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
-  if (z * QB >= n_qh) return;                      // uniform
+  if (qg * QP >= n_qh) return;                     // uniform
   const int n_act = min(p.n_splits, (L_end + p.split_len - 1) / p.split_len);
-  const float* base = p.part + (size_t)(kvh * p.n_qblocks + z) * p.n_splits * REC;
-  if (tid < QB) {
+  const float* base = p.part + (size_t)(kvh * p.n_qblocks + qg) * p.n_splits * REC;
+  if (tid < QP) {
     float M = -INFINITY;
-    for (int s = 0; s < n_act; ++s) M = fmaxf(M, base[(size_t)s * REC + QB * HD + tid]);
+    for (int s = 0; s < n_act; ++s) M = fmaxf(M, base[(size_t)s * REC + QP * HD + tid]);
+    const float M_use = M == -INFINITY ? 0.f : M;
     float L = 0.f;
-    for (int s = 0; s < n_act; ++s) {
-      const float ms = base[(size_t)s * REC + QB * HD + tid];
-      L += (ms == -INFINITY) ? 0.f : base[(size_t)s * REC + QB * HD + QB + tid] * expf(ms - M);
-    }
-    Ms[tid] = M;
+    for (int s = 0; s < n_act; ++s)
+      L += base[(size_t)s * REC + QP * HD + QP + tid] *
+           __builtin_amdgcn_exp2f(base[(size_t)s * REC + QP * HD + tid] - M_use);
+    Ms[tid] = M_use;
     Linv[tid] = 1.0f / L;
   }
   __syncthreads();
-  constexpr int PER = QB * HD / kMergeParts;
-  for (int e = part * PER + tid; e < (part + 1) * PER; e += 256) {
-    const int q = e / HD, dim = e % HD;
-    const int qh = z * QB + q;
+  constexpr int NV = QP * HD / 8;                  // 8-dim vectors of the group
+  constexpr int PER = (NV + kMergeParts - 1) / kMergeParts;
+  for (int e = part * PER + tid; e < min(NV, (part + 1) * PER); e += 256) {
+    const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
+    const int qh = qg * QP + q;
     if (qh >= n_qh) continue;
     const float M = Ms[q];
-    float O = 0.f;
-    for (int s0 = 0; s0 < n_act; s0 += 8) {
-      float ov[8], mv[8];
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, b = a;
+    for (int s0 = 0; s0 < n_act; s0 += 4) {
+      f32x4 va[4], vb[4];
+      float mv[4];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 4; ++u) {
         const int sx = min(s0 + u, n_act - 1);
-        ov[u] = base[(size_t)sx * REC + e];
-        mv[u] = base[(size_t)sx * REC + QB * HD + q];
+        const float* r = base + (size_t)sx * REC;
+        va[u] = *reinterpret_cast<const f32x4*>(r + q * HD + d0);
+        vb[u] = *reinterpret_cast<const f32x4*>(r + q * HD + d0 + 4);
+        mv[u] = r[QP * HD + q];
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
-        if (s0 + u < n_act && mv[u] != -INFINITY) O += ov[u] * expf(mv[u] - M);
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < n_act) {
+          const float sc = __builtin_amdgcn_exp2f(mv[u] - M);
+          a += va[u] * sc;
+          b += vb[u] * sc;
+        }
     }
     const int row = qh / group, head = kvh * group + qh % group;
-    p.out[act_index(row, head * HD + dim)] = (uint16_t)f2bf_bits(O * Linv[q]);
+    const float li = Linv[q];
+    const u32x4 v = u32x4{pack_bf16x2(a[0] * li, a[1] * li), pack_bf16x2(a[2] * li, a[3] * li),
+                          pack_bf16x2(b[0] * li, b[1] * li), pack_bf16x2(b[2] * li, b[3] * li)};
+    *reinterpret_cast<u32x4*>(p.out + act_index(row, head * HD + d0)) = v;
   }
 }
 
-template <int HD, int NQT>
-hipError_t launch_hd_nqt(const AttnArgs& a, hipStream_t st) {
-  k_attn<HD, NQT><<<dim3(a.n_kv, a.n_qblocks, a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
+template <int HD, int NQ>
+hipError_t launch_hd_nq(const AttnArgs& a, hipStream_t st) {
+  k_attn<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
-  k_attn_merge<HD, NQT><<<dim3(a.n_kv, a.n_qblocks, kMergeParts), dim3(256), 0, st>>>(a);
+  k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, kMergeParts), dim3(256), 0, st>>>(a);
   return hipGetLastError();
 }
 
 template <int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t st) {
   switch (a.nqt) {
-    case 1: return launch_hd_nqt<HD, 1>(a, st);
-    case 2: if constexpr (HD == 64) return launch_hd_nqt<HD, 2>(a, st); break;
+    case 1: return launch_hd_nq<HD, 1>(a, st);
+    case 2: return launch_hd_nq<HD, 2>(a, st);
+    case 3: return launch_hd_nq<HD, 3>(a, st);
+    case 4: if constexpr (HD == 64) return launch_hd_nq<HD, 4>(a, st); break;
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
+int attn_max_q_tiles(int head_dim) { return head_dim == 128 ? 3 : 4; }
+
 size_t attn_part_floats(int head_dim, int nqt) { return (size_t)16 * nqt * head_dim + 2 * 16 * nqt; }
 
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st) {
-  if (a.split_len % 32 || a.split_len <= 0) return hipErrorInvalidValue;
+  if (a.split_len % 128 || a.split_len <= 0) return hipErrorInvalidValue;
+  if (a.nqt < 1 || a.nqt > attn_max_q_tiles(head_dim)) return hipErrorInvalidValue;
   if (head_dim == 64) return launch_hd<64>(a, st);
   if (head_dim == 128) return launch_hd<128>(a, st);
   return hipErrorInvalidValue;

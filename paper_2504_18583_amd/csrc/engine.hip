@@ -20,7 +20,6 @@ using namespace pard;
 
 namespace {
 
-constexpr int kTargetWaves = 2048;       // per GEMM launch: 2 per SIMD on 256 CUs
 constexpr int kPrefillRows = kMaxRows;
 constexpr int kDescRing = 512;
 constexpr int kGatherMax = 4096;
@@ -55,7 +54,8 @@ struct Bump {
 // counts of decode passes), so per-element summation order does not depend on
 // how many rows a pass has.
 struct GemmPlan {
-  int n_strips = 0, kb_total = 0, nw = 4;
+  int n_strips = 0, kb_total = 0;
+  int nw = 4;   // one wavefront per SIMD: more waves per workgroup measured slower at every decode shape
 };
 
 int pick_S(int epi, int n_strips, int mt) {
@@ -71,8 +71,7 @@ GemmPlan plan_gemm(int epi, int n_pad, int k_pad) {
   GemmPlan p;
   p.n_strips = n_pad / 16;
   p.kb_total = k_pad / 32;
-  const int wgs = p.n_strips / pick_S(epi, p.n_strips, 1);
-  while (wgs * p.nw < kTargetWaves && p.nw < 8 && p.kb_total / (2 * p.nw) >= 4) p.nw *= 2;
+  (void)epi;
   return p;
 }
 
@@ -264,7 +263,7 @@ size_t layout(pard_ctx* c, char* base) {
     M.desc = b.take<FwdDesc>(1);
     max_lm_tiles = std::max(max_lm_tiles, M.p_lm.n_strips);
     attn_part = std::max(attn_part, (size_t)s.n_kv_heads * kAttnRecords *
-                                        attn_part_floats(s.head_dim, s.head_dim == 128 ? 1 : 2));
+                                        attn_part_floats(s.head_dim, attn_max_q_tiles(s.head_dim)));
   }
   c->amax_val = b.take<float>((size_t)max_lm_tiles * kMaxLmRows);
   c->amax_idx = b.take<int>((size_t)max_lm_tiles * kMaxLmRows);
@@ -393,23 +392,19 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
                             ps.max_rows, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
-  // attention plan: query blocks of up to 48/64 (row, head) pairs; keys split
-  // over workgroups of ~kAttnSplit keys (merged by a second kernel), with at
-  // most kAttnRecords (query block, split) records per KV head
+  // attention plan: one workgroup per (KV head, query group, key chunk); a
+  // query group holds every (row, head) pair of the KV head for decode passes
+  // (up to 48 / 64 pairs); chunks of kAttnChunk keys start at fixed multiples
+  // whatever the pass, so a query's result does not depend on the other rows
+  // of its pass (only very long prefill chunks, with many query groups, use
+  // longer chunks to bound the partial records)
   const int qpairs = ps.max_rows * M.group;
-  const int nqt = std::min(s.head_dim == 128 ? 1 : 2, ceil_div(qpairs, 16));
+  const int nqt = std::min(attn_max_q_tiles(s.head_dim), ceil_div(qpairs, 16));
   const int n_qblocks = ceil_div(qpairs, 16 * nqt);
   const int l_bound = std::min(std::max(ps.l_bound, 1), c->kv_cap);
-  // one workgroup per (KV head, query block) up to 2*kAttnSplit keys; beyond,
-  // split boundaries sit at multiples of kAttnSplit whatever the pass length,
-  // so a query's result does not depend on the other rows of its pass (only
-  // very long prefill chunks, with many query blocks, use longer splits)
-  int n_splits = l_bound <= 2 * kAttnSplit ? 1 : ceil_div(l_bound, kAttnSplit);
-  int split_len = n_splits == 1 ? c->kv_cap : kAttnSplit;
-  if (n_splits * n_qblocks > kAttnRecords) {
-    n_splits = std::max(1, kAttnRecords / n_qblocks);
-    split_len = ceil_div(ceil_div(l_bound, n_splits), 32) * 32;
-  }
+  int split_len = kAttnChunk;
+  while (n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
+  const int n_splits = ceil_div(l_bound, split_len);
   uint16_t* kc_seq = M.kcache + c->kv_seq_stride[w] * seq;
   uint16_t* vc_seq = M.vcache + c->kv_seq_stride[w] * seq;
   for (int l = 0; l < s.n_layers; ++l) {
@@ -583,9 +578,9 @@ pard_status check_seq(pard_ctx* c, int seq, bool need_prefill) {
 }
 
 // Upper bound of the context length used to plan attention for a batch of
-// steps: one class up to two splits' worth, then multiples of 4 splits.
+// steps (one captured step graph per class): multiples of 1024 keys.
 int attn_l_class(int l) {
-  return l <= 2 * kAttnSplit ? 2 * kAttnSplit : ceil_div(l, 4 * kAttnSplit) * 4 * kAttnSplit;
+  return ceil_div(l, 1024) * 1024;
 }
 
 // One fused step: draft pass (pending + K-1 masks) then verify pass, each

@@ -71,9 +71,6 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int nw = blockDim.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wavefront
-  const FwdDesc d = *p.desc;
-  const int row_begin = p.lm_mode ? d.lm_row0 : 0;
-  const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
 
   // wave w streams k-blocks w, w + nw, w + 2*nw, ...: at any time the
   // workgroup reads nw consecutive k-blocks of each strip
@@ -94,6 +91,30 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.W), 0, (int)min((size_t)n_strips * p.kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
   const int w_voff = (tile * S * 64 + lane) * 16;
+
+  // Two register stages of U k-blocks each: loads of stage i+1 are in flight
+  // while stage i feeds the MFMAs.  Iterations past the wave's range are
+  // clamped (cache hits) and their A fragment is zeroed.
+  u32x4 w0[U][S], a0[U][MT], w1[U][S], a1[U][MT];
+  auto load_w = [&](u32x4 (&w)[U][S], int its) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = wave + min(its + u, n_it - 1) * nw;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
+    }
+  };
+
+  // The weight stream does not depend on the pass: its first stage is in
+  // flight before the pass descriptor is read.
+  if (n_it > 0) load_w(w0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  const FwdDesc d = *p.desc;
+  const int row_begin = p.lm_mode ? d.lm_row0 : 0;
+  const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
+
   // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at
   // 8*(lane/16); A is k-blocked, so k-block kb of all rows is one contiguous
   // run at kb * kMaxRows * 64 bytes.  Rows past the pass get an offset beyond
@@ -107,21 +128,47 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     const int r = mt * 16 + (lane & 15);
     a_voff[mt] = r < row_count ? ((row_begin + r) * 32 + (lane >> 4) * 8) * 2 : kOutOfRange;
   }
-
-  // Two register stages of U k-blocks each: loads of stage i+1 are in flight
-  // while stage i feeds the MFMAs.  Iterations past the wave's range are
-  // clamped (cache hits) and their A fragment is zeroed.
-  u32x4 w0[U][S], a0[U][MT], w1[U][S], a1[U][MT];
-  auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int its) {
+  auto load_a = [&](u32x4 (&a)[U][MT], int its) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kb = wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
-      for (int s = 0; s < S; ++s)
-        w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
-#pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (kMaxRows * 64), 0);
+    }
+  };
+  auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int its) {
+    load_w(w, its);
+    load_a(a, its);
+  };
+
+  // thread tid (< 256) of the epilogue owns, for j = s*MT + mt, element
+  // (row, col) below; its epilogue operands are fetched while the weights stream
+  const bool epi = tid < 256;
+  const int ew = tid >> 6;
+  const int rsub = (lane >> 4) * 4 + ew;
+  const int csub = lane & 15;
+  float e0[NJ], e1[NJ];
+  float2 e2[NJ];
+  auto prefetch_epilogue = [&]() {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int s = j / MT, mt = j % MT;
+      const int row = mt * 16 + rsub;
+      const int n = (tile * S + s) * 16 + csub;
+      e0[j] = 0.f;
+      e1[j] = 0.f;
+      e2[j] = float2{1.f, 0.f};
+      if constexpr (EPI == EPI_RESID) {
+        if (epi && row < row_count) {
+          e0[j] = p.x[(size_t)(row_begin + row) * p.ldx + n];
+          e1[j] = p.g_next[n];
+        }
+      } else if constexpr (EPI == EPI_QKV) {
+        if (epi && p.bias) e0[j] = p.bias[n];
+        if (epi && row < row_count && n < p.q_dim + p.kv_dim)
+          e2[j] = p.rope[(size_t)(d.pos0 + row) * (p.hd / 2) + ((n % p.hd) >> 1)];
+      }
     }
   };
   auto compute = [&](const u32x4 (&w)[U][S], const u32x4 (&a)[U][MT], int its) {
@@ -169,12 +216,14 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   // sched_barrier keeps the compiler from sinking the prefetch next to its use
   if (n_it > 0) {
     int its = 0;
-    load(w0, a0, its);
+    load_a(a0, its);
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (EPI != EPI_RESID) row_scales();   // overlaps the first weight loads
+    load(w1, a1, its + U);
+    __builtin_amdgcn_sched_barrier(0);
+    prefetch_epilogue();
+    __builtin_amdgcn_sched_barrier(0);
     while (true) {
-      load(w1, a1, its + U);
-      __builtin_amdgcn_sched_barrier(0);
       compute(w0, a0, its);
       __builtin_amdgcn_sched_barrier(0);
       its += U;
@@ -185,9 +234,12 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       __builtin_amdgcn_sched_barrier(0);
       its += U;
       if (its >= n_it) break;
+      load(w1, a1, its + U);
+      __builtin_amdgcn_sched_barrier(0);
     }
-  } else if constexpr (EPI != EPI_RESID) {
-    row_scales();
+  } else {
+    if constexpr (EPI != EPI_RESID) row_scales();
+    prefetch_epilogue();
   }
 
   // ---- workgroup reduction over the NW input-dimension slices (wave order) ----
@@ -202,7 +254,6 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 
   // the first four wavefronts run the epilogue; all waves stay until the end
   // so that every barrier below is reached by the whole workgroup
-  const bool epi = tid < 256;
   float v[NJ];
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
@@ -212,11 +263,6 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     v[j] = t;
   }
 
-  // thread tid (< 256) holds, for j = s*MT + mt, element (row, col) below
-  const int ew = tid >> 6;
-  const int rsub = (lane >> 4) * 4 + ew;
-  const int csub = lane & 15;
-
   if constexpr (EPI == EPI_QKV) {
     if (!epi) return;   // no barrier follows in this epilogue
     const int pos0 = d.pos0;
@@ -225,22 +271,20 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       const int s = j / MT, mt = j % MT;
       const int row = mt * 16 + rsub;
       const int n = (tile * S + s) * 16 + csub;
-      float y = v[j] * rs_s[row];
-      if (p.bias) y += p.bias[n];
+      float y = v[j] * rs_s[row] + e0[j];            // + bias
       const float partner = __shfl_xor(y, 1);
       if (row < row_count) {
         const int pos = pos0 + row;
         if (n < p.q_dim + p.kv_dim) {
-          const int pp = n % p.hd;
-          const float2 cs = p.rope[(size_t)pos * (p.hd / 2) + (pp >> 1)];
-          y = (pp & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
+          const float2 cs = e2[j];                     // rotary (cos, sin) of (pos, pair)
+          y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
         }
         const uint16_t b = (uint16_t)f2bf_bits(y);
         if (n < p.q_dim) {
           p.out[(size_t)row * p.ld_out + n] = b;
         } else if (n < p.q_dim + p.kv_dim) {
           const int c = n - p.q_dim;
-          p.kc[((size_t)(c / p.hd) * p.cap + pos) * p.hd + (c % p.hd)] = b;
+          p.kc[(size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd)] = b;
         } else {
           const int c = n - p.q_dim - p.kv_dim;
           const size_t blk = (size_t)(c / p.hd) * (p.cap / 32) + (pos >> 5);
@@ -260,9 +304,9 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       const int n = (tile * S + s) * 16 + csub;
       if (row < row_count) {
         const size_t o = (size_t)(row_begin + row) * p.ldx + n;
-        const float xn = p.x[o] + v[j];
+        const float xn = e0[j] + v[j];                 // residual + projection
         p.x[o] = xn;
-        p.xg[act_index(row_begin + row, n)] = (uint16_t)f2bf_bits(xn * p.g_next[n]);
+        p.xg[act_index(row_begin + row, n)] = (uint16_t)f2bf_bits(xn * e1[j]);
         sq[mt] += xn * xn;
       }
     }

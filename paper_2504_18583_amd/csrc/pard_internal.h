@@ -13,7 +13,11 @@
 //     neighbouring lanes; K is cached in that order and attention's q.k is
 //     invariant to it.  Gate/up rows are interleaved by strips (gate strip,
 //     up strip, ...) so one tile holds matching gate and up columns.
-//   * KV cache: K and V bf16 [batch][layer][kv_head][max_ctx][head_dim].
+//   * KV cache, bf16, per [batch][layer][kv_head] a region of cap keys:
+//     K in blocks of 16 keys, each stored as head_dim/32 MFMA A-operand
+//     fragments of 1 KiB (k_index); V in blocks of 32 keys stored transposed
+//     ([dim][key slot], see the attention kernel), so both are read as
+//     contiguous 1 KiB wavefront loads.
 //   * activations that feed a GEMM (x*g, attention output, silu(gate)*up) are
 //     k-blocked bf16: element (row, k) sits at act_index(row, k), i.e. the 64
 //     row slots of one 32-column block are contiguous (64 bytes per row), so
@@ -30,13 +34,19 @@ constexpr int kMaxK = 32;
 constexpr int kMaxRows = 64;      // rows of one forward pass (prefill chunk, 2*max_k)
 constexpr int kMaxLmRows = kMaxK + 1;
 constexpr int kBlock = 256;
-constexpr int kAttnWaves = 8;      // wavefronts per attention workgroup
-constexpr int kAttnSplit = 1024;   // keys per workgroup once a context is split (> 2 splits' worth)
-constexpr int kAttnRecords = 512;  // max (query block, key split) partial records per KV head
+constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
+constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes)
+constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head
 
 // Position of activation element (row, k) in a k-blocked [kMaxRows x K] buffer.
 __host__ __device__ inline size_t act_index(int row, int k) {
   return ((size_t)(k >> 5) * kMaxRows + row) * 32 + (k & 31);
+}
+
+// Position of element (key, dim) in one KV head's K cache region.
+__host__ __device__ inline size_t k_index(int key, int dim, int hd) {
+  return (((size_t)(key >> 4) * (hd >> 5) + (dim >> 5)) * 64 + (key & 15) + 16 * ((dim & 31) >> 3)) * 8 +
+         (dim & 7);
 }
 
 // Rows of the next forward pass of one model.  Written by the host (granular
@@ -115,8 +125,8 @@ struct AttnArgs {
   uint16_t* out;                              // k-blocked (act_index), H_q*hd columns, bf16
   const FwdDesc* desc;
   int n_heads, n_kv;
-  int nqt, n_qblocks;                         // 16*nqt query pairs per block
-  int split_len, n_splits;                    // keys per split (multiple of 32)
+  int nqt, n_qblocks;                         // 16*nqt query pairs per workgroup, query groups
+  int split_len, n_splits;                    // keys per chunk (multiple of 128), chunks
   float scale;
   float* part;                                // split partials when n_splits > 1
 };
@@ -126,5 +136,6 @@ hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStr
 hipError_t launch_tail(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
 size_t attn_part_floats(int head_dim, int nqt);
+int attn_max_q_tiles(int head_dim);
 
 }  // namespace pard

@@ -29,10 +29,53 @@ from paper_2504_18583_amd import bytes_model as bm  # noqa: E402
 
 METRIC = "tokens/sec batch-1 PARD decode, 1B draft/8B target K=8; step HBM GB/s vs peak"
 PEAK_HBM_GBPS = 8000.0
+# measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
+# scaled by a copy of known size); valid only while the kernel source is unchanged
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_swiglu_8b_gateup_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f) for f in ("gemm.hip", "pard_internal.h")]
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_source_sha256() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary, or None when it is missing or the kernel source changed since."""
+    try:
+        kv = {}
+        with open(TRAFFIC_FILE) as fh:
+            for line in fh:
+                if ":" in line and not line.startswith("#"):
+                    k, v = line.split(":", 1)
+                    kv[k.strip()] = v.strip()
+        if kv.get("kernel_source_sha256") != kernel_source_sha256():
+            return None
+        return int(float(kv["traffic_bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+def copy_calibration() -> int:
+    """A device-to-device copy of known size, for scaling rocprofv3 byte counters."""
+    import torch
+    n = 1 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n, "copy_bytes_written": n, "copies": 3}), flush=True)
+    return 0
 
 
 def cpu_baseline(wl, tokens_per_step: float, context: int) -> dict:
@@ -89,7 +132,11 @@ def main() -> int:
     ap.add_argument("--workload", default="llama8b_1b")
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB device copy (byte-counter calibration under rocprofv3)")
     args = ap.parse_args()
+    if args.copy_calibration:
+        return copy_calibration()
     if args.gpus != 1:
         log("bench.py measures one GPU: the decode step of one batch-1 sequence does not shard "
             "(see the design notes); run with --gpus 1")
@@ -160,7 +207,7 @@ def main() -> int:
     gu_bytes = 2 * (2 * f_pad * t_spec.d_model) + (k + 1) * t_spec.d_model * 2 + (k + 1) * f_pad * 2
     achieved = gu_bytes / avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": None,
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(),
                 "kernel": "k_gemm<MT=1,S=2,EPI_SWIGLU> (target gate/up, 8B shape)",
                 "launches": launches, "avg_us": round(avg_s * 1e6, 2),
                 "bytes_per_launch": gu_bytes}

@@ -169,9 +169,10 @@ pard_status pard_read_weight(const pard_ctx *ctx, int32_t which, int32_t tensor,
                              int32_t col0, int32_t n, float *out);
 
 /* Per-kernel timer: HIP events around each launch of one kernel class
- * (class = which * 8 + op, op: 0 embed, 1 qkv, 2 attention, 3 o-proj,
- * 4 gate/up, 5 down, 6 lm_head) on the context's stream, for up to
- * max_launches launches after enabling.  pard_timer_read synchronises the
+ * (class = which * 8 + op, op: 0 embed, 1 qkv, 2 attention (with its chunk
+ * merge), 3 o-proj, 4 gate/up, 5 down, 6 lm_head, 7 argmax reduction and step
+ * tail) on the context's stream, for up to max_launches launches after
+ * enabling.  pard_timer_read synchronises the
  * stream and returns the number of timed launches and their summed duration.
  * kernel_class < 0 disables.  Errors: ARG, DEVICE. */
 pard_status pard_timer_enable(pard_ctx *ctx, int32_t kernel_class, int32_t max_launches);

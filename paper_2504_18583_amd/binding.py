@@ -26,7 +26,7 @@ PARD_OK, PARD_ERR_ARG, PARD_ERR_STATE, PARD_ERR_CAPACITY = 0, -1, -2, -3
 PARD_ERR_NOMEM, PARD_ERR_DEVICE, PARD_ERR_UNSUPPORTED = -4, -5, -6
 PARD_F32, PARD_BF16 = 0, 1
 PARD_TARGET, PARD_DRAFT = 0, 1
-OP_EMBED, OP_QKV, OP_ATTN, OP_O, OP_GATEUP, OP_DOWN, OP_LM = range(7)
+OP_EMBED, OP_QKV, OP_ATTN, OP_O, OP_GATEUP, OP_DOWN, OP_LM, OP_TAIL = range(8)
 
 
 class pard_model_spec(C.Structure):

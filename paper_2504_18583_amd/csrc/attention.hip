@@ -1,18 +1,20 @@
 // Grouped-query causal attention of a short block of query rows against the
-// bf16 KV cache (the draft pass with its mask rows, the verify pass, prefill
-// chunks), on gfx950 MFMA.
+// fp16 KV cache (the draft pass with its mask rows, the verify pass, prefill
+// chunks), on gfx950 MFMA.  Q, K, V, the probabilities and the output are
+// fp16 (10-bit mantissa: bf16 scores drift past the logit tolerance at 8B
+// width).
 //
 // A workgroup serves one KV head, one group of 16*NQ (row, head-in-group)
 // query pairs -- for decode passes every pair of the KV head, so each key is
 // read once per pass -- and one chunk of split_len keys.  Its four wavefronts
 // take the chunk's 32-key tiles round-robin; per tile a wavefront computes
-//   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_bf16, K as A,
+//   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_f16, K as A,
 //                                          Q as B, accumulated over head_dim)
 //   O^T[dim][q] += V^T[dim][key] P^T[key][q]
 // with an online softmax (running max m, sum l, fp32, base 2) in between.  The
 // S^T accumulator of lane l holds keys 4g..4g+3 (and 16+4g..) for query l%16,
 // g = l/16, which is exactly the B-operand fragment P^T needs once packed to
-// bf16; the V cache stores each 32-key block transposed ([dim][key]) with those
+// fp16; the V cache stores each 32-key block transposed ([dim][key]) with those
 // eight keys of group g contiguous, and the K cache stores each 16-key block as
 // ready A fragments, so every K or V fragment is one contiguous 1 KiB
 // wavefront load.  Q fragments are staged once in LDS.
@@ -34,16 +36,23 @@
 namespace pard {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-// two floats to packed bf16, round to nearest even (v_cvt_pk_bf16_f32)
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+// two floats to packed fp16, round to nearest even (v_cvt_pk_f16_f32)
+__device__ __forceinline__ uint32_t pack_f16x2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, f16x2));
+}
+
+// 8 consecutive fp16 outputs as one 16-byte store
+__device__ __forceinline__ void store_f16x8(uint16_t* dst, f32x4 a, f32x4 b) {
+  *reinterpret_cast<u32x4*>(dst) = u32x4{pack_f16x2(a[0], a[1]), pack_f16x2(a[2], a[3]),
+                                         pack_f16x2(b[0], b[1]), pack_f16x2(b[2], b[3])};
 }
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -145,8 +154,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
           s[tt][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks)
-            s[tt][kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                __builtin_bit_cast(bf16x8, kf[tt][kb][ks]), __builtin_bit_cast(bf16x8, q_lds[(t * KS + ks) * 64 + lane]),
+            s[tt][kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                __builtin_bit_cast(f16x8, kf[tt][kb][ks]), __builtin_bit_cast(f16x8, q_lds[(t * KS + ks) * 64 + lane]),
                 s[tt][kb], 0, 0, 0);
         }
       // causal / range mask; only tiles that reach past the context end or the
@@ -189,7 +198,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
             rs += pv[kb * 4 + i];
           }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pf[tt][i] = pack_bf16x2(pv[2 * i], pv[2 * i + 1]);
+        for (int i = 0; i < 4; ++i) pf[tt][i] = pack_f16x2(pv[2 * i], pv[2 * i + 1]);
       }
       rs += __shfl_xor(rs, 16);
       rs += __shfl_xor(rs, 32);
@@ -203,8 +212,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int db = 0; db < DB; ++db)
-          o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, vf[tt][db]),
-                                                             __builtin_bit_cast(bf16x8, pf[tt]), o[t][db], 0, 0, 0);
+          o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, vf[tt][db]),
+                                                             __builtin_bit_cast(f16x8, pf[tt]), o[t][db], 0, 0, 0);
     }
   }
 
@@ -242,7 +251,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
     }
   }
   __syncthreads();
-  // each thread finishes 8 consecutive dims of one pair: one 16-byte bf16
+  // each thread finishes 8 consecutive dims of one pair: one 16-byte fp16
   // store (or two 16-byte fp32 stores of the chunk record)
   for (int e = tid; e < QP * HD / 8; e += 64 * NWA) {
     const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
@@ -257,10 +266,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
       const int qh = qg * QP + q;
       if (qh < n_qh) {
         const int row = qh / group, head = kvh * group + qh % group;
-        const float li = linv_lds[q];
-        const u32x4 v = u32x4{pack_bf16x2(a[0] * li, a[1] * li), pack_bf16x2(a[2] * li, a[3] * li),
-                              pack_bf16x2(b[0] * li, b[1] * li), pack_bf16x2(b[2] * li, b[3] * li)};
-        *reinterpret_cast<u32x4*>(p.out + act_index(row, head * HD + d0)) = v;
+        store_f16x8(p.out + act_index(row, head * HD + d0), a * linv_lds[q], b * linv_lds[q]);
       }
     } else {
       float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * (QP * HD + 2 * QP);
@@ -328,10 +334,7 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
         }
     }
     const int row = qh / group, head = kvh * group + qh % group;
-    const float li = Linv[q];
-    const u32x4 v = u32x4{pack_bf16x2(a[0] * li, a[1] * li), pack_bf16x2(a[2] * li, a[3] * li),
-                          pack_bf16x2(b[0] * li, b[1] * li), pack_bf16x2(b[2] * li, b[3] * li)};
-    *reinterpret_cast<u32x4*>(p.out + act_index(row, head * HD + d0)) = v;
+    store_f16x8(p.out + act_index(row, head * HD + d0), a * Linv[q], b * Linv[q]);
   }
 }
 

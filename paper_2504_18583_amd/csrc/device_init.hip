@@ -164,7 +164,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
     dst[1] = make_float4(v[4], v[5], v[6], v[7]);
     uint32_t o[4];
     for (int i = 0; i < 4; ++i) {
-      o[i] = (uint32_t)f2bf(v[2 * i] * g[k0 + 2 * i]) | ((uint32_t)f2bf(v[2 * i + 1] * g[k0 + 2 * i + 1]) << 16);
+      o[i] = (uint32_t)f16_bits(v[2 * i] * g[k0 + 2 * i]) | ((uint32_t)f16_bits(v[2 * i + 1] * g[k0 + 2 * i + 1]) << 16);
       sq += v[2 * i] * v[2 * i] + v[2 * i + 1] * v[2 * i + 1];
     }
     *reinterpret_cast<uint4*>(xg + act_index(r, k0)) = make_uint4(o[0], o[1], o[2], o[3]);

@@ -97,7 +97,7 @@ struct ModelDev {
   uint16_t *kcache = nullptr, *vcache = nullptr;
   float2* rope = nullptr;
   float* x = nullptr;                 // residual stream, fp32 [kMaxRows][d]
-  uint16_t* xg = nullptr;             // bf16(x * g) of the next normalised GEMM
+  uint16_t* xg = nullptr;             // x * g of the next normalised GEMM (fp16, k-blocked)
   float* ss = nullptr;                // per-tile row sums of squares of x [tiles][kMaxRows]
   int ss_tiles_resid = 1;             // tiles of the residual GEMMs (producers of ss)
   uint16_t *q = nullptr, *attn = nullptr, *h = nullptr;

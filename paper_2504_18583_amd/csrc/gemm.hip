@@ -1,15 +1,16 @@
 // Skinny bf16 GEMM for decode-sized row counts, on gfx950 MFMA.
 //
-//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W block-packed, bf16)
+//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W block-packed bf16, A fp16)
 //
 // Decode streams every weight once per forward (Sec. 2.1: decoding is bound by
 // reloading the weights), so the kernel is organised around the weight
 // stream.  A workgroup owns S strips (16 output columns each) over the whole
 // input dimension; its NW wavefronts split the input dimension, each one
 // streaming its slice of the strips' 1 KiB blocks (one 16-byte load per lane,
-// directly in the v_mfma_f32_16x16x32_bf16 B-operand layout) through a
-// double-buffered register pipeline and accumulating MT 16x16 fp32 tiles.
-// Activation rows (<= 16*MT) are the A operand.
+// directly in the 16x16x32 MFMA B-operand layout) through a double-buffered
+// register pipeline and accumulating MT 16x16 fp32 tiles.  Activation rows
+// (<= 16*MT) are the A operand, in fp16; each weight fragment is widened from
+// bf16 to fp16 in registers and fed to v_mfma_f32_16x16x32_f16.
 //
 // The wavefront partials are summed in LDS in wave order, so results are
 // deterministic; the split depends only on the weight shape, so a row's result
@@ -17,13 +18,14 @@
 // waits for another one.
 //
 // Epilogues fuse the surrounding element-wise work of a Llama block:
-//   EPI_QKV     RMSNorm row scale (A holds x*g in bf16, written by the
+//   EPI_QKV     RMSNorm row scale (A holds x*g in fp16, written by the
 //               producer; 1/rms comes from the producer's per-tile sums of
-//               squares), bias, rotate-half RoPE on Q/K, Q to a bf16 buffer,
-//               K (row-major) and V (key-blocked, transposed) to the cache.
-//   EPI_RESID   x += Y (O-projection, down-projection), plus bf16(x * g_next)
+//               squares), bias, rotate-half RoPE on Q/K, Q to an fp16 buffer,
+//               K (16-key MFMA fragments) and V (32-key blocks, transposed)
+//               to the fp16 cache.
+//   EPI_RESID   x += Y (O-projection, down-projection), plus fp16(x * g_next)
 //               and per-tile row sums of squares for the next normalised GEMM.
-//   EPI_SWIGLU  RMSNorm row scale, h = silu(gate) * up, bf16.
+//   EPI_SWIGLU  RMSNorm row scale, h = silu(gate) * up, fp16.
 //   EPI_LOGITS  final RMSNorm scale, fp32 logits and per-tile (max, argmax).
 // k_lm_tail then reduces the tiles per row (lowest id on ties) and runs the
 // step tail: candidates for a draft pass; greedy prefix acceptance, KV
@@ -35,14 +37,23 @@
 namespace pard {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t f2bf_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;   // round to nearest, ties to even
+// 8 bf16 weights to 8 fp16 values (exact inside fp16's normal range)
+__device__ __forceinline__ f16x8 widen_bf16x8(u32x4 w) {
+  u32x4 r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const f32x2 x = f32x2{__uint_as_float(w[i] << 16), __uint_as_float(w[i] & 0xFFFF0000u)};
+    r[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, f16x2));
+  }
+  return __builtin_bit_cast(f16x8, r);
 }
+
 
 constexpr int kRsrcWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-family raw buffers
 constexpr int kCachePolicyNT = 2;        // non-temporal: weights are streamed once
@@ -126,7 +137,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int r = mt * 16 + (lane & 15);
-    a_voff[mt] = r < row_count ? ((row_begin + r) * 32 + (lane >> 4) * 8) * 2 : kOutOfRange;
+    a_voff[mt] = r < row_count ? (row_begin + r) * 64 + (lane >> 4) * 16 : kOutOfRange;
   }
   auto load_a = [&](u32x4 (&a)[U][MT], int its) {
 #pragma unroll
@@ -175,14 +186,16 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool live = its + u < n_it;
+      f16x8 wf[S];
+#pragma unroll
+      for (int s = 0; s < S; ++s) wf[s] = widen_bf16x8(w[u][s]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const u32x4 av = live ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int s = 0; s < S; ++s)
-          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, av),
-                                                               __builtin_bit_cast(bf16x8, w[u][s]),
-                                                               acc[s][mt], 0, 0, 0);
+          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av), wf[s],
+                                                              acc[s][mt], 0, 0, 0);
       }
     }
   };
@@ -279,7 +292,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
           const float2 cs = e2[j];                     // rotary (cos, sin) of (pos, pair)
           y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
         }
-        const uint16_t b = (uint16_t)f2bf_bits(y);
+        const uint16_t b = f16_bits(y);
         if (n < p.q_dim) {
           p.out[(size_t)row * p.ld_out + n] = b;
         } else if (n < p.q_dim + p.kv_dim) {
@@ -306,7 +319,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         const size_t o = (size_t)(row_begin + row) * p.ldx + n;
         const float xn = e0[j] + v[j];                 // residual + projection
         p.x[o] = xn;
-        p.xg[act_index(row_begin + row, n)] = (uint16_t)f2bf_bits(xn * e1[j]);
+        p.xg[act_index(row_begin + row, n)] = f16_bits(xn * e1[j]);
         sq[mt] += xn * xn;
       }
     }
@@ -330,7 +343,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * (S / 2) + q) * 16 + csub;
-        if (row < row_count) p.out[act_index(row, f)] = (uint16_t)f2bf_bits(h);
+        if (row < row_count) p.out[act_index(row, f)] = f16_bits(h);
       }
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;

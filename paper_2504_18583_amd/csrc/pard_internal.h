@@ -13,16 +13,19 @@
 //     neighbouring lanes; K is cached in that order and attention's q.k is
 //     invariant to it.  Gate/up rows are interleaved by strips (gate strip,
 //     up strip, ...) so one tile holds matching gate and up columns.
-//   * KV cache, bf16, per [batch][layer][kv_head] a region of cap keys:
+//   * KV cache, fp16, per [batch][layer][kv_head] a region of cap keys:
 //     K in blocks of 16 keys, each stored as head_dim/32 MFMA A-operand
 //     fragments of 1 KiB (k_index); V in blocks of 32 keys stored transposed
 //     ([dim][key slot], see the attention kernel), so both are read as
 //     contiguous 1 KiB wavefront loads.
 //   * activations that feed a GEMM (x*g, attention output, silu(gate)*up) are
-//     k-blocked bf16: element (row, k) sits at act_index(row, k), i.e. the 64
-//     row slots of one 32-column block are contiguous (64 bytes per row), so
-//     the MFMA A fragment of one k-block is one contiguous run of rows * 64
-//     bytes instead of one 64-byte piece per row.
+//     fp16 and the GEMMs run fp16 MFMAs, each bf16 weight fragment widened to
+//     fp16 in registers (exact for weights in fp16's normal range): a 10-bit
+//     mantissa on the activation side (bf16 activations drift past the logit
+//     tolerance at 8B width and depth).  They are k-blocked: element (row, k)
+//     sits at act_index(row, k), i.e. the 64 row slots of one 32-column block
+//     are contiguous (64 bytes per row), so the MFMA A fragment of one k-block
+//     is one contiguous run of rows * 64 bytes.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -48,6 +51,9 @@ __host__ __device__ inline size_t k_index(int key, int dim, int hd) {
   return (((size_t)(key >> 4) * (hd >> 5) + (dim >> 5)) * 64 + (key & 15) + 16 * ((dim & 31) >> 3)) * 8 +
          (dim & 7);
 }
+
+// fp16 bits of v, nearest even.
+__device__ inline uint16_t f16_bits(float v) { return __builtin_bit_cast(uint16_t, (_Float16)v); }
 
 // Rows of the next forward pass of one model.  Written by the host (granular
 // calls) or by the tail of the previous pass (fused loop).
@@ -83,7 +89,7 @@ struct GemmArgs {
   const uint16_t* W;      // strip-packed bf16 weight
   int kb_total;           // padded input dim / 32
   int n_tiles;            // output tiles (S strips each) = grid size
-  const uint16_t* A;      // bf16 activations, k-blocked (act_index), lda columns
+  const uint16_t* A;      // fp16 activations, k-blocked (act_index), lda columns
   int lda;
   const FwdDesc* desc;
   int lm_mode;            // 0: rows [0, n_rows)   1: rows [lm_row0, lm_row0 + lm_rows)
@@ -119,10 +125,10 @@ struct TailArgs {
 };
 
 struct AttnArgs {
-  const uint16_t* q; int ldq;                 // [rows][H_q*hd] bf16, pair-interleaved dims
+  const uint16_t* q; int ldq;                 // [rows][H_q*hd] fp16, pair-interleaved dims
   const uint16_t* kc; const uint16_t* vc;     // this layer's cache of one sequence
   int cap;                                    // KV capacity (multiple of 32)
-  uint16_t* out;                              // k-blocked (act_index), H_q*hd columns, bf16
+  uint16_t* out;                              // fp16, k-blocked (act_index), H_q*hd columns
   const FwdDesc* desc;
   int n_heads, n_kv;
   int nqt, n_qblocks;                         // 16*nqt query pairs per workgroup, query groups

@@ -1,0 +1,140 @@
+"""GPU parity at the benchmark shapes.
+
+* Full-width slices: the LLaMA3.1-8B / LLaMA3.2-1B-shaped pair and the
+  Qwen2.5-7B / 0.5B-shaped pair at their full width, heads and vocabulary but
+  with 2 (target) and 1-2 (draft) layers.  Every kernel runs with the grid and
+  tile plan of the full models (they depend on widths, heads, vocabulary and
+  context, not on depth), on the benchmark's prompt; the fp64 oracle runs the
+  same slices in lock-step.
+* Full depth (32 / 16 layers): properties that hold at any size -- the accept
+  rule against the engine's own logits, KV-length bookkeeping, fused loop ==
+  granular calls token for token, bitwise determinism.
+* 16k-token context: the attention chunk/merge path at the long-context
+  workload's length, on a narrow pair the oracle can follow.
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+import oracle
+import pard_inputs as pi
+from gpu_common import lockstep, require_gpu, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def B():
+    require_gpu()
+    from paper_2504_18583_amd import binding
+    return binding
+
+
+def _slice(spec, n_layers):
+    return replace(pi.with_dtype(spec, "bf16"), n_layers=n_layers)
+
+
+def test_llama_8b_1b_full_width_slice_lockstep(B):
+    wl = pi.WORKLOADS["llama8b_1b"]
+    t_spec, d_spec = _slice(wl.target, 2), _slice(wl.draft, 1)
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0]]
+    say(f"[gpu] 8B/1B full-width slice: oracle build (prompt {len(prompt)}, K={wl.k})")
+    target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)
+    say("[gpu] 8B/1B full-width slice: engine load")
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=len(prompt) + 64, max_k=wl.k)
+    try:
+        say("[gpu] 8B/1B full-width slice: lock-step")
+        worst = lockstep(eng, target, draft, prompt, wl.k, steps=2, mask_id=wl.mask_id, tag="8B/1B")
+        say(f"    max |logit err| {worst:.3g}")
+        say("[gpu] 8B/1B full-width slice: fused loop (graph replay) vs granular calls")
+        first = eng.prefill(prompt)
+        toks, stats = eng.generate(wl.k, 20)
+        # granular replay of the same steps
+        eng.prefill(prompt)
+        hist = prompt + [first]
+        out = [first]
+        while len(out) < 20:
+            cands = eng.draft(hist, wl.k)
+            a, bonus = eng.verify(cands)
+            out += cands[:a] + [bonus]
+            hist += cands[:a] + [bonus]
+        assert toks == out[:20]
+    finally:
+        eng.close()
+
+
+QWEN = pi.WORKLOADS["qwen7b_05b"]
+QWEN_T, QWEN_D = _slice(QWEN.target, 2), _slice(QWEN.draft, 2)
+
+
+@pytest.fixture(scope="module")
+def qwen_models(B):
+    say("[gpu] Qwen 7B/0.5B full-width slice: oracle build")
+    return oracle.build_model(QWEN_T), oracle.build_model(QWEN_D)
+
+
+@pytest.mark.parametrize("k", QWEN.k_sweep)
+def test_qwen_7b_05b_full_width_slice_lockstep(B, qwen_models, k):
+    target, draft = qwen_models
+    prompt = [int(x) for x in pi.workload_prompts(QWEN)[0]]
+    say(f"[gpu] Qwen 7B/0.5B full-width slice: engine load, lock-step K={k} (prompt {len(prompt)})")
+    eng = B.Engine(QWEN_T, QWEN_D, QWEN.mask_id, max_ctx=len(prompt) + 64, max_k=max(QWEN.k_sweep))
+    try:
+        worst = lockstep(eng, target, draft, prompt, k, steps=1, mask_id=QWEN.mask_id, tag=f"qwen K={k}")
+        say(f"    max |logit err| {worst:.3g}")
+    finally:
+        eng.close()
+
+
+def test_llama_8b_1b_full_depth_properties(B):
+    wl = pi.WORKLOADS["llama8b_1b"]
+    t_spec, d_spec = pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0]]
+    say("[gpu] 8B/1B full depth: engine load")
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=len(prompt) + 128, max_k=wl.k)
+    try:
+        say("[gpu] 8B/1B full depth: granular steps")
+        first = eng.prefill(prompt)
+        assert eng.kv_len(B.PARD_TARGET) == eng.kv_len(B.PARD_DRAFT) == len(prompt)
+        hist = prompt + [first]
+        out = [first]
+        for step in range(4):
+            lt = eng.kv_len(B.PARD_TARGET)
+            cands = eng.draft(hist, wl.k)
+            dl = eng.read_logits(B.PARD_DRAFT, wl.k)
+            assert np.isfinite(dl).all() and cands == [int(i) for i in np.argmax(dl, axis=-1)]
+            assert eng.kv_len(B.PARD_DRAFT) == len(hist)
+            a, bonus = eng.verify(cands)
+            vl = eng.read_logits(B.PARD_TARGET, wl.k + 1)
+            assert np.isfinite(vl).all()
+            assert (a, bonus) == oracle.accept_prefix(cands, np.argmax(vl, axis=-1)), step
+            assert eng.kv_len(B.PARD_TARGET) == lt + a + 1
+            out += cands[:a] + [bonus]
+            hist += cands[:a] + [bonus]
+        say("[gpu] 8B/1B full depth: fused loop twice")
+        runs = []
+        for _ in range(2):
+            assert eng.prefill(prompt) == first
+            toks, stats = eng.generate(wl.k, len(out))
+            runs.append((toks, eng.read_logits(B.PARD_TARGET, wl.k + 1).copy()))
+        assert runs[0][0] == out
+        assert runs[0][0] == runs[1][0] and np.array_equal(runs[0][1], runs[1][1])
+    finally:
+        eng.close()
+
+
+def test_16k_context_chunked_attention_lockstep(B):
+    wl = pi.WORKLOADS["tiny"]
+    t_spec, d_spec = pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")
+    n = pi.WORKLOADS["llama8b_1b_long"].prompt_len
+    prompt = [int(x) for x in pi.gen_prompt(21, t_spec.vocab, n)]
+    say(f"[gpu] {n}-token context on the narrow pair: oracle build")
+    target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=n + 64, max_k=8)
+    try:
+        say(f"[gpu] {n}-token context: lock-step K=8")
+        worst = lockstep(eng, target, draft, prompt, 8, steps=2, mask_id=wl.mask_id, tag="16k")
+        say(f"    max |logit err| {worst:.3g}")
+    finally:
+        eng.close()

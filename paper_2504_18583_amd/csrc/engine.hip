@@ -368,8 +368,15 @@ hipError_t run_gemm(pard_ctx* c, int cls, int epi, int mt, GemmArgs a, const Gem
   const int S = pick_S(epi, p.n_strips, mt);
   a.kb_total = p.kb_total;
   a.n_tiles = p.n_strips / S;
-  Timed t(c, cls);
-  return launch_gemm(epi, mt, S, plan_nw(p, S, mt), a, c->stream);
+  // a timed GEMM launch carries its events: they take the kernel's own start
+  // and end timestamps, not those of separate marker packets
+  LaunchEvents ev;
+  if (c->timer_class == cls && c->timer_used < c->timer_max) {
+    ev.start = c->timer_ev[2 * c->timer_used];
+    ev.stop = c->timer_ev[2 * c->timer_used + 1];
+    ++c->timer_used;
+  }
+  return launch_gemm(epi, mt, S, plan_nw(p, S, mt), a, c->stream, ev);
 }
 
 struct PassSpec {

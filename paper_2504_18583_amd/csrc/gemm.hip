@@ -32,6 +32,8 @@
 // rollback and next-pass staging for a verify pass.
 #include "pard_internal.h"
 
+#include <hip/hip_ext.h>
+
 #include <climits>
 
 namespace pard {
@@ -482,43 +484,48 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
 }
 
 template <int EPI, int MT, int S>
-hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   const size_t lds = (size_t)nw * S * MT * 256 * sizeof(float);
   if (nw > 8) return hipErrorInvalidValue;
-  k_gemm<MT, S, EPI><<<dim3(a.n_tiles), dim3(64 * nw), lds, st>>>(a);
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_gemm<MT, S, EPI>, dim3(a.n_tiles), dim3(64 * nw), (uint32_t)lds, st, ev.start, ev.stop,
+                          0u, a);
+  } else {
+    k_gemm<MT, S, EPI><<<dim3(a.n_tiles), dim3(64 * nw), lds, st>>>(a);
+  }
   return hipGetLastError();
 }
 
 template <int EPI, int MT>
-hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   switch (S) {
-    case 1: if constexpr (EPI != EPI_SWIGLU) return launch_one<EPI, MT, 1>(nw, a, st); break;
-    case 2: return launch_one<EPI, MT, 2>(nw, a, st);
-    case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st); break;
+    case 1: if constexpr (EPI != EPI_SWIGLU) return launch_one<EPI, MT, 1>(nw, a, st, ev); break;
+    case 2: return launch_one<EPI, MT, 2>(nw, a, st, ev);
+    case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st, ev); break;
   }
   return hipErrorInvalidValue;
 }
 
 template <int EPI>
-hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   switch (mt) {
-    case 1: return launch_s<EPI, 1>(S, nw, a, st);
-    case 2: return launch_s<EPI, 2>(S, nw, a, st);
-    case 3: return launch_s<EPI, 3>(S, nw, a, st);
-    case 4: return launch_s<EPI, 4>(S, nw, a, st);
+    case 1: return launch_s<EPI, 1>(S, nw, a, st, ev);
+    case 2: return launch_s<EPI, 2>(S, nw, a, st, ev);
+    case 3: return launch_s<EPI, 3>(S, nw, a, st, ev);
+    case 4: return launch_s<EPI, 4>(S, nw, a, st, ev);
   }
   return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st) {
+hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   if (nw < 4 || nw > 8 || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
   switch (epi) {
-    case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, nw, a, st);
-    case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, nw, a, st);
-    case EPI_SWIGLU: return launch_mt<EPI_SWIGLU>(mt, S, nw, a, st);
-    case EPI_LOGITS: return launch_mt<EPI_LOGITS>(mt, S, nw, a, st);
+    case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, nw, a, st, ev);
+    case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, nw, a, st, ev);
+    case EPI_SWIGLU: return launch_mt<EPI_SWIGLU>(mt, S, nw, a, st, ev);
+    case EPI_LOGITS: return launch_mt<EPI_LOGITS>(mt, S, nw, a, st, ev);
   }
   return hipErrorInvalidValue;
 }

@@ -137,8 +137,14 @@ struct AttnArgs {
   float* part;                                // split partials when n_splits > 1
 };
 
+// Optional timing events of one launch (recorded at the kernel's start and end).
+struct LaunchEvents {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+
 // Launchers (return hipSuccess or the launch error).
-hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st);
+hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st,
+                       LaunchEvents ev = LaunchEvents{});
 hipError_t launch_tail(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
 size_t attn_part_floats(int head_dim, int nqt);

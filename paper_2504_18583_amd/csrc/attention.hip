@@ -6,8 +6,9 @@
 //
 // A workgroup serves one KV head, one group of 16*NQ (row, head-in-group)
 // query pairs -- for decode passes every pair of the KV head, so each key is
-// read once per pass -- and one chunk of split_len keys.  Its four wavefronts
-// take the chunk's 32-key tiles round-robin; per tile a wavefront computes
+// read once per pass -- and one chunk of split_len keys (256 for decode
+// passes: two 32-key tiles per wavefront).  Its four wavefronts take the
+// chunk's tiles round-robin; per tile a wavefront computes
 //   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_f16, K as A,
 //                                          Q as B, accumulated over head_dim)
 //   O^T[dim][q] += V^T[dim][key] P^T[key][q]
@@ -57,6 +58,30 @@ __device__ __forceinline__ void store_f16x8(uint16_t* dst, f32x4 a, f32x4 b) {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Reductions across lanes l and l^16 / l^32 with the gfx950 lane-swap
+// instructions (VALU, no LDS round trip).  Both lanes of a pair combine the
+// same two operands in the same order.
+__device__ __forceinline__ f32x2 swap16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return f32x2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ f32x2 swap32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return f32x2{__uint_as_float(r[0]), __uint_as_float(r[1])};
+}
+__device__ __forceinline__ float max4g(float x) {    // max over the 4 lane groups (l, l^16, l^32, l^48)
+  f32x2 r = swap16(x);
+  x = fmaxf(r[0], r[1]);
+  r = swap32(x);
+  return fmaxf(r[0], r[1]);
+}
+__device__ __forceinline__ float sum4g(float x) {
+  f32x2 r = swap16(x);
+  x = r[0] + r[1];
+  r = swap32(x);
+  return r[0] + r[1];
+}
+
 template <int HD, int NQ>
 __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   constexpr int NWA = kAttnWaves;
@@ -64,6 +89,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   constexpr int KS = HD / 32;        // 32-dim steps of Q.K
   constexpr int DB = HD / 16;        // 16-dim blocks of the output
   constexpr int OS = HD + 4;         // row stride of the per-wave output tiles in LDS
+  constexpr int REC = QP * HD + 2 * QP;   // floats of one chunk record: o [QP][HD], m [QP], l [QP]
   __shared__ u32x4 q_lds[NQ * KS * 64];   // Q fragments in B-operand lane order
   __shared__ __attribute__((aligned(16))) float o_lds[NWA][QP][OS];
   __shared__ float m_lds[NWA][QP], l_lds[NWA][QP], sc_lds[NWA][QP], linv_lds[QP];
@@ -103,21 +129,28 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
 #pragma unroll
     for (int db = 0; db < DB; ++db) vf[tt][db] = *reinterpret_cast<const u32x4*>(vp + db * 16 * 32);
   };
-  if (n_my > 0) {
-    load(0, 0);
-    load(1, 1);
-  }
 
-  // stage the Q fragments: entry (t, ks, l) = pair t*16 + l%16, dims ks*32 + 8*(l/16) .. +7
-  for (int e = tid; e < NQ * KS * 64; e += 64 * NWA) {
+  // stage the Q fragments: entry (t, ks, l) = pair t*16 + l%16, dims ks*32 + 8*(l/16) .. +7.
+  // Their loads go out before the K/V loads (returns are in order per wavefront).
+  constexpr int QE = (NQ * KS * 64 + 64 * NWA - 1) / (64 * NWA);   // entries per thread
+  u32x4 qv[QE];
+#pragma unroll
+  for (int j = 0; j < QE; ++j) {
+    const int e = tid + j * 64 * NWA;
     const int t = e / (KS * 64), ks = (e / 64) % KS, l = e & 63;
     const int qh = qg * QP + t * 16 + (l & 15);
-    u32x4 v = u32x4{0u, 0u, 0u, 0u};
-    if (qh < n_qh) {
+    qv[j] = u32x4{0u, 0u, 0u, 0u};
+    if (e < NQ * KS * 64 && qh < n_qh) {
       const int row = qh / group, head = kvh * group + qh % group;
-      v = *reinterpret_cast<const u32x4*>(p.q + (size_t)row * p.ldq + head * HD + ks * 32 + (l >> 4) * 8);
+      qv[j] = *reinterpret_cast<const u32x4*>(p.q + (size_t)row * p.ldq + head * HD + ks * 32 + (l >> 4) * 8);
     }
-    q_lds[e] = v;
+  }
+  if (n_my > 0) load(0, 0);
+  if (n_my > 1) load(1, 1);
+#pragma unroll
+  for (int j = 0; j < QE; ++j) {
+    const int e = tid + j * 64 * NWA;
+    if (e < NQ * KS * 64) q_lds[e] = qv[j];
   }
   int qpos[NQ];
 #pragma unroll
@@ -139,54 +172,68 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   const float scale2 = p.scale * kLog2e;   // scores in base 2
 
   for (int it0 = 0; it0 < n_my; it0 += 2) {
+    const int nt = min(2, n_my - it0);     // tiles in this pair (uniform)
     if (it0 > 0) {
       load(0, it0);
-      load(1, it0 + 1);
+      if (nt > 1) load(1, it0 + 1);
     }
-    const int nt = min(2, n_my - it0);     // tiles in this pair (uniform)
+    // scores of every query tile first, then the softmax of all of them, so
+    // the dependent steps of different query tiles overlap
+    f32x4 s[NQ][2][2];
 #pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      f32x4 s[2][2];
+    for (int t = 0; t < NQ; ++t)
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-          s[tt][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          s[t][tt][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+          if (tt == 0 || nt > 1) {             // uniform: the second tile may be absent
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            s[tt][kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-                __builtin_bit_cast(f16x8, kf[tt][kb][ks]), __builtin_bit_cast(f16x8, q_lds[(t * KS + ks) * 64 + lane]),
-                s[tt][kb], 0, 0, 0);
+            for (int ks = 0; ks < KS; ++ks)
+              s[t][tt][kb] = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+                  __builtin_bit_cast(f16x8, kf[tt][kb][ks]), __builtin_bit_cast(f16x8, q_lds[(t * KS + ks) * 64 + lane]),
+                  s[t][tt][kb], 0, 0, 0);
+          }
         }
-      // causal / range mask; only tiles that reach past the context end or the
-      // first query's position need it
+    // causal / range mask; only tiles that reach past the context end or the
+    // first query's position need it
 #pragma unroll
-      for (int tt = 0; tt < 2; ++tt) {
-        const int key0 = k_begin + (wave + NWA * (it0 + tt)) * 32;
-        if (tt >= nt || key0 + 31 >= k_end || key0 + 31 > d.pos0) {
+    for (int tt = 0; tt < 2; ++tt) {
+      const int key0 = k_begin + (wave + NWA * (it0 + tt)) * 32;
+      if (tt >= nt || key0 + 31 >= k_end || key0 + 31 > d.pos0) {
+#pragma unroll
+        for (int t = 0; t < NQ; ++t)
 #pragma unroll
           for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int key = key0 + kb * 16 + g4 * 4 + i;
-              if (tt >= nt || key >= k_end || key > qpos[t]) s[tt][kb][i] = -INFINITY;
+              if (tt >= nt || key >= k_end || key > qpos[t]) s[t][tt][kb][i] = -INFINITY;
             }
-        }
       }
-      float mx = -INFINITY;
+    }
+    float mx[NQ];
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      mx[t] = -INFINITY;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) mx = fmaxf(mx, s[tt][kb][i]);
-      mx = fmaxf(mx, __shfl_xor(mx, 16));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float m_new = fmaxf(m[t], mx * scale2);
+          for (int i = 0; i < 4; ++i) mx[t] = fmaxf(mx[t], s[t][tt][kb][i]);
+    }
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) mx[t] = max4g(mx[t]);
+    float corr[NQ], rs[NQ];
+    u32x4 pf[NQ][2];
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+      const float m_new = fmaxf(m[t], mx[t] * scale2);
       const float m_use = m_new == -INFINITY ? 0.f : m_new;   // keeps 2^(-inf - m) = 0 well defined
-      const float corr = __builtin_amdgcn_exp2f(m[t] - m_use);
-      float rs = 0.f;
-      u32x4 pf[2];
+      corr[t] = __builtin_amdgcn_exp2f(m[t] - m_use);
+      m[t] = m_new;
+      rs[t] = 0.f;
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt) {
         float pv[8];
@@ -194,26 +241,29 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            pv[kb * 4 + i] = __builtin_amdgcn_exp2f(fmaf(s[tt][kb][i], scale2, -m_use));
-            rs += pv[kb * 4 + i];
+            pv[kb * 4 + i] = __builtin_amdgcn_exp2f(fmaf(s[t][tt][kb][i], scale2, -m_use));
+            rs[t] += pv[kb * 4 + i];
           }
 #pragma unroll
-        for (int i = 0; i < 4; ++i) pf[tt][i] = pack_f16x2(pv[2 * i], pv[2 * i + 1]);
+        for (int i = 0; i < 4; ++i) pf[t][tt][i] = pack_f16x2(pv[2 * i], pv[2 * i + 1]);
       }
-      rs += __shfl_xor(rs, 16);
-      rs += __shfl_xor(rs, 32);
-      l[t] = l[t] * corr + rs;
-      m[t] = m_new;
+    }
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) l[t] = l[t] * corr[t] + sum4g(rs[t]);
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
       if (it0 > 0) {                       // uniform; o is still zero for the first pair
 #pragma unroll
-        for (int db = 0; db < DB; ++db) o[t][db] *= corr;
+        for (int db = 0; db < DB; ++db) o[t][db] *= corr[t];
       }
 #pragma unroll
       for (int tt = 0; tt < 2; ++tt)
+        if (tt == 0 || nt > 1) {
 #pragma unroll
-        for (int db = 0; db < DB; ++db)
-          o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, vf[tt][db]),
-                                                             __builtin_bit_cast(f16x8, pf[tt]), o[t][db], 0, 0, 0);
+          for (int db = 0; db < DB; ++db)
+            o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, vf[tt][db]),
+                                                               __builtin_bit_cast(f16x8, pf[t][tt]), o[t][db], 0, 0, 0);
+        }
     }
   }
 
@@ -232,6 +282,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
     for (int db = 0; db < DB; ++db)
       *reinterpret_cast<f32x4*>(&o_lds[wave][t * 16 + c16][db * 16 + g4 * 4]) = o[t][db];
   __syncthreads();
+  float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * REC;   // this chunk's record
   if (tid < QP) {
     float M = m_lds[0][tid];
     for (int w = 1; w < NWA; ++w) M = fmaxf(M, m_lds[w][tid]);
@@ -243,9 +294,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
       L += l_lds[w][tid] * sc;
     }
     if (p.n_splits == 1) {
-      linv_lds[tid] = 1.0f / L;            // same arithmetic as k_attn_merge with one chunk
+      linv_lds[tid] = 1.0f / L;            // same arithmetic as the chunk merge with one chunk
     } else {
-      float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * (QP * HD + 2 * QP);
       rec[QP * HD + tid] = M;
       rec[QP * HD + QP + tid] = L;
     }
@@ -269,7 +319,6 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
         store_f16x8(p.out + act_index(row, head * HD + d0), a * linv_lds[q], b * linv_lds[q]);
       }
     } else {
-      float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * (QP * HD + 2 * QP);
       *reinterpret_cast<f32x4*>(rec + q * HD + d0) = a;
       *reinterpret_cast<f32x4*>(rec + q * HD + d0 + 4) = b;
     }

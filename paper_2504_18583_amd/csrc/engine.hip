@@ -60,6 +60,9 @@ struct GemmPlan {
 
 int pick_S(int epi, int n_strips, int mt) {
   int s = 1;
+  // two strips share one activation stream once that still leaves >= 192
+  // workgroups (measured faster for the 8B QKV shape: 384 strips)
+  if ((epi == EPI_QKV || epi == EPI_RESID) && n_strips >= 384) s = 2;
   if (epi == EPI_SWIGLU) s = 2;
   if (epi == EPI_LOGITS) s = (mt == 1) ? 4 : 2;
   while (s > 1 && n_strips % s) s >>= 1;

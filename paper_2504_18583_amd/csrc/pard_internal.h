@@ -38,7 +38,7 @@ constexpr int kMaxRows = 64;      // rows of one forward pass (prefill chunk, 2*
 constexpr int kMaxLmRows = kMaxK + 1;
 constexpr int kBlock = 256;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
-constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes)
+constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
 constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head
 
 // Position of activation element (row, k) in a k-blocked [kMaxRows x K] buffer.
@@ -134,7 +134,7 @@ struct AttnArgs {
   int nqt, n_qblocks;                         // 16*nqt query pairs per workgroup, query groups
   int split_len, n_splits;                    // keys per chunk (multiple of 128), chunks
   float scale;
-  float* part;                                // split partials when n_splits > 1
+  float* part;                                // chunk records when n_splits > 1
 };
 
 // Optional timing events of one launch (recorded at the kernel's start and end).

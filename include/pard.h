@@ -53,7 +53,10 @@ enum { PARD_TARGET = 0, PARD_DRAFT = 1 };
 
 /* Shape and initialisation of one Llama-family decoder (Sec. 4.1 names
  * LLaMA3 and Qwen2.5 members).  Weights are drawn N(0, init_std^2) with the
- * counter-based generator below and stored in bf16; RMSNorm gains are 1.
+ * counter-based generator below and rounded to bf16; RMSNorm gains are 1.
+ * The device keeps each bf16 weight in fp16 encoding for its fp16 matrix
+ * cores (the same value when |w| >= 2^-14; smaller weights round to fp16
+ * subnormals, within 2^-25).  Q/K/V biases stay fp32 holding the bf16 value.
  * Constraints: d_model % 32 == 0, head_dim in {64, 128},
  * n_heads % n_kv_heads == 0, vocab % 16 == 0, dtype == PARD_BF16.
  *
@@ -163,8 +166,9 @@ pard_status pard_read_logits(const pard_ctx *ctx, int32_t which, int32_t seq, fl
 
 /* Read n consecutive canonical weight elements [row, col0 .. col0+n) of one
  * tensor (ordinal as in the generator comment; layer tensors use their layer's
- * ordinal) of model `which`, as float.  Debug/parity of the generator and the
- * on-device weight layout.  Errors: ARG, DEVICE. */
+ * ordinal) of model `which`, as float: the value the device stores (the bf16
+ * weight in fp16 encoding).  Debug/parity of the generator and the on-device
+ * weight layout.  Errors: ARG, DEVICE. */
 pard_status pard_read_weight(const pard_ctx *ctx, int32_t which, int32_t tensor, int32_t row,
                              int32_t col0, int32_t n, float *out);
 

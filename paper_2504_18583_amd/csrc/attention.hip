@@ -344,11 +344,25 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
   const int n_act = min(p.n_splits, (L_end + p.split_len - 1) / p.split_len);
   const float* base = p.part + (size_t)(kvh * p.n_qblocks + qg) * p.n_splits * REC;
   if (tid < QP) {
+    // the (m, l) of up to 8 chunks are requested together
+    float mv[8], lv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int sx = min(u, n_act - 1);
+      mv[u] = base[(size_t)sx * REC + QP * HD + tid];
+      lv[u] = base[(size_t)sx * REC + QP * HD + QP + tid];
+    }
     float M = -INFINITY;
-    for (int s = 0; s < n_act; ++s) M = fmaxf(M, base[(size_t)s * REC + QP * HD + tid]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n_act) M = fmaxf(M, mv[u]);
+    for (int s = 8; s < n_act; ++s) M = fmaxf(M, base[(size_t)s * REC + QP * HD + tid]);
     const float M_use = M == -INFINITY ? 0.f : M;
     float L = 0.f;
-    for (int s = 0; s < n_act; ++s)
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n_act) L += lv[u] * __builtin_amdgcn_exp2f(mv[u] - M_use);
+    for (int s = 8; s < n_act; ++s)
       L += base[(size_t)s * REC + QP * HD + QP + tid] *
            __builtin_amdgcn_exp2f(base[(size_t)s * REC + QP * HD + tid] - M_use);
     Ms[tid] = M_use;

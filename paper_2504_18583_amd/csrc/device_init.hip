@@ -1,5 +1,6 @@
 // Load-time kernels: seeded weight generation straight into the strip-packed
-// layout, rotary tables, fills; and the per-pass embedding gather.
+// layout (each bf16 weight kept in fp16 encoding), rotary tables, fills; and
+// the per-pass embedding gather.
 #include "device_init.h"
 
 namespace pard {
@@ -31,8 +32,15 @@ __device__ __forceinline__ void normal_pair(uint64_t key, uint64_t j, double* n0
   *n1 = r * sin(th);
 }
 
+// bf16 value of the weight (the model's parameter)
 __device__ __forceinline__ uint16_t weight_bits(double n, double stdv) {
   return f2bf((float)(n * stdv));
+}
+
+// The same value in the fp16 encoding the GEMMs read (exact when |w| >= 2^-14;
+// smaller weights round to the nearest fp16 subnormal, within 2^-25).
+__device__ __forceinline__ uint16_t weight_f16(double n, double stdv) {
+  return f16_bits(__uint_as_float((uint32_t)weight_bits(n, stdv) << 16));
 }
 
 // Canonical (tensor, row) of packed row `n`; false for padding rows.
@@ -90,8 +98,8 @@ __global__ void k_gen_packed(const GenArgs a) {
         const uint64_t idx = (uint64_t)row * a.cols + k;   // even: cols is even
         double n0, n1;
         normal_pair(key, idx >> 1, &n0, &n1);
-        out[e] = weight_bits(n0, a.stdv);
-        out[e + 1] = weight_bits(n1, a.stdv);
+        out[e] = weight_f16(n0, a.stdv);
+        out[e + 1] = weight_f16(n1, a.stdv);
       }
     }
     uint4 v;
@@ -156,8 +164,8 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
     const uint32_t wv[4] = {w.x, w.y, w.z, w.w};
     float v[8];
     for (int i = 0; i < 4; ++i) {
-      v[2 * i] = __uint_as_float(wv[i] << 16);
-      v[2 * i + 1] = __uint_as_float(wv[i] & 0xFFFF0000u);
+      v[2 * i] = (float)__builtin_bit_cast(_Float16, (uint16_t)(wv[i] & 0xFFFFu));
+      v[2 * i + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(wv[i] >> 16));
     }
     float4* dst = reinterpret_cast<float4*>(x + (size_t)r * d + k0);
     dst[0] = make_float4(v[0], v[1], v[2], v[3]);
@@ -177,7 +185,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
 
 __global__ void k_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) out[i] = __uint_as_float((uint32_t)src[idx[i]] << 16);
+  if (i < n) out[i] = (float)__builtin_bit_cast(_Float16, src[idx[i]]);
 }
 
 int blocks_for(size_t n, int per_block) {

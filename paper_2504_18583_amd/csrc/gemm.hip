@@ -1,6 +1,6 @@
 // Skinny bf16 GEMM for decode-sized row counts, on gfx950 MFMA.
 //
-//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W block-packed bf16, A fp16)
+//   Y[r, n] = sum_k A[r, k] * W[n, k]            (W block-packed, A fp16)
 //
 // Decode streams every weight once per forward (Sec. 2.1: decoding is bound by
 // reloading the weights), so the kernel is organised around the weight
@@ -9,8 +9,8 @@
 // streaming its slice of the strips' 1 KiB blocks (one 16-byte load per lane,
 // directly in the 16x16x32 MFMA B-operand layout) through a double-buffered
 // register pipeline and accumulating MT 16x16 fp32 tiles.  Activation rows
-// (<= 16*MT) are the A operand, in fp16; each weight fragment is widened from
-// bf16 to fp16 in registers and fed to v_mfma_f32_16x16x32_f16.
+// (<= 16*MT) are the A operand, in fp16; the weights (bf16 values kept in fp16
+// encoding) feed v_mfma_f32_16x16x32_f16 directly.
 //
 // The wavefront partials are summed in LDS in wave order, so results are
 // deterministic; the split depends only on the weight shape, so a row's result
@@ -40,25 +40,23 @@ namespace pard {
 namespace {
 
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-// 8 bf16 weights to 8 fp16 values (exact inside fp16's normal range)
-__device__ __forceinline__ f16x8 widen_bf16x8(u32x4 w) {
-  u32x4 r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const f32x2 x = f32x2{__uint_as_float(w[i] << 16), __uint_as_float(w[i] & 0xFFFF0000u)};
-    r[i] = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, f16x2));
-  }
-  return __builtin_bit_cast(f16x8, r);
-}
 
 
 constexpr int kRsrcWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-family raw buffers
 constexpr int kCachePolicyNT = 2;        // non-temporal: weights are streamed once
+
+// Sum over the 16 lanes of a DPP row (lanes 16g .. 16g+15), fixed order:
+// quad_perm swaps (1 0 3 2), (2 3 0 1), then half-row and row mirrors.
+__device__ __forceinline__ float sum16(float x) {
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xF, 0xF, false));
+  x += __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xF, 0xF, false));
+  return x;
+}
 
 __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
@@ -188,16 +186,13 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool live = its + u < n_it;
-      f16x8 wf[S];
-#pragma unroll
-      for (int s = 0; s < S; ++s) wf[s] = widen_bf16x8(w[u][s]);
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const u32x4 av = live ? a[u][mt] : u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
         for (int s = 0; s < S; ++s)
-          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av), wf[s],
-                                                              acc[s][mt], 0, 0, 0);
+          acc[s][mt] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av),
+                                                              __builtin_bit_cast(f16x8, w[u][s]), acc[s][mt], 0, 0, 0);
       }
     }
   };
@@ -327,11 +322,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      float t = sq[mt];
-      t += __shfl_xor(t, 1);
-      t += __shfl_xor(t, 2);
-      t += __shfl_xor(t, 4);
-      t += __shfl_xor(t, 8);
+      const float t = sum16(sq[mt]);
       if (csub == 0) p.ss_out[(size_t)tile * kMaxRows + mt * 16 + rsub] = t;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {

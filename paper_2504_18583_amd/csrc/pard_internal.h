@@ -1,7 +1,10 @@
 // Internal structures shared by the engine (host) and the HIP kernels.
 //
 // Device data layout (all carved from the caller's arena):
-//   * every weight matrix W [out, in] is stored bf16 in 1 KiB blocks of 16
+//   * every weight matrix W [out, in] holds the model's bf16 values in fp16
+//     encoding (exact for |w| >= 2^-14, smaller ones round to fp16
+//     subnormals within 2^-25), so the fp16 MFMAs read it directly.  It is
+//     stored in 1 KiB blocks of 16
 //     output rows ("strip") x 32 input columns ("k-block"), each laid out in
 //     the lane order of the v_mfma_f32_16x16x32_bf16 B operand (lane l holds
 //     row l%16, columns 8*(l/16) .. +7).  Blocks are k-block-major: block
@@ -19,10 +22,9 @@
 //     ([dim][key slot], see the attention kernel), so both are read as
 //     contiguous 1 KiB wavefront loads.
 //   * activations that feed a GEMM (x*g, attention output, silu(gate)*up) are
-//     fp16 and the GEMMs run fp16 MFMAs, each bf16 weight fragment widened to
-//     fp16 in registers (exact for weights in fp16's normal range): a 10-bit
-//     mantissa on the activation side (bf16 activations drift past the logit
-//     tolerance at 8B width and depth).  They are k-blocked: element (row, k)
+//     fp16 and the GEMMs run fp16 MFMAs: a 10-bit mantissa on the activation
+//     side (bf16 activations drift past the logit tolerance at 8B width and
+//     depth).  They are k-blocked: element (row, k)
 //     sits at act_index(row, k), i.e. the 64 row slots of one 32-column block
 //     are contiguous (64 bytes per row), so the MFMA A fragment of one k-block
 //     is one contiguous run of rows * 64 bytes.

@@ -47,37 +47,48 @@ def assert_tokens_match(gpu_tokens, ref_logits: np.ndarray, what: str) -> None:
             assert int(g) == int(r), f"{what}: row {i} gpu {g} oracle {r} (margin {m[i]:.3f})"
 
 
-def lockstep(eng, target, draft, prompt, k, steps, mask_id, seq=0, tag=""):
-    """Run `steps` PARD steps on the GPU and the oracle with identical inputs.
+class Lockstep:
+    """One sequence slot run on the GPU and the oracle side by side.
 
-    Returns the max logit error seen.  The oracle is re-synchronised to the
-    GPU's decisions, which may differ from its own only at near-ties."""
-    from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
-    worst = 0.0
-    first = eng.prefill(prompt, seq=seq)
-    cache_t, cache_d, first_o, lg = oracle.prefill(target, draft, prompt)
-    worst = max(worst, assert_logits_close(eng.read_logits(PARD_TARGET, 1, seq=seq), lg,
-                                           f"{tag} prefill logits"))
-    assert_tokens_match([first], lg, f"{tag} first token")
-    if first != first_o:                       # near-tie: follow the GPU
-        pass
-    hist = list(prompt) + [first]
-    pending = [first]
-    for step in range(steps):
+    The oracle is re-synchronised to the GPU's decisions, which may differ from
+    its own only at near-ties.  `worst` is the largest logit error seen."""
+
+    def __init__(self, eng, target, draft, prompt, k, mask_id, seq=0, tag=""):
+        self.eng, self.target, self.draft = eng, target, draft
+        self.prompt, self.k, self.mask_id, self.seq, self.tag = list(prompt), k, mask_id, seq, tag
+        self.worst = 0.0
+        self.step_no = 0
+
+    def prefill(self):
+        from paper_2504_18583_amd.binding import PARD_TARGET
+        eng, seq, tag = self.eng, self.seq, self.tag
+        first = eng.prefill(self.prompt, seq=seq)
+        self.cache_t, self.cache_d, _, lg = oracle.prefill(self.target, self.draft, self.prompt)
+        self.worst = max(self.worst, assert_logits_close(eng.read_logits(PARD_TARGET, 1, seq=seq), lg,
+                                                         f"{tag} prefill logits"))
+        assert_tokens_match([first], lg, f"{tag} first token")
+        self.hist = list(self.prompt) + [first]
+        self.pending = [first]
+        return first
+
+    def step(self):
+        from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
+        eng, seq, tag, k, step = self.eng, self.seq, self.tag, self.k, self.step_no
         if k > 0:
-            cands = eng.draft(hist, k, seq=seq)
+            cands = eng.draft(self.hist, k, seq=seq)
             g_dl = eng.read_logits(PARD_DRAFT, k, seq=seq)
-            _, o_dl = oracle.draft_step(draft, cache_d, pending, k, mask_id)
-            worst = max(worst, assert_logits_close(g_dl, o_dl, f"{tag} step {step} draft logits"))
+            _, o_dl = oracle.draft_step(self.draft, self.cache_d, self.pending, k, self.mask_id)
+            self.worst = max(self.worst, assert_logits_close(g_dl, o_dl, f"{tag} step {step} draft logits"))
             assert_tokens_match(cands, o_dl, f"{tag} step {step} candidates")
-            assert eng.kv_len(PARD_DRAFT, seq=seq) == cache_d.length == len(hist)
+            assert eng.kv_len(PARD_DRAFT, seq=seq) == self.cache_d.length == len(self.hist)
         else:
             cands = []
+        cache_t = self.cache_t
         lt = cache_t.length
         a, bonus = eng.verify(cands, seq=seq)
         g_vl = eng.read_logits(PARD_TARGET, k + 1, seq=seq)
-        o_a, o_bonus, o_t, o_vl = oracle.verify_step(target, cache_t, pending[-1], cands)
-        worst = max(worst, assert_logits_close(g_vl, o_vl, f"{tag} step {step} verify logits"))
+        o_a, o_bonus, o_t, o_vl = oracle.verify_step(self.target, cache_t, self.pending[-1], cands)
+        self.worst = max(self.worst, assert_logits_close(g_vl, o_vl, f"{tag} step {step} verify logits"))
         # the GPU's decision is consistent with its own argmax ...
         g_t = np.argmax(g_vl, axis=-1)
         assert (a, bonus) == oracle.accept_prefix(cands, g_t), f"{tag} step {step} accept rule"
@@ -87,8 +98,20 @@ def lockstep(eng, target, draft, prompt, k, steps, mask_id, seq=0, tag=""):
             assert (a, bonus) == (o_a, o_bonus), f"{tag} step {step}: gpu {(a, bonus)} oracle {(o_a, o_bonus)}"
         if a != o_a:
             cache_t.truncate(lt)
-            oracle.forward_cached(target, cache_t, [pending[-1]] + list(cands[:a]), logits_rows=[])
+            oracle.forward_cached(self.target, cache_t, [self.pending[-1]] + list(cands[:a]), logits_rows=[])
         assert eng.kv_len(PARD_TARGET, seq=seq) == cache_t.length == lt + a + 1
-        pending = list(cands[:a]) + [bonus]
-        hist += pending
-    return worst
+        self.pending = list(cands[:a]) + [bonus]
+        self.hist += self.pending
+        self.step_no += 1
+        return a, bonus
+
+
+def lockstep(eng, target, draft, prompt, k, steps, mask_id, seq=0, tag=""):
+    """Run `steps` PARD steps on the GPU and the oracle with identical inputs.
+
+    Returns the max logit error seen."""
+    ls = Lockstep(eng, target, draft, prompt, k, mask_id, seq=seq, tag=tag)
+    ls.prefill()
+    for _ in range(steps):
+        ls.step()
+    return ls.worst

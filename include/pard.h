@@ -144,23 +144,32 @@ pard_status pard_kv_truncate(pard_ctx *ctx, int32_t seq, int32_t which, int32_t 
 /* Current committed KV length of `which` for slot `seq`. */
 pard_status pard_kv_len(const pard_ctx *ctx, int32_t seq, int32_t which, int32_t *len);
 
-/* Fused device-resident loop for slot seqs[0] (n_seq must be 1 in this build):
- * repeated draft (one pass) -> verify -> accept steps with no host round trip
- * per step.  out_tokens[0] is the current pending token; every step appends
- * its accepted candidates and bonus; exactly n_tokens tokens are written
- * (surplus tokens of the last step are dropped).  max_steps > 0 caps the
- * number of steps (then fewer tokens may be written; stats->tokens says how
- * many).  K = 0 runs plain greedy target steps.  stats may be NULL.
- * Errors: ARG, STATE, CAPACITY (the KV would exceed max_ctx), UNSUPPORTED
- * (n_seq != 1), DEVICE. */
+/* Fused device-resident loop (Sec. 2.2: draft stage, verification stage) over
+ * the n_seq slots seqs[0..n_seq) (distinct, prefilled): repeated draft (one
+ * pass) -> verify -> accept steps with no host round trip per step.  With
+ * n_seq > 1 every pass holds all unfinished slots' rows (per slot: its a+1
+ * pending tokens and K-1 mask rows in the draft pass, K+1 rows in the verify
+ * pass), each slot with its own positions, acceptance and KV rollback; a slot
+ * that has its n_tokens leaves the batch.  Limits: n_seq <= min(max_batch,
+ * 64); for n_seq > 1, n_seq*2K <= 512 and n_seq*(K+1) <= 512.
+ * out_tokens is [n_seq][n_tokens] row-major: row i starts with slot seqs[i]'s
+ * current pending token, then every step appends its accepted candidates and
+ * bonus; exactly n_tokens tokens are written per slot (surplus tokens of the
+ * last step are dropped).  max_steps > 0 caps the number of steps (then fewer
+ * tokens may be written; stats->tokens is the total over the slots).  K = 0
+ * runs plain greedy target steps.  stats may be NULL.
+ * Errors: ARG (bad pointer, repeated slot), STATE (slot not prefilled),
+ * CAPACITY (the KV would exceed max_ctx, too many slots or rows), DEVICE. */
 pard_status pard_generate(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, int32_t K,
                           int32_t n_tokens, int32_t max_steps, int32_t *out_tokens,
                           pard_stats *stats);
 
-/* Copy the fp32 logits of the last lm_head pass of `which` (rows x vocab,
- * row-major; draft rows are the K candidate rows, target rows the verify
- * rows, prefill the single last-prompt row).  rows must not exceed the rows of
- * that pass.  Parity/debug.  Errors: ARG, STATE, DEVICE. */
+/* Copy the fp32 logits of slot `seq`'s rows in the last lm_head pass of
+ * `which` that included the slot (rows x vocab, row-major; draft rows are the
+ * K candidate rows, target rows the verify rows, prefill the single
+ * last-prompt row).  rows must not exceed that slot's rows.  A slot that left
+ * a batched pard_generate has none until its next pass.  Parity/debug.
+ * Errors: ARG, STATE, DEVICE. */
 pard_status pard_read_logits(const pard_ctx *ctx, int32_t which, int32_t seq, float *out,
                              int32_t rows, int32_t vocab);
 

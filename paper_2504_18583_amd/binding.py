@@ -187,6 +187,21 @@ class Engine:
                                       out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate")
         return out[:stats.tokens].tolist(), stats
 
+    def generate_batch(self, seqs: Sequence[int], k: int, n_tokens: int, max_steps: int = 0):
+        """Fused loop over several slots at once (batched passes).  Returns one
+        token list per slot (the pending token first) and the summed stats."""
+        before = [self.kv_len(PARD_TARGET, seq=s) for s in seqs]
+        out = np.zeros((len(seqs), n_tokens), np.int32)
+        stats = pard_stats()
+        arr, sptr = _i32(list(seqs))
+        self._check(lib.pard_generate(self.ctx, len(seqs), sptr, k, n_tokens, max_steps,
+                                      out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate")
+        res = []
+        for i, s in enumerate(seqs):
+            n = min(n_tokens, 1 + self.kv_len(PARD_TARGET, seq=s) - before[i])
+            res.append(out[i, :n].tolist())
+        return res, stats
+
     def read_logits(self, which: int, rows: int, seq: int = 0) -> np.ndarray:
         out = np.zeros((rows, self.vocab), np.float32)
         self._check(lib.pard_read_logits(self.ctx, which, seq,

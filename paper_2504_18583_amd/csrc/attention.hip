@@ -4,10 +4,10 @@
 // fp16 (10-bit mantissa: bf16 scores drift past the logit tolerance at 8B
 // width).
 //
-// A workgroup serves one KV head, one group of 16*NQ (row, head-in-group)
-// query pairs -- for decode passes every pair of the KV head, so each key is
-// read once per pass -- and one chunk of split_len keys (256 for decode
-// passes: two 32-key tiles per wavefront).  Its four wavefronts take the
+// A workgroup serves one sequence of the pass, one KV head, one group of 16*NQ
+// (row, head-in-group) query pairs -- for decode passes every pair of the KV
+// head, so each key is read once per pass -- and one chunk of split_len keys
+// (256 for decode passes: two 32-key tiles per wavefront).  Its four wavefronts take the
 // chunk's tiles round-robin; per tile a wavefront computes
 //   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_f16, K as A,
 //                                          Q as B, accumulated over head_dim)
@@ -94,14 +94,16 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   __shared__ __attribute__((aligned(16))) float o_lds[NWA][QP][OS];
   __shared__ float m_lds[NWA][QP], l_lds[NWA][QP], sc_lds[NWA][QP], linv_lds[QP];
 
-  const int kvh = blockIdx.x, qg = blockIdx.y, ch = blockIdx.z;
+  const int kvh = blockIdx.x, qg = blockIdx.y;
+  const int sj = blockIdx.z / p.n_splits, ch = blockIdx.z % p.n_splits;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int group = p.n_heads / p.n_kv;
-  const FwdDesc d = *p.desc;
+  if (sj >= p.desc->n_seq) return;                 // uniform: the whole block leaves
+  const PassSeq d = p.desc->seq[sj];
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
-  if (qg * QP >= n_qh) return;                     // uniform: the whole block leaves
+  if (qg * QP >= n_qh) return;                     // uniform
   const int k_begin = ch * p.split_len;            // multiple of 128
   if (k_begin >= L_end) return;                    // uniform: chunk beyond the context
   const int k_end = min(L_end, k_begin + p.split_len);
@@ -111,8 +113,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   const int n_t = (k_end - k_begin + 31) / 32;
   const int n_my = (n_t - wave + NWA - 1) / NWA;
 
-  const uint16_t* kbase = p.kc + (size_t)kvh * p.cap * HD;
-  const uint16_t* vbase = p.vc + (size_t)kvh * p.cap * HD;
+  const size_t cache = (size_t)d.slot * p.kv_seq_stride + (size_t)kvh * p.cap * HD;
+  const uint16_t* kbase = p.kc + cache;
+  const uint16_t* vbase = p.vc + cache;
   const int g4 = lane >> 4, c16 = lane & 15;
 
   // K and V fragments of two tiles (a pair of tiles shares one softmax max)
@@ -142,7 +145,8 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
     qv[j] = u32x4{0u, 0u, 0u, 0u};
     if (e < NQ * KS * 64 && qh < n_qh) {
       const int row = qh / group, head = kvh * group + qh % group;
-      qv[j] = *reinterpret_cast<const u32x4*>(p.q + (size_t)row * p.ldq + head * HD + ks * 32 + (l >> 4) * 8);
+      qv[j] = *reinterpret_cast<const u32x4*>(p.q + (size_t)(d.row0 + row) * p.ldq + head * HD + ks * 32 +
+                                              (l >> 4) * 8);
     }
   }
   if (n_my > 0) load(0, 0);
@@ -282,7 +286,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
     for (int db = 0; db < DB; ++db)
       *reinterpret_cast<f32x4*>(&o_lds[wave][t * 16 + c16][db * 16 + g4 * 4]) = o[t][db];
   __syncthreads();
-  float* rec = p.part + ((size_t)(kvh * p.n_qblocks + qg) * p.n_splits + ch) * REC;   // this chunk's record
+  float* rec = p.part + (((size_t)(sj * p.n_kv + kvh) * p.n_qblocks + qg) * p.n_splits + ch) * REC;   // this chunk's record
   if (tid < QP) {
     float M = m_lds[0][tid];
     for (int w = 1; w < NWA; ++w) M = fmaxf(M, m_lds[w][tid]);
@@ -316,7 +320,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
       const int qh = qg * QP + q;
       if (qh < n_qh) {
         const int row = qh / group, head = kvh * group + qh % group;
-        store_f16x8(p.out + act_index(row, head * HD + d0), a * linv_lds[q], b * linv_lds[q]);
+        store_f16x8(p.out + act_index(d.row0 + row, head * HD + d0, p.act_rows), a * linv_lds[q], b * linv_lds[q]);
       }
     } else {
       *reinterpret_cast<f32x4*>(rec + q * HD + d0) = a;
@@ -326,8 +330,9 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
 }
 
 // Combine the key chunks of k_attn in chunk order.  Grid (kv head, query
-// group, kMergeParts): per-query (max, sum) first, then each thread merges 8
-// consecutive dims of one pair with the loads of 4 chunks in flight at a time.
+// group, sequence x kMergeParts): per-query (max, sum) first, then each thread
+// merges 8 consecutive dims of one pair with the loads of 4 chunks in flight
+// at a time.
 constexpr int kMergeParts = 8;
 
 template <int HD, int NQ>
@@ -335,14 +340,16 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
   constexpr int QP = 16 * NQ;
   constexpr int REC = QP * HD + 2 * QP;
   __shared__ float Ms[QP], Linv[QP];
-  const int kvh = blockIdx.x, qg = blockIdx.y, part = blockIdx.z, tid = threadIdx.x;
+  const int kvh = blockIdx.x, qg = blockIdx.y, tid = threadIdx.x;
+  const int sj = blockIdx.z / kMergeParts, part = blockIdx.z % kMergeParts;
   const int group = p.n_heads / p.n_kv;
-  const FwdDesc d = *p.desc;
+  if (sj >= p.desc->n_seq) return;                 // uniform
+  const PassSeq d = p.desc->seq[sj];
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
   if (qg * QP >= n_qh) return;                     // uniform
   const int n_act = min(p.n_splits, (L_end + p.split_len - 1) / p.split_len);
-  const float* base = p.part + (size_t)(kvh * p.n_qblocks + qg) * p.n_splits * REC;
+  const float* base = p.part + ((size_t)(sj * p.n_kv + kvh) * p.n_qblocks + qg) * p.n_splits * REC;
   if (tid < QP) {
     // the (m, l) of up to 8 chunks are requested together
     float mv[8], lv[8];
@@ -397,16 +404,16 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
         }
     }
     const int row = qh / group, head = kvh * group + qh % group;
-    store_f16x8(p.out + act_index(row, head * HD + d0), a * Linv[q], b * Linv[q]);
+    store_f16x8(p.out + act_index(d.row0 + row, head * HD + d0, p.act_rows), a * Linv[q], b * Linv[q]);
   }
 }
 
 template <int HD, int NQ>
 hipError_t launch_hd_nq(const AttnArgs& a, hipStream_t st) {
-  k_attn<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
+  k_attn<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
-  k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, kMergeParts), dim3(256), 0, st>>>(a);
+  k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * kMergeParts), dim3(256), 0, st>>>(a);
   return hipGetLastError();
 }
 
@@ -430,6 +437,7 @@ size_t attn_part_floats(int head_dim, int nqt) { return (size_t)16 * nqt * head_
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st) {
   if (a.split_len % 128 || a.split_len <= 0) return hipErrorInvalidValue;
   if (a.nqt < 1 || a.nqt > attn_max_q_tiles(head_dim)) return hipErrorInvalidValue;
+  if (a.n_seq < 1 || a.n_seq > kMaxPassSeqs || (size_t)a.n_seq * a.n_splits > 65535) return hipErrorInvalidValue;
   if (head_dim == 64) return launch_hd<64>(a, st);
   if (head_dim == 128) return launch_hd<128>(a, st);
   return hipErrorInvalidValue;

@@ -24,7 +24,7 @@ hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
 hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStream_t st);
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
-                        uint16_t* xg, float* ss, int max_rows, hipStream_t st);
+                        uint16_t* xg, int act_rows, float* ss, int max_rows, hipStream_t st);
 hipError_t launch_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out, hipStream_t st);
 
 }  // namespace pard

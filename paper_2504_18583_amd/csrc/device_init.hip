@@ -148,9 +148,9 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta) {
 }
 
 // x[r, :] = E[ids[r], :] (fp32) from the strip-packed embedding, plus the
-// first normalised GEMM's operand xg = bf16(x * g) and the row's sum of squares.
+// first normalised GEMM's operand xg = fp16(x * g) and the row's sum of squares.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc,
-                                               float* x, const float* g, uint16_t* xg, float* ss) {
+                                               float* x, const float* g, uint16_t* xg, int act_rows, float* ss) {
   __shared__ float wsum[4];
   const int r = blockIdx.x;
   if (r >= desc->n_rows) return;
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
       o[i] = (uint32_t)f16_bits(v[2 * i] * g[k0 + 2 * i]) | ((uint32_t)f16_bits(v[2 * i + 1] * g[k0 + 2 * i + 1]) << 16);
       sq += v[2 * i] * v[2 * i] + v[2 * i + 1] * v[2 * i + 1];
     }
-    *reinterpret_cast<uint4*>(xg + act_index(r, k0)) = make_uint4(o[0], o[1], o[2], o[3]);
+    *reinterpret_cast<uint4*>(xg + act_index(r, k0, act_rows)) = make_uint4(o[0], o[1], o[2], o[3]);
   }
   for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
@@ -223,8 +223,8 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStre
 }
 
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
-                        uint16_t* xg, float* ss, int max_rows, hipStream_t st) {
-  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, ss);
+                        uint16_t* xg, int act_rows, float* ss, int max_rows, hipStream_t st) {
+  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss);
   return hipGetLastError();
 }
 

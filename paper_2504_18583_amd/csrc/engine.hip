@@ -21,8 +21,9 @@ using namespace pard;
 namespace {
 
 constexpr int kPrefillRows = kMaxRows;
-constexpr int kDescRing = 512;
+constexpr int kDescRing = 128;
 constexpr int kGatherMax = 4096;
+constexpr size_t kRowsPartBudget = 640;   // fp32 partial tiles of split row-block GEMMs (96 KiB each)
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -85,6 +86,35 @@ int plan_nw(const GemmPlan& p, int S, int mt) {
   return nw;
 }
 
+// Row-block GEMM plan (passes of more than kMaxRows rows): the grid covers
+// the row bound; narrow shapes split the input dimension so that about 256
+// workgroups work at the typical row count, with the partial tiles in budget.
+struct RowsPlan {
+  int n_tiles = 0, m_blocks = 0, ksplit = 1;
+};
+
+RowsPlan plan_rows(const GemmPlan& p, int max_rows, int typ_rows) {
+  RowsPlan r;
+  r.n_tiles = ceil_div(p.n_strips, kRowsTileStrips);
+  r.m_blocks = ceil_div(max_rows, kRowTiles * 16);
+  const int live = r.n_tiles * ceil_div(std::max(1, std::min(typ_rows, max_rows)), kRowTiles * 16);
+  if (live < 160) r.ksplit = ceil_div(256, live);
+  r.ksplit = std::min({r.ksplit, 16, std::max(1, p.kb_total / 8)});
+  while (r.ksplit > 1 && (size_t)r.ksplit * r.n_tiles * r.m_blocks > kRowsPartBudget) --r.ksplit;
+  return r;
+}
+
+// Tiles that write row sums of squares per residual GEMM (the consumers'
+// ss_tiles) for passes served by the skinny or the row-block GEMM.
+int resid_ss_tiles(const GemmPlan& p, bool rows) {
+  return rows ? ceil_div(p.n_strips, kRowsTileStrips) * kRowsWaves : p.n_strips / pick_S(EPI_RESID, p.n_strips, 1);
+}
+
+// (max, argmax) entries per lm row.
+int lm_entries(const GemmPlan& p, bool rows, int mt) {
+  return rows ? ceil_div(p.n_strips, kRowsTileStrips) * kRowsWaves : p.n_strips / pick_S(EPI_LOGITS, p.n_strips, mt);
+}
+
 struct Layer {
   uint16_t *wqkv = nullptr, *wo = nullptr, *wgu = nullptr, *wd = nullptr;
   float *bqkv = nullptr, *g_attn = nullptr, *g_mlp = nullptr;
@@ -99,15 +129,15 @@ struct ModelDev {
   float* g_final = nullptr;
   uint16_t *kcache = nullptr, *vcache = nullptr;
   float2* rope = nullptr;
-  float* x = nullptr;                 // residual stream, fp32 [kMaxRows][d]
+  float* x = nullptr;                 // residual stream, fp32 [kMaxPassRows][d]
   uint16_t* xg = nullptr;             // x * g of the next normalised GEMM (fp16, k-blocked)
-  float* ss = nullptr;                // per-tile row sums of squares of x [tiles][kMaxRows]
-  int ss_tiles_resid = 1;             // tiles of the residual GEMMs (producers of ss)
+  float* ss = nullptr;                // per-tile row sums of squares of x [tiles][kMaxPassRows]
+  int ss_tiles_max = 1;               // ss buffer tiles
   uint16_t *q = nullptr, *attn = nullptr, *h = nullptr;
-  float* logits = nullptr;
+  float* logits = nullptr;            // lm rows of the last pass [kMaxLmRows][vocab]
   int* result = nullptr;
+  int2* lm_map = nullptr;             // per slot: (first lm row, lm rows) of the last pass
   FwdDesc* desc = nullptr;
-  int last_lm_rows = 0;
 };
 
 }  // namespace
@@ -122,6 +152,7 @@ struct pard_ctx {
   float* amax_val = nullptr;
   int* amax_idx = nullptr;
   float* attn_part = nullptr;
+  float* rows_part = nullptr;
   SeqState* seq_dev = nullptr;
   int* out_dev = nullptr;
   size_t* gather_idx_dev = nullptr;
@@ -135,7 +166,7 @@ struct pard_ctx {
   int* h_out = nullptr;
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
   // captured fused steps (draft pass + verify pass), replayed on `stream`
-  struct StepGraph { int seq, k, l_class; hipGraphExec_t exec; };
+  struct StepGraph { int n_seq, k, l_class; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
   hipStream_t cap_stream = nullptr;     // private stream used only for capture
   bool use_graphs = true;
@@ -149,6 +180,7 @@ struct pard_ctx {
   size_t kv_seq_stride[2] = {0, 0};
   size_t kv_elems[2] = {0, 0};
   int kv_cap = 0;                       // KV capacity per sequence, max_ctx rounded up to 32
+  int lm_rows_cap = 0;                  // lm rows of one pass
 };
 
 namespace {
@@ -222,7 +254,7 @@ void derive(ModelDev& M, const pard_model_spec& s, int max_ctx) {
   M.p_gu = plan_gemm(EPI_SWIGLU, 2 * M.f_pad, M.d);
   M.p_d = plan_gemm(EPI_RESID, M.d, M.f_pad);
   M.p_lm = plan_gemm(EPI_LOGITS, s.vocab, M.d);
-  M.ss_tiles_resid = M.p_o.n_strips / pick_S(EPI_RESID, M.p_o.n_strips, 1);
+  M.ss_tiles_max = std::max(resid_ss_tiles(M.p_o, false), resid_ss_tiles(M.p_o, true));
 }
 
 // Lays out (base == nullptr: sizes) every device region of a context.
@@ -230,6 +262,9 @@ size_t layout(pard_ctx* c, char* base) {
   Bump b;
   b.base = base;
   int max_lm_tiles = 1;
+  // lm rows of one pass: K + 1 per sequence of a batched step (or a prefill row)
+  const int lm_rows_cap = std::min(kMaxLmRows, std::min(c->max_batch, kMaxPassSeqs) * (c->max_k + 1));
+  c->lm_rows_cap = lm_rows_cap;
   size_t attn_part = 1;
   const int cap = c->kv_cap;
   for (int w = 0; w < 2; ++w) {
@@ -255,22 +290,24 @@ size_t layout(pard_ctx* c, char* base) {
     M.kcache = b.take<uint16_t>(kv);
     M.vcache = b.take<uint16_t>(kv);
     M.rope = b.take<float2>((size_t)cap * s.head_dim / 2);
-    M.x = b.take<float>((size_t)kMaxRows * M.d);
-    M.xg = b.take<uint16_t>((size_t)kMaxRows * M.d);
-    M.ss = b.take<float>((size_t)std::max(1, M.ss_tiles_resid) * kMaxRows);
-    M.q = b.take<uint16_t>((size_t)kMaxRows * M.q_dim);
-    M.attn = b.take<uint16_t>((size_t)kMaxRows * M.q_dim);
-    M.h = b.take<uint16_t>((size_t)kMaxRows * M.f_pad);
-    M.logits = b.take<float>((size_t)kMaxLmRows * s.vocab);
+    M.x = b.take<float>((size_t)kMaxPassRows * M.d);
+    M.xg = b.take<uint16_t>((size_t)kMaxPassRows * M.d);
+    M.ss = b.take<float>((size_t)std::max(1, M.ss_tiles_max) * kMaxPassRows);
+    M.q = b.take<uint16_t>((size_t)kMaxPassRows * M.q_dim);
+    M.attn = b.take<uint16_t>((size_t)kMaxPassRows * M.q_dim);
+    M.h = b.take<uint16_t>((size_t)kMaxPassRows * M.f_pad);
+    M.logits = b.take<float>((size_t)lm_rows_cap * s.vocab);
     M.result = b.take<int>(kMaxLmRows);
+    M.lm_map = b.take<int2>(c->max_batch);
     M.desc = b.take<FwdDesc>(1);
     max_lm_tiles = std::max(max_lm_tiles, M.p_lm.n_strips);
     attn_part = std::max(attn_part, (size_t)s.n_kv_heads * kAttnRecords *
                                         attn_part_floats(s.head_dim, attn_max_q_tiles(s.head_dim)));
   }
-  c->amax_val = b.take<float>((size_t)max_lm_tiles * kMaxLmRows);
-  c->amax_idx = b.take<int>((size_t)max_lm_tiles * kMaxLmRows);
+  c->amax_val = b.take<float>((size_t)max_lm_tiles * lm_rows_cap);
+  c->amax_idx = b.take<int>((size_t)max_lm_tiles * lm_rows_cap);
   c->attn_part = b.take<float>(attn_part);
+  c->rows_part = b.take<float>(kRowsPartBudget * kRowsPartFloats);
   c->seq_dev = b.take<SeqState>(c->max_batch);
   c->out_dev = b.take<int>((size_t)c->max_batch * c->max_ctx);
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
@@ -358,19 +395,31 @@ struct Timed {
   }
 };
 
-GemmArgs gemm_base(const ModelDev& M, const uint16_t* W) {
+GemmArgs gemm_base(const ModelDev& M, const uint16_t* W, int act_rows) {
   GemmArgs a{};
   a.W = W;
+  a.act_rows = act_rows;
   a.desc = M.desc;
   a.eps = M.spec.rms_eps;
   a.inv_k = 1.0f / (float)M.d;
   return a;
 }
 
-hipError_t run_gemm(pard_ctx* c, int cls, int epi, int mt, GemmArgs a, const GemmPlan& p) {
-  const int S = pick_S(epi, p.n_strips, mt);
-  a.kb_total = p.kb_total;
-  a.n_tiles = p.n_strips / S;
+struct PassSpec {
+  int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
+  int typ_rows = 0;       // row count the split plan is tuned for (0: max_rows)
+  int max_lm_rows = 0;    // 0: no lm_head
+  int n_seq = 1;          // upper bound of the pass's sequences
+  int max_seq_rows = 0;   // upper bound of one sequence's rows (0: max_rows)
+  int l_bound = 0;        // upper bound of pos0 + n_rows (attention split plan)
+  int tail = TAIL_NONE;
+  FwdDesc* next_desc = nullptr;
+  bool emit = false;
+};
+
+// One GEMM of a pass: the skinny kernel up to kMaxRows rows, the row-block
+// kernel above.
+hipError_t run_gemm(pard_ctx* c, int cls, int epi, int max_rows, int typ_rows, GemmArgs a, const GemmPlan& p) {
   // a timed GEMM launch carries its events: they take the kernel's own start
   // and end timestamps, not those of separate marker packets
   LaunchEvents ev;
@@ -379,65 +428,78 @@ hipError_t run_gemm(pard_ctx* c, int cls, int epi, int mt, GemmArgs a, const Gem
     ev.stop = c->timer_ev[2 * c->timer_used + 1];
     ++c->timer_used;
   }
+  a.kb_total = p.kb_total;
+  a.n_strips = p.n_strips;
+  if (max_rows > kMaxRows) {
+    const RowsPlan r = plan_rows(p, max_rows, typ_rows > 0 ? typ_rows : max_rows);
+    a.n_tiles = r.n_tiles;
+    a.m_blocks = r.m_blocks;
+    a.ksplit = r.ksplit;
+    a.part = c->rows_part;
+    return launch_gemm_rows(epi, a, c->stream, ev);
+  }
+  const int mt = ceil_div(max_rows, 16);
+  const int S = pick_S(epi, p.n_strips, mt);
+  a.n_tiles = p.n_strips / S;
   return launch_gemm(epi, mt, S, plan_nw(p, S, mt), a, c->stream, ev);
 }
 
-struct PassSpec {
-  int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
-  int max_lm_rows = 0;    // 0: no lm_head
-  int l_bound = 0;        // upper bound of pos0 + n_rows (attention split plan)
-  int tail = TAIL_NONE;
-  FwdDesc* next_desc = nullptr;
-  bool emit = false;
-};
-
-pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
+pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   ModelDev& M = c->m[w];
   const pard_model_spec& s = M.spec;
-  const int mt = ceil_div(ps.max_rows, 16);
+  const bool rows = ps.max_rows > kMaxRows;
+  const int typ = ps.typ_rows > 0 ? ps.typ_rows : ps.max_rows;
+  const int ss_tiles = resid_ss_tiles(M.p_o, rows);
+  const int act_rows = rows ? kMaxPassRows : kMaxRows;
   const int cls0 = w * 8;
+  if (ps.max_rows < 1 || ps.max_rows > kMaxPassRows || ps.n_seq < 1 || ps.n_seq > kMaxPassSeqs ||
+      ps.max_lm_rows > c->lm_rows_cap)
+    return fail(c, PARD_ERR_CAPACITY, "pass of %d rows / %d sequences exceeds the engine's limits", ps.max_rows,
+                ps.n_seq);
   {
     Timed t(c, cls0 + 0);
-    HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, M.ss,
+    HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, act_rows, M.ss,
                             ps.max_rows, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
-  // attention plan: one workgroup per (KV head, query group, key chunk); a
-  // query group holds every (row, head) pair of the KV head for decode passes
-  // (up to 48 / 64 pairs); chunks of kAttnChunk keys start at fixed multiples
-  // whatever the pass, so a query's result does not depend on the other rows
-  // of its pass (only very long prefill chunks, with many query groups, use
-  // longer chunks to bound the partial records)
-  const int qpairs = ps.max_rows * M.group;
+  // attention plan: one workgroup per (sequence, KV head, query group, key
+  // chunk); a query group holds every (row, head) pair of the KV head for
+  // decode passes (up to 48 / 64 pairs); chunks of kAttnChunk keys start at
+  // fixed multiples whatever the pass, so a query's result does not depend on
+  // the other rows of its pass (only very long prefill chunks, with many query
+  // groups, use longer chunks to bound the partial records)
+  const int seq_rows = ps.max_seq_rows > 0 ? std::min(ps.max_seq_rows, ps.max_rows) : ps.max_rows;
+  const int qpairs = seq_rows * M.group;
   const int nqt = std::min(attn_max_q_tiles(s.head_dim), ceil_div(qpairs, 16));
   const int n_qblocks = ceil_div(qpairs, 16 * nqt);
   const int l_bound = std::min(std::max(ps.l_bound, 1), c->kv_cap);
+  if (ps.n_seq * n_qblocks > kAttnRecords)
+    return fail(c, PARD_ERR_CAPACITY, "attention plan: %d query blocks exceed the record budget", ps.n_seq * n_qblocks);
   int split_len = kAttnChunk;
-  while (n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
+  while ((int64_t)ps.n_seq * n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
   const int n_splits = ceil_div(l_bound, split_len);
-  uint16_t* kc_seq = M.kcache + c->kv_seq_stride[w] * seq;
-  uint16_t* vc_seq = M.vcache + c->kv_seq_stride[w] * seq;
   for (int l = 0; l < s.n_layers; ++l) {
     const Layer& L = M.layers[l];
-    uint16_t* kc = kc_seq + layer_kv * l;
-    uint16_t* vc = vc_seq + layer_kv * l;
+    uint16_t* kc = M.kcache + layer_kv * l;
+    uint16_t* vc = M.vcache + layer_kv * l;
     {  // norm + QKV + bias + RoPE + KV append
-      GemmArgs a = gemm_base(M, L.wqkv);
+      GemmArgs a = gemm_base(M, L.wqkv, act_rows);
       a.A = M.xg;
       a.lda = M.d;
       a.ss_in = M.ss;
-      a.ss_tiles = l == 0 ? 1 : M.ss_tiles_resid;
+      a.ss_tiles = l == 0 ? 1 : ss_tiles;
       a.out = M.q;
       a.ld_out = M.q_dim;
       a.kc = kc;
       a.vc = vc;
       a.cap = c->kv_cap;
+      a.kv_seq_stride = c->kv_seq_stride[w];
       a.bias = L.bqkv;
       a.rope = M.rope;
       a.q_dim = M.q_dim;
       a.kv_dim = M.kv_dim;
       a.hd = s.head_dim;
-      HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, mt, a, M.p_qkv));
+      HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
     }
     {  // attention
       AttnArgs a{};
@@ -445,8 +507,10 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.ldq = M.q_dim;
       a.kc = kc;
       a.vc = vc;
+      a.kv_seq_stride = c->kv_seq_stride[w];
       a.cap = c->kv_cap;
       a.out = M.attn;
+      a.act_rows = act_rows;
       a.desc = M.desc;
       a.n_heads = s.n_heads;
       a.n_kv = s.n_kv_heads;
@@ -454,13 +518,14 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.n_qblocks = n_qblocks;
       a.split_len = split_len;
       a.n_splits = n_splits;
+      a.n_seq = ps.n_seq;
       a.scale = 1.0f / std::sqrt((float)s.head_dim);
       a.part = c->attn_part;
       Timed t(c, cls0 + 2);
       HIP_TRY(c, launch_attention(s.head_dim, a, c->stream));
     }
     {  // O-projection + residual
-      GemmArgs a = gemm_base(M, L.wo);
+      GemmArgs a = gemm_base(M, L.wo, act_rows);
       a.A = M.attn;
       a.lda = M.q_dim;
       a.x = M.x;
@@ -468,19 +533,19 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.g_next = L.g_mlp;
       a.xg = M.xg;
       a.ss_out = M.ss;
-      HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, mt, a, M.p_o));
+      HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, ps.max_rows, typ, a, M.p_o));
     }
     {  // norm + gate/up + SiLU * up
-      GemmArgs a = gemm_base(M, L.wgu);
+      GemmArgs a = gemm_base(M, L.wgu, act_rows);
       a.A = M.xg;
       a.lda = M.d;
       a.ss_in = M.ss;
-      a.ss_tiles = M.ss_tiles_resid;
+      a.ss_tiles = ss_tiles;
       a.out = M.h;
-      HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, mt, a, M.p_gu));
+      HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, ps.max_rows, typ, a, M.p_gu));
     }
     {  // down + residual
-      GemmArgs a = gemm_base(M, L.wd);
+      GemmArgs a = gemm_base(M, L.wd, act_rows);
       a.A = M.h;
       a.lda = M.f_pad;
       a.x = M.x;
@@ -488,36 +553,40 @@ pard_status forward(pard_ctx* c, int w, int seq, const PassSpec& ps) {
       a.g_next = (l + 1 < s.n_layers) ? M.layers[l + 1].g_attn : M.g_final;
       a.xg = M.xg;
       a.ss_out = M.ss;
-      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, mt, a, M.p_d));
+      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, ps.max_rows, typ, a, M.p_d));
     }
   }
   if (ps.max_lm_rows > 0) {
-    GemmArgs a = gemm_base(M, M.lm_head);
+    const bool lm_rows = ps.max_lm_rows > kMaxRows;
+    const int mt_lm = ceil_div(ps.max_lm_rows, 16);
+    GemmArgs a = gemm_base(M, M.lm_head, act_rows);
     a.A = M.xg;
     a.lda = M.d;
     a.ss_in = M.ss;
-    a.ss_tiles = M.ss_tiles_resid;
-    a.lm_mode = 1;
+    a.ss_tiles = ss_tiles;
     a.logits = M.logits;
     a.vocab = s.vocab;
     a.amax_val = c->amax_val;
     a.amax_idx = c->amax_idx;
-    const int mt_lm = ceil_div(ps.max_lm_rows, 16);
-    HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, mt_lm, a, M.p_lm));
+    a.amax_stride = lm_entries(M.p_lm, lm_rows, mt_lm);
+    HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, ps.max_lm_rows, ps.max_lm_rows, a, M.p_lm));
     TailArgs ta{};
     ta.desc = M.desc;
     ta.amax_val = c->amax_val;
     ta.amax_idx = c->amax_idx;
-    ta.n_tiles = M.p_lm.n_strips / pick_S(EPI_LOGITS, M.p_lm.n_strips, mt_lm);
+    ta.n_tiles = a.amax_stride;
     ta.vocab = s.vocab;
     ta.result = M.result;
     ta.tail = ps.tail;
-    ta.seq = c->seq_dev + seq;
+    ta.states = c->seq_dev;
+    ta.lm_map = M.lm_map;
+    ta.lm_map_draft = c->m[PARD_DRAFT].lm_map;
     ta.next_desc = ps.next_desc;
-    ta.out_tokens = ps.emit ? c->out_dev + (size_t)seq * c->max_ctx : nullptr;
+    ta.out_tokens = ps.emit ? c->out_dev : nullptr;
     ta.out_cap = c->max_ctx;
     Timed t(c, cls0 + 7);
-    HIP_TRY(c, launch_tail(ta, c->stream));
+    HIP_TRY(c, launch_tail(ta, ps.n_seq, c->stream));
+    if (ps.n_seq > 1 && ps.next_desc) HIP_TRY(c, launch_stage(ta, c->stream));
   }
   return PARD_OK;
 }
@@ -539,37 +608,58 @@ pard_status push_seq(pard_ctx* c, int seq) {
   return PARD_OK;
 }
 
-pard_status pull_seq_sync(pard_ctx* c, int seq) {
-  HIP_TRY(c, hipMemcpyAsync(c->h_seq + seq, c->seq_dev + seq, sizeof(SeqState), hipMemcpyDeviceToHost, c->stream));
+pard_status pull_seqs_sync(pard_ctx* c, const int* seqs, int n) {
+  for (int i = 0; i < n; ++i)
+    HIP_TRY(c, hipMemcpyAsync(c->h_seq + seqs[i], c->seq_dev + seqs[i], sizeof(SeqState), hipMemcpyDeviceToHost,
+                              c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   c->desc_slot = 0;
   return PARD_OK;
 }
 
-FwdDesc make_desc(const int* ids, int n_ids, int n_masks, int mask_id, int pos0, int n_real, int lm_row0,
+pard_status pull_seq_sync(pard_ctx* c, int seq) { return pull_seqs_sync(c, &seq, 1); }
+
+// Appends one sequence's rows to a host-built pass: n_ids tokens then n_masks
+// mask rows at positions pos0.., the first n_real committed; lm rows are rows
+// lm_first .. lm_first + lm_rows - 1 of the sequence.
+void append_seq(FwdDesc& d, int slot, const int* ids, int n_ids, int n_masks, int mask_id, int pos0, int n_real,
+                int lm_first, int lm_rows) {
+  PassSeq& q = d.seq[d.n_seq++];
+  q.slot = slot;
+  q.row0 = d.n_rows;
+  q.n_rows = n_ids + n_masks;
+  q.n_real = n_real;
+  q.pos0 = pos0;
+  q.lm0 = d.n_lm;
+  q.lm_rows = lm_rows;
+  for (int i = 0; i < q.n_rows; ++i) {
+    const int r = q.row0 + i;
+    d.ids[r] = i < n_ids ? ids[i] : mask_id;
+    d.pos[r] = pos0 + i;
+    d.slot[r] = slot;
+  }
+  for (int j = 0; j < lm_rows; ++j) d.lm_src[q.lm0 + j] = q.row0 + lm_first + j;
+  d.n_rows += q.n_rows;
+  d.n_lm += lm_rows;
+}
+
+FwdDesc make_desc(int slot, const int* ids, int n_ids, int n_masks, int mask_id, int pos0, int n_real, int lm_first,
                   int lm_rows) {
   FwdDesc d{};
-  int n = 0;
-  for (int i = 0; i < n_ids; ++i) d.ids[n++] = ids[i];
-  for (int i = 0; i < n_masks; ++i) d.ids[n++] = mask_id;
-  d.n_rows = n;
-  d.n_real = n_real;
-  d.pos0 = pos0;
-  d.lm_row0 = lm_row0;
-  d.lm_rows = lm_rows;
+  append_seq(d, slot, ids, n_ids, n_masks, mask_id, pos0, n_real, lm_first, lm_rows);
   return d;
 }
 
-// Ingest tokens[0..n) at positions pos0.. into model w's cache (no lm_head).
+// Ingest tokens[0..n) at positions pos0.. into model w's cache of one slot (no lm_head).
 pard_status ingest(pard_ctx* c, int w, int seq, const int* tokens, int n, int pos0) {
   for (int off = 0; off < n; off += kPrefillRows) {
     const int rows = std::min(kPrefillRows, n - off);
-    pard_status st = stage_desc(c, w, make_desc(tokens + off, rows, 0, 0, pos0 + off, rows, rows - 1, 1));
+    pard_status st = stage_desc(c, w, make_desc(seq, tokens + off, rows, 0, 0, pos0 + off, rows, rows - 1, 1));
     if (st != PARD_OK) return st;
     PassSpec ps;
     ps.max_rows = rows;
     ps.l_bound = pos0 + off + rows;
-    st = forward(c, w, seq, ps);
+    st = forward(c, w, ps);
     if (st != PARD_OK) return st;
   }
   return PARD_OK;
@@ -593,40 +683,54 @@ int attn_l_class(int l) {
   return ceil_div(l, 1024) * 1024;
 }
 
-// One fused step: draft pass (pending + K-1 masks) then verify pass, each
-// followed by its argmax tail; K = 0 runs the verify pass only.
-pard_status step_passes(pard_ctx* c, int seq, int K, int draft_rows, int l_class) {
+// Pass bounds of one fused step over n_seq sequences.
+struct StepShape {
+  int n_seq = 1, K = 0;
+  int draft_rows = 0;     // bound of the draft pass's rows
+  int l_class = 0;
+};
+
+// One fused step: draft pass (pending + K-1 masks per sequence) then verify
+// pass, each followed by its argmax tail; K = 0 runs the verify pass only.
+pard_status step_passes(pard_ctx* c, const StepShape& sh) {
   pard_status st;
+  const int K = sh.K, n = sh.n_seq;
   if (K > 0) {
     PassSpec pd;
-    pd.max_rows = draft_rows;
-    pd.max_lm_rows = K;
-    pd.l_bound = l_class;
+    pd.max_rows = sh.draft_rows;
+    pd.typ_rows = n * K;
+    pd.max_lm_rows = n * K;
+    pd.n_seq = n;
+    pd.max_seq_rows = n > 1 ? 2 * K : sh.draft_rows;
+    pd.l_bound = sh.l_class;
     pd.tail = TAIL_DRAFT;
     pd.next_desc = c->m[PARD_TARGET].desc;
-    if ((st = forward(c, PARD_DRAFT, seq, pd)) != PARD_OK) return st;
+    if ((st = forward(c, PARD_DRAFT, pd)) != PARD_OK) return st;
   }
   PassSpec pv;
-  pv.max_rows = K + 1;
-  pv.max_lm_rows = K + 1;
-  pv.l_bound = l_class;
+  pv.max_rows = n * (K + 1);
+  pv.max_lm_rows = n * (K + 1);
+  pv.n_seq = n;
+  pv.max_seq_rows = K + 1;
+  pv.l_bound = sh.l_class;
   pv.tail = TAIL_VERIFY;
   pv.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
   pv.emit = true;
-  return forward(c, PARD_TARGET, seq, pv);
+  return forward(c, PARD_TARGET, pv);
 }
 
-// Replays the captured step for (seq, K, l_class), capturing it on first use.
-// A capture failure switches the context to eager launches.
-pard_status launch_step_graph(pard_ctx* c, int seq, int K, int l_class) {
+// Replays the captured step for (n_seq, K, l_class), capturing it on first
+// use; the sequences themselves come from the device descriptors.  A capture
+// failure switches the context to eager launches.
+pard_status launch_step_graph(pard_ctx* c, const StepShape& sh) {
   for (const auto& g : c->graphs)
-    if (g.seq == seq && g.k == K && g.l_class == l_class) {
+    if (g.n_seq == sh.n_seq && g.k == sh.K && g.l_class == sh.l_class) {
       HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
       return PARD_OK;
     }
   if (!c->cap_stream && hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess) {
     c->use_graphs = false;
-    return step_passes(c, seq, K, 2 * K, l_class);
+    return step_passes(c, sh);
   }
   hipStream_t user = c->stream;
   hipGraph_t graph = nullptr;
@@ -634,7 +738,7 @@ pard_status launch_step_graph(pard_ctx* c, int seq, int K, int l_class) {
   bool ok = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeThreadLocal) == hipSuccess;
   if (ok) {
     c->stream = c->cap_stream;
-    const pard_status st = step_passes(c, seq, K, 2 * K, l_class);
+    const pard_status st = step_passes(c, sh);
     c->stream = user;
     ok = hipStreamEndCapture(c->cap_stream, &graph) == hipSuccess && st == PARD_OK && graph;
   }
@@ -643,9 +747,9 @@ pard_status launch_step_graph(pard_ctx* c, int seq, int K, int l_class) {
   (void)hipGetLastError();
   if (!ok) {
     c->use_graphs = false;
-    return step_passes(c, seq, K, 2 * K, l_class);
+    return step_passes(c, sh);
   }
-  c->graphs.push_back({seq, K, l_class, exec});
+  c->graphs.push_back({sh.n_seq, sh.K, sh.l_class, exec});
   HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return PARD_OK;
 }
@@ -732,6 +836,8 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   for (int w = 0; w < 2; ++w)
     if (generate(c, w) != PARD_OK) return bail(PARD_ERR_DEVICE);
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->m[1].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   *out = c;
@@ -774,7 +880,7 @@ pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_
     for (int off = 0; off < n; off += kPrefillRows) {
       const int rows = std::min(kPrefillRows, n - off);
       const bool last = (off + rows == n) && w == PARD_TARGET;
-      st = stage_desc(c, w, make_desc(prompt + off, rows, 0, 0, off, rows, rows - 1, 1));
+      st = stage_desc(c, w, make_desc(seq, prompt + off, rows, 0, 0, off, rows, rows - 1, 1));
       if (st != PARD_OK) return st;
       PassSpec ps;
       ps.max_rows = rows;
@@ -783,11 +889,10 @@ pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_
         ps.max_lm_rows = 1;
         ps.tail = TAIL_PREFILL;
       }
-      if ((st = forward(c, w, seq, ps)) != PARD_OK) return st;
+      if ((st = forward(c, w, ps)) != PARD_OK) return st;
     }
   }
   if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
-  c->m[PARD_TARGET].last_lm_rows = 1;
   *first_token = S.bonus;
   c->hist[seq].assign(prompt, prompt + n);
   c->hist[seq].push_back(S.bonus);
@@ -819,7 +924,7 @@ pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t 
   S.k = K;
   S.L[1] = Ld;
   if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
-  const FwdDesc d = make_desc(prefix + Ld, n_new, K - 1, c->mask_id, Ld, n_new, n_new - 1, K);
+  const FwdDesc d = make_desc(seq, prefix + Ld, n_new, K - 1, c->mask_id, Ld, n_new, n_new - 1, K);
   if ((st = stage_desc(c, PARD_DRAFT, d)) != PARD_OK) { S = saved; return st; }
   PassSpec ps;
   ps.max_rows = d.n_rows;
@@ -827,9 +932,8 @@ pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t 
   ps.max_lm_rows = K;
   ps.tail = TAIL_DRAFT;
   ps.next_desc = c->m[PARD_TARGET].desc;
-  if ((st = forward(c, PARD_DRAFT, seq, ps)) != PARD_OK) { S = saved; return st; }
+  if ((st = forward(c, PARD_DRAFT, ps)) != PARD_OK) { S = saved; return st; }
   if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
-  c->m[PARD_DRAFT].last_lm_rows = K;
   for (int i = 0; i < K; ++i) cand[i] = S.cand[i];
   return PARD_OK;
 }
@@ -855,7 +959,7 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
   }
   S.k = K;
   if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
-  if ((st = stage_desc(c, PARD_TARGET, make_desc(ids, K + 1, 0, 0, Lt, K + 1, 0, K + 1))) != PARD_OK) {
+  if ((st = stage_desc(c, PARD_TARGET, make_desc(seq, ids, K + 1, 0, 0, Lt, K + 1, 0, K + 1))) != PARD_OK) {
     S = saved;
     return st;
   }
@@ -865,9 +969,8 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
   ps.max_lm_rows = K + 1;
   ps.tail = TAIL_VERIFY;
   ps.next_desc = c->m[K > 0 ? PARD_DRAFT : PARD_TARGET].desc;
-  if ((st = forward(c, PARD_TARGET, seq, ps)) != PARD_OK) { S = saved; return st; }
+  if ((st = forward(c, PARD_TARGET, ps)) != PARD_OK) { S = saved; return st; }
   if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
-  c->m[PARD_TARGET].last_lm_rows = K + 1;
   *n_accepted = S.a;
   *bonus = S.bonus;
   std::vector<int>& h = c->hist[seq];
@@ -911,95 +1014,132 @@ pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32
                           int32_t max_steps, int32_t* out_tokens, pard_stats* stats) {
   if (!c) return PARD_ERR_ARG;
   if (!seqs || !out_tokens || n_tokens < 1) return fail(c, PARD_ERR_ARG, "generate: null pointer or n_tokens < 1");
-  if (n_seq != 1) return fail(c, PARD_ERR_UNSUPPORTED, "generate: only one sequence per call in this build");
-  const int seq = seqs[0];
-  pard_status st = check_seq(c, seq, true);
-  if (st != PARD_OK) return st;
+  if (n_seq < 1 || n_seq > std::min(c->max_batch, kMaxPassSeqs))
+    return fail(c, PARD_ERR_CAPACITY, "generate: n_seq=%d outside [1, %d]", n_seq, std::min(c->max_batch, kMaxPassSeqs));
   if (K < 0 || K > c->max_k) return fail(c, PARD_ERR_ARG, "generate: K=%d outside [0, max_k=%d]", K, c->max_k);
-  SeqState& S = c->h_seq[seq];
-  std::vector<int>& hist = c->hist[seq];
-  const int Lt = S.L[0];
-  if ((int64_t)Lt + n_tokens + 2 * K + 1 > c->max_ctx)
-    return fail(c, PARD_ERR_CAPACITY, "generate: %d tokens from length %d may exceed max_ctx=%d", n_tokens, Lt,
-                c->max_ctx);
-  const SeqState saved = S;
+  if (n_seq > 1 && (n_seq * 2 * K > kMaxPassRows || n_seq * (K + 1) > c->lm_rows_cap))
+    return fail(c, PARD_ERR_CAPACITY, "generate: %d sequences at K=%d exceed %d rows per pass", n_seq, K,
+                kMaxPassRows);
+  pard_status st;
+  for (int i = 0; i < n_seq; ++i) {
+    if ((st = check_seq(c, seqs[i], true)) != PARD_OK) return st;
+    for (int j = 0; j < i; ++j)
+      if (seqs[j] == seqs[i]) return fail(c, PARD_ERR_ARG, "generate: slot %d listed twice", seqs[i]);
+    const int Lt = c->h_seq[seqs[i]].L[0];
+    if ((int64_t)Lt + n_tokens + 2 * K + 1 > c->max_ctx)
+      return fail(c, PARD_ERR_CAPACITY, "generate: %d tokens from length %d may exceed max_ctx=%d", n_tokens, Lt,
+                  c->max_ctx);
+  }
+  std::vector<SeqState> saved(n_seq);
+  for (int i = 0; i < n_seq; ++i) saved[i] = c->h_seq[seqs[i]];
   auto restore = [&](pard_status s) {
-    S = saved;
+    for (int i = 0; i < n_seq; ++i) c->h_seq[seqs[i]] = saved[i];
     return s;
   };
-  // the draft catches up with every committed token it has not seen
-  int Ld = std::min(S.L[1], Lt);
-  if (K > 0) {
-    const int total = Lt + 1;                  // committed tokens + pending
-    const int max_first = kMaxRows - (K - 1);
-    if (total - Ld > max_first) {
-      const int extra = total - Ld - max_first;
-      if ((st = ingest(c, PARD_DRAFT, seq, hist.data() + Ld, extra, Ld)) != PARD_OK) return restore(st);
-      Ld += extra;
+  // every draft catches up with the committed tokens it has not seen; a
+  // sequence's first draft pass holds at most kMaxRows rows alone, 2K in a batch
+  FwdDesc first{};
+  for (int i = 0; i < n_seq; ++i) {
+    const int seq = seqs[i];
+    SeqState& S = c->h_seq[seq];
+    const std::vector<int>& hist = c->hist[seq];
+    const int Lt = S.L[0];
+    int Ld = std::min(S.L[1], Lt);
+    if (K > 0) {
+      const int total = Lt + 1;                  // committed tokens + pending
+      const int max_first = (n_seq == 1 ? kMaxRows : 2 * K) - (K - 1);
+      if (total - Ld > max_first) {
+        const int extra = total - Ld - max_first;
+        if ((st = ingest(c, PARD_DRAFT, seq, hist.data() + Ld, extra, Ld)) != PARD_OK) return restore(st);
+        Ld += extra;
+      }
+      S.n_pending = total - Ld;
+      for (int j = 0; j < S.n_pending; ++j) S.pending[j] = hist[Ld + j];
     }
-    S.n_pending = total - Ld;
-    for (int i = 0; i < S.n_pending; ++i) S.pending[i] = hist[Ld + i];
+    S.L[1] = Ld;
+    S.k = K;
+    S.n_out = 1;
+    S.n_target = n_tokens;
+    S.steps = 0;
+    S.mask_id = c->mask_id;
+    memset(S.accept_hist, 0, sizeof S.accept_hist);
+    if ((st = push_seq(c, seq)) != PARD_OK) return restore(st);
+    if (K > 0) {
+      append_seq(first, seq, S.pending, S.n_pending, K - 1, c->mask_id, Ld, S.n_pending, S.n_pending - 1, K);
+    } else {
+      const int b = S.bonus;
+      append_seq(first, seq, &b, 1, 0, 0, Lt, 1, 0, 1);
+    }
   }
-  S.L[1] = Ld;
-  S.k = K;
-  S.n_out = 1;
-  S.n_target = n_tokens;
-  S.steps = 0;
-  S.mask_id = c->mask_id;
-  memset(S.accept_hist, 0, sizeof S.accept_hist);
-  if ((st = push_seq(c, seq)) != PARD_OK) return restore(st);
-  int first_rows;
-  if (K > 0) {
-    const FwdDesc d = make_desc(S.pending, S.n_pending, K - 1, c->mask_id, Ld, S.n_pending, S.n_pending - 1, K);
-    first_rows = d.n_rows;
-    if ((st = stage_desc(c, PARD_DRAFT, d)) != PARD_OK) return restore(st);
-  } else {
-    const int b = S.bonus;
-    if ((st = stage_desc(c, PARD_TARGET, make_desc(&b, 1, 0, 0, Lt, 1, 0, 1))) != PARD_OK) return restore(st);
-    first_rows = 1;
-  }
+  if ((st = stage_desc(c, K > 0 ? PARD_DRAFT : PARD_TARGET, first)) != PARD_OK) return restore(st);
   HIP_TRY(c, hipEventRecord(c->ev_start, c->stream));
-  int produced = 1, steps = 0;
-  bool first = true;
-  while (produced < n_tokens && (max_steps <= 0 || steps < max_steps)) {
-    int batch = ceil_div(n_tokens - produced, K + 1);
+  // active: sequences that still need tokens (a finished one leaves the
+  // batch when the device stages the next draft pass)
+  std::vector<int> active(seqs, seqs + n_seq);
+  int steps = 0;
+  bool first_step = true;
+  while (!active.empty() && (max_steps <= 0 || steps < max_steps)) {
+    int min_left = INT32_MAX, max_L = 0;
+    for (int seq : active) {
+      min_left = std::min(min_left, n_tokens - c->h_seq[seq].n_out);
+      max_L = std::max(max_L, c->h_seq[seq].L[0]);
+    }
+    int batch = ceil_div(min_left, K + 1);
     if (max_steps > 0) batch = std::min(batch, max_steps - steps);
     // L_t grows by at most K+1 per step: one attention plan covers the batch
-    const int l_class = attn_l_class(S.L[0] + batch * (K + 1) + K + 1);
+    StepShape sh;
+    sh.n_seq = (int)active.size();
+    sh.K = K;
+    sh.l_class = attn_l_class(max_L + batch * (K + 1) + K + 1);
     for (int i = 0; i < batch; ++i) {
-      if (first || !c->use_graphs || c->timer_class >= 0) {
-        if ((st = step_passes(c, seq, K, first ? std::max(first_rows, 2 * K) : 2 * K, l_class)) != PARD_OK)
-          return st;
+      // a single sequence's first draft pass may carry more pending rows
+      sh.draft_rows = sh.n_seq > 1 ? sh.n_seq * 2 * K : (first_step ? std::max(first.n_rows, 2 * K) : 2 * K);
+      if (first_step || !c->use_graphs || c->timer_class >= 0) {
+        if ((st = step_passes(c, sh)) != PARD_OK) return st;
       } else {
-        if ((st = launch_step_graph(c, seq, K, l_class)) != PARD_OK) return st;
+        if ((st = launch_step_graph(c, sh)) != PARD_OK) return st;
       }
-      first = false;
+      first_step = false;
     }
     HIP_TRY(c, hipEventRecord(c->ev_stop, c->stream));
-    if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
-    produced = S.n_out;
-    steps = S.steps;
+    if ((st = pull_seqs_sync(c, active.data(), (int)active.size())) != PARD_OK) return st;
+    std::vector<int> still;
+    for (int seq : active) {
+      steps = std::max(steps, c->h_seq[seq].steps);
+      if (c->h_seq[seq].n_out < n_tokens) still.push_back(seq);
+    }
+    if (n_seq > 1) active.swap(still);          // batched passes drop finished sequences
+    else if (still.empty()) active.clear();
   }
   float ms = 0.f;
   if (steps > 0) HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_start, c->ev_stop));
-  const int n_new = produced - 1;   // tokens appended after the pending one
-  if (n_new > 0) {
-    HIP_TRY(c, hipMemcpyAsync(c->h_out, c->out_dev + (size_t)seq * c->max_ctx + 1, sizeof(int) * n_new,
-                              hipMemcpyDeviceToHost, c->stream));
-    HIP_TRY(c, hipStreamSynchronize(c->stream));
+  int64_t total_written = 0;
+  int64_t hist_sum[kMaxK + 1] = {0};
+  for (int i = 0; i < n_seq; ++i) {
+    const int seq = seqs[i];
+    SeqState& S = c->h_seq[seq];
+    std::vector<int>& hist = c->hist[seq];
+    const int produced = S.n_out;
+    const int n_new = produced - 1;   // tokens appended after the pending one
+    if (n_new > 0) {
+      HIP_TRY(c, hipMemcpyAsync(c->h_out, c->out_dev + (size_t)seq * c->max_ctx + 1, sizeof(int) * n_new,
+                                hipMemcpyDeviceToHost, c->stream));
+      HIP_TRY(c, hipStreamSynchronize(c->stream));
+    }
+    const int written = std::min(produced, n_tokens);
+    int32_t* out = out_tokens + (size_t)i * n_tokens;
+    out[0] = hist.back();
+    for (int j = 1; j < written; ++j) out[j] = c->h_out[j - 1];
+    for (int j = 0; j < n_new; ++j) hist.push_back(c->h_out[j]);
+    total_written += written;
+    for (int j = 0; j <= kMaxK; ++j) hist_sum[j] += S.accept_hist[j];
   }
-  const int written = std::min(produced, n_tokens);
-  out_tokens[0] = hist.back();
-  for (int i = 1; i < written; ++i) out_tokens[i] = c->h_out[i - 1];
-  for (int i = 0; i < n_new; ++i) hist.push_back(c->h_out[i]);
-  if (K > 0) c->m[PARD_DRAFT].last_lm_rows = K;
-  c->m[PARD_TARGET].last_lm_rows = K + 1;
   if (stats) {
     memset(stats, 0, sizeof *stats);
     stats->steps = steps;
-    stats->tokens = written;
+    stats->tokens = total_written;
     stats->elapsed_ms = ms;
-    for (int i = 0; i <= kMaxK; ++i) stats->accept_hist[i] = S.accept_hist[i];
+    for (int i = 0; i <= kMaxK; ++i) stats->accept_hist[i] = hist_sum[i];
   }
   return PARD_OK;
 }
@@ -1011,10 +1151,13 @@ pard_status pard_read_logits(const pard_ctx* cc, int32_t which, int32_t seq, flo
   if (seq < 0 || seq >= c->max_batch) return fail(c, PARD_ERR_ARG, "read_logits: bad seq");
   const ModelDev& M = c->m[which];
   if (vocab != M.spec.vocab) return fail(c, PARD_ERR_ARG, "read_logits: vocab mismatch");
-  if (M.last_lm_rows == 0) return fail(c, PARD_ERR_STATE, "read_logits: no lm_head pass yet");
-  if (rows < 1 || rows > M.last_lm_rows)
-    return fail(c, PARD_ERR_ARG, "read_logits: rows %d outside [1, %d]", rows, M.last_lm_rows);
-  HIP_TRY(c, hipMemcpyAsync(out, M.logits, sizeof(float) * rows * vocab, hipMemcpyDeviceToHost, c->stream));
+  int2 lm{0, 0};
+  HIP_TRY(c, hipMemcpyAsync(&lm, M.lm_map + seq, sizeof lm, hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
+  if (lm.y == 0) return fail(c, PARD_ERR_STATE, "read_logits: no lm_head pass of this model for slot %d yet", seq);
+  if (rows < 1 || rows > lm.y) return fail(c, PARD_ERR_ARG, "read_logits: rows %d outside [1, %d]", rows, lm.y);
+  HIP_TRY(c, hipMemcpyAsync(out, M.logits + (size_t)lm.x * vocab, sizeof(float) * rows * vocab, hipMemcpyDeviceToHost,
+                            c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   return PARD_OK;
 }

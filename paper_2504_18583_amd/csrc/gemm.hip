@@ -62,13 +62,6 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
-// Slot of key (pos % 32) inside its 32-key block of the transposed V cache:
-// attention's P^T fragment holds keys {4g..4g+3, 16+4g..16+4g+3} in lane
-// group g, so those eight keys are stored contiguously at 8g..8g+7.
-__device__ __forceinline__ int v_slot(int k) {
-  return (k & 16) ? ((k & 12) << 1) + 4 + (k & 3) : ((k & 12) << 1) + (k & 3);
-}
-
 template <int MT, int S, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
@@ -122,22 +115,24 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   if (n_it > 0) load_w(w0, 0);
   __builtin_amdgcn_sched_barrier(0);
 
-  const FwdDesc d = *p.desc;
-  const int row_begin = p.lm_mode ? d.lm_row0 : 0;
-  const int row_count = p.lm_mode ? d.lm_rows : d.n_rows;
+  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
+  const FwdDesc* dp = p.desc;
+  const int row_count = LM ? dp->n_lm : dp->n_rows;
 
   // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at
   // 8*(lane/16); A is k-blocked, so k-block kb of all rows is one contiguous
-  // run at kb * kMaxRows * 64 bytes.  Rows past the pass get an offset beyond
-  // the buffer: the hardware returns zeros for them without a memory access.
+  // run at kb * act_rows * 64 bytes.  Rows past the pass get an offset
+  // beyond the buffer: the hardware returns zeros for them without a memory
+  // access.  lm rows read their source row.
   const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(p.A), 0, kMaxRows * p.lda * 2, kRsrcWord3);
+      const_cast<uint16_t*>(p.A), 0, p.act_rows * p.lda * 2, kRsrcWord3);
   constexpr int kOutOfRange = 0x7FFFFFF0;
   int a_voff[MT];
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int r = mt * 16 + (lane & 15);
-    a_voff[mt] = r < row_count ? (row_begin + r) * 64 + (lane >> 4) * 16 : kOutOfRange;
+    const int src = r < row_count ? (LM ? dp->lm_src[r] : r) : 0;
+    a_voff[mt] = r < row_count ? src * 64 + (lane >> 4) * 16 : kOutOfRange;
   }
   auto load_a = [&](u32x4 (&a)[U][MT], int its) {
 #pragma unroll
@@ -145,7 +140,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       const int kb = wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
-        a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (kMaxRows * 64), 0);
+        a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (p.act_rows * 64), 0);
     }
   };
   auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int its) {
@@ -172,13 +167,13 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       e2[j] = float2{1.f, 0.f};
       if constexpr (EPI == EPI_RESID) {
         if (epi && row < row_count) {
-          e0[j] = p.x[(size_t)(row_begin + row) * p.ldx + n];
+          e0[j] = p.x[(size_t)row * p.ldx + n];
           e1[j] = p.g_next[n];
         }
       } else if constexpr (EPI == EPI_QKV) {
         if (epi && p.bias) e0[j] = p.bias[n];
         if (epi && row < row_count && n < p.q_dim + p.kv_dim)
-          e2[j] = p.rope[(size_t)(d.pos0 + row) * (p.hd / 2) + ((n % p.hd) >> 1)];
+          e2[j] = p.rope[(size_t)dp->pos[row] * (p.hd / 2) + ((n % p.hd) >> 1)];
       }
     }
   };
@@ -202,14 +197,14 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   auto row_scales = [&]() {
     if (tid < 256) {
       for (int r = tid >> 4; r < MT * 16; r += 16) {
-        const int row = min(row_begin + r, kMaxRows - 1);
+        const int row = r < row_count ? (LM ? dp->lm_src[r] : r) : 0;
         float t = 0.f;
         for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 256) {
           float part[16];
 #pragma unroll
           for (int u = 0; u < 16; ++u) {
             const int q = q0 + 16 * u;
-            part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxRows + row] : 0.f;
+            part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
           }
 #pragma unroll
           for (int u = 0; u < 16; ++u) t += part[u];
@@ -275,7 +270,6 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 
   if constexpr (EPI == EPI_QKV) {
     if (!epi) return;   // no barrier follows in this epilogue
-    const int pos0 = d.pos0;
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       const int s = j / MT, mt = j % MT;
@@ -284,7 +278,8 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       float y = v[j] * rs_s[row] + e0[j];            // + bias
       const float partner = __shfl_xor(y, 1);
       if (row < row_count) {
-        const int pos = pos0 + row;
+        const int pos = dp->pos[row];
+        const size_t cache = (size_t)dp->slot[row] * p.kv_seq_stride;
         if (n < p.q_dim + p.kv_dim) {
           const float2 cs = e2[j];                     // rotary (cos, sin) of (pos, pair)
           y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
@@ -294,11 +289,11 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
           p.out[(size_t)row * p.ld_out + n] = b;
         } else if (n < p.q_dim + p.kv_dim) {
           const int c = n - p.q_dim;
-          p.kc[(size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd)] = b;
+          p.kc[cache + (size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd)] = b;
         } else {
           const int c = n - p.q_dim - p.kv_dim;
           const size_t blk = (size_t)(c / p.hd) * (p.cap / 32) + (pos >> 5);
-          p.vc[(blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31)] = b;
+          p.vc[cache + (blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31)] = b;
         }
       }
     }
@@ -313,17 +308,17 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       const int row = mt * 16 + rsub;
       const int n = (tile * S + s) * 16 + csub;
       if (row < row_count) {
-        const size_t o = (size_t)(row_begin + row) * p.ldx + n;
+        const size_t o = (size_t)row * p.ldx + n;
         const float xn = e0[j] + v[j];                 // residual + projection
         p.x[o] = xn;
-        p.xg[act_index(row_begin + row, n)] = f16_bits(xn * e1[j]);
+        p.xg[act_index(row, n, p.act_rows)] = f16_bits(xn * e1[j]);
         sq[mt] += xn * xn;
       }
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const float t = sum16(sq[mt]);
-      if (csub == 0) p.ss_out[(size_t)tile * kMaxRows + mt * 16 + rsub] = t;
+      if (csub == 0) p.ss_out[(size_t)tile * kMaxPassRows + mt * 16 + rsub] = t;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
     if (!epi) return;   // no barrier follows in this epilogue
@@ -336,7 +331,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * (S / 2) + q) * 16 + csub;
-        if (row < row_count) p.out[act_index(row, f)] = f16_bits(h);
+        if (row < row_count) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
       }
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;
@@ -367,16 +362,19 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
       }
       if (lane == 0) {
-        p.amax_val[(size_t)r * p.n_tiles + tile] = bv;
-        p.amax_idx[(size_t)r * p.n_tiles + tile] = (bi == INT_MAX) ? INT_MAX : tile * TW + bi;
+        p.amax_val[(size_t)r * p.amax_stride + tile] = bv;
+        p.amax_idx[(size_t)r * p.amax_stride + tile] = (bi == INT_MAX) ? INT_MAX : tile * TW + bi;
       }
     }
   }
 }
 
-// Step tail, run by one thread once every argmax of the pass is known.
-__device__ void run_tail(const TailArgs& p, const FwdDesc& d, const int* res) {
-  SeqState* s = p.seq;
+// Decode-state update of one sequence once the argmax of its lm rows is
+// known (one thread).  Draft: store the candidates, commit only the real rows
+// (the mask rows are never committed).  Verify: longest agreeing prefix a
+// (eq. 2), bonus t_a, L_t += a + 1, emit the a + 1 tokens.
+__device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
+  SeqState* s = p.states + ps.slot;
   if (p.tail == TAIL_PREFILL) {
     s->bonus = res[0];
     s->t[0] = res[0];
@@ -385,15 +383,7 @@ __device__ void run_tail(const TailArgs& p, const FwdDesc& d, const int* res) {
   } else if (p.tail == TAIL_DRAFT) {
     const int k = s->k;
     for (int i = 0; i < k; ++i) s->cand[i] = res[i];
-    s->L[1] = d.pos0 + d.n_real;                   // mask rows are not committed
-    FwdDesc* nd = p.next_desc;                      // verify pass: [pending, c_1..c_k]
-    nd->ids[0] = s->bonus;
-    for (int i = 0; i < k; ++i) nd->ids[1 + i] = res[i];
-    nd->n_rows = k + 1;
-    nd->n_real = k + 1;
-    nd->pos0 = s->L[0];
-    nd->lm_row0 = 0;
-    nd->lm_rows = k + 1;
+    s->L[1] = ps.pos0 + ps.n_real;
   } else if (p.tail == TAIL_VERIFY) {
     const int k = s->k;
     int a = 0;
@@ -402,51 +392,134 @@ __device__ void run_tail(const TailArgs& p, const FwdDesc& d, const int* res) {
     for (int i = 0; i <= k; ++i) s->t[i] = res[i];
     s->a = a;
     s->bonus = bonus;
-    s->L[0] = d.pos0 + a + 1;                      // keep pending + accepted rows
+    s->L[0] = ps.pos0 + a + 1;                     // keep pending + accepted rows
     for (int i = 0; i < a; ++i) s->pending[i] = s->cand[i];
     s->pending[a] = bonus;
     s->n_pending = a + 1;
     if (p.out_tokens) {
+      int* out = p.out_tokens + (size_t)ps.slot * p.out_cap;
       for (int i = 0; i <= a; ++i) {
-        if (s->n_out < p.out_cap) p.out_tokens[s->n_out] = s->pending[i];
+        if (s->n_out < p.out_cap) out[s->n_out] = s->pending[i];
         ++s->n_out;
       }
     }
     ++s->steps;
     ++s->accept_hist[a];
-    FwdDesc* nd = p.next_desc;
-    if (k > 0) {                                    // next draft: pending + k-1 masks
-      int n = 0;
-      for (int i = 0; i <= a; ++i) nd->ids[n++] = s->pending[i];
-      for (int i = 0; i < k - 1; ++i) nd->ids[n++] = s->mask_id;
-      nd->n_rows = n;
-      nd->n_real = a + 1;
-      nd->pos0 = s->L[1];
-      nd->lm_row0 = a;
-      nd->lm_rows = k;
-    } else {                                        // plain target step
-      nd->ids[0] = bonus;
-      nd->n_rows = 1;
-      nd->n_real = 1;
-      nd->pos0 = s->L[0];
-      nd->lm_row0 = 0;
-      nd->lm_rows = 1;
-    }
   }
 }
 
-// One workgroup of 1024 threads: wave w reduces lm rows w, w+16, ... over
-// tiles, 16 independent loads per lane in flight at a time.
+// Rows of one sequence in the pass that follows a draft pass (the verify
+// pass: [pending, c_1..c_k] at L_t), a verify pass with k > 0 (the next draft
+// pass: the a+1 pending tokens and k-1 mask rows at L_d, lm rows from the last
+// pending row on) or a verify pass with k = 0 (the next plain target step).
+__device__ void next_rows(int after, const SeqState& s, int* n_rows, int* n_real, int* pos0, int* lm_first,
+                          int* lm_rows) {
+  const int k = s.k;
+  if (after == TAIL_DRAFT) {
+    *n_rows = k + 1; *n_real = k + 1; *pos0 = s.L[0]; *lm_first = 0; *lm_rows = k + 1;
+  } else if (k > 0) {
+    *n_rows = s.n_pending + k - 1; *n_real = s.n_pending; *pos0 = s.L[1]; *lm_first = s.n_pending - 1; *lm_rows = k;
+  } else {
+    *n_rows = 1; *n_real = 1; *pos0 = s.L[0]; *lm_first = 0; *lm_rows = 1;
+  }
+}
+
+__device__ int next_id(int after, const SeqState& s, int i) {
+  if (after == TAIL_DRAFT) return i == 0 ? s.bonus : s.cand[i - 1];
+  if (s.k > 0) return i < s.n_pending ? s.pending[i] : s.mask_id;
+  return s.bonus;
+}
+
+// Stages the next pass of the step for the sequences of the current pass, in
+// the same order (run by a whole workgroup).  With drop_done, sequences that
+// have written all requested tokens leave the batch.  The current pass's
+// sequence list is read before anything is written, so the next descriptor
+// may be the current one (plain target steps).
+__device__ void stage_next(const TailArgs& p, bool drop_done) {
+  __shared__ int sl[kMaxPassSeqs], r0[kMaxPassSeqs + 1], l0[kMaxPassSeqs + 1];
+  __shared__ int n_next_s;
+  const int tid = threadIdx.x, nth = blockDim.x;
+  const int after = p.tail;
+  if (tid == 0) {
+    const int n_cur = p.desc->n_seq;
+    int n = 0, rows = 0, lm = 0;
+    for (int j = 0; j < n_cur; ++j) {
+      const int slot = p.desc->seq[j].slot;
+      const SeqState& s = p.states[slot];
+      if (drop_done && after == TAIL_VERIFY && s.n_out >= s.n_target) {
+        // its logits are overwritten by the passes that follow without it
+        p.lm_map[slot] = int2{0, 0};
+        if (p.lm_map_draft) p.lm_map_draft[slot] = int2{0, 0};
+        continue;
+      }
+      int nr, nreal, pos0, lmf, lmr;
+      next_rows(after, s, &nr, &nreal, &pos0, &lmf, &lmr);
+      sl[n] = slot;
+      r0[n] = rows;
+      l0[n] = lm;
+      rows += nr;
+      lm += lmr;
+      ++n;
+    }
+    r0[n] = rows;
+    l0[n] = lm;
+    n_next_s = n;
+  }
+  __syncthreads();
+  const int n = n_next_s;
+  FwdDesc* nd = p.next_desc;
+  for (int j = tid; j < n; j += nth) {
+    const SeqState& s = p.states[sl[j]];
+    PassSeq q{};
+    int lmf;
+    next_rows(after, s, &q.n_rows, &q.n_real, &q.pos0, &lmf, &q.lm_rows);
+    q.slot = sl[j];
+    q.row0 = r0[j];
+    q.lm0 = l0[j];
+    nd->seq[j] = q;
+  }
+  // rows and lm rows: a thread finds its sequence by binary search over the
+  // row offsets
+  for (int r = tid; r < r0[n]; r += nth) {
+    int lo = 0, hi = n - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (r0[mid] <= r) lo = mid; else hi = mid - 1;
+    }
+    const SeqState& s = p.states[sl[lo]];
+    int nr, nreal, pos0, lmf, lmr;
+    next_rows(after, s, &nr, &nreal, &pos0, &lmf, &lmr);
+    const int i = r - r0[lo];
+    nd->ids[r] = next_id(after, s, i);
+    nd->pos[r] = pos0 + i;
+    nd->slot[r] = sl[lo];
+    if (i >= lmf && i < lmf + lmr) nd->lm_src[l0[lo] + i - lmf] = r;
+  }
+  if (tid == 0) {
+    nd->n_rows = r0[n];
+    nd->n_seq = n;
+    nd->n_lm = l0[n];
+  }
+}
+
+// Second argmax pass and step tail.  Workgroup j serves sequence j of the
+// pass: wave w reduces its lm rows w, w+16, ... over the tiles, 16
+// independent loads per lane in flight at a time; then one thread updates
+// the sequence's decode state.  A single-sequence pass also stages the next
+// pass here; batched passes stage it in k_stage.
 __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
-  __shared__ int res_s[kMaxLmRows];
+  __shared__ int res_s[kMaxK + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const FwdDesc d = *p.desc;
-  const int rows = d.lm_rows;
+  const FwdDesc* dp = p.desc;
+  const int sj = blockIdx.x;
+  if (sj >= dp->n_seq) return;                    // uniform: the whole block leaves
+  const PassSeq ps = dp->seq[sj];
+  const int rows = min(ps.lm_rows, kMaxK + 1);
   for (int r = wave; r < rows; r += 16) {
     float bv = -INFINITY;
     int bi = INT_MAX;
-    const float* vals = p.amax_val + (size_t)r * p.n_tiles;
-    const int* idxs = p.amax_idx + (size_t)r * p.n_tiles;
+    const float* vals = p.amax_val + (size_t)(ps.lm0 + r) * p.n_tiles;
+    const int* idxs = p.amax_idx + (size_t)(ps.lm0 + r) * p.n_tiles;
     for (int t0 = lane; t0 < p.n_tiles; t0 += 64 * 16) {
       float xv[16];
       int xi[16];
@@ -469,9 +542,392 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
   }
   __syncthreads();
   if (tid == 0) {
-    for (int r = 0; r < rows; ++r) p.result[r] = res_s[r];
-    run_tail(p, d, res_s);
+    for (int r = 0; r < rows; ++r) p.result[ps.lm0 + r] = res_s[r];
+    p.lm_map[ps.slot] = int2{ps.lm0, rows};
+    seq_tail(p, ps, res_s);
   }
+  if (gridDim.x == 1 && p.next_desc) {
+    __syncthreads();
+    stage_next(p, false);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_stage(const TailArgs p) { stage_next(p, true); }
+
+// ============================================================================
+// Row-block GEMM: passes of more than kMaxRows rows (batched decode passes,
+// where the GEMMs are dense contractions at a few hundred rows).
+//
+// A workgroup of kRowsWaves wavefronts owns kRowTiles*16 (96) rows x 16
+// strips (256 columns) over one input range.  The block's rows of A are staged
+// in LDS, two k-blocks (12 KiB) per stage, and shared by the wavefronts; each
+// wavefront streams its own 4 strips of W from HBM straight into the MFMA
+// B-operand registers and accumulates 6 x 4 tiles of 16x16 (per k-block:
+// 6 KiB of LDS reads and 4 KiB of weights for 24 MFMAs).  Row tiles past the
+// pass's rows skip their MFMAs; row blocks past them leave at once.
+//
+// Blocks are numbered so that the row blocks of one column tile run on the
+// same XCD at about the same time (the hardware deals block i to XCD i % 8):
+// the later blocks' weight reads then hit that XCD's L2 rather than HBM.
+// Narrow GEMMs split the input dimension (ksplit > 1) to fill the chip; each
+// split writes an fp32 partial tile and k_gemm_rows_red adds them in split
+// order and runs the epilogue, so results are deterministic.
+// ============================================================================
+
+typedef f32x4 RowsAcc[kRowTiles][kRowsWaveStrips];
+
+// 1/rms of the block's rows from the producer's per-tile sums of squares
+// (fixed order), 16 threads per row.
+template <bool LM>
+__device__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s) {
+  const int tid = threadIdx.x;
+  for (int r = tid >> 4; r < kRowTiles * 16; r += blockDim.x >> 4) {
+    const int gr = row0 + r;
+    const int row = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
+    float t = 0.f;
+    for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 256) {
+      float part[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int q = q0 + 16 * u;
+        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) t += part[u];
+    }
+    t += __shfl_xor(t, 8);
+    t += __shfl_xor(t, 4);
+    t += __shfl_xor(t, 2);
+    t += __shfl_xor(t, 1);
+    if ((tid & 15) == 0) rs_s[r] = 1.0f / sqrtf(t * p.inv_k + p.eps);
+  }
+}
+
+// Epilogue of one wavefront's accumulators.  Lane l holds, for row tile mt and
+// strip s, column (strip*16 + l%16) of rows mt*16 + 4*(l/16) + i.
+template <int EPI>
+__device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc, int tile, int row0, int row_count,
+                              int mt_live, int wave, int lane, const float* rs_s) {
+  const int c16 = lane & 15, g4 = lane >> 4;
+  const int strip0 = tile * kRowsTileStrips + wave * kRowsWaveStrips;
+  if constexpr (EPI == EPI_QKV) {
+#pragma unroll
+    for (int mt = 0; mt < kRowTiles; ++mt) {
+      if (mt >= mt_live) break;                      // uniform
+#pragma unroll
+      for (int s = 0; s < kRowsWaveStrips; ++s) {
+        const int n = (strip0 + s) * 16 + c16;
+        const bool col_ok = strip0 + s < p.n_strips;
+        const float bias = (col_ok && p.bias) ? p.bias[n] : 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
+          float y = acc[mt][s][i] * rs_s[rl] + bias;
+          const float partner = __shfl_xor(y, 1);
+          if (col_ok && r < row_count) {
+            const int pos = dp->pos[r];
+            const size_t cache = (size_t)dp->slot[r] * p.kv_seq_stride;
+            if (n < p.q_dim + p.kv_dim) {
+              const float2 cs = p.rope[(size_t)pos * (p.hd / 2) + ((n % p.hd) >> 1)];
+              y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
+            }
+            const uint16_t b = f16_bits(y);
+            if (n < p.q_dim) {
+              p.out[(size_t)r * p.ld_out + n] = b;
+            } else if (n < p.q_dim + p.kv_dim) {
+              const int c = n - p.q_dim;
+              p.kc[cache + (size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd)] = b;
+            } else {
+              const int c = n - p.q_dim - p.kv_dim;
+              const size_t blk = (size_t)(c / p.hd) * (p.cap / 32) + (pos >> 5);
+              p.vc[cache + (blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31)] = b;
+            }
+          }
+        }
+      }
+    }
+  } else if constexpr (EPI == EPI_RESID) {
+    float* ss = p.ss_out + (size_t)(tile * kRowsWaves + wave) * kMaxPassRows;
+#pragma unroll
+    for (int mt = 0; mt < kRowTiles; ++mt) {
+      if (mt >= mt_live) break;                      // uniform
+      float sq[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < kRowsWaveStrips; ++s) {
+        const int n = (strip0 + s) * 16 + c16;
+        if (strip0 + s >= p.n_strips) continue;      // uniform
+        const float g = p.g_next[n];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int r = row0 + mt * 16 + g4 * 4 + i;
+          if (r < row_count) {
+            const size_t o = (size_t)r * p.ldx + n;
+            const float xn = p.x[o] + acc[mt][s][i];   // residual + projection
+            p.x[o] = xn;
+            p.xg[act_index(r, n, p.act_rows)] = f16_bits(xn * g);
+            sq[i] += xn * xn;
+          }
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float t = sum16(sq[i]);
+        const int r = row0 + mt * 16 + g4 * 4 + i;
+        if (c16 == 0 && r < row_count) ss[r] = t;
+      }
+    }
+  } else if constexpr (EPI == EPI_SWIGLU) {
+#pragma unroll
+    for (int mt = 0; mt < kRowTiles; ++mt) {
+      if (mt >= mt_live) break;                      // uniform
+#pragma unroll
+      for (int q = 0; q < kRowsWaveStrips / 2; ++q) {
+        if (strip0 + 2 * q >= p.n_strips) continue;  // uniform
+        const int f = ((strip0 >> 1) + q) * 16 + c16;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
+          const float gt = acc[mt][2 * q][i] * rs_s[rl];
+          const float up = acc[mt][2 * q + 1][i] * rs_s[rl];
+          const float h = gt / (1.0f + expf(-gt)) * up;
+          if (r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_bits(h);
+        }
+      }
+    }
+  } else {  // EPI_LOGITS
+#pragma unroll
+    for (int mt = 0; mt < kRowTiles; ++mt) {
+      if (mt >= mt_live) break;                      // uniform
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
+        float bv = -INFINITY;
+        int bi = INT_MAX;
+#pragma unroll
+        for (int s = 0; s < kRowsWaveStrips; ++s) {
+          const int n = (strip0 + s) * 16 + c16;
+          if (strip0 + s >= p.n_strips) continue;    // uniform
+          const float val = acc[mt][s][i] * rs_s[rl];
+          if (r < row_count) p.logits[(size_t)r * p.vocab + n] = val;
+          if (better(val, n, bv, bi)) { bv = val; bi = n; }
+        }
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) {
+          const float ov = __shfl_xor(bv, off);
+          const int oi = __shfl_xor(bi, off);
+          if (better(ov, oi, bv, bi)) { bv = ov; bi = oi; }
+        }
+        if (c16 == 0 && r < row_count) {
+          p.amax_val[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = bv;
+          p.amax_idx[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = bi;
+        }
+      }
+    }
+  }
+}
+
+// Block id -> (column tile, input split, row block), row blocks fastest and
+// consecutive ids on one XCD.
+__device__ __forceinline__ void rows_block(const GemmArgs& p, int* tile, int* ks, int* mb) {
+  const int G = gridDim.x, bid = blockIdx.x;
+  const int per = G / 8, rem = G % 8, xcd = bid % 8, slot = bid / 8;
+  const int lid = xcd * per + min(xcd, rem) + slot;
+  *mb = lid % p.m_blocks;
+  const int rest = lid / p.m_blocks;
+  *ks = rest % p.ksplit;
+  *tile = rest / p.ksplit;
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
+  constexpr int MB = kRowTiles, NS = kRowsWaveStrips;
+  constexpr int U = 2;                               // k-blocks per stage
+  constexpr int AE = U * MB * 64;                    // 16-byte A elements per stage
+  constexpr int AJ = (AE + 255) / 256;               // per thread
+  __shared__ __attribute__((aligned(16))) u32x4 a_lds[2][U][MB * 64];
+  __shared__ float rs_s[MB * 16];
+
+  int tile, ks, mb;
+  rows_block(p, &tile, &ks, &mb);
+  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
+  const FwdDesc* dp = p.desc;
+  const int row_count = LM ? dp->n_lm : dp->n_rows;
+  const int row0 = mb * MB * 16;
+  if (row0 >= row_count) return;                     // uniform: the whole block leaves
+  const int mt_live = min(MB, (row_count - row0 + 15) / 16);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kb0 = ks * p.kb_total / p.ksplit, kb1 = (ks + 1) * p.kb_total / p.ksplit;
+  const int n_kb = kb1 - kb0;
+  const int n_st = (n_kb + U - 1) / U;
+
+  // W: this wavefront's strips, block (kb, strip) at (kb * n_strips + strip) KiB
+  const int strip0 = tile * kRowsTileStrips + wave * NS;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.W), 0, (int)min((size_t)p.n_strips * p.kb_total * 1024, (size_t)0x7fffffff),
+      kRsrcWord3);
+  const int w_voff = (strip0 * 64 + lane) * 16;
+  int ns_live = min(NS, p.n_strips - strip0);        // strips of this wavefront inside W
+  ns_live = max(ns_live, 0);
+  u32x4 w0[U][NS], w1[U][NS];
+  auto load_w = [&](u32x4 (&w)[U][NS], int st) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int kb = kb0 + min(st * U + u, n_kb - 1);
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        w[u][s] = s < ns_live
+                      ? __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT)
+                      : u32x4{0u, 0u, 0u, 0u};
+    }
+  };
+
+  // A: element e of a stage is 16 bytes of row (e / 4) % (16 MB), k-block e / (64 MB)
+  const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.A), 0, p.act_rows * p.lda * 2, kRsrcWord3);
+  constexpr int kOutOfRange = 0x7FFFFFF0;
+  int a_voff[AJ];
+#pragma unroll
+  for (int j = 0; j < AJ; ++j) {
+    const int e = tid + 256 * j;
+    const int rr = (e % (MB * 64)) >> 2, part = e & 3;
+    const int gr = row0 + rr;
+    const int src = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
+    a_voff[j] = (e < AE && gr < row_count) ? src * 64 + part * 16 : kOutOfRange;
+  }
+  u32x4 areg[AJ];
+  auto load_a = [&](int st) {
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+      const int e = tid + 256 * j;
+      const int u = e / (MB * 64);
+      const int kb = kb0 + min(st * U + u, n_kb - 1);
+      areg[j] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[j], kb * (p.act_rows * 64), 0);
+    }
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+      const int e = tid + 256 * j;
+      if (e < AE) a_lds[buf][e / (MB * 64)][e % (MB * 64)] = areg[j];
+    }
+  };
+
+  RowsAcc acc;
+#pragma unroll
+  for (int mt = 0; mt < MB; ++mt)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int buf, const u32x4 (&w)[U][NS], int st) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (st * U + u >= n_kb) break;                 // uniform
+#pragma unroll
+      for (int mt = 0; mt < MB; ++mt) {
+        if (mt >= mt_live) break;                    // uniform
+        const u32x4 av = a_lds[buf][u][(mt * 16 + (lane & 15)) * 4 + (lane >> 4)];
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+          acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av),
+                                                              __builtin_bit_cast(f16x8, w[u][s]), acc[mt][s], 0, 0, 0);
+      }
+    }
+  };
+
+  if (n_st > 0) {
+    load_w(w0, 0);
+    load_a(0);
+    store_a(0);
+    if (n_st > 1) load_w(w1, 1);
+    __syncthreads();
+    for (int st = 0; st < n_st; ++st) {
+      const int buf = st & 1;
+      if (st + 1 < n_st) load_a(st + 1);
+      __builtin_amdgcn_sched_barrier(0);
+      if (buf == 0) {
+        compute(0, w0, st);
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 2 < n_st) load_w(w0, st + 2);
+      } else {
+        compute(1, w1, st);
+        __builtin_amdgcn_sched_barrier(0);
+        if (st + 2 < n_st) load_w(w1, st + 2);
+      }
+      if (st + 1 < n_st) store_a(buf ^ 1);
+      __syncthreads();
+    }
+  }
+
+  if (p.ksplit > 1) {
+    // partial tile of this split, in register order (coalesced)
+    float* part = p.part + ((size_t)(tile * p.m_blocks + mb) * p.ksplit + ks) * kRowsPartFloats;
+#pragma unroll
+    for (int mt = 0; mt < MB; ++mt) {
+      if (mt >= mt_live) break;                      // uniform
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        *reinterpret_cast<f32x4*>(part + (((wave * MB + mt) * NS + s) * 64 + lane) * 4) = acc[mt][s];
+    }
+    return;
+  }
+  if constexpr (EPI != EPI_RESID) {
+    rows_scales<LM>(p, dp, row0, row_count, rs_s);
+    __syncthreads();
+  }
+  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, mt_live, wave, lane, rs_s);
+}
+
+// Sum of the input splits of k_gemm_rows in split order, then the epilogue.
+template <int EPI>
+__global__ __launch_bounds__(256) void k_gemm_rows_red(const GemmArgs p) {
+  constexpr int MB = kRowTiles, NS = kRowsWaveStrips;
+  __shared__ float rs_s[MB * 16];
+  const int tile = blockIdx.x / p.m_blocks, mb = blockIdx.x % p.m_blocks;
+  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
+  const FwdDesc* dp = p.desc;
+  const int row_count = LM ? dp->n_lm : dp->n_rows;
+  const int row0 = mb * MB * 16;
+  if (row0 >= row_count) return;                     // uniform
+  const int mt_live = min(MB, (row_count - row0 + 15) / 16);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  if constexpr (EPI != EPI_RESID) rows_scales<LM>(p, dp, row0, row_count, rs_s);
+  const float* base = p.part + (size_t)(tile * p.m_blocks + mb) * p.ksplit * kRowsPartFloats;
+  RowsAcc acc;
+#pragma unroll
+  for (int mt = 0; mt < MB; ++mt) {
+#pragma unroll
+    for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (mt >= mt_live) continue;                     // uniform
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const size_t o = (size_t)(((wave * MB + mt) * NS + s) * 64 + lane) * 4;
+      for (int k = 0; k < p.ksplit; ++k) acc[mt][s] += *reinterpret_cast<const f32x4*>(base + k * kRowsPartFloats + o);
+    }
+  }
+  if constexpr (EPI != EPI_RESID) __syncthreads();
+  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, mt_live, wave, lane, rs_s);
+}
+
+template <int EPI>
+hipError_t launch_rows(const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
+  const int grid = a.n_tiles * a.m_blocks * a.ksplit;
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_gemm_rows<EPI>, dim3(grid), dim3(256), 0u, st, ev.start, a.ksplit > 1 ? nullptr : ev.stop,
+                          0u, a);
+  } else {
+    k_gemm_rows<EPI><<<grid, 256, 0, st>>>(a);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.ksplit == 1) return e;
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_gemm_rows_red<EPI>, dim3(a.n_tiles * a.m_blocks), dim3(256), 0u, st, nullptr, ev.stop,
+                          0u, a);
+  } else {
+    k_gemm_rows_red<EPI><<<a.n_tiles * a.m_blocks, 256, 0, st>>>(a);
+  }
+  return hipGetLastError();
 }
 
 template <int EPI, int MT, int S>
@@ -521,8 +977,28 @@ hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStr
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_tail(const TailArgs& a, hipStream_t st) {
-  k_lm_tail<<<1, 1024, 0, st>>>(a);
+hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
+  if (a.n_tiles < 1 || a.m_blocks < 1 || a.ksplit < 1 || a.ksplit > a.kb_total) return hipErrorInvalidValue;
+  if (a.n_tiles * kRowsTileStrips < a.n_strips || (a.ksplit > 1 && !a.part)) return hipErrorInvalidValue;
+  if ((size_t)a.n_tiles * a.m_blocks * a.ksplit >= (1u << 31)) return hipErrorInvalidValue;
+  if (a.m_blocks * kRowTiles * 16 > kMaxPassRows + kRowTiles * 16) return hipErrorInvalidValue;
+  switch (epi) {
+    case EPI_QKV: return launch_rows<EPI_QKV>(a, st, ev);
+    case EPI_RESID: return launch_rows<EPI_RESID>(a, st, ev);
+    case EPI_SWIGLU: return launch_rows<EPI_SWIGLU>(a, st, ev);
+    case EPI_LOGITS: return launch_rows<EPI_LOGITS>(a, st, ev);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st) {
+  if (n_seq < 1 || n_seq > kMaxPassSeqs) return hipErrorInvalidValue;
+  k_lm_tail<<<n_seq, 1024, 0, st>>>(a);
+  return hipGetLastError();
+}
+
+hipError_t launch_stage(const TailArgs& a, hipStream_t st) {
+  k_stage<<<1, 256, 0, st>>>(a);
   return hipGetLastError();
 }
 

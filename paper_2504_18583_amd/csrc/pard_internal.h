@@ -25,9 +25,9 @@
 //     fp16 and the GEMMs run fp16 MFMAs: a 10-bit mantissa on the activation
 //     side (bf16 activations drift past the logit tolerance at 8B width and
 //     depth).  They are k-blocked: element (row, k)
-//     sits at act_index(row, k), i.e. the 64 row slots of one 32-column block
-//     are contiguous (64 bytes per row), so the MFMA A fragment of one k-block
-//     is one contiguous run of rows * 64 bytes.
+//     sits at act_index(row, k, slots), i.e. the row slots of one 32-column
+//     block are contiguous (64 bytes per row), so the MFMA A fragment of one
+//     k-block is one contiguous run of rows * 64 bytes.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -36,16 +36,28 @@
 namespace pard {
 
 constexpr int kMaxK = 32;
-constexpr int kMaxRows = 64;      // rows of one forward pass (prefill chunk, 2*max_k)
-constexpr int kMaxLmRows = kMaxK + 1;
+constexpr int kMaxRows = 64;          // rows of a pass served by the skinny GEMM (prefill chunk)
+constexpr int kMaxPassRows = 512;     // rows of one forward pass over all of its sequences
+constexpr int kMaxPassSeqs = 64;      // sequences in one pass
+constexpr int kMaxLmRows = kMaxPassRows;
+// row-block GEMM: a workgroup of kRowsWaves wavefronts computes kRowTiles*16
+// rows x kRowsWaves*kRowsWaveStrips strips of 16 columns
+constexpr int kRowTiles = 6;
+constexpr int kRowsWaves = 4;
+constexpr int kRowsWaveStrips = 4;
+constexpr int kRowsTileStrips = kRowsWaves * kRowsWaveStrips;
+constexpr int kRowsPartFloats = kRowsWaves * kRowTiles * kRowsWaveStrips * 256;   // one partial tile
 constexpr int kBlock = 256;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
 constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
-constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head
+constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head and sequence
 
-// Position of activation element (row, k) in a k-blocked [kMaxRows x K] buffer.
-__host__ __device__ inline size_t act_index(int row, int k) {
-  return ((size_t)(k >> 5) * kMaxRows + row) * 32 + (k & 31);
+// Position of activation element (row, k) in a k-blocked buffer with `slots`
+// row slots per 32-column block: kMaxRows for passes served by the skinny
+// GEMM (so a decode pass's few rows stay close together), kMaxPassRows for the
+// row-block GEMM's passes.
+__host__ __device__ inline size_t act_index(int row, int k, int slots) {
+  return ((size_t)(k >> 5) * slots + row) * 32 + (k & 31);
 }
 
 // Position of element (key, dim) in one KV head's K cache region.
@@ -54,19 +66,40 @@ __host__ __device__ inline size_t k_index(int key, int dim, int hd) {
          (dim & 7);
 }
 
+// Slot of key (pos % 32) inside its 32-key block of the transposed V cache:
+// attention's P^T fragment holds keys {4g..4g+3, 16+4g..16+4g+3} in lane
+// group g, so those eight keys are stored contiguously at 8g..8g+7.
+__host__ __device__ inline int v_slot(int k) {
+  return (k & 16) ? ((k & 12) << 1) + 4 + (k & 3) : ((k & 12) << 1) + (k & 3);
+}
+
 // fp16 bits of v, nearest even.
 __device__ inline uint16_t f16_bits(float v) { return __builtin_bit_cast(uint16_t, (_Float16)v); }
 
-// Rows of the next forward pass of one model.  Written by the host (granular
-// calls) or by the tail of the previous pass (fused loop).
+// One sequence's share of a forward pass: rows [row0, row0 + n_rows) at
+// positions pos0.., of which the first n_real carry real tokens (committed
+// afterwards; the rest are the draft's mask rows); lm rows [lm0, lm0 +
+// lm_rows) of the pass's compacted lm_head rows belong to it.
+struct PassSeq {
+  int slot;       // sequence slot (KV cache, decode state)
+  int row0, n_rows, n_real, pos0;
+  int lm0, lm_rows;
+  int pad;
+};
+
+// Rows of the next forward pass of one model: one or several sequences, each
+// a contiguous run of rows.  Written by the host (granular calls, prefill) or
+// by the step tail of the previous pass (fused loop).
 struct FwdDesc {
-  int n_rows;     // rows in the pass
-  int n_real;     // leading rows that carry real tokens (committed afterwards)
-  int pos0;       // absolute position of row 0 (= committed KV length)
-  int lm_row0;    // first row fed to the lm_head
-  int lm_rows;    // rows fed to the lm_head
-  int pad[3];
-  int ids[kMaxRows];
+  int n_rows;                  // rows in the pass
+  int n_seq;                   // sequences in the pass
+  int n_lm;                    // rows fed to the lm_head
+  int pad;
+  PassSeq seq[kMaxPassSeqs];
+  int ids[kMaxPassRows];       // token id of each row
+  int pos[kMaxPassRows];       // absolute position of each row
+  int slot[kMaxPassRows];      // sequence slot of each row
+  int lm_src[kMaxPassRows];    // pass row of each lm row
 };
 
 // Decode state of one sequence slot.
@@ -88,53 +121,65 @@ enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3 };
 
 struct GemmArgs {
-  const uint16_t* W;      // strip-packed bf16 weight
+  const uint16_t* W;      // strip-packed weight (fp16 encoding)
   int kb_total;           // padded input dim / 32
-  int n_tiles;            // output tiles (S strips each) = grid size
+  int n_tiles;            // output column tiles
   const uint16_t* A;      // fp16 activations, k-blocked (act_index), lda columns
   int lda;
-  const FwdDesc* desc;
-  int lm_mode;            // 0: rows [0, n_rows)   1: rows [lm_row0, lm_row0 + lm_rows)
+  int act_rows;           // row slots of the pass's activation layout
+  const FwdDesc* desc;   // rows: the pass's rows; EPI_LOGITS: its lm rows (row j reads pass row lm_src[j])
   // RMSNorm of the A operand (QKV, SWIGLU, LOGITS): A already holds x*g in
-  // bf16; 1/rms comes from the producer's per-tile sums of squares.
+  // fp16; 1/rms comes from the producer's per-tile sums of squares.
   const float* ss_in; int ss_tiles;
   float eps, inv_k;
-  // EPI_RESID: x += Y, and for the next consumer xg = bf16(x * g_next) and
-  // per-tile sums of squares of x.
+  // EPI_RESID: x += Y, and for the next consumer xg = fp16(x * g_next) and
+  // per-tile sums of squares of x ([tile][kMaxPassRows]).
   float* x; int ldx;
   const float* g_next; uint16_t* xg; float* ss_out;
   // EPI_QKV / EPI_SWIGLU
   uint16_t* out; int ld_out;
-  uint16_t* kc; uint16_t* vc; int cap;
+  uint16_t* kc; uint16_t* vc; int cap;        // this layer's cache of slot 0
+  size_t kv_seq_stride;                       // elements between two slots' caches
   const float* bias; const float2* rope;
   int q_dim, kv_dim, hd;
   // EPI_LOGITS: fp32 logits and the per-tile (max, argmax) of every lm row
   float* logits; int vocab;
-  float* amax_val; int* amax_idx;
+  float* amax_val; int* amax_idx; int amax_stride;   // entries per lm row
+  // row-block GEMM (passes of more than kMaxRows rows): weight strips, row
+  // blocks, input splits and the fp32 partial tiles of split inputs
+  int n_strips;
+  int m_blocks, ksplit;
+  float* part;
 };
 
-// Second argmax pass over the lm_head tiles and the step tail (one workgroup).
+// Second argmax pass over the lm_head tiles and the step tail: one workgroup
+// per sequence of the pass.
 struct TailArgs {
   const FwdDesc* desc;
   const float* amax_val; const int* amax_idx;
-  int n_tiles, vocab;
+  int n_tiles, vocab;     // n_tiles: (max, argmax) entries per lm row
   int* result;            // argmax per lm row
   int tail;
-  SeqState* seq;
-  FwdDesc* next_desc;     // staged by the tail
-  int* out_tokens;        // emitted tokens of the fused loop (verify tail)
+  SeqState* states;       // decode state, indexed by slot
+  int2* lm_map;           // per slot: (first lm row, lm rows) of the last pass
+  int2* lm_map_draft;     // the draft's map (entries of sequences that leave a batch are cleared)
+  FwdDesc* next_desc;     // staged by the tail (single-sequence passes) or k_stage
+  int* out_tokens;        // emitted tokens of the fused loop, out_cap per slot (verify tail)
   int out_cap;
 };
 
 struct AttnArgs {
   const uint16_t* q; int ldq;                 // [rows][H_q*hd] fp16, pair-interleaved dims
-  const uint16_t* kc; const uint16_t* vc;     // this layer's cache of one sequence
+  const uint16_t* kc; const uint16_t* vc;     // this layer's cache of slot 0
+  size_t kv_seq_stride;                       // elements between two slots' caches
   int cap;                                    // KV capacity (multiple of 32)
   uint16_t* out;                              // fp16, k-blocked (act_index), H_q*hd columns
+  int act_rows;                               // row slots of the pass's activation layout
   const FwdDesc* desc;
   int n_heads, n_kv;
-  int nqt, n_qblocks;                         // 16*nqt query pairs per workgroup, query groups
+  int nqt, n_qblocks;                         // 16*nqt query pairs per workgroup, query groups per sequence
   int split_len, n_splits;                    // keys per chunk (multiple of 128), chunks
+  int n_seq;                                  // sequences the grid covers (>= the pass's)
   float scale;
   float* part;                                // chunk records when n_splits > 1
 };
@@ -147,7 +192,9 @@ struct LaunchEvents {
 // Launchers (return hipSuccess or the launch error).
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st,
                        LaunchEvents ev = LaunchEvents{});
-hipError_t launch_tail(const TailArgs& a, hipStream_t st);
+hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEvents ev = LaunchEvents{});
+hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st);
+hipError_t launch_stage(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
 size_t attn_part_floats(int head_dim, int nqt);
 int attn_max_q_tiles(int head_dim);

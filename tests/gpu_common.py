@@ -72,25 +72,47 @@ class Lockstep:
         return first
 
     def step(self):
+        """One step through the granular calls (pard_draft, pard_verify)."""
         from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
-        eng, seq, tag, k, step = self.eng, self.seq, self.tag, self.k, self.step_no
+        eng, seq, k = self.eng, self.seq, self.k
         if k > 0:
             cands = eng.draft(self.hist, k, seq=seq)
             g_dl = eng.read_logits(PARD_DRAFT, k, seq=seq)
+        else:
+            cands, g_dl = [], None
+        a, bonus = eng.verify(cands, seq=seq)
+        g_vl = eng.read_logits(PARD_TARGET, k + 1, seq=seq)
+        return self._check(cands, g_dl, g_vl, a, bonus)
+
+    def check_fused_step(self, tokens):
+        """Checks one step the fused loop has just run for this slot; `tokens`
+        are the slot's output (the pending token, then the a+1 new ones)."""
+        from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
+        eng, seq, k = self.eng, self.seq, self.k
+        assert tokens[0] == self.pending[-1], f"{self.tag}: pending token"
+        g_dl = eng.read_logits(PARD_DRAFT, k, seq=seq) if k > 0 else None
+        cands = [int(x) for x in np.argmax(g_dl, axis=-1)] if k > 0 else []
+        g_vl = eng.read_logits(PARD_TARGET, k + 1, seq=seq)
+        a, bonus = self._check(cands, g_dl, g_vl, None, None)
+        assert list(tokens[1:]) == list(cands[:a]) + [bonus], f"{self.tag}: emitted tokens"
+        return a, bonus
+
+    def _check(self, cands, g_dl, g_vl, a, bonus):
+        from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
+        eng, seq, tag, k, step = self.eng, self.seq, self.tag, self.k, self.step_no
+        if k > 0:
             _, o_dl = oracle.draft_step(self.draft, self.cache_d, self.pending, k, self.mask_id)
             self.worst = max(self.worst, assert_logits_close(g_dl, o_dl, f"{tag} step {step} draft logits"))
             assert_tokens_match(cands, o_dl, f"{tag} step {step} candidates")
             assert eng.kv_len(PARD_DRAFT, seq=seq) == self.cache_d.length == len(self.hist)
-        else:
-            cands = []
         cache_t = self.cache_t
         lt = cache_t.length
-        a, bonus = eng.verify(cands, seq=seq)
-        g_vl = eng.read_logits(PARD_TARGET, k + 1, seq=seq)
         o_a, o_bonus, o_t, o_vl = oracle.verify_step(self.target, cache_t, self.pending[-1], cands)
         self.worst = max(self.worst, assert_logits_close(g_vl, o_vl, f"{tag} step {step} verify logits"))
         # the GPU's decision is consistent with its own argmax ...
         g_t = np.argmax(g_vl, axis=-1)
+        if a is None:
+            a, bonus = oracle.accept_prefix(cands, g_t)
         assert (a, bonus) == oracle.accept_prefix(cands, g_t), f"{tag} step {step} accept rule"
         # ... and equals the oracle's wherever the inspected rows are not near-ties
         inspected = o_vl[:min(o_a, a) + 1]
@@ -104,6 +126,31 @@ class Lockstep:
         self.hist += self.pending
         self.step_no += 1
         return a, bonus
+
+
+class BatchLockstep:
+    """Several slots stepped together by the fused loop (one batched draft
+    pass and one batched verify pass per step), each slot checked against its
+    own oracle run."""
+
+    def __init__(self, eng, target, draft, prompts, k, mask_id, slots=None, tag=""):
+        self.eng, self.k = eng, k
+        self.slots = list(slots) if slots is not None else list(range(len(prompts)))
+        self.seqs = [Lockstep(eng, target, draft, p, k, mask_id, seq=s, tag=f"{tag} slot {s} (L={len(p)})")
+                     for s, p in zip(self.slots, prompts)]
+
+    @property
+    def worst(self):
+        return max(ls.worst for ls in self.seqs)
+
+    def prefill(self):
+        for ls in self.seqs:
+            ls.prefill()
+
+    def step(self, n_tokens):
+        res, stats = self.eng.generate_batch(self.slots, self.k, n_tokens, max_steps=1)
+        assert stats.steps == 1
+        return [ls.check_fused_step(toks) for ls, toks in zip(self.seqs, res)]
 
 
 def lockstep(eng, target, draft, prompt, k, steps, mask_id, seq=0, tag=""):

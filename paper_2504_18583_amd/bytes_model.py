@@ -60,3 +60,19 @@ def step_bytes(target, draft, k: int, accepted_prev: int, l_t: int, l_d: int) ->
 def gemm_bytes(n: int, k: int, rows: int, a_bytes: int = 4, out_bytes: int = 4) -> int:
     """One skinny GEMM: bf16 weight [n, k] once, activations in, results out."""
     return n * k * BF16 + rows * k * a_bytes + rows * n * out_bytes
+
+
+def batch_step_bytes(target, draft, k: int, contexts_t, contexts_d, pending) -> int:
+    """One batched step over several sequences: each weight once per pass, and
+    each sequence's own embedding rows and KV reads and writes (a forward_bytes
+    per sequence without the weights)."""
+    total = (streamed_params(target) + streamed_params(draft)) * BF16
+    for lt, ld, n_pend in zip(contexts_t, contexts_d, pending):
+        total += forward_bytes(target, k + 1, lt) - streamed_params(target) * BF16
+        total += forward_bytes(draft, n_pend + k - 1, ld) - streamed_params(draft) * BF16
+    return total
+
+
+def gemm_flops(spec, rows: int) -> int:
+    """Multiply-add flops of one forward's weight GEMMs (layers and lm_head) over ``rows`` rows."""
+    return 2 * rows * (streamed_params(spec) - spec.n_layers * 2 * spec.d_model - spec.d_model)

@@ -20,10 +20,10 @@ using namespace pard;
 
 namespace {
 
-constexpr int kPrefillRows = kMaxRows;
+constexpr int kPrefillRows = kMaxPassRows;   // prefill chunks run the row-block GEMM
 constexpr int kDescRing = 128;
 constexpr int kGatherMax = 4096;
-constexpr size_t kRowsPartBudget = 640;   // fp32 partial tiles of split row-block GEMMs (96 KiB each)
+constexpr size_t kRowsPartBudget = 512;   // fp32 partial tiles of split row-block GEMMs (144 KiB each)
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }

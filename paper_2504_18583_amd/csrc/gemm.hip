@@ -35,6 +35,7 @@
 #include <hip/hip_ext.h>
 
 #include <climits>
+#include <type_traits>
 
 namespace pard {
 namespace {
@@ -558,13 +559,15 @@ __global__ __launch_bounds__(256) void k_stage(const TailArgs p) { stage_next(p,
 // Row-block GEMM: passes of more than kMaxRows rows (batched decode passes,
 // where the GEMMs are dense contractions at a few hundred rows).
 //
-// A workgroup of kRowsWaves wavefronts owns kRowTiles*16 (96) rows x 16
-// strips (256 columns) over one input range.  The block's rows of A are staged
-// in LDS, two k-blocks (12 KiB) per stage, and shared by the wavefronts; each
-// wavefront streams its own 4 strips of W from HBM straight into the MFMA
-// B-operand registers and accumulates 6 x 4 tiles of 16x16 (per k-block:
-// 6 KiB of LDS reads and 4 KiB of weights for 24 MFMAs).  Row tiles past the
-// pass's rows skip their MFMAs; row blocks past them leave at once.
+// A workgroup of kRowsWaves wavefronts owns kRowTiles*16 (144) rows x 16
+// strips (256 columns) over one input range.  The block's rows of A pass
+// through LDS one k-block (9 KiB) at a time and are shared by the wavefronts;
+// each wavefront streams its own 4 strips of W from HBM straight into the MFMA
+// B-operand registers and accumulates 9 x 4 tiles of 16x16 (per k-block:
+// 9 KiB of LDS reads and 4 KiB of weights for 36 MFMAs).  Both operands go
+// through a register ring kRowsDepth k-blocks deep, so that several k-blocks
+// of loads are in flight while one is multiplied.  Row tiles past the pass's
+// rows skip their MFMAs; row blocks past them leave at once.
 //
 // Blocks are numbered so that the row blocks of one column tile run on the
 // same XCD at about the same time (the hardware deals block i to XCD i % 8):
@@ -576,10 +579,22 @@ __global__ __launch_bounds__(256) void k_stage(const TailArgs p) { stage_next(p,
 
 typedef f32x4 RowsAcc[kRowTiles][kRowsWaveStrips];
 
+// Compile-time loop: f(integral_constant<int, I>) for I in [B, E).  The row
+// tiles of an accumulator are walked this way so that every index is a
+// constant whatever the loop body's size: the accumulators then stay in
+// registers (a rolled loop would index them dynamically, in scratch memory).
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
+  }
+}
+
 // 1/rms of the block's rows from the producer's per-tile sums of squares
 // (fixed order), 16 threads per row.
 template <bool LM>
-__device__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s) {
+__device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s) {
   const int tid = threadIdx.x;
   for (int r = tid >> 4; r < kRowTiles * 16; r += blockDim.x >> 4) {
     const int gr = row0 + r;
@@ -603,17 +618,19 @@ __device__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int 
   }
 }
 
-// Epilogue of one wavefront's accumulators.  Lane l holds, for row tile mt and
-// strip s, column (strip*16 + l%16) of rows mt*16 + 4*(l/16) + i.
+// Epilogue of one wavefront's accumulators, row tiles [mt_lo, mt_live).  Lane
+// l holds, for row tile mt and strip s, column (strip*16 + l%16) of rows
+// mt*16 + 4*(l/16) + i.
 template <int EPI>
-__device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc, int tile, int row0, int row_count,
-                              int mt_live, int wave, int lane, const float* rs_s) {
+__device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc, int tile, int row0,
+                                              int row_count, int mt_lo, int mt_live, int wave, int lane,
+                                              const float* rs_s) {
   const int c16 = lane & 15, g4 = lane >> 4;
   const int strip0 = tile * kRowsTileStrips + wave * kRowsWaveStrips;
   if constexpr (EPI == EPI_QKV) {
-#pragma unroll
-    for (int mt = 0; mt < kRowTiles; ++mt) {
-      if (mt >= mt_live) break;                      // uniform
+    static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
+      constexpr int mt = decltype(mtc)::value;
+      if (mt < mt_lo || mt >= mt_live) return;       // uniform
 #pragma unroll
       for (int s = 0; s < kRowsWaveStrips; ++s) {
         const int n = (strip0 + s) * 16 + c16;
@@ -645,12 +662,12 @@ __device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc
           }
         }
       }
-    }
+    });
   } else if constexpr (EPI == EPI_RESID) {
     float* ss = p.ss_out + (size_t)(tile * kRowsWaves + wave) * kMaxPassRows;
-#pragma unroll
-    for (int mt = 0; mt < kRowTiles; ++mt) {
-      if (mt >= mt_live) break;                      // uniform
+    static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
+      constexpr int mt = decltype(mtc)::value;
+      if (mt < mt_lo || mt >= mt_live) return;       // uniform
       float sq[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int s = 0; s < kRowsWaveStrips; ++s) {
@@ -675,11 +692,11 @@ __device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc
         const int r = row0 + mt * 16 + g4 * 4 + i;
         if (c16 == 0 && r < row_count) ss[r] = t;
       }
-    }
+    });
   } else if constexpr (EPI == EPI_SWIGLU) {
-#pragma unroll
-    for (int mt = 0; mt < kRowTiles; ++mt) {
-      if (mt >= mt_live) break;                      // uniform
+    static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
+      constexpr int mt = decltype(mtc)::value;
+      if (mt < mt_lo || mt >= mt_live) return;       // uniform
 #pragma unroll
       for (int q = 0; q < kRowsWaveStrips / 2; ++q) {
         if (strip0 + 2 * q >= p.n_strips) continue;  // uniform
@@ -693,11 +710,11 @@ __device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc
           if (r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_bits(h);
         }
       }
-    }
+    });
   } else {  // EPI_LOGITS
-#pragma unroll
-    for (int mt = 0; mt < kRowTiles; ++mt) {
-      if (mt >= mt_live) break;                      // uniform
+    static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
+      constexpr int mt = decltype(mtc)::value;
+      if (mt < mt_lo || mt >= mt_live) return;       // uniform
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
@@ -722,7 +739,7 @@ __device__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc
           p.amax_idx[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = bi;
         }
       }
-    }
+    });
   }
 }
 
@@ -740,16 +757,15 @@ __device__ __forceinline__ void rows_block(const GemmArgs& p, int* tile, int* ks
 
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
-  constexpr int MB = kRowTiles, NS = kRowsWaveStrips;
-  constexpr int U = 2;                               // k-blocks per stage
-  constexpr int AE = U * MB * 64;                    // 16-byte A elements per stage
+  constexpr int MB = kRowTiles, NS = kRowsWaveStrips, D = kRowsDepth;
+  constexpr int AE = MB * 64;                        // 16-byte A elements of one k-block
   constexpr int AJ = (AE + 255) / 256;               // per thread
-  __shared__ __attribute__((aligned(16))) u32x4 a_lds[2][U][MB * 64];
+  constexpr bool LM = EPI == EPI_LOGITS;             // rows are the pass's lm rows
+  __shared__ __attribute__((aligned(16))) u32x4 a_lds[2][AE];
   __shared__ float rs_s[MB * 16];
 
   int tile, ks, mb;
   rows_block(p, &tile, &ks, &mb);
-  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
   const FwdDesc* dp = p.desc;
   const int row_count = LM ? dp->n_lm : dp->n_rows;
   const int row0 = mb * MB * 16;
@@ -759,30 +775,18 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int kb0 = ks * p.kb_total / p.ksplit, kb1 = (ks + 1) * p.kb_total / p.ksplit;
   const int n_kb = kb1 - kb0;
-  const int n_st = (n_kb + U - 1) / U;
 
   // W: this wavefront's strips, block (kb, strip) at (kb * n_strips + strip) KiB
   const int strip0 = tile * kRowsTileStrips + wave * NS;
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.W), 0, (int)min((size_t)p.n_strips * p.kb_total * 1024, (size_t)0x7fffffff),
       kRsrcWord3);
+  // strips past the weight's last one (only in the last column tile) read
+  // zeros or neighbouring weights: their columns are never stored
   const int w_voff = (strip0 * 64 + lane) * 16;
-  int ns_live = min(NS, p.n_strips - strip0);        // strips of this wavefront inside W
-  ns_live = max(ns_live, 0);
-  u32x4 w0[U][NS], w1[U][NS];
-  auto load_w = [&](u32x4 (&w)[U][NS], int st) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kb = kb0 + min(st * U + u, n_kb - 1);
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-        w[u][s] = s < ns_live
-                      ? __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT)
-                      : u32x4{0u, 0u, 0u, 0u};
-    }
-  };
 
-  // A: element e of a stage is 16 bytes of row (e / 4) % (16 MB), k-block e / (64 MB)
+  // A: element e of a k-block is 16 bytes of block row e / 4; rows past the
+  // pass read as zeros (offset beyond the buffer)
   const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.A), 0, p.act_rows * p.lda * 2, kRsrcWord3);
   constexpr int kOutOfRange = 0x7FFFFFF0;
@@ -790,26 +794,29 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
 #pragma unroll
   for (int j = 0; j < AJ; ++j) {
     const int e = tid + 256 * j;
-    const int rr = (e % (MB * 64)) >> 2, part = e & 3;
-    const int gr = row0 + rr;
+    const int gr = row0 + (e >> 2);
     const int src = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
-    a_voff[j] = (e < AE && gr < row_count) ? src * 64 + part * 16 : kOutOfRange;
+    a_voff[j] = (e < AE && gr < row_count) ? src * 64 + (e & 3) * 16 : kOutOfRange;
   }
-  u32x4 areg[AJ];
-  auto load_a = [&](int st) {
+
+  // Register ring of D k-blocks: the loads of k-block it + D go out as soon as
+  // k-block it has been used, so D - 1 k-blocks of W and A are in flight while
+  // one is multiplied.
+  u32x4 wr[D][NS], ar[D][AJ];
+  auto issue = [&](int slot, int it) {
+    const int kb = kb0 + min(it, n_kb - 1);
 #pragma unroll
-    for (int j = 0; j < AJ; ++j) {
-      const int e = tid + 256 * j;
-      const int u = e / (MB * 64);
-      const int kb = kb0 + min(st * U + u, n_kb - 1);
-      areg[j] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[j], kb * (p.act_rows * 64), 0);
-    }
+    for (int s = 0; s < NS; ++s)
+      wr[slot][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT);
+#pragma unroll
+    for (int j = 0; j < AJ; ++j)
+      ar[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[j], kb * (p.act_rows * 64), 0);
   };
-  auto store_a = [&](int buf) {
+  auto put_a = [&](int slot, int buf) {
 #pragma unroll
     for (int j = 0; j < AJ; ++j) {
       const int e = tid + 256 * j;
-      if (e < AE) a_lds[buf][e / (MB * 64)][e % (MB * 64)] = areg[j];
+      if (e < AE) a_lds[buf][e] = ar[slot][j];
     }
   };
 
@@ -819,95 +826,114 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute = [&](int buf, const u32x4 (&w)[U][NS], int st) {
+  // all A fragments of the k-block are read from LDS first, so their
+  // latencies overlap; row tiles past the pass multiply zeros (no branches
+  // between the fragment reads and the MFMAs)
+  auto mma = [&](int slot, int buf) {
+    u32x4 av[MB];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (st * U + u >= n_kb) break;                 // uniform
+    for (int mt = 0; mt < MB; ++mt) av[mt] = a_lds[buf][(mt * 16 + (lane & 15)) * 4 + (lane >> 4)];
 #pragma unroll
-      for (int mt = 0; mt < MB; ++mt) {
-        if (mt >= mt_live) break;                    // uniform
-        const u32x4 av = a_lds[buf][u][(mt * 16 + (lane & 15)) * 4 + (lane >> 4)];
+    for (int mt = 0; mt < MB; ++mt) {
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-          acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av),
-                                                              __builtin_bit_cast(f16x8, w[u][s]), acc[mt][s], 0, 0, 0);
-      }
+      for (int s = 0; s < NS; ++s)
+        acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av[mt]),
+                                                            __builtin_bit_cast(f16x8, wr[slot][s]), acc[mt][s], 0, 0, 0);
     }
   };
 
-  if (n_st > 0) {
-    load_w(w0, 0);
-    load_a(0);
-    store_a(0);
-    if (n_st > 1) load_w(w1, 1);
+  if (n_kb > 0) {
+    // Every iteration issues its loads and stages A whether or not its
+    // k-block exists (indices are clamped: past the end they re-read the last
+    // k-block, from cache), so the number of loads in flight is the same on
+    // every path and each wait covers exactly the k-block about to be used.
+    // The loop runs whole turns of the ring; only the MFMAs are skipped.
+#pragma unroll
+    for (int d = 0; d < D; ++d) issue(d, d);
+    put_a(0, 0);
     __syncthreads();
-    for (int st = 0; st < n_st; ++st) {
-      const int buf = st & 1;
-      if (st + 1 < n_st) load_a(st + 1);
-      __builtin_amdgcn_sched_barrier(0);
-      if (buf == 0) {
-        compute(0, w0, st);
+    const int n_it = (n_kb + D - 1) / D * D;
+    for (int it0 = 0; it0 < n_it; it0 += D) {
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int it = it0 + d;
+        // k-block it+1's A goes to the other LDS buffer (free since the last
+        // barrier), k-block it is multiplied, its ring slot is refilled
+        put_a((d + 1) % D, (it + 1) & 1);
         __builtin_amdgcn_sched_barrier(0);
-        if (st + 2 < n_st) load_w(w0, st + 2);
-      } else {
-        compute(1, w1, st);
+        if (it < n_kb) mma(d, it & 1);               // uniform
         __builtin_amdgcn_sched_barrier(0);
-        if (st + 2 < n_st) load_w(w1, st + 2);
+        issue(d, it + D);
+        __syncthreads();
       }
-      if (st + 1 < n_st) store_a(buf ^ 1);
-      __syncthreads();
     }
   }
 
   if (p.ksplit > 1) {
     // partial tile of this split, in register order (coalesced)
     float* part = p.part + ((size_t)(tile * p.m_blocks + mb) * p.ksplit + ks) * kRowsPartFloats;
-#pragma unroll
-    for (int mt = 0; mt < MB; ++mt) {
-      if (mt >= mt_live) break;                      // uniform
+    static_for<0, MB>([&](auto mtc) __attribute__((always_inline)) {
+      constexpr int mt = decltype(mtc)::value;
+      if (mt >= mt_live) return;                     // uniform
 #pragma unroll
       for (int s = 0; s < NS; ++s)
         *reinterpret_cast<f32x4*>(part + (((wave * MB + mt) * NS + s) * 64 + lane) * 4) = acc[mt][s];
-    }
+    });
     return;
   }
   if constexpr (EPI != EPI_RESID) {
     rows_scales<LM>(p, dp, row0, row_count, rs_s);
     __syncthreads();
   }
-  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, mt_live, wave, lane, rs_s);
+  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, 0, mt_live, wave, lane, rs_s);
 }
 
 // Sum of the input splits of k_gemm_rows in split order, then the epilogue.
+// One workgroup per 16-row tile of a row block (wavefront w takes GEMM
+// wavefront w's columns); each thread has the loads of up to 8 splits in
+// flight at a time.
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_rows_red(const GemmArgs p) {
   constexpr int MB = kRowTiles, NS = kRowsWaveStrips;
+  constexpr bool LM = EPI == EPI_LOGITS;
   __shared__ float rs_s[MB * 16];
-  const int tile = blockIdx.x / p.m_blocks, mb = blockIdx.x % p.m_blocks;
-  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
+  const int mt_sel = blockIdx.x % MB;
+  const int tile = blockIdx.x / (MB * p.m_blocks), mb = (blockIdx.x / MB) % p.m_blocks;
   const FwdDesc* dp = p.desc;
   const int row_count = LM ? dp->n_lm : dp->n_rows;
   const int row0 = mb * MB * 16;
-  if (row0 >= row_count) return;                     // uniform
+  if (row0 + mt_sel * 16 >= row_count) return;      // uniform
   const int mt_live = min(MB, (row_count - row0 + 15) / 16);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   if constexpr (EPI != EPI_RESID) rows_scales<LM>(p, dp, row0, row_count, rs_s);
-  const float* base = p.part + (size_t)(tile * p.m_blocks + mb) * p.ksplit * kRowsPartFloats;
-  RowsAcc acc;
+  const float* base = p.part + (size_t)(tile * p.m_blocks + mb) * p.ksplit * kRowsPartFloats +
+                      (size_t)(((wave * MB + mt_sel) * NS) * 64 + lane) * 4;
+  f32x4 sum[NS];
 #pragma unroll
-  for (int mt = 0; mt < MB; ++mt) {
+  for (int s = 0; s < NS; ++s) sum[s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int k0 = 0; k0 < p.ksplit; k0 += 8) {
+    f32x4 v[8][NS];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (mt >= mt_live) continue;                     // uniform
+    for (int u = 0; u < 8; ++u)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const size_t o = (size_t)(((wave * MB + mt) * NS + s) * 64 + lane) * 4;
-      for (int k = 0; k < p.ksplit; ++k) acc[mt][s] += *reinterpret_cast<const f32x4*>(base + k * kRowsPartFloats + o);
-    }
+      for (int s = 0; s < NS; ++s)
+        v[u][s] = k0 + u < p.ksplit ? *reinterpret_cast<const f32x4*>(base + (size_t)(k0 + u) * kRowsPartFloats + s * 256)
+                                    : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+#pragma unroll
+      for (int s = 0; s < NS; ++s)
+        if (k0 + u < p.ksplit) sum[s] += v[u][s];
   }
+  RowsAcc acc;
+  static_for<0, MB>([&](auto mtc) __attribute__((always_inline)) {
+    constexpr int mt = decltype(mtc)::value;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) acc[mt][s] = mt == mt_sel ? sum[s] : f32x4{0.f, 0.f, 0.f, 0.f};
+  });
   if constexpr (EPI != EPI_RESID) __syncthreads();
-  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, mt_live, wave, lane, rs_s);
+  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, mt_sel, min(mt_live, mt_sel + 1), wave, lane, rs_s);
 }
 
 template <int EPI>
@@ -922,10 +948,10 @@ hipError_t launch_rows(const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.ksplit == 1) return e;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_gemm_rows_red<EPI>, dim3(a.n_tiles * a.m_blocks), dim3(256), 0u, st, nullptr, ev.stop,
+    hipExtLaunchKernelGGL(k_gemm_rows_red<EPI>, dim3(a.n_tiles * a.m_blocks * kRowTiles), dim3(256), 0u, st, nullptr, ev.stop,
                           0u, a);
   } else {
-    k_gemm_rows_red<EPI><<<a.n_tiles * a.m_blocks, 256, 0, st>>>(a);
+    k_gemm_rows_red<EPI><<<a.n_tiles * a.m_blocks * kRowTiles, 256, 0, st>>>(a);
   }
   return hipGetLastError();
 }

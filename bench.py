@@ -130,6 +130,37 @@ def cpu_baseline(wl, tokens_per_step: float, context: int) -> dict:
 PEAK_F16_TFLOPS = 2500.0   # MI355X dense fp16 / bf16 MFMA
 
 
+def measure_baselines(eng, B, prompt, k, pard_step_s, pard_tok_s, steps=64, warmup=4):
+    """The decoding schemes PARD is compared with, on the same kernels and the
+    same prompt: plain greedy target steps (K = 0, one target pass per token)
+    and vanilla speculative decoding (K sequential one-row draft passes, then
+    the verify pass; eq. 3).  Each is timed over `steps` fused steps after a
+    fresh prefill; per step, T_AR = T_T, T_vanilla = K*T_D + T_T and
+    T_PARD = T_D' + T_T (T_D' one draft pass over K + a rows)."""
+    import torch
+    out = {"steps": steps}
+    for name, kk, mode in (("ar", 0, B.PARD_MODE_PARALLEL), ("vanilla_sd", k, B.PARD_MODE_VANILLA)):
+        eng.prefill(prompt)
+        eng.generate(kk, eng.max_ctx - len(prompt) - 2 * k - 2, max_steps=warmup, mode=mode)
+        budget = eng.max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        _, st = eng.generate(kk, budget, max_steps=steps, mode=mode)
+        torch.cuda.synchronize()
+        w = time.perf_counter() - t0
+        hist = list(st.accept_hist)
+        em = sum((a + 1) * c for a, c in enumerate(hist))
+        out[name] = {"ms_per_step": round(w / st.steps * 1e3, 4), "tokens_per_step": round(em / st.steps, 4),
+                     "tokens_per_s": round(em / w, 3)}
+    t_ar = out["ar"]["ms_per_step"]
+    out["pard"] = {"ms_per_step": round(pard_step_s * 1e3, 4), "tokens_per_s": round(pard_tok_s, 3)}
+    out["draft_ms_per_step"] = {"pard": round(pard_step_s * 1e3 - t_ar, 4),
+                                "vanilla_sd": round(out["vanilla_sd"]["ms_per_step"] - t_ar, 4)}
+    out["note"] = ("acceptance with random weights is ~0, so every scheme emits ~1 token per step; "
+                   "draft_ms_per_step = step time minus the plain target step")
+    return out
+
+
 def bench_batched(args, wl) -> int:
     """The batched workload: wl.batch independent sequences with ragged prompt
     lengths, stepped together (one batched draft pass and one batched verify
@@ -333,6 +364,8 @@ def main() -> int:
                 "launches": launches, "avg_us": round(avg_s * 1e6, 2),
                 "bytes_per_launch": gu_bytes}
 
+    baselines = measure_baselines(eng, B, prompt, k, wall / steps, emitted / wall)
+
     result = {
         "metric": METRIC,
         "value": round(emitted / wall, 3),
@@ -359,6 +392,7 @@ def main() -> int:
         "ttft_ms": round(ttft_ms, 2),
         "device_ms_per_step": round(stats.elapsed_ms / steps, 4),
         "roofline": roofline,
+        "baselines": baselines,
     }
     eng.close()
     del eng

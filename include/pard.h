@@ -50,6 +50,11 @@ typedef enum {
 
 enum { PARD_F32 = 0, PARD_BF16 = 1 };
 enum { PARD_TARGET = 0, PARD_DRAFT = 1 };
+/* Drafting of the fused loop: PARD's one parallel pass over the pending tokens
+ * and K-1 mask tokens (Sec. 3.1, eq. 7), or vanilla speculative decoding's K
+ * sequential one-token draft passes (Sec. 2.1, eq. 3; the baseline PARD is
+ * compared with). */
+enum { PARD_MODE_PARALLEL = 0, PARD_MODE_VANILLA = 1 };
 
 /* Shape and initialisation of one Llama-family decoder (Sec. 4.1 names
  * LLaMA3 and Qwen2.5 members).  Weights are drawn N(0, init_std^2) with the
@@ -163,6 +168,17 @@ pard_status pard_kv_len(const pard_ctx *ctx, int32_t seq, int32_t which, int32_t
 pard_status pard_generate(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, int32_t K,
                           int32_t n_tokens, int32_t max_steps, int32_t *out_tokens,
                           pard_stats *stats);
+
+/* pard_generate with an explicit drafting mode (PARD_MODE_PARALLEL: same as
+ * pard_generate; PARD_MODE_VANILLA: each step runs K draft passes of one row
+ * per slot, every pass feeding the previous candidate, then the same verify
+ * pass; after verification the draft cache keeps the pending token and the
+ * candidates that agree (eq. 3: T = K*T_draft + T_target per step).  Greedy
+ * acceptance, outputs, limits and errors as pard_generate; ARG for an unknown
+ * mode. */
+pard_status pard_generate_ex(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, int32_t K,
+                             int32_t mode, int32_t n_tokens, int32_t max_steps,
+                             int32_t *out_tokens, pard_stats *stats);
 
 /* Copy the fp32 logits of slot `seq`'s rows in the last lm_head pass of
  * `which` that included the slot (rows x vocab, row-major; draft rows are the

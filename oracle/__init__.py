@@ -21,7 +21,7 @@ forced-candidate acceptance; the draft-equals-target special case.
 from .model import (KVCache, Model, attention, forward_cached, forward_full, linear,
                     rms_norm, rope, silu)
 from .pard import (PardTrace, accept_prefix, argmax_rows, draft_step, greedy_ar,
-                   pard_generate, prefill, verify_step)
+                   pard_generate, prefill, vanilla_draft_step, vanilla_generate, verify_step)
 
 
 def build_model(spec, layers=None) -> Model:

@@ -8,6 +8,9 @@ Paper passages followed:
 * Speculative decoding, Sec. 2.2: a drafting stage proposes K candidates
   C = (x'_n .. x'_{n+K-1}); a verification stage scores them with the target
   in one parallel pass.
+* Vanilla speculative decoding, Sec. 2.1 eq. 3: the drafting stage is K
+  sequential greedy steps of the draft model (its cost K times one draft
+  step), each conditioned on the candidates before it.
 * PARD drafting, Sec. 3.1 eq. 7 and the PARD-inference figure: the draft runs
   ONE forward over the known prefix followed by shared mask tokens
   m_0 = ... = m_{K-1} (Sec. 4.3, shared mask id), and the k-th candidate
@@ -120,6 +123,50 @@ def pard_generate(target: Model, draft: Model, prompt: Sequence[int], k: int,
         a, bonus, _, _ = verify_step(target, cache_t, pending[-1], cands)
         pending = list(cands[:a]) + [bonus]
         trace.tokens += pending
+        trace.accepts.append(a)
+        trace.candidates.append(list(cands))
+    trace.tokens = trace.tokens[:n_tokens]
+    return trace
+
+
+def vanilla_draft_step(draft: Model, cache_d: KVCache, pending: Sequence[int],
+                       k: int) -> Tuple[List[int], np.ndarray]:
+    """Vanilla drafting (Sec. 2.1, eq. 3): k sequential greedy draft steps.
+
+    The first step reads the pending tokens, every later one the candidate
+    before it.  Afterwards the draft cache holds the pending tokens and
+    c_1..c_{k-1} (c_k is proposed, not read).  Returns the candidates and the
+    logits row each was taken from."""
+    if k < 1 or len(pending) < 1:
+        raise ValueError("need k >= 1 and at least one pending token")
+    ids, cands, rows = list(pending), [], []
+    for _ in range(k):
+        logits = forward_cached(draft, cache_d, ids, logits_rows=[len(ids) - 1])
+        c = argmax_rows(logits)[0]
+        cands.append(c)
+        rows.append(logits[0])
+        ids = [c]
+    return cands, np.stack(rows)
+
+
+def vanilla_generate(target: Model, draft: Model, prompt: Sequence[int], k: int,
+                     n_tokens: int) -> PardTrace:
+    """Vanilla speculative decoding with greedy verification: k sequential
+    draft steps, then the same verify / accept as PARD.  After verification
+    the draft cache keeps the pending token(s) and the candidates that agree
+    with the committed tokens; the tokens after them are pending for the
+    next drafting stage."""
+    cache_t, cache_d, first, _ = prefill(target, draft, prompt)
+    trace = PardTrace(tokens=[first])
+    pending = [first]
+    while len(trace.tokens) < n_tokens:
+        start_d = cache_d.length
+        cands, _ = vanilla_draft_step(draft, cache_d, pending, k)
+        a, bonus, _, _ = verify_step(target, cache_t, pending[-1], cands)
+        keep = min(a, k - 1)
+        cache_d.truncate(start_d + len(pending) + keep)
+        pending = list(cands[keep:a]) + [bonus]
+        trace.tokens += list(cands[:a]) + [bonus]
         trace.accepts.append(a)
         trace.candidates.append(list(cands))
     trace.tokens = trace.tokens[:n_tokens]

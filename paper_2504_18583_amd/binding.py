@@ -26,6 +26,7 @@ PARD_OK, PARD_ERR_ARG, PARD_ERR_STATE, PARD_ERR_CAPACITY = 0, -1, -2, -3
 PARD_ERR_NOMEM, PARD_ERR_DEVICE, PARD_ERR_UNSUPPORTED = -4, -5, -6
 PARD_F32, PARD_BF16 = 0, 1
 PARD_TARGET, PARD_DRAFT = 0, 1
+PARD_MODE_PARALLEL, PARD_MODE_VANILLA = 0, 1
 OP_EMBED, OP_QKV, OP_ATTN, OP_O, OP_GATEUP, OP_DOWN, OP_LM, OP_TAIL = range(8)
 
 
@@ -57,6 +58,8 @@ _sig = {
     "pard_kv_len": (C.c_int, [_CTX, C.c_int32, C.c_int32, _I32P]),
     "pard_generate": (C.c_int, [_CTX, C.c_int32, _I32P, C.c_int32, C.c_int32, C.c_int32, _I32P,
                                 C.POINTER(pard_stats)]),
+    "pard_generate_ex": (C.c_int, [_CTX, C.c_int32, _I32P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
+                                   _I32P, C.POINTER(pard_stats)]),
     "pard_read_logits": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                    C.c_int32]),
     "pard_read_weight": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -179,23 +182,25 @@ class Engine:
     def kv_truncate(self, which: int, new_len: int, seq: int = 0) -> None:
         self._check(lib.pard_kv_truncate(self.ctx, seq, which, new_len), "pard_kv_truncate")
 
-    def generate(self, k: int, n_tokens: int, max_steps: int = 0, seq: int = 0):
+    def generate(self, k: int, n_tokens: int, max_steps: int = 0, seq: int = 0,
+                 mode: int = PARD_MODE_PARALLEL):
         out = np.zeros(n_tokens, np.int32)
         stats = pard_stats()
         seqs, sptr = _i32([seq])
-        self._check(lib.pard_generate(self.ctx, 1, sptr, k, n_tokens, max_steps,
-                                      out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate")
+        self._check(lib.pard_generate_ex(self.ctx, 1, sptr, k, mode, n_tokens, max_steps,
+                                         out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate_ex")
         return out[:stats.tokens].tolist(), stats
 
-    def generate_batch(self, seqs: Sequence[int], k: int, n_tokens: int, max_steps: int = 0):
+    def generate_batch(self, seqs: Sequence[int], k: int, n_tokens: int, max_steps: int = 0,
+                       mode: int = PARD_MODE_PARALLEL):
         """Fused loop over several slots at once (batched passes).  Returns one
         token list per slot (the pending token first) and the summed stats."""
         before = [self.kv_len(PARD_TARGET, seq=s) for s in seqs]
         out = np.zeros((len(seqs), n_tokens), np.int32)
         stats = pard_stats()
         arr, sptr = _i32(list(seqs))
-        self._check(lib.pard_generate(self.ctx, len(seqs), sptr, k, n_tokens, max_steps,
-                                      out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate")
+        self._check(lib.pard_generate_ex(self.ctx, len(seqs), sptr, k, mode, n_tokens, max_steps,
+                                         out.ctypes.data_as(_I32P), C.byref(stats)), "pard_generate_ex")
         res = []
         for i, s in enumerate(seqs):
             n = min(n_tokens, 1 + self.kv_len(PARD_TARGET, seq=s) - before[i])

@@ -166,7 +166,7 @@ struct pard_ctx {
   int* h_out = nullptr;
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
   // captured fused steps (draft pass + verify pass), replayed on `stream`
-  struct StepGraph { int n_seq, k, l_class; hipGraphExec_t exec; };
+  struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
   hipStream_t cap_stream = nullptr;     // private stream used only for capture
   bool use_graphs = true;
@@ -686,8 +686,9 @@ int attn_l_class(int l) {
 // Pass bounds of one fused step over n_seq sequences.
 struct StepShape {
   int n_seq = 1, K = 0;
-  int draft_rows = 0;     // bound of the draft pass's rows
+  int draft_rows = 0;     // bound of the (first) draft pass's rows
   int l_class = 0;
+  bool vsd = false;       // vanilla speculative decoding: K one-row draft passes
 };
 
 // One fused step: draft pass (pending + K-1 masks per sequence) then verify
@@ -695,7 +696,21 @@ struct StepShape {
 pard_status step_passes(pard_ctx* c, const StepShape& sh) {
   pard_status st;
   const int K = sh.K, n = sh.n_seq;
-  if (K > 0) {
+  if (K > 0 && sh.vsd) {
+    // vanilla drafting (eq. 3): K passes of one row per sequence, the first
+    // also ingesting the tokens the draft has not seen
+    for (int j = 0; j < K; ++j) {
+      PassSpec pd;
+      pd.max_rows = j == 0 ? sh.draft_rows : n;
+      pd.max_lm_rows = n;
+      pd.n_seq = n;
+      pd.max_seq_rows = j == 0 ? (n > 1 ? 2 : sh.draft_rows) : 1;
+      pd.l_bound = sh.l_class;
+      pd.tail = TAIL_VSD_DRAFT;
+      pd.next_desc = c->m[j + 1 < K ? PARD_DRAFT : PARD_TARGET].desc;
+      if ((st = forward(c, PARD_DRAFT, pd)) != PARD_OK) return st;
+    }
+  } else if (K > 0) {
     PassSpec pd;
     pd.max_rows = sh.draft_rows;
     pd.typ_rows = n * K;
@@ -724,7 +739,7 @@ pard_status step_passes(pard_ctx* c, const StepShape& sh) {
 // failure switches the context to eager launches.
 pard_status launch_step_graph(pard_ctx* c, const StepShape& sh) {
   for (const auto& g : c->graphs)
-    if (g.n_seq == sh.n_seq && g.k == sh.K && g.l_class == sh.l_class) {
+    if (g.n_seq == sh.n_seq && g.k == sh.K && g.l_class == sh.l_class && g.vsd == sh.vsd) {
       HIP_TRY(c, hipGraphLaunch(g.exec, c->stream));
       return PARD_OK;
     }
@@ -749,7 +764,7 @@ pard_status launch_step_graph(pard_ctx* c, const StepShape& sh) {
     c->use_graphs = false;
     return step_passes(c, sh);
   }
-  c->graphs.push_back({sh.n_seq, sh.K, sh.l_class, exec});
+  c->graphs.push_back({sh.n_seq, sh.K, sh.l_class, sh.vsd, exec});
   HIP_TRY(c, hipGraphLaunch(exec, c->stream));
   return PARD_OK;
 }
@@ -922,6 +937,7 @@ pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t 
   }
   const int n_new = n_prefix - Ld;
   S.k = K;
+  S.vsd = 0;
   S.L[1] = Ld;
   if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
   const FwdDesc d = make_desc(seq, prefix + Ld, n_new, K - 1, c->mask_id, Ld, n_new, n_new - 1, K);
@@ -958,6 +974,7 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
     S.cand[i] = cand[i];
   }
   S.k = K;
+  S.vsd = 0;
   if ((st = push_seq(c, seq)) != PARD_OK) { S = saved; return st; }
   if ((st = stage_desc(c, PARD_TARGET, make_desc(seq, ids, K + 1, 0, 0, Lt, K + 1, 0, K + 1))) != PARD_OK) {
     S = saved;
@@ -1012,7 +1029,14 @@ pard_status pard_kv_len(const pard_ctx* c, int32_t seq, int32_t which, int32_t* 
 
 pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32_t K, int32_t n_tokens,
                           int32_t max_steps, int32_t* out_tokens, pard_stats* stats) {
+  return pard_generate_ex(c, n_seq, seqs, K, PARD_MODE_PARALLEL, n_tokens, max_steps, out_tokens, stats);
+}
+
+pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32_t K, int32_t mode,
+                             int32_t n_tokens, int32_t max_steps, int32_t* out_tokens, pard_stats* stats) {
   if (!c) return PARD_ERR_ARG;
+  if (mode != PARD_MODE_PARALLEL && mode != PARD_MODE_VANILLA) return fail(c, PARD_ERR_ARG, "generate: bad mode %d", mode);
+  const bool vsd = mode == PARD_MODE_VANILLA;
   if (!seqs || !out_tokens || n_tokens < 1) return fail(c, PARD_ERR_ARG, "generate: null pointer or n_tokens < 1");
   if (n_seq < 1 || n_seq > std::min(c->max_batch, kMaxPassSeqs))
     return fail(c, PARD_ERR_CAPACITY, "generate: n_seq=%d outside [1, %d]", n_seq, std::min(c->max_batch, kMaxPassSeqs));
@@ -1047,7 +1071,9 @@ pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32
     int Ld = std::min(S.L[1], Lt);
     if (K > 0) {
       const int total = Lt + 1;                  // committed tokens + pending
-      const int max_first = (n_seq == 1 ? kMaxRows : 2 * K) - (K - 1);
+      // pending rows of the first draft pass: PARD adds K-1 mask rows, a
+      // vanilla pass none (later vanilla passes see at most 2 pending tokens)
+      const int max_first = vsd ? (n_seq == 1 ? kMaxRows : 2) : (n_seq == 1 ? kMaxRows : 2 * K) - (K - 1);
       if (total - Ld > max_first) {
         const int extra = total - Ld - max_first;
         if ((st = ingest(c, PARD_DRAFT, seq, hist.data() + Ld, extra, Ld)) != PARD_OK) return restore(st);
@@ -1058,13 +1084,17 @@ pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32
     }
     S.L[1] = Ld;
     S.k = K;
+    S.vsd = vsd && K > 0 ? 1 : 0;
+    S.j = 0;
     S.n_out = 1;
     S.n_target = n_tokens;
     S.steps = 0;
     S.mask_id = c->mask_id;
     memset(S.accept_hist, 0, sizeof S.accept_hist);
     if ((st = push_seq(c, seq)) != PARD_OK) return restore(st);
-    if (K > 0) {
+    if (K > 0 && vsd) {
+      append_seq(first, seq, S.pending, S.n_pending, 0, 0, Ld, S.n_pending, S.n_pending - 1, 1);
+    } else if (K > 0) {
       append_seq(first, seq, S.pending, S.n_pending, K - 1, c->mask_id, Ld, S.n_pending, S.n_pending - 1, K);
     } else {
       const int b = S.bonus;
@@ -1090,10 +1120,14 @@ pard_status pard_generate(pard_ctx* c, int32_t n_seq, const int32_t* seqs, int32
     StepShape sh;
     sh.n_seq = (int)active.size();
     sh.K = K;
+    sh.vsd = vsd;
     sh.l_class = attn_l_class(max_L + batch * (K + 1) + K + 1);
     for (int i = 0; i < batch; ++i) {
       // a single sequence's first draft pass may carry more pending rows
-      sh.draft_rows = sh.n_seq > 1 ? sh.n_seq * 2 * K : (first_step ? std::max(first.n_rows, 2 * K) : 2 * K);
+      if (vsd)
+        sh.draft_rows = sh.n_seq > 1 ? sh.n_seq * 2 : (first_step ? std::max(first.n_rows, 2) : 2);
+      else
+        sh.draft_rows = sh.n_seq > 1 ? sh.n_seq * 2 * K : (first_step ? std::max(first.n_rows, 2 * K) : 2 * K);
       if (first_step || !c->use_graphs || c->timer_class >= 0) {
         if ((st = step_passes(c, sh)) != PARD_OK) return st;
       } else {

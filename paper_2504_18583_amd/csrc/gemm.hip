@@ -372,8 +372,10 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 
 // Decode-state update of one sequence once the argmax of its lm rows is
 // known (one thread).  Draft: store the candidates, commit only the real rows
-// (the mask rows are never committed).  Verify: longest agreeing prefix a
-// (eq. 2), bonus t_a, L_t += a + 1, emit the a + 1 tokens.
+// (the mask rows are never committed).  Vanilla draft pass (one of K per
+// step, eq. 3): one more candidate, every row committed.  Verify: longest
+// agreeing prefix a (eq. 2), bonus t_a, L_t += a + 1, emit the a + 1 tokens;
+// in vanilla mode the draft cache keeps the candidates that agree.
 __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
   SeqState* s = p.states + ps.slot;
   if (p.tail == TAIL_PREFILL) {
@@ -385,6 +387,10 @@ __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
     const int k = s->k;
     for (int i = 0; i < k; ++i) s->cand[i] = res[i];
     s->L[1] = ps.pos0 + ps.n_real;
+  } else if (p.tail == TAIL_VSD_DRAFT) {
+    s->cand[s->j] = res[0];
+    ++s->j;
+    s->L[1] = ps.pos0 + ps.n_real;
   } else if (p.tail == TAIL_VERIFY) {
     const int k = s->k;
     int a = 0;
@@ -394,13 +400,25 @@ __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
     s->a = a;
     s->bonus = bonus;
     s->L[0] = ps.pos0 + a + 1;                     // keep pending + accepted rows
-    for (int i = 0; i < a; ++i) s->pending[i] = s->cand[i];
-    s->pending[a] = bonus;
-    s->n_pending = a + 1;
-    if (p.out_tokens) {
+    if (s->vsd && k > 0) {
+      // the draft cache holds the pending token and c_1..c_{k-1}; it keeps
+      // those that agree, and the tokens after them become pending
+      const int keep = min(a, k - 1);
+      s->L[1] = ps.pos0 + 1 + keep;
+      int n = 0;
+      for (int i = keep; i < a; ++i) s->pending[n++] = s->cand[i];
+      s->pending[n++] = bonus;
+      s->n_pending = n;
+      s->j = 0;
+    } else {
+      for (int i = 0; i < a; ++i) s->pending[i] = s->cand[i];
+      s->pending[a] = bonus;
+      s->n_pending = a + 1;
+    }
+    if (p.out_tokens) {                             // emitted: c_1..c_a, then the bonus
       int* out = p.out_tokens + (size_t)ps.slot * p.out_cap;
       for (int i = 0; i <= a; ++i) {
-        if (s->n_out < p.out_cap) out[s->n_out] = s->pending[i];
+        if (s->n_out < p.out_cap) out[s->n_out] = i < a ? s->cand[i] : bonus;
         ++s->n_out;
       }
     }
@@ -409,15 +427,26 @@ __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
   }
 }
 
-// Rows of one sequence in the pass that follows a draft pass (the verify
-// pass: [pending, c_1..c_k] at L_t), a verify pass with k > 0 (the next draft
-// pass: the a+1 pending tokens and k-1 mask rows at L_d, lm rows from the last
-// pending row on) or a verify pass with k = 0 (the next plain target step).
+// Rows of one sequence in the pass that follows
+//   a draft pass (PARD), or the last vanilla draft pass of a step: the verify
+//     pass, [pending, c_1..c_k] at L_t;
+//   an earlier vanilla draft pass: the next one, the candidate just drafted;
+//   a verify pass with k > 0: the next draft pass, the pending tokens at L_d
+//     followed (PARD) by k-1 mask rows, lm rows from the last pending row on;
+//   a verify pass with k = 0: the next plain target step.
+__device__ bool to_verify(int after, const SeqState& s) {
+  return after == TAIL_DRAFT || (after == TAIL_VSD_DRAFT && s.j >= s.k);
+}
+
 __device__ void next_rows(int after, const SeqState& s, int* n_rows, int* n_real, int* pos0, int* lm_first,
                           int* lm_rows) {
   const int k = s.k;
-  if (after == TAIL_DRAFT) {
+  if (to_verify(after, s)) {
     *n_rows = k + 1; *n_real = k + 1; *pos0 = s.L[0]; *lm_first = 0; *lm_rows = k + 1;
+  } else if (after == TAIL_VSD_DRAFT) {
+    *n_rows = 1; *n_real = 1; *pos0 = s.L[1]; *lm_first = 0; *lm_rows = 1;
+  } else if (k > 0 && s.vsd) {
+    *n_rows = s.n_pending; *n_real = s.n_pending; *pos0 = s.L[1]; *lm_first = s.n_pending - 1; *lm_rows = 1;
   } else if (k > 0) {
     *n_rows = s.n_pending + k - 1; *n_real = s.n_pending; *pos0 = s.L[1]; *lm_first = s.n_pending - 1; *lm_rows = k;
   } else {
@@ -426,7 +455,8 @@ __device__ void next_rows(int after, const SeqState& s, int* n_rows, int* n_real
 }
 
 __device__ int next_id(int after, const SeqState& s, int i) {
-  if (after == TAIL_DRAFT) return i == 0 ? s.bonus : s.cand[i - 1];
+  if (to_verify(after, s)) return i == 0 ? s.bonus : s.cand[i - 1];
+  if (after == TAIL_VSD_DRAFT) return s.cand[s.j - 1];
   if (s.k > 0) return i < s.n_pending ? s.pending[i] : s.mask_id;
   return s.bonus;
 }

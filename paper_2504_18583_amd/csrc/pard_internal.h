@@ -116,10 +116,12 @@ struct SeqState {
   int steps;
   int mask_id;
   int accept_hist[kMaxK + 1];
+  int vsd;                   // vanilla speculative decoding: K one-row draft passes per step
+  int j;                     // draft passes done in the current step (vanilla)
 };
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
-enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3 };
+enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3, TAIL_VSD_DRAFT = 4 };
 
 struct GemmArgs {
   const uint16_t* W;      // strip-packed weight (fp16 encoding)

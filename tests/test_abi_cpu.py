@@ -106,6 +106,7 @@ def test_null_context_calls_return_arg(b):
     assert b.lib.pard_kv_truncate(None, 0, 0, 0) == b.PARD_ERR_ARG
     assert b.lib.pard_kv_len(None, 0, 0, C.byref(out)) == b.PARD_ERR_ARG
     assert b.lib.pard_generate(None, 1, one, 2, 4, 0, one, None) == b.PARD_ERR_ARG
+    assert b.lib.pard_generate_ex(None, 1, one, 2, b.PARD_MODE_VANILLA, 4, 0, one, None) == b.PARD_ERR_ARG
     assert b.lib.pard_last_error(None) == b"null context"
     b.lib.pard_free(None)
     assert b.lib.pard_status_string(b.PARD_ERR_CAPACITY) == b"PARD_ERR_CAPACITY"

@@ -134,3 +134,61 @@ def test_accept_prefix_cases():
     assert accept_prefix([7, 2], [1, 2, 3]) == (0, 1)
     with pytest.raises(ValueError):
         accept_prefix([1, 2], [1, 2])
+
+
+# ---- vanilla speculative decoding (Sec. 2.1, eq. 3), the baseline PARD is compared with ----
+
+@pytest.mark.parametrize("k", [1, 3, 6])
+def test_vanilla_draft_is_the_drafts_greedy_continuation(tiny, prompt, k):
+    """K sequential draft steps propose exactly the draft model's own greedy
+    continuation (recomputed from scratch by plain greedy decoding)."""
+    _, draft = tiny
+    hist = prompt + [17, 400]
+    cache = KVCache(draft)
+    forward_cached(draft, cache, hist[:-2], logits_rows=[])
+    cands, rows = oracle.vanilla_draft_step(draft, cache, hist[-2:], k)
+    assert cands == greedy_ar(draft, hist, k)
+    assert rows.shape == (k, draft.spec.vocab)
+    # the cache holds the pending tokens and c_1..c_{k-1}
+    assert cache.length == len(hist) + k - 1
+
+
+@pytest.mark.parametrize("k", [1, 2, 4, 8])
+def test_vanilla_sd_is_lossless_vs_greedy(tiny, prompt, k):
+    target, draft = tiny
+    n = 40
+    trace = oracle.vanilla_generate(target, draft, prompt, k, n)
+    assert trace.tokens == greedy_ar(target, prompt, n)
+    assert all(0 <= a <= k for a in trace.accepts)
+
+
+def test_vanilla_sd_self_draft_accepts_everything(tiny, prompt):
+    """With the target as its own draft every candidate is the target's greedy
+    token: a = K every step, and the rolled-back draft cache stays consistent."""
+    target, _ = tiny
+    trace = oracle.vanilla_generate(target, target, prompt, 4, 26)
+    assert all(a == 4 for a in trace.accepts)
+    assert trace.tokens == greedy_ar(target, prompt, 26)
+
+
+def test_vanilla_sd_draft_cache_matches_fresh_prefill(tiny, prompt):
+    """After each step's rollback the draft cache equals a fresh prefill of the
+    committed tokens it claims to hold (brute force)."""
+    target, draft = tiny
+    k = 3
+    cache_t, cache_d, first, _ = prefill(target, draft, prompt)
+    hist, pending = list(prompt) + [first], [first]
+    for _ in range(5):
+        start_d = cache_d.length
+        cands, _ = oracle.vanilla_draft_step(draft, cache_d, pending, k)
+        a, bonus, _, _ = verify_step(target, cache_t, pending[-1], cands)
+        keep = min(a, k - 1)
+        cache_d.truncate(start_d + len(pending) + keep)
+        hist += list(cands[:a]) + [bonus]
+        pending = list(cands[keep:a]) + [bonus]
+        fresh = KVCache(draft)
+        forward_cached(draft, fresh, hist[:cache_d.length], logits_rows=[])
+        for l in range(draft.spec.n_layers):
+            np.testing.assert_allclose(cache_d.k[l][:cache_d.length], fresh.k[l][:cache_d.length], atol=1e-12)
+            np.testing.assert_allclose(cache_d.v[l][:cache_d.length], fresh.v[l][:cache_d.length], atol=1e-12)
+        assert cache_d.length + len(pending) == len(hist)

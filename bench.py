@@ -360,7 +360,7 @@ def main() -> int:
     achieved = gu_bytes / avg_s / 1e9
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": measured_traffic(),
-                "kernel": "k_gemm<MT=1,S=2,EPI_SWIGLU> (target gate/up, 8B shape)",
+                "kernel": "k_gemm<MT=1,S=7,EPI_SWIGLU> (target gate/up, 8B shape, 256 workgroups)",
                 "launches": launches, "avg_us": round(avg_s * 1e6, 2),
                 "bytes_per_launch": gu_bytes}
 

@@ -68,12 +68,13 @@ __device__ __forceinline__ bool map_row(const GenArgs& a, int n, uint64_t* key, 
     }
     return false;
   }
-  // MAP_GATEUP: strips alternate gate / up
-  const int strip = n >> 4, pair = strip >> 1;
-  const int r = pair * 16 + (n & 15);
+  // MAP_GATEUP: every strip holds 8 gate rows then the 8 up rows of the same
+  // features
+  const int c = n & 15;
+  const int r = (n >> 4) * 8 + (c & 7);
   if (r >= a.rows) return false;
   *row = r;
-  *key = (strip & 1) ? a.key1 : a.key0;
+  *key = (c & 8) ? a.key1 : a.key0;
   return true;
 }
 

@@ -60,6 +60,22 @@ struct GemmPlan {
 };
 
 int pick_S(int epi, int n_strips, int mt) {
+  if (epi == EPI_SWIGLU && mt == 1) {
+    // the largest strips-per-workgroup count that divides the strips and fills
+    // the 256 CUs most evenly (8B shape: 7 strips -> exactly one workgroup per CU)
+    int best = 1;
+    double best_u = 0.0;
+    for (int s : {7, 4, 2, 1}) {
+      if (n_strips % s) continue;
+      const int tiles = n_strips / s;
+      const double u = (double)tiles / (ceil_div(tiles, 256) * 256);
+      if (u > best_u + 1e-9) {
+        best_u = u;
+        best = s;
+      }
+    }
+    return best;
+  }
   int s = 1;
   // two strips share one activation stream once that still leaves >= 192
   // workgroups (measured faster for the 8B QKV shape: 384 strips)
@@ -67,7 +83,6 @@ int pick_S(int epi, int n_strips, int mt) {
   if (epi == EPI_SWIGLU) s = 2;
   if (epi == EPI_LOGITS) s = (mt == 1) ? 4 : 2;
   while (s > 1 && n_strips % s) s >>= 1;
-  if (epi == EPI_SWIGLU && s < 2) s = 2;
   return s;
 }
 
@@ -1219,8 +1234,8 @@ pard_status pard_read_weight(const pard_ctx* cc, int32_t which, int32_t tensor, 
       case 1: buf = L.wqkv; rows = M.kv_dim; cols = M.d; npad = M.nqkv; prow = M.q_dim + qk_row(row); break;
       case 2: buf = L.wqkv; rows = M.kv_dim; cols = M.d; npad = M.nqkv; prow = M.q_dim + M.kv_dim + row; break;
       case 3: buf = L.wo; rows = M.d; cols = M.q_dim; npad = M.d; prow = row; break;
-      case 4: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 16) * 32 + row % 16; break;
-      case 5: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 16) * 32 + 16 + row % 16; break;
+      case 4: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 8) * 16 + row % 8; break;
+      case 5: buf = L.wgu; rows = s.ffn_dim; cols = M.d; npad = 2 * M.f_pad; prow = (row / 8) * 16 + 8 + row % 8; break;
       case 6: buf = L.wd; rows = M.d; cols = s.ffn_dim; npad = M.d; prow = row; break;
       case 7: case 8: case 9:
         if (!L.bqkv) return fail(c, PARD_ERR_ARG, "read_weight: model has no bias");

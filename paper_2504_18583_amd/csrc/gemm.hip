@@ -25,7 +25,8 @@
 //               to the fp16 cache.
 //   EPI_RESID   x += Y (O-projection, down-projection), plus fp16(x * g_next)
 //               and per-tile row sums of squares for the next normalised GEMM.
-//   EPI_SWIGLU  RMSNorm row scale, h = silu(gate) * up, fp16.
+//   EPI_SWIGLU  RMSNorm row scale, h = silu(gate) * up, fp16 (each strip
+//               holds 8 gate and the 8 matching up columns).
 //   EPI_LOGITS  final RMSNorm scale, fp32 logits and per-tile (max, argmax).
 // k_lm_tail then reduces the tiles per row (lowest id on ties) and runs the
 // step tail: candidates for a draft pass; greedy prefix acceptance, KV
@@ -322,17 +323,19 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       if (csub == 0) p.ss_out[(size_t)tile * kMaxPassRows + mt * 16 + rsub] = t;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
-    if (!epi) return;   // no barrier follows in this epilogue
+    // a strip holds 8 gate columns then the 8 up columns of the same features:
+    // the up value of column csub < 8 is in lane ^ 8 (same row)
+    if (!epi) return;   // whole wavefronts; no barrier follows in this epilogue
 #pragma unroll
-    for (int q = 0; q < S / 2; ++q)
+    for (int s = 0; s < S; ++s)
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const int row = mt * 16 + rsub;
-        const float gt = v[(2 * q) * MT + mt] * rs_s[row];
-        const float up = v[(2 * q + 1) * MT + mt] * rs_s[row];
+        const float gt = v[s * MT + mt] * rs_s[row];
+        const float up = __shfl_xor(gt, 8);
         const float h = gt / (1.0f + expf(-gt)) * up;
-        const int f = (tile * (S / 2) + q) * 16 + csub;
-        if (row < row_count) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
+        const int f = (tile * S + s) * 8 + csub;
+        if (csub < 8 && row < row_count) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
       }
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;
@@ -724,20 +727,21 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
       }
     });
   } else if constexpr (EPI == EPI_SWIGLU) {
+    // 8 gate columns then the 8 up columns of the same features per strip
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
       constexpr int mt = decltype(mtc)::value;
       if (mt < mt_lo || mt >= mt_live) return;       // uniform
 #pragma unroll
-      for (int q = 0; q < kRowsWaveStrips / 2; ++q) {
-        if (strip0 + 2 * q >= p.n_strips) continue;  // uniform
-        const int f = ((strip0 >> 1) + q) * 16 + c16;
+      for (int s = 0; s < kRowsWaveStrips; ++s) {
+        if (strip0 + s >= p.n_strips) continue;      // uniform
+        const int f = (strip0 + s) * 8 + c16;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
-          const float gt = acc[mt][2 * q][i] * rs_s[rl];
-          const float up = acc[mt][2 * q + 1][i] * rs_s[rl];
+          const float gt = acc[mt][s][i] * rs_s[rl];
+          const float up = __shfl_xor(gt, 8);
           const float h = gt / (1.0f + expf(-gt)) * up;
-          if (r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_bits(h);
+          if (c16 < 8 && r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_bits(h);
         }
       }
     });
@@ -1002,9 +1006,10 @@ hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev
 template <int EPI, int MT>
 hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   switch (S) {
-    case 1: if constexpr (EPI != EPI_SWIGLU) return launch_one<EPI, MT, 1>(nw, a, st, ev); break;
+    case 1: return launch_one<EPI, MT, 1>(nw, a, st, ev);
     case 2: return launch_one<EPI, MT, 2>(nw, a, st, ev);
     case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st, ev); break;
+    case 7: if constexpr (MT == 1 && EPI == EPI_SWIGLU) return launch_one<EPI, MT, 7>(nw, a, st, ev); break;
   }
   return hipErrorInvalidValue;
 }

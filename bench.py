@@ -285,6 +285,8 @@ def main() -> int:
     ap.add_argument("--workload", default="llama8b_1b")
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-baselines", action="store_true",
+                    help="skip the plain-target and vanilla-SD comparison runs (profiling runs)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (byte-counter calibration under rocprofv3)")
     args = ap.parse_args()
@@ -364,7 +366,7 @@ def main() -> int:
                 "launches": launches, "avg_us": round(avg_s * 1e6, 2),
                 "bytes_per_launch": gu_bytes}
 
-    baselines = measure_baselines(eng, B, prompt, k, wall / steps, emitted / wall)
+    baselines = None if args.no_baselines else measure_baselines(eng, B, prompt, k, wall / steps, emitted / wall)
 
     result = {
         "metric": METRIC,

@@ -61,16 +61,21 @@ struct GemmPlan {
 
 int pick_S(int epi, int n_strips, int mt) {
   if (epi == EPI_SWIGLU && mt == 1) {
-    // the largest strips-per-workgroup count that divides the strips and fills
-    // the 256 CUs most evenly (8B shape: 7 strips -> exactly one workgroup per CU)
-    int best = 1;
+    // the strips-per-workgroup count that divides the strips and fills the 256
+    // CUs most evenly; among equally even ones, the one closest to two rounds
+    // of workgroups (measured: 8B shape 7 strips = one workgroup per CU, 41 us,
+    // against 54 us at 1 strip; 1B shape 2 strips, two rounds, slightly ahead
+    // of 4 strips)
+    int best = 1, best_d = 1 << 30;
     double best_u = 0.0;
     for (int s : {7, 4, 2, 1}) {
       if (n_strips % s) continue;
       const int tiles = n_strips / s;
       const double u = (double)tiles / (ceil_div(tiles, 256) * 256);
-      if (u > best_u + 1e-9) {
+      const int d = std::abs(tiles - 512);
+      if (u > best_u + 1e-9 || (u > best_u - 1e-9 && d < best_d)) {
         best_u = u;
+        best_d = d;
         best = s;
       }
     }

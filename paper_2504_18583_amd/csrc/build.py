@@ -2,7 +2,9 @@
 
 Usage: python -m paper_2504_18583_amd.csrc.build   (or call build()).
 Objects go to ``_build/`` beside the package; the shared library is written
-into the package directory, where the binding loads it from.
+into the package directory, where the binding loads it from.  The same call
+links ``gemm_counters`` (a stand-alone launch of the gate/up GEMM for
+hardware-counter runs) from the GEMM object.
 """
 from __future__ import annotations
 
@@ -17,8 +19,10 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpard.so")
+COUNTERS_EXE = os.path.join(PKG, "gemm_counters")
 
-SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip"]
+SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "gemm_counters.hip"]
+LIB_SOURCES = SOURCES[:4]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -47,15 +51,21 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with ThreadPoolExecutor(len(SOURCES)) as ex:
         objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    obj = dict(zip(SOURCES, objs))
+    _link(LIB, ["-shared", "-fPIC"], [obj[s] for s in LIB_SOURCES])
+    _link(COUNTERS_EXE, [], [obj["gemm_counters.hip"], obj["gemm.hip"]])
+    if verbose:
+        print(f"built {LIB} and {COUNTERS_EXE}")
+    return LIB
+
+
+def _link(out: str, flags: list, objs: list) -> None:
+    tmp = out + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", *flags, "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError(f"linking failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
-    if verbose:
-        print(f"built {LIB}")
-    return LIB
+        raise RuntimeError(f"linking {os.path.basename(out)} failed:\n{' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    os.replace(tmp, out)
 
 
 if __name__ == "__main__":

@@ -24,6 +24,7 @@ constexpr int kPrefillRows = kMaxPassRows;   // prefill chunks run the row-block
 constexpr int kDescRing = 128;
 constexpr int kGatherMax = 4096;
 constexpr size_t kRowsPartBudget = 512;   // fp32 partial tiles of split row-block GEMMs (144 KiB each)
+static_assert(kRowsPartBudget * kRowsPartFloats >= kSplitPartFloats, "split partial tiles share the row-block buffer");
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 int ceil_div(int a, int b) { return (a + b - 1) / b; }
@@ -57,6 +58,7 @@ struct Bump {
 struct GemmPlan {
   int n_strips = 0, kb_total = 0;
   int nw = 4;   // one wavefront per SIMD: more waves per workgroup measured slower at every decode shape
+  int ksplit = 1;   // input ranges of the skinny GEMM
 };
 
 int pick_S(int epi, int n_strips, int mt) {
@@ -95,7 +97,11 @@ GemmPlan plan_gemm(int epi, int n_pad, int k_pad) {
   GemmPlan p;
   p.n_strips = n_pad / 16;
   p.kb_total = k_pad / 32;
-  (void)epi;
+  // A long, narrow residual GEMM (the 1B down projection: 128 strips x 256
+  // k-blocks) fills only half the CUs with one workgroup per strip; two input
+  // ranges per strip measured 11.8 against 13.6 us.  Shorter or wider shapes
+  // measured slower split (the partial-tile exchange adds ~2 us of tail).
+  if (epi == EPI_RESID && p.n_strips <= 128 && p.kb_total >= 256) p.ksplit = 2;
   return p;
 }
 
@@ -172,7 +178,8 @@ struct pard_ctx {
   float* amax_val = nullptr;
   int* amax_idx = nullptr;
   float* attn_part = nullptr;
-  float* rows_part = nullptr;
+  float* rows_part = nullptr;           // also the skinny GEMM's split partial tiles
+  int* split_counters = nullptr;
   SeqState* seq_dev = nullptr;
   int* out_dev = nullptr;
   size_t* gather_idx_dev = nullptr;
@@ -328,6 +335,7 @@ size_t layout(pard_ctx* c, char* base) {
   c->amax_idx = b.take<int>((size_t)max_lm_tiles * lm_rows_cap);
   c->attn_part = b.take<float>(attn_part);
   c->rows_part = b.take<float>(kRowsPartBudget * kRowsPartFloats);
+  c->split_counters = b.take<int>(kSplitCounters);
   c->seq_dev = b.take<SeqState>(c->max_batch);
   c->out_dev = b.take<int>((size_t)c->max_batch * c->max_ctx);
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
@@ -461,6 +469,10 @@ hipError_t run_gemm(pard_ctx* c, int cls, int epi, int max_rows, int typ_rows, G
   const int mt = ceil_div(max_rows, 16);
   const int S = pick_S(epi, p.n_strips, mt);
   a.n_tiles = p.n_strips / S;
+  a.ksplit = p.ksplit;
+  a.kb_split = ceil_div(p.kb_total, p.ksplit);
+  a.part = c->rows_part;
+  a.counters = c->split_counters;
   return launch_gemm(epi, mt, S, plan_nw(p, S, mt), a, c->stream, ev);
 }
 
@@ -873,6 +885,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[1].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->split_counters, 0, sizeof(int) * kSplitCounters, c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   *out = c;

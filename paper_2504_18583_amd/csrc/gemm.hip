@@ -17,6 +17,14 @@
 // does not depend on how many other rows are in the pass.  No workgroup ever
 // waits for another one.
 //
+// Shapes with few strips also split the input dimension over the grid's y
+// dimension (P contiguous ranges of k-blocks), so that narrow GEMMs still
+// occupy every CU and one activation fragment feeds several strips.  Each
+// workgroup stores its fp32 partial tile and counts itself in on the tile's
+// counter; the last of the P to arrive adds the P partials in range order
+// (the same order whichever workgroup is last) and runs the epilogue, then
+// resets the counter for the next launch.
+//
 // Epilogues fuse the surrounding element-wise work of a Llama block:
 //   EPI_QKV     RMSNorm row scale (A holds x*g in fp16, written by the
 //               producer; 1/rms comes from the producer's per-tile sums of
@@ -49,6 +57,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kRsrcWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-family raw buffers
 constexpr int kCachePolicyNT = 2;        // non-temporal: weights are streamed once
+constexpr int kWaitVmcnt0 = 0x0F70;      // s_waitcnt vmcnt(0), expcnt and lgkmcnt not waited for
 
 // Sum over the 16 lanes of a DPP row (lanes 16g .. 16g+15), fixed order:
 // quad_perm swaps (1 0 3 2), (2 3 0 1), then half-row and row mirrors.
@@ -78,9 +87,12 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   const int nw = blockDim.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wavefront
 
-  // wave w streams k-blocks w, w + nw, w + 2*nw, ...: at any time the
+  // input range of this workgroup: k-blocks [kb0, kb0 + kb_n)
+  const int kb0 = blockIdx.y * p.kb_split;
+  const int kb_n = min(p.kb_split, p.kb_total - kb0);
+  // wave w streams k-blocks kb0 + w, kb0 + w + nw, ...: at any time the
   // workgroup reads nw consecutive k-blocks of each strip
-  const int n_it = (p.kb_total - wave + nw - 1) / nw;
+  const int n_it = (kb_n - wave + nw - 1) / nw;
 
   f32x4 acc[S][MT];
 #pragma unroll
@@ -105,7 +117,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   auto load_w = [&](u32x4 (&w)[U][S], int its) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kb = wave + min(its + u, n_it - 1) * nw;
+      const int kb = kb0 + wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
       for (int s = 0; s < S; ++s)
         w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
@@ -139,7 +151,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   auto load_a = [&](u32x4 (&a)[U][MT], int its) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kb = wave + min(its + u, n_it - 1) * nw;
+      const int kb = kb0 + wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
         a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (p.act_rows * 64), 0);
@@ -268,6 +280,40 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     float t = red[e];
     for (int w = 1; w < nw; ++w) t += red[w * NE + e];
     v[j] = t;
+  }
+
+  // ---- split input dimension: the last workgroup of the tile to finish sums the partials ----
+  // Partials are stored and loaded at device scope (written through to, and
+  // read from, the level shared by all XCDs), so the count needs no cache
+  // write-back or invalidation: each wavefront waits until its stores are
+  // complete before the workgroup counts itself in.
+  const int n_split = gridDim.y;
+  if (n_split > 1) {
+    __shared__ int last_s;
+    float* part = p.part + (size_t)tile * n_split * NE;
+    if (epi) {
+#pragma unroll
+      for (int j = 0; j < NJ; ++j)
+        __hip_atomic_store(part + (size_t)blockIdx.y * NE + j * 256 + tid, v[j], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    __syncthreads();
+    if (tid == 0) {
+      const int prev = __hip_atomic_fetch_add(p.counters + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      last_s = prev == n_split - 1;
+      if (prev == n_split - 1) __hip_atomic_store(p.counters + tile, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (!last_s) return;    // uniform over the workgroup
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int e = j * 256 + (tid & 255);
+      float t = 0.f;
+      for (int q = 0; q < n_split; ++q)
+        t += __hip_atomic_load(part + (size_t)q * NE + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      v[j] = t;
+    }
   }
 
   if constexpr (EPI == EPI_QKV) {
@@ -995,10 +1041,10 @@ hipError_t launch_one(int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev
   const size_t lds = (size_t)nw * S * MT * 256 * sizeof(float);
   if (nw > 8) return hipErrorInvalidValue;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_gemm<MT, S, EPI>, dim3(a.n_tiles), dim3(64 * nw), (uint32_t)lds, st, ev.start, ev.stop,
+    hipExtLaunchKernelGGL(k_gemm<MT, S, EPI>, dim3(a.n_tiles, a.ksplit), dim3(64 * nw), (uint32_t)lds, st, ev.start, ev.stop,
                           0u, a);
   } else {
-    k_gemm<MT, S, EPI><<<dim3(a.n_tiles), dim3(64 * nw), lds, st>>>(a);
+    k_gemm<MT, S, EPI><<<dim3(a.n_tiles, a.ksplit), dim3(64 * nw), lds, st>>>(a);
   }
   return hipGetLastError();
 }
@@ -1029,6 +1075,13 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, L
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   if (nw < 4 || nw > 8 || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
+  // split input: every range non-empty, partial tiles and counters supplied
+  if (a.ksplit < 1 || a.kb_split < 1 || (a.ksplit - 1) * a.kb_split >= a.kb_total ||
+      a.ksplit * a.kb_split < a.kb_total)
+    return hipErrorInvalidValue;
+  if (a.ksplit > 1 && (!a.part || !a.counters || a.n_tiles > kSplitCounters ||
+                       (size_t)a.n_tiles * a.ksplit * S * mt * 256 > kSplitPartFloats))
+    return hipErrorInvalidValue;
   switch (epi) {
     case EPI_QKV: return launch_mt<EPI_QKV>(mt, S, nw, a, st, ev);
     case EPI_RESID: return launch_mt<EPI_RESID>(mt, S, nw, a, st, ev);

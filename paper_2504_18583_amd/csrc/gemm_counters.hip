@@ -1,17 +1,26 @@
-// Stand-alone run of one skinny GEMM launch shape, for hardware counters.
+// Stand-alone launches of one skinny GEMM shape, for hardware counters and
+// launch-shape timing.
 //
-// Launches the SwiGLU gate/up GEMM (k_gemm<MT=1, S, EPI_SWIGLU>) at the
-// LLaMA3.1-8B shape (hidden 4096, intermediate 14336, gate and up stacked:
-// 1792 strips of 16 columns) over `rows` decode rows, 20 times untimed and
-// 100 times timed, and prints the mean launch time.  It exists so that
-// rocprofv3 --pmc can count the HBM bytes of exactly this kernel in a short
-// program of its own.  Weights and activations are seeded pseudo-random fp16
-// values; the result is not checked (the parity tests do that through the
-// library).
+// Launches k_gemm<MT=1, S, EPI> (EPI_SWIGLU or EPI_RESID) over `rows` decode
+// rows of a weight of `strips` 16-column strips x `kb` 32-column k-blocks,
+// with the input dimension split into P ranges, 20 times untimed and 100 times
+// timed, and prints the mean launch time.  The defaults are the LLaMA3.1-8B
+// gate/up GEMM (hidden 4096, intermediate 14336, gate and up stacked: 1792
+// strips) as the decode step launches it.  `copies` > 1 cycles the launches
+// through that many weight copies, so that a small weight is not served from
+// the last-level cache on every launch as it would not be in a decode step.
+// Weights and activations are seeded pseudo-random fp16 values.  With check
+// = 1 it then runs, for every weight copy in turn, the same launch unsplit and
+// split and compares the two outputs (they differ only by summation order), a
+// test of the split's partial-tile exchange; the numerics of the kernel itself
+// are tested against the oracle through the library.
 //
-// usage: gemm_counters [rows (1..64, default 9)] [strips per workgroup S (1, 2, 4, 7; default 7)]
+// usage: gemm_counters [rows 9] [S 7] [P 1] [strips 1792] [kb 128] [epi swiglu|resid] [copies 1] [check 0]
 #include <cstdio>
 #include <cstdlib>
+#include <cmath>
+#include <cstring>
+#include <vector>
 
 #include "pard_internal.h"
 
@@ -35,31 +44,54 @@ __global__ void k_fill_f16(uint16_t* p, size_t n, uint32_t seed) {
   }
 }
 
+__global__ void k_fill_value(float* p, size_t n, float v) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
+}
+
 int main(int argc, char** argv) {
   const int rows = argc > 1 ? atoi(argv[1]) : 9;
   const int S = argc > 2 ? atoi(argv[2]) : 7;
-  const int hidden = 4096, n_strips = 2 * 14336 / 16, kb_total = hidden / 32;
-  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || S == 7) || n_strips % S != 0) {
-    fprintf(stderr, "rows must be in 1..%d and S one of 1, 2, 4, 7\n", kMaxRows);
+  const int P = argc > 3 ? atoi(argv[3]) : 1;
+  const int n_strips = argc > 4 ? atoi(argv[4]) : 2 * 14336 / 16;
+  const int kb_total = argc > 5 ? atoi(argv[5]) : 4096 / 32;
+  const bool resid = argc > 6 && strcmp(argv[6], "resid") == 0;
+  const int copies = argc > 7 ? atoi(argv[7]) : 1;
+  const bool check = argc > 8 && atoi(argv[8]) != 0;
+  const int epi = resid ? EPI_RESID : EPI_SWIGLU;
+  const int kb_split = P > 0 ? (kb_total + P - 1) / P : 0;
+  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || (S == 7 && !resid)) || n_strips < 1 ||
+      n_strips % S != 0 || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 || copies > 64 ||
+      (size_t)n_strips * kb_total * 1024 * copies > ((size_t)8 << 30)) {
+    fprintf(stderr, "bad shape: rows 1..%d, S in {1, 2, 4, 7 (swiglu)}, S | strips, every input range non-empty, "
+            "copies 1..64 of at most 8 GiB in all\n", kMaxRows);
     return 2;
   }
+  const int hidden = kb_total * 32;
+  const int out_cols = n_strips * 16;
   const size_t w_elems = (size_t)n_strips * kb_total * 512;
   const size_t a_elems = (size_t)kMaxRows * hidden;
-  const size_t o_elems = (size_t)kMaxRows * n_strips * 8;
+  const size_t o_elems = ((size_t)n_strips * 16 / 32 + 1) * kMaxRows * 32;   // k-blocked rows, one block spare
   uint16_t *W, *A, *out;
-  float* ss;
+  float *ss, *x, *g, *ss_out, *part;
+  int* counters;
   FwdDesc* desc;
-  CHECK(hipMalloc(&W, w_elems * 2));
+  CHECK(hipMalloc(&W, w_elems * 2 * copies));
   CHECK(hipMalloc(&A, a_elems * 2));
   CHECK(hipMalloc(&out, o_elems * 2));
   CHECK(hipMalloc(&ss, sizeof(float) * kMaxPassRows));
+  CHECK(hipMalloc(&x, sizeof(float) * kMaxRows * out_cols));
+  CHECK(hipMalloc(&g, sizeof(float) * out_cols));
+  CHECK(hipMalloc(&ss_out, sizeof(float) * (size_t)kMaxPassRows * n_strips));
+  CHECK(hipMalloc(&part, sizeof(float) * kSplitPartFloats));
+  CHECK(hipMalloc(&counters, sizeof(int) * kSplitCounters));
   CHECK(hipMalloc(&desc, sizeof(FwdDesc)));
-  k_fill_f16<<<1024, 256>>>(W, w_elems, 1u);
+  CHECK(hipMemset(counters, 0, sizeof(int) * kSplitCounters));
+  k_fill_f16<<<1024, 256>>>(W, w_elems * copies, 1u);
   k_fill_f16<<<64, 256>>>(A, a_elems, 2u);
+  k_fill_value<<<64, 256>>>(ss, kMaxPassRows, (float)hidden / 3072.0f);   // rms ~ 1/sqrt(3072)
+  k_fill_value<<<64, 256>>>(x, (size_t)kMaxRows * out_cols, 0.5f);
+  k_fill_value<<<64, 256>>>(g, out_cols, 1.0f);
   CHECK(hipGetLastError());
-  static float hs[kMaxPassRows];
-  for (float& v : hs) v = (float)hidden / 3072.0f;    // sum of squares of each row: rms ~ 1/sqrt(3072)
-  CHECK(hipMemcpy(ss, hs, sizeof hs, hipMemcpyHostToDevice));
   static FwdDesc hd;
   hd.n_rows = rows;
   hd.n_seq = 1;
@@ -68,26 +100,69 @@ int main(int argc, char** argv) {
   CHECK(hipMemcpy(desc, &hd, sizeof hd, hipMemcpyHostToDevice));
 
   GemmArgs a{};
-  a.W = W; a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = n_strips / S;
+  a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = n_strips / S;
+  a.ksplit = P; a.kb_split = kb_split; a.part = part; a.counters = counters;
   a.A = A; a.lda = hidden; a.act_rows = kMaxRows; a.desc = desc;
   a.ss_in = ss; a.ss_tiles = 1; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
-  a.out = out; a.ld_out = n_strips * 8;
+  a.out = out; a.ld_out = out_cols;
+  a.x = x; a.ldx = out_cols; a.g_next = g; a.xg = out; a.ss_out = ss_out;
 
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
   CHECK(hipEventCreate(&e1));
-  for (int i = 0; i < 20; ++i) CHECK(launch_gemm(EPI_SWIGLU, 1, S, 4, a, 0));
+  int launch = 0;
+  auto run = [&]() {
+    a.W = W + w_elems * (launch++ % copies);
+    return launch_gemm(epi, 1, S, 4, a, 0);
+  };
+  for (int i = 0; i < 20; ++i) CHECK(run());
   CHECK(hipDeviceSynchronize());
   const int n = 100;
   CHECK(hipEventRecord(e0, 0));
-  for (int i = 0; i < n; ++i) CHECK(launch_gemm(EPI_SWIGLU, 1, S, 4, a, 0));
+  for (int i = 0; i < n; ++i) CHECK(run());
   CHECK(hipEventRecord(e1, 0));
   CHECK(hipEventSynchronize(e1));
   float ms = 0.f;
   CHECK(hipEventElapsedTime(&ms, e0, e1));
   const double us = ms * 1e3 / n;
-  printf("k_gemm<1, %d, 2> gate/up 8B shape, %d rows, %d workgroups: %.2f us per launch, weights %.2f TB/s\n", S,
-         rows, n_strips / S, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
-  CHECK(hipFree(W)); CHECK(hipFree(A)); CHECK(hipFree(out)); CHECK(hipFree(ss)); CHECK(hipFree(desc));
+  printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups, %d weight copies: "
+         "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : "swiglu", n_strips, kb_total, rows,
+         n_strips / S, P, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
+  if (check) {
+    // unsplit reference and split launch per copy, x reset before each (the
+    // residual epilogue updates it in place); outputs compared as fp16
+    std::vector<uint16_t> ref(o_elems), got(o_elems);
+    GemmArgs r = a;
+    r.ksplit = 1;
+    r.kb_split = kb_total;
+    auto to_f = [](uint16_t b) { return (float)__builtin_bit_cast(_Float16, b); };
+    double worst = 0.0;
+    long bad = 0, compared = 0;
+    for (int c = 0; c < copies; ++c) {
+      for (int pass = 0; pass < 2; ++pass) {
+        GemmArgs& q = pass == 0 ? r : a;
+        q.W = W + w_elems * c;
+        k_fill_value<<<64, 256>>>(x, (size_t)kMaxRows * out_cols, 0.5f);
+        CHECK(hipMemset(out, 0, o_elems * 2));
+        CHECK(launch_gemm(epi, 1, S, 4, q, 0));
+        CHECK(hipMemcpy(pass == 0 ? ref.data() : got.data(), out, o_elems * 2, hipMemcpyDeviceToHost));
+      }
+      const int cols = resid ? out_cols : out_cols / 2;
+      for (int row = 0; row < rows; ++row)
+        for (int k = 0; k < cols; ++k) {
+          const size_t i = ((size_t)(k >> 5) * kMaxRows + row) * 32 + (k & 31);
+          const double x0 = to_f(ref[i]), x1 = to_f(got[i]);
+          const double d = std::fabs(x1 - x0);
+          worst = std::max(worst, d);
+          bad += !(d <= 2e-3 + 1e-2 * std::fabs(x0));
+          ++compared;
+        }
+    }
+    printf("check split %d vs unsplit over %d copies: %ld of %ld outputs outside 2e-3 + 1e-2|ref|, max |diff| %.3g\n",
+           P, copies, bad, compared, worst);
+    if (bad) return 3;
+  }
+  CHECK(hipFree(W)); CHECK(hipFree(A)); CHECK(hipFree(out)); CHECK(hipFree(ss)); CHECK(hipFree(x));
+  CHECK(hipFree(g)); CHECK(hipFree(ss_out)); CHECK(hipFree(part)); CHECK(hipFree(counters)); CHECK(hipFree(desc));
   return 0;
 }

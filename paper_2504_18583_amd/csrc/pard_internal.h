@@ -49,6 +49,9 @@ constexpr int kRowsWaveStrips = 4;
 constexpr int kRowsTileStrips = kRowsWaves * kRowsWaveStrips;
 constexpr int kRowsPartFloats = kRowsWaves * kRowTiles * kRowsWaveStrips * 256;   // one partial tile
 constexpr int kBlock = 256;
+// skinny GEMM with a split input dimension: tile counters and fp32 partial tiles
+constexpr int kSplitCounters = 4096;
+constexpr size_t kSplitPartFloats = (size_t)4 << 20;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
 constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
 constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head and sequence
@@ -149,10 +152,15 @@ struct GemmArgs {
   float* logits; int vocab;
   float* amax_val; int* amax_idx; int amax_stride;   // entries per lm row
   // row-block GEMM (passes of more than kMaxRows rows): weight strips, row
-  // blocks, input splits and the fp32 partial tiles of split inputs
+  // blocks, input splits and the fp32 partial tiles of split inputs.  The
+  // skinny GEMM splits its input into ksplit ranges of kb_split k-blocks
+  // (ksplit = 1: one range) and counts arrivals per tile in counters (zero
+  // between launches).
   int n_strips;
   int m_blocks, ksplit;
   float* part;
+  int kb_split;
+  int* counters;
 };
 
 // Second argmax pass over the lm_head tiles and the step tail: one workgroup

@@ -8,7 +8,7 @@
   same slices in lock-step.
 * Full depth (32 / 16 layers): properties that hold at any size -- the accept
   rule against the engine's own logits, KV-length bookkeeping, fused loop ==
-  granular calls token for token, bitwise determinism.
+  granular calls token for token, bitwise determinism of both models' logits.
 * 16k-token context: the attention chunk/merge path at the long-context
   workload's length, on a narrow pair the oracle can follow.
 """
@@ -117,9 +117,13 @@ def test_llama_8b_1b_full_depth_properties(B):
         for _ in range(2):
             assert eng.prefill(prompt) == first
             toks, stats = eng.generate(wl.k, len(out))
-            runs.append((toks, eng.read_logits(B.PARD_TARGET, wl.k + 1).copy()))
+            runs.append((toks, eng.read_logits(B.PARD_TARGET, wl.k + 1).copy(),
+                         eng.read_logits(B.PARD_DRAFT, wl.k).copy()))
         assert runs[0][0] == out
+        # bitwise: fixed reduction orders everywhere, including the draft's
+        # down projection, whose input is split over two workgroups per strip
         assert runs[0][0] == runs[1][0] and np.array_equal(runs[0][1], runs[1][1])
+        assert np.array_equal(runs[0][2], runs[1][2])
     finally:
         eng.close()
 

@@ -10,6 +10,9 @@ Modules:
 * ``oracle.model`` -- the decoder (forward with and without a KV cache).
 * ``oracle.pard``  -- greedy decoding (eq. 2) and the PARD draft / verify /
   accept loop (Sec. 2.2, Sec. 3.1 eq. 7).
+* ``oracle.sampling`` -- speculative sampling at temperature T > 0 (the
+  rejection rule Sec. 1 and Sec. 2.2 cite) on the PARD draft, with a
+  counter-based SplitMix64 generator.
 
 Pins (tests marked "not gpu"): the decoder against the independent
 Hugging Face Llama/Qwen2 implementations and torch's attention/normalisation
@@ -17,11 +20,17 @@ routines; cached vs. uncached forward position by position; the one-pass draft
 against K separate uncached passes (eq. 7); lossless greedy speculative
 decoding against plain greedy decoding (eq. 2) for K in {1, 2, 4, 8, 12};
 forced-candidate acceptance; the draft-equals-target special case.
+Sampling: SplitMix64's published outputs; inverse-CDF drawing against the
+weights; the keep / residual / bonus rule against the target distribution at
+every position (chi-square); the whole sampled loop against enumerated
+autoregressive marginals on a small vocabulary; vanishing temperature ==
+greedy.
 """
 from .model import (KVCache, Model, attention, forward_cached, forward_full, linear,
                     rms_norm, rope, silu)
 from .pard import (PardTrace, accept_prefix, argmax_rows, draft_step, greedy_ar,
                    pard_generate, prefill, vanilla_draft_step, vanilla_generate, verify_step)
+from . import sampling
 
 
 def build_model(spec, layers=None) -> Model:

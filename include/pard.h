@@ -180,6 +180,28 @@ pard_status pard_generate_ex(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, 
                              int32_t mode, int32_t n_tokens, int32_t max_steps,
                              int32_t *out_tokens, pard_stats *stats);
 
+/* Speculative sampling (Sec. 1 and Sec. 2.2: speculative decoding combined
+ * with speculative sampling keeps the target's output distribution).  With
+ * temperature T > 0 every later pard_prefill, pard_draft, pard_verify and
+ * pard_generate samples instead of taking the argmax:
+ *   - distributions are softmax(logits / T) of either model;
+ *   - pard_prefill draws the first token from the target;
+ *   - pard_draft draws candidate j+1 from the draft's row j (eq. 7 rows);
+ *   - pard_verify keeps candidate x at position j iff u * q_j(x) < p_j(x)
+ *     (p target, q draft), in order; at the first candidate not kept the
+ *     step's last token is drawn from max(0, p_j - q_j) (normalised), if all
+ *     K are kept from p_K; *n_accepted / *bonus report the kept count and
+ *     that last token (K = 0: one token drawn from p_0).
+ * Draws use the inverse CDF in token-id order.  The uniforms u come from a
+ * SplitMix64 counter generator keyed by (seed, slot, the slot's verify steps
+ * since its prefill, position, purpose), so results are reproducible and
+ * independent of batching.  T = 0 restores greedy decoding (eq. 2).  Captured
+ * step graphs are dropped (rebuilt on the next pard_generate).  With sampling,
+ * pard_verify with K > 0 needs this slot's pard_draft of the same K since its
+ * last verify (STATE otherwise), and PARD_MODE_VANILLA is UNSUPPORTED.
+ * Errors: ARG (T negative, not finite, or in (0, 1e-3)), DEVICE. */
+pard_status pard_set_sampling(pard_ctx *ctx, float temperature, uint64_t seed);
+
 /* Copy the fp32 logits of slot `seq`'s rows in the last lm_head pass of
  * `which` that included the slot (rows x vocab, row-major; draft rows are the
  * K candidate rows, target rows the verify rows, prefill the single

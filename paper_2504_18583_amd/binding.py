@@ -60,6 +60,7 @@ _sig = {
                                 C.POINTER(pard_stats)]),
     "pard_generate_ex": (C.c_int, [_CTX, C.c_int32, _I32P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                    _I32P, C.POINTER(pard_stats)]),
+    "pard_set_sampling": (C.c_int, [_CTX, C.c_float, C.c_uint64]),
     "pard_read_logits": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                    C.c_int32]),
     "pard_read_weight": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -173,6 +174,11 @@ class Engine:
         self._check(lib.pard_verify(self.ctx, seq, ptr, len(cand), C.byref(a), C.byref(bonus)),
                     "pard_verify")
         return a.value, bonus.value
+
+    def set_sampling(self, temperature: float, seed: int = 0) -> None:
+        """Speculative sampling at temperature T > 0 for later calls; 0 = greedy."""
+        self._check(lib.pard_set_sampling(self.ctx, float(temperature), int(seed) & ((1 << 64) - 1)),
+                    "pard_set_sampling")
 
     def kv_len(self, which: int, seq: int = 0) -> int:
         n = C.c_int32()

@@ -6,15 +6,6 @@
 namespace pard {
 namespace {
 
-constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
-
-// SplitMix64 output function (Steele, Lea, Flood 2014).
-__device__ __forceinline__ uint64_t mix64(uint64_t z) {
-  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
-  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
-  return z ^ (z >> 31);
-}
-
 __device__ __forceinline__ uint16_t f2bf(float f) {
   const uint32_t u = __float_as_uint(f);
   return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);

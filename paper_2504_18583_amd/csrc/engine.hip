@@ -177,6 +177,11 @@ struct pard_ctx {
   // shared device workspaces
   float* amax_val = nullptr;
   int* amax_idx = nullptr;
+  float* amax_sum = nullptr;            // per-tile softmax sums (sampling)
+  // speculative sampling: log2(e) / T (0: greedy) and the generator's seed
+  float samp_k = 0.f;
+  uint64_t samp_seed = 0;
+  std::vector<int> draft_k;             // K of each slot's last granular draft pass (0: none since verify)
   float* attn_part = nullptr;
   float* rows_part = nullptr;           // also the skinny GEMM's split partial tiles
   int* split_counters = nullptr;
@@ -333,6 +338,7 @@ size_t layout(pard_ctx* c, char* base) {
   }
   c->amax_val = b.take<float>((size_t)max_lm_tiles * lm_rows_cap);
   c->amax_idx = b.take<int>((size_t)max_lm_tiles * lm_rows_cap);
+  c->amax_sum = b.take<float>((size_t)max_lm_tiles * lm_rows_cap);
   c->attn_part = b.take<float>(attn_part);
   c->rows_part = b.take<float>(kRowsPartBudget * kRowsPartFloats);
   c->split_counters = b.take<int>(kSplitCounters);
@@ -601,6 +607,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     a.amax_val = c->amax_val;
     a.amax_idx = c->amax_idx;
     a.amax_stride = lm_entries(M.p_lm, lm_rows, mt_lm);
+    a.samp_k = c->samp_k;
+    a.amax_sum = c->amax_sum;
     HIP_TRY(c, run_gemm(c, cls0 + 6, EPI_LOGITS, ps.max_lm_rows, ps.max_lm_rows, a, M.p_lm));
     TailArgs ta{};
     ta.desc = M.desc;
@@ -616,6 +624,12 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     ta.next_desc = ps.next_desc;
     ta.out_tokens = ps.emit ? c->out_dev : nullptr;
     ta.out_cap = c->max_ctx;
+    ta.samp_k = c->samp_k;
+    ta.seed = c->samp_seed;
+    ta.amax_sum = c->amax_sum;
+    ta.logits = M.logits;
+    ta.q_logits = c->m[PARD_DRAFT].logits;
+    ta.tile_w = lm_rows ? kRowsWaveStrips * 16 : pick_S(EPI_LOGITS, M.p_lm.n_strips, mt_lm) * 16;
     Timed t(c, cls0 + 7);
     HIP_TRY(c, launch_tail(ta, ps.n_seq, c->stream));
     if (ps.n_seq > 1 && ps.next_desc) HIP_TRY(c, launch_stage(ta, c->stream));
@@ -865,6 +879,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   c->hist.assign(max_batch, {});
   if (const char* e = getenv("PARD_NO_GRAPH")) c->use_graphs = e[0] == '0';
   c->prefilled.assign(max_batch, 0);
+  c->draft_k.assign(max_batch, 0);
 
   auto bail = [&](pard_status s) {
     pard_free(c);
@@ -910,6 +925,19 @@ void pard_free(pard_ctx* c) {
 
 const char* pard_last_error(const pard_ctx* c) { return c ? c->err.c_str() : "null context"; }
 
+pard_status pard_set_sampling(pard_ctx* c, float temperature, uint64_t seed) {
+  if (!c) return PARD_ERR_ARG;
+  if (!(temperature >= 0.f) || !std::isfinite(temperature) || (temperature > 0.f && temperature < 1e-3f))
+    return fail(c, PARD_ERR_ARG, "set_sampling: temperature %g outside {0} and [1e-3, inf)", (double)temperature);
+  c->samp_k = temperature > 0.f ? (float)(1.4426950408889634 / temperature) : 0.f;
+  c->samp_seed = seed;
+  // captured steps hold the old settings in their kernel arguments
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return fail(c, PARD_ERR_DEVICE, "set_sampling: stream");
+  for (auto& g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  c->graphs.clear();
+  return PARD_OK;
+}
+
 pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_t n, int32_t* first_token) {
   if (!c) return PARD_ERR_ARG;
   pard_status st = check_seq(c, seq, false);
@@ -945,6 +973,7 @@ pard_status pard_prefill(pard_ctx* c, int32_t seq, const int32_t* prompt, int32_
   c->hist[seq].assign(prompt, prompt + n);
   c->hist[seq].push_back(S.bonus);
   c->prefilled[seq] = 1;
+  c->draft_k[seq] = 0;
   return PARD_OK;
 }
 
@@ -984,6 +1013,7 @@ pard_status pard_draft(pard_ctx* c, int32_t seq, const int32_t* prefix, int32_t 
   if ((st = forward(c, PARD_DRAFT, ps)) != PARD_OK) { S = saved; return st; }
   if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
   for (int i = 0; i < K; ++i) cand[i] = S.cand[i];
+  c->draft_k[seq] = K;
   return PARD_OK;
 }
 
@@ -998,6 +1028,8 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
   SeqState& S = c->h_seq[seq];
   if ((int64_t)S.L[0] + K + 1 > c->max_ctx)
     return fail(c, PARD_ERR_CAPACITY, "verify: %d rows at position %d exceed max_ctx", K + 1, S.L[0]);
+  if (c->samp_k > 0.f && K > 0 && c->draft_k[seq] != K)
+    return fail(c, PARD_ERR_STATE, "verify: sampling needs this slot's draft pass of the same K=%d first", K);
   const SeqState saved = S;
   const int Lt = S.L[0];
   int ids[kMaxK + 1];
@@ -1023,6 +1055,7 @@ pard_status pard_verify(pard_ctx* c, int32_t seq, const int32_t* cand, int32_t K
   if ((st = pull_seq_sync(c, seq)) != PARD_OK) return st;
   *n_accepted = S.a;
   *bonus = S.bonus;
+  c->draft_k[seq] = 0;
   std::vector<int>& h = c->hist[seq];
   h.resize(Lt + 1);
   for (int i = 0; i < S.a; ++i) h.push_back(cand[i]);
@@ -1070,6 +1103,8 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
   if (!c) return PARD_ERR_ARG;
   if (mode != PARD_MODE_PARALLEL && mode != PARD_MODE_VANILLA) return fail(c, PARD_ERR_ARG, "generate: bad mode %d", mode);
   const bool vsd = mode == PARD_MODE_VANILLA;
+  if (vsd && c->samp_k > 0.f)
+    return fail(c, PARD_ERR_UNSUPPORTED, "generate: vanilla drafting runs greedy only (sampling is set)");
   if (!seqs || !out_tokens || n_tokens < 1) return fail(c, PARD_ERR_ARG, "generate: null pointer or n_tokens < 1");
   if (n_seq < 1 || n_seq > std::min(c->max_batch, kMaxPassSeqs))
     return fail(c, PARD_ERR_CAPACITY, "generate: n_seq=%d outside [1, %d]", n_seq, std::min(c->max_batch, kMaxPassSeqs));
@@ -1123,6 +1158,7 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
     S.n_target = n_tokens;
     S.steps = 0;
     S.mask_id = c->mask_id;
+    c->draft_k[seq] = 0;
     memset(S.accept_hist, 0, sizeof S.accept_hist);
     if ((st = push_seq(c, seq)) != PARD_OK) return restore(st);
     if (K > 0 && vsd) {

@@ -73,6 +73,23 @@ __device__ __forceinline__ bool better(float v, int i, float bv, int bi) {
   return v > bv || (v == bv && i < bi);
 }
 
+// Wavefront reductions and scan in a fixed order (results do not depend on timing).
+__device__ __forceinline__ float wave_sum(float v) {
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+  return v;
+}
+__device__ __forceinline__ float wave_incl_scan(float v, int lane) {
+  for (int off = 1; off < 64; off <<= 1) {
+    const float o = __shfl_up(v, off);
+    if (lane >= off) v += o;
+  }
+  return v;
+}
+
 template <int MT, int S, int EPI>
 __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
@@ -415,9 +432,17 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         p.amax_val[(size_t)r * p.amax_stride + tile] = bv;
         p.amax_idx[(size_t)r * p.amax_stride + tile] = (bi == INT_MAX) ? INT_MAX : tile * TW + bi;
       }
+      if (p.samp_k > 0.f) {         // sampling: the tile's softmax weight relative to its max
+        float sw = 0.f;
+        for (int c = lane; c < TW; c += 64) sw += __builtin_amdgcn_exp2f((red[r * TW + c] - bv) * p.samp_k);
+        sw = wave_sum(sw);
+        if (lane == 0) p.amax_sum[(size_t)r * p.amax_stride + tile] = sw;
+      }
     }
   }
 }
+
+__device__ void commit_verify(const TailArgs& p, const PassSeq& ps, int a, int bonus, const int* res);
 
 // Decode-state update of one sequence once the argmax of its lm rows is
 // known (one thread).  Draft: store the candidates, commit only the real rows
@@ -444,7 +469,17 @@ __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
     const int k = s->k;
     int a = 0;
     while (a < k && s->cand[a] == res[a]) ++a;      // longest agreeing prefix
-    const int bonus = res[a];
+    commit_verify(p, ps, a, res[a], res);
+  }
+}
+
+// Verify step of one sequence with a accepted candidates and the step's last
+// token (greedy: the target's argmax t_a; sampling: the residual or bonus
+// draw): L_t += a + 1, emit c_1..c_a and the last token, count the step.
+__device__ void commit_verify(const TailArgs& p, const PassSeq& ps, int a, int bonus, const int* res) {
+  SeqState* s = p.states + ps.slot;
+  {
+    const int k = s->k;
     for (int i = 0; i <= k; ++i) s->t[i] = res[i];
     s->a = a;
     s->bonus = bonus;
@@ -472,6 +507,7 @@ __device__ void seq_tail(const TailArgs& p, const PassSeq& ps, const int* res) {
       }
     }
     ++s->steps;
+    ++s->draw;
     ++s->accept_hist[a];
   }
 }
@@ -587,6 +623,130 @@ __device__ void stage_next(const TailArgs& p, bool drop_done) {
 // independent loads per lane in flight at a time; then one thread updates
 // the sequence's decode state.  A single-sequence pass also stages the next
 // pass here; batched passes stage it in k_stage.
+// ---- speculative sampling (temperature T; samp_k = log2(e) / T) ----
+// A row's distribution is softmax(z / T).  The LM GEMM left, per tile of
+// tile_w columns, the tile's max m_t and s_t = sum 2^((z - m_t) k); the row's
+// max M and normaliser S = sum_t s_t 2^((m_t - M) k) follow.  A token is
+// drawn by inverse CDF in token-id order: the smallest x whose cumulative
+// weight exceeds u S.  All sums run in a fixed order.
+
+__device__ __forceinline__ float tile_weight(float m, float s, float M, float k) {
+  return m == -INFINITY ? 0.f : s * __builtin_amdgcn_exp2f((m - M) * k);
+}
+
+// (M, S) of lm row `lmr` (one wavefront).
+__device__ void row_stats(const TailArgs& p, int lmr, int lane, float* M, float* S) {
+  const float* mv = p.amax_val + (size_t)lmr * p.n_tiles;
+  const float* sv = p.amax_sum + (size_t)lmr * p.n_tiles;
+  float m = -INFINITY;
+  for (int t = lane; t < p.n_tiles; t += 64) m = fmaxf(m, mv[t]);
+  m = wave_max(m);
+  float w = 0.f;
+  for (int t = lane; t < p.n_tiles; t += 64) w += tile_weight(mv[t], sv[t], m, p.samp_k);
+  *M = m;
+  *S = wave_sum(w);
+}
+
+// Draw from lm row `lmr` with uniform u (one wavefront; every lane returns the token).
+__device__ int wave_sample(const TailArgs& p, int lmr, float M, float S, float u, int lane) {
+  const float* mv = p.amax_val + (size_t)lmr * p.n_tiles;
+  const float* sv = p.amax_sum + (size_t)lmr * p.n_tiles;
+  const float k = p.samp_k, target = u * S;
+  // lane l owns a contiguous run of tiles; the lanes' sums are scanned in lane order
+  const int per = (p.n_tiles + 63) / 64;
+  const int t0 = min(lane * per, p.n_tiles), t1 = min(t0 + per, p.n_tiles);
+  float own = 0.f;
+  for (int t = t0; t < t1; ++t) own += tile_weight(mv[t], sv[t], M, k);
+  const float incl = wave_incl_scan(own, lane);
+  float excl = __shfl_up(incl, 1);
+  if (lane == 0) excl = 0.f;
+  const uint64_t hit = __ballot(incl > target && own > 0.f);
+  const uint64_t nz = __ballot(own > 0.f);
+  // the first lane whose prefix passes the target (after rounding: the last lane with weight)
+  const int sel = hit ? __ffsll((unsigned long long)hit) - 1 : (nz ? 63 - __clzll((long long)nz) : 0);
+  int tsel = -1;
+  float rem = 0.f;
+  if (lane == sel) {
+    float acc = excl, last_w = 0.f;
+    int last = -1;
+    for (int t = t0; t < t1; ++t) {
+      const float w = tile_weight(mv[t], sv[t], M, k);
+      if (w > 0.f) { last = t; last_w = w; }
+      if (w > 0.f && acc + w > target) { tsel = t; rem = target - acc; break; }
+      acc += w;
+    }
+    if (tsel < 0) { tsel = last; rem = last_w; }
+  }
+  tsel = __shfl(tsel, sel);
+  rem = __shfl(rem, sel);
+  if (tsel < 0) return 0;
+  // columns of the chosen tile, one per lane
+  const int col = tsel * p.tile_w + lane;
+  float w = 0.f;
+  if (lane < p.tile_w && col < p.vocab)
+    w = __builtin_amdgcn_exp2f((p.logits[(size_t)lmr * p.vocab + col] - M) * k);
+  const float cincl = wave_incl_scan(w, lane);
+  const uint64_t chit = __ballot(cincl > rem && w > 0.f);
+  const uint64_t cnz = __ballot(w > 0.f);
+  const int x = chit ? __ffsll((unsigned long long)chit) - 1 : (cnz ? 63 - __clzll((long long)cnz) : 0);
+  return tsel * p.tile_w + x;
+}
+
+// Residual draw at a rejected position: weights max(0, p(x) - q(x)) over the
+// vocabulary, p from the target row zp (M_p, S_p), q from the draft row zq
+// (M_q, S_q); thread t owns a contiguous run of ids.  Whole workgroup; returns
+// -1 when the residual has no mass (only through rounding).
+__device__ int block_sample_residual(const TailArgs& p, const float* zp, float Mp, float Sp, const float* zq,
+                                     float Mq, float Sq, float u, float* scan_s, int* pick_s) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int V = p.vocab, per = (V + 1023) / 1024;
+  const int x0 = min(tid * per, V), x1 = min(x0 + per, V);
+  const float k = p.samp_k, ip = 1.0f / Sp, iq = 1.0f / Sq;
+  auto resid = [&](int x) {
+    return fmaxf(__builtin_amdgcn_exp2f((zp[x] - Mp) * k) * ip - __builtin_amdgcn_exp2f((zq[x] - Mq) * k) * iq, 0.f);
+  };
+  float own = 0.f;
+  for (int x = x0; x < x1; ++x) own += resid(x);
+  float incl = wave_incl_scan(own, lane);
+  if (lane == 63) scan_s[wave] = incl;
+  if (tid == 0) { pick_s[0] = INT_MAX; pick_s[1] = -1; }
+  __syncthreads();
+  if (wave == 0) {
+    float t = lane < 16 ? scan_s[lane] : 0.f;
+    t = wave_incl_scan(t, lane);
+    if (lane < 16) scan_s[16 + lane] = t;
+  }
+  __syncthreads();
+  const float base = wave > 0 ? scan_s[16 + wave - 1] : 0.f;
+  const float total = scan_s[31];
+  incl += base;
+  float excl = __shfl_up(incl, 1);
+  if (lane == 0) excl = base;
+  const float target = u * total;
+  // owner: the first thread whose prefix passes the target; after rounding,
+  // the last thread with mass
+  if (own > 0.f && incl > target) atomicMin(pick_s, tid);
+  if (own > 0.f) atomicMax(pick_s + 1, tid);
+  __syncthreads();
+  if (!(total > 0.f)) return -1;                  // uniform
+  const bool found = pick_s[0] != INT_MAX;
+  const int owner = found ? pick_s[0] : pick_s[1];
+  __syncthreads();
+  if (tid == owner) {
+    float acc = excl;
+    int last = -1, x_sel = -1;
+    for (int x = x0; x < x1; ++x) {
+      const float r = resid(x);
+      if (r > 0.f) last = x;
+      if (found && r > 0.f && acc + r > target) { x_sel = x; break; }
+      acc += r;
+    }
+    pick_s[0] = x_sel >= 0 ? x_sel : last;
+  }
+  __syncthreads();
+  return pick_s[0];
+}
+
 __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
   __shared__ int res_s[kMaxK + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -620,11 +780,87 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
     }
     if (lane == 0) res_s[r] = (bi >= 0 && bi < p.vocab) ? bi : 0;
   }
-  __syncthreads();
-  if (tid == 0) {
-    for (int r = 0; r < rows; ++r) p.result[ps.lm0 + r] = res_s[r];
-    p.lm_map[ps.slot] = int2{ps.lm0, rows};
-    seq_tail(p, ps, res_s);
+  const bool sampling =
+      p.samp_k > 0.f && (p.tail == TAIL_PREFILL || p.tail == TAIL_DRAFT || p.tail == TAIL_VERIFY);
+  if (!sampling) {
+    __syncthreads();
+    if (tid == 0) {
+      for (int r = 0; r < rows; ++r) p.result[ps.lm0 + r] = res_s[r];
+      p.lm_map[ps.slot] = int2{ps.lm0, rows};
+      seq_tail(p, ps, res_s);
+    }
+  } else {
+    // speculative sampling: draft candidates and the first token are drawn
+    // from their rows; a verify pass runs the keep tests in order and draws
+    // the step's last token from the residual (first rejection) or from the
+    // bonus row (all kept)
+    __shared__ float Ms[kMaxK + 1], Ss[kMaxK + 1];
+    __shared__ float scan_s[32];
+    __shared__ int pick_s[2], a_s, tok_s;
+    SeqState* st = p.states + ps.slot;
+    const int draw = st->draw;
+    for (int r = wave; r < rows; r += 16) {
+      float M, S;
+      row_stats(p, ps.lm0 + r, lane, &M, &S);
+      if (lane == 0) { Ms[r] = M; Ss[r] = S; }
+    }
+    __syncthreads();
+    if (p.tail == TAIL_DRAFT || p.tail == TAIL_PREFILL) {
+      const int purpose = p.tail == TAIL_PREFILL ? PURPOSE_FIRST : PURPOSE_DRAFT;
+      for (int r = wave; r < rows; r += 16) {
+        const int x = wave_sample(p, ps.lm0 + r, Ms[r], Ss[r], sample_uniform(p.seed, ps.slot, draw, r, purpose), lane);
+        if (lane == 0) res_s[r] = x;
+      }
+      if (p.tail == TAIL_DRAFT && tid < min(rows, kMaxK)) {   // the draft's rows, for the keep tests
+        st->qM[tid] = Ms[tid];
+        st->qS[tid] = Ss[tid];
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int r = 0; r < rows; ++r) p.result[ps.lm0 + r] = res_s[r];
+        p.lm_map[ps.slot] = int2{ps.lm0, rows};
+        seq_tail(p, ps, res_s);
+      }
+    } else {   // TAIL_VERIFY
+      const int k = st->k;
+      if (tid == 0) {
+        const int2 dm = p.lm_map_draft[ps.slot];   // this slot's rows of the draft's last pass
+        int a = 0;
+        for (; a < k; ++a) {
+          const int x = st->cand[a];
+          const float pz = p.logits[(size_t)(ps.lm0 + a) * p.vocab + x];
+          const float qz = p.q_logits[(size_t)(dm.x + a) * p.vocab + x];
+          const float pp = __builtin_amdgcn_exp2f((pz - Ms[a]) * p.samp_k) / Ss[a];
+          const float qq = __builtin_amdgcn_exp2f((qz - st->qM[a]) * p.samp_k) / st->qS[a];
+          if (!(sample_uniform(p.seed, ps.slot, draw, a, PURPOSE_KEEP) * qq < pp)) break;
+        }
+        a_s = a;
+      }
+      __syncthreads();
+      const int a = a_s;
+      const float u = sample_uniform(p.seed, ps.slot, draw, a, PURPOSE_LAST);
+      int tok = -1;
+      if (a < k) {
+        const int2 dm = p.lm_map_draft[ps.slot];
+        tok = block_sample_residual(p, p.logits + (size_t)(ps.lm0 + a) * p.vocab, Ms[a], Ss[a],
+                                    p.q_logits + (size_t)(dm.x + a) * p.vocab, st->qM[a], st->qS[a], u, scan_s,
+                                    pick_s);
+      }
+      if (tok < 0) {                                // bonus row (or a residual without mass)
+        if (wave == 0) {
+          const int x = wave_sample(p, ps.lm0 + a, Ms[a], Ss[a], u, lane);
+          if (lane == 0) tok_s = x;
+        }
+      } else if (tid == 0) {
+        tok_s = tok;
+      }
+      __syncthreads();
+      if (tid == 0) {
+        for (int r = 0; r < rows; ++r) p.result[ps.lm0 + r] = res_s[r];
+        p.lm_map[ps.slot] = int2{ps.lm0, rows};
+        commit_verify(p, ps, a, tok_s, res_s);
+      }
+    }
   }
   if (gridDim.x == 1 && p.next_desc) {
     __syncthreads();
@@ -817,6 +1053,17 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
         if (c16 == 0 && r < row_count) {
           p.amax_val[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = bv;
           p.amax_idx[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = bi;
+        }
+        if (p.samp_k > 0.f) {       // sampling: the entry's softmax weight relative to its max
+          float sw = 0.f;
+#pragma unroll
+          for (int s = 0; s < kRowsWaveStrips; ++s) {
+            if (strip0 + s >= p.n_strips) continue;  // uniform
+            sw += __builtin_amdgcn_exp2f((acc[mt][s][i] * rs_s[rl] - bv) * p.samp_k);
+          }
+#pragma unroll
+          for (int off = 8; off > 0; off >>= 1) sw += __shfl_xor(sw, off);
+          if (c16 == 0 && r < row_count) p.amax_sum[(size_t)r * p.amax_stride + tile * kRowsWaves + wave] = sw;
         }
       }
     });

@@ -77,6 +77,27 @@ __host__ __device__ inline int v_slot(int k) {
   return (k & 16) ? ((k & 12) << 1) + 4 + (k & 3) : ((k & 12) << 1) + (k & 3);
 }
 
+// SplitMix64 (Steele, Lea, Flood 2014): the state advances by kGamma before
+// each output; mix64 is the output function.
+constexpr uint64_t kGamma = 0x9E3779B97F4A7C15ull;
+__host__ __device__ inline uint64_t mix64(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Random numbers of speculative sampling: the uniform in [0, 1) (24 bits) of
+// (sequence slot, verify step `draw`, position j, purpose) -- output
+// 4j + purpose of the stream seeded with output `draw` of the stream seeded
+// with output `slot` of the stream seeded with `seed`.
+enum Purpose { PURPOSE_DRAFT = 0, PURPOSE_KEEP = 1, PURPOSE_LAST = 2, PURPOSE_FIRST = 3 };
+__host__ __device__ inline float sample_uniform(uint64_t seed, int slot, int draw, int j, int purpose) {
+  uint64_t z = mix64(seed + ((uint64_t)slot + 1) * kGamma);
+  z = mix64(z + ((uint64_t)draw + 1) * kGamma);
+  z = mix64(z + ((uint64_t)(4 * j + purpose) + 1) * kGamma);
+  return (float)(z >> 40) * (1.0f / 16777216.0f);
+}
+
 // fp16 bits of v, nearest even.
 __device__ inline uint16_t f16_bits(float v) { return __builtin_bit_cast(uint16_t, (_Float16)v); }
 
@@ -121,6 +142,8 @@ struct SeqState {
   int accept_hist[kMaxK + 1];
   int vsd;                   // vanilla speculative decoding: K one-row draft passes per step
   int j;                     // draft passes done in the current step (vanilla)
+  int draw;                  // verify steps since the prefill (speculative sampling's counter)
+  float qM[kMaxK], qS[kMaxK];   // sampling: max logit and softmax normaliser of the draft's rows
 };
 
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
@@ -148,9 +171,11 @@ struct GemmArgs {
   size_t kv_seq_stride;                       // elements between two slots' caches
   const float* bias; const float2* rope;
   int q_dim, kv_dim, hd;
-  // EPI_LOGITS: fp32 logits and the per-tile (max, argmax) of every lm row
+  // EPI_LOGITS: fp32 logits and the per-tile (max, argmax) of every lm row;
+  // with samp_k = log2(e) / T > 0 also the per-tile sum of 2^((z - max) samp_k)
   float* logits; int vocab;
   float* amax_val; int* amax_idx; int amax_stride;   // entries per lm row
+  float samp_k; float* amax_sum;
   // row-block GEMM (passes of more than kMaxRows rows): weight strips, row
   // blocks, input splits and the fp32 partial tiles of split inputs.  The
   // skinny GEMM splits its input into ksplit ranges of kb_split k-blocks
@@ -177,6 +202,14 @@ struct TailArgs {
   FwdDesc* next_desc;     // staged by the tail (single-sequence passes) or k_stage
   int* out_tokens;        // emitted tokens of the fused loop, out_cap per slot (verify tail)
   int out_cap;
+  // speculative sampling (samp_k = log2(e) / T > 0; 0: greedy): per-tile sums,
+  // this model's logits (tile_w columns per tile), the draft's logits (verify)
+  float samp_k;
+  uint64_t seed;
+  const float* amax_sum;
+  const float* logits;
+  const float* q_logits;
+  int tile_w;
 };
 
 struct AttnArgs {

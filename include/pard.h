@@ -199,7 +199,8 @@ pard_status pard_generate_ex(pard_ctx *ctx, int32_t n_seq, const int32_t *seqs, 
  * step graphs are dropped (rebuilt on the next pard_generate).  With sampling,
  * pard_verify with K > 0 needs this slot's pard_draft of the same K since its
  * last verify (STATE otherwise), and PARD_MODE_VANILLA is UNSUPPORTED.
- * Errors: ARG (T negative, not finite, or in (0, 1e-3)), DEVICE. */
+ * Errors: ARG (T negative, not finite, or in (0, 1e-3)), UNSUPPORTED (vocab above
+ * 262144), DEVICE. */
 pard_status pard_set_sampling(pard_ctx *ctx, float temperature, uint64_t seed);
 
 /* Copy the fp32 logits of slot `seq`'s rows in the last lm_head pass of

@@ -929,6 +929,8 @@ pard_status pard_set_sampling(pard_ctx* c, float temperature, uint64_t seed) {
   if (!c) return PARD_ERR_ARG;
   if (!(temperature >= 0.f) || !std::isfinite(temperature) || (temperature > 0.f && temperature < 1e-3f))
     return fail(c, PARD_ERR_ARG, "set_sampling: temperature %g outside {0} and [1e-3, inf)", (double)temperature);
+  if (temperature > 0.f && c->m[0].spec.vocab > kMaxSampleVocab)
+    return fail(c, PARD_ERR_UNSUPPORTED, "set_sampling: vocab above %d", kMaxSampleVocab);
   c->samp_k = temperature > 0.f ? (float)(1.4426950408889634 / temperature) : 0.f;
   c->samp_seed = seed;
   // captured steps hold the old settings in their kernel arguments

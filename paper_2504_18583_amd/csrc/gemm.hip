@@ -634,52 +634,75 @@ __device__ __forceinline__ float tile_weight(float m, float s, float M, float k)
   return m == -INFINITY ? 0.f : s * __builtin_amdgcn_exp2f((m - M) * k);
 }
 
-// (M, S) of lm row `lmr` (one wavefront).
-__device__ void row_stats(const TailArgs& p, int lmr, int lane, float* M, float* S) {
+constexpr int kScanBatch = 8;       // blocks of 64 tiles whose loads are in flight together
+constexpr int kResidBlock = 256;    // vocabulary entries per wavefront block of the residual draw (4 per lane)
+constexpr int kMaxResidBlocks = kMaxSampleVocab / kResidBlock;
+
+// Tile weights of blocks b0 .. b0 + kScanBatch*64 of lm row lmr, lane-strided (coalesced).
+__device__ __forceinline__ void tile_block_weights(const TailArgs& p, int lmr, int b0, float M, int lane,
+                                                   float (&w)[kScanBatch]) {
   const float* mv = p.amax_val + (size_t)lmr * p.n_tiles;
   const float* sv = p.amax_sum + (size_t)lmr * p.n_tiles;
+#pragma unroll
+  for (int u = 0; u < kScanBatch; ++u) {
+    const int t = b0 + 64 * u + lane;
+    w[u] = t < p.n_tiles ? tile_weight(mv[t], sv[t], M, p.samp_k) : 0.f;
+  }
+}
+
+// (M, S) of lm row `lmr` (one wavefront): S adds the blocks' sums in block order.
+__device__ void row_stats(const TailArgs& p, int lmr, int lane, float* M, float* S) {
+  const float* mv = p.amax_val + (size_t)lmr * p.n_tiles;
   float m = -INFINITY;
   for (int t = lane; t < p.n_tiles; t += 64) m = fmaxf(m, mv[t]);
   m = wave_max(m);
-  float w = 0.f;
-  for (int t = lane; t < p.n_tiles; t += 64) w += tile_weight(mv[t], sv[t], m, p.samp_k);
+  float acc = 0.f;
+  for (int b0 = 0; b0 < p.n_tiles; b0 += 64 * kScanBatch) {
+    float w[kScanBatch];
+    tile_block_weights(p, lmr, b0, m, lane, w);
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) acc += wave_sum(w[u]);
+  }
   *M = m;
-  *S = wave_sum(w);
+  *S = acc;
 }
 
-// Draw from lm row `lmr` with uniform u (one wavefront; every lane returns the token).
+// Draw from lm row `lmr` with uniform u (one wavefront; every lane returns the
+// token): the block of 64 tiles where the running sum (the same block sums in
+// the same order as S) passes u S, the tile inside it, then the column.
 __device__ int wave_sample(const TailArgs& p, int lmr, float M, float S, float u, int lane) {
-  const float* mv = p.amax_val + (size_t)lmr * p.n_tiles;
-  const float* sv = p.amax_sum + (size_t)lmr * p.n_tiles;
   const float k = p.samp_k, target = u * S;
-  // lane l owns a contiguous run of tiles; the lanes' sums are scanned in lane order
-  const int per = (p.n_tiles + 63) / 64;
-  const int t0 = min(lane * per, p.n_tiles), t1 = min(t0 + per, p.n_tiles);
-  float own = 0.f;
-  for (int t = t0; t < t1; ++t) own += tile_weight(mv[t], sv[t], M, k);
-  const float incl = wave_incl_scan(own, lane);
-  float excl = __shfl_up(incl, 1);
-  if (lane == 0) excl = 0.f;
-  const uint64_t hit = __ballot(incl > target && own > 0.f);
-  const uint64_t nz = __ballot(own > 0.f);
-  // the first lane whose prefix passes the target (after rounding: the last lane with weight)
-  const int sel = hit ? __ffsll((unsigned long long)hit) - 1 : (nz ? 63 - __clzll((long long)nz) : 0);
+  float carry = 0.f, rem = 0.f;
   int tsel = -1;
-  float rem = 0.f;
-  if (lane == sel) {
-    float acc = excl, last_w = 0.f;
-    int last = -1;
-    for (int t = t0; t < t1; ++t) {
-      const float w = tile_weight(mv[t], sv[t], M, k);
-      if (w > 0.f) { last = t; last_w = w; }
-      if (w > 0.f && acc + w > target) { tsel = t; rem = target - acc; break; }
-      acc += w;
+  for (int b0 = 0; b0 < p.n_tiles && tsel < 0; b0 += 64 * kScanBatch) {
+    float w[kScanBatch];
+    tile_block_weights(p, lmr, b0, M, lane, w);
+#pragma unroll
+    for (int v = 0; v < kScanBatch; ++v) {
+      if (tsel >= 0) break;                          // uniform
+      const float tot = wave_sum(w[v]);
+      if (carry + tot > target) {                    // uniform
+        const float incl = wave_incl_scan(w[v], lane);
+        const uint64_t hit = __ballot(w[v] > 0.f && carry + incl > target);
+        const uint64_t nz = __ballot(w[v] > 0.f);
+        const int l = hit ? __ffsll((unsigned long long)hit) - 1 : 63 - __clzll((long long)nz);
+        tsel = b0 + 64 * v + l;
+        rem = target - (carry + __shfl(incl - w[v], l));
+      }
+      carry += tot;
     }
-    if (tsel < 0) { tsel = last; rem = last_w; }
   }
-  tsel = __shfl(tsel, sel);
-  rem = __shfl(rem, sel);
-  if (tsel < 0) return 0;
+  if (tsel < 0) {          // u S rounded up to S: the last tile with weight, its last column
+    for (int b = (p.n_tiles - 1) / 64 * 64; b >= 0 && tsel < 0; b -= 64) {
+      const int t = b + lane;
+      const float w = t < p.n_tiles ? tile_weight(p.amax_val[(size_t)lmr * p.n_tiles + t],
+                                                  p.amax_sum[(size_t)lmr * p.n_tiles + t], M, k) : 0.f;
+      const uint64_t nz = __ballot(w > 0.f);
+      if (nz) tsel = b + 63 - __clzll((long long)nz);
+    }
+    if (tsel < 0) return 0;
+    rem = INFINITY;
+  }
   // columns of the chosen tile, one per lane
   const int col = tsel * p.tile_w + lane;
   float w = 0.f;
@@ -694,54 +717,92 @@ __device__ int wave_sample(const TailArgs& p, int lmr, float M, float S, float u
 
 // Residual draw at a rejected position: weights max(0, p(x) - q(x)) over the
 // vocabulary, p from the target row zp (M_p, S_p), q from the draft row zq
-// (M_q, S_q); thread t owns a contiguous run of ids.  Whole workgroup; returns
-// -1 when the residual has no mass (only through rounding).
+// (M_q, S_q).  Block g holds entries [256 g, 256 g + 256), 4 per lane; the
+// wavefronts take blocks round-robin and keep each block's sum in LDS; wave 0
+// then scans the block sums in order and the chosen block inside.  Whole
+// workgroup; returns -1 when the residual has no mass (only through rounding).
 __device__ int block_sample_residual(const TailArgs& p, const float* zp, float Mp, float Sp, const float* zq,
-                                     float Mq, float Sq, float u, float* scan_s, int* pick_s) {
+                                     float Mq, float Sq, float u, float* part_s, int* pick_s) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int V = p.vocab, per = (V + 1023) / 1024;
-  const int x0 = min(tid * per, V), x1 = min(x0 + per, V);
+  const int V = p.vocab, n_blocks = (V + kResidBlock - 1) / kResidBlock;
   const float k = p.samp_k, ip = 1.0f / Sp, iq = 1.0f / Sq;
-  auto resid = [&](int x) {
-    return fmaxf(__builtin_amdgcn_exp2f((zp[x] - Mp) * k) * ip - __builtin_amdgcn_exp2f((zq[x] - Mq) * k) * iq, 0.f);
+  auto resid4 = [&](int g, float (&r)[4]) {      // V is a multiple of 16: a lane's 4 entries are all in range or not
+    const int x0 = g * kResidBlock + 4 * lane;
+    if (x0 < V) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(zp + x0);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(zq + x0);
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        r[e] = fmaxf(__builtin_amdgcn_exp2f((a[e] - Mp) * k) * ip - __builtin_amdgcn_exp2f((b[e] - Mq) * k) * iq, 0.f);
+    } else {
+      r[0] = r[1] = r[2] = r[3] = 0.f;
+    }
   };
-  float own = 0.f;
-  for (int x = x0; x < x1; ++x) own += resid(x);
-  float incl = wave_incl_scan(own, lane);
-  if (lane == 63) scan_s[wave] = incl;
-  if (tid == 0) { pick_s[0] = INT_MAX; pick_s[1] = -1; }
-  __syncthreads();
-  if (wave == 0) {
-    float t = lane < 16 ? scan_s[lane] : 0.f;
-    t = wave_incl_scan(t, lane);
-    if (lane < 16) scan_s[16 + lane] = t;
+  for (int g0 = wave; g0 < n_blocks; g0 += 16 * kScanBatch) {
+    float r[kScanBatch][4];
+#pragma unroll
+    for (int v = 0; v < kScanBatch; ++v) {
+      const int g = g0 + 16 * v;
+      if (g < n_blocks) resid4(g, r[v]);
+      else r[v][0] = r[v][1] = r[v][2] = r[v][3] = 0.f;
+    }
+#pragma unroll
+    for (int v = 0; v < kScanBatch; ++v) {
+      const float t = wave_sum(((r[v][0] + r[v][1]) + r[v][2]) + r[v][3]);
+      const int g = g0 + 16 * v;
+      if (lane == 0 && g < n_blocks) part_s[g] = t;
+    }
   }
   __syncthreads();
-  const float base = wave > 0 ? scan_s[16 + wave - 1] : 0.f;
-  const float total = scan_s[31];
-  incl += base;
-  float excl = __shfl_up(incl, 1);
-  if (lane == 0) excl = base;
-  const float target = u * total;
-  // owner: the first thread whose prefix passes the target; after rounding,
-  // the last thread with mass
-  if (own > 0.f && incl > target) atomicMin(pick_s, tid);
-  if (own > 0.f) atomicMax(pick_s + 1, tid);
-  __syncthreads();
-  if (!(total > 0.f)) return -1;                  // uniform
-  const bool found = pick_s[0] != INT_MAX;
-  const int owner = found ? pick_s[0] : pick_s[1];
-  __syncthreads();
-  if (tid == owner) {
-    float acc = excl;
-    int last = -1, x_sel = -1;
-    for (int x = x0; x < x1; ++x) {
-      const float r = resid(x);
-      if (r > 0.f) last = x;
-      if (found && r > 0.f && acc + r > target) { x_sel = x; break; }
-      acc += r;
+  if (wave == 0) {
+    float total = 0.f;
+    for (int g0 = 0; g0 < n_blocks; g0 += 64) total += wave_sum(g0 + lane < n_blocks ? part_s[g0 + lane] : 0.f);
+    int x_sel = -1;
+    if (total > 0.f) {
+      const float target = u * total;
+      float carry = 0.f, rem = INFINITY;
+      int gsel = -1;
+      for (int g0 = 0; g0 < n_blocks && gsel < 0; g0 += 64) {
+        const float w = g0 + lane < n_blocks ? part_s[g0 + lane] : 0.f;
+        const float tot = wave_sum(w);
+        if (carry + tot > target) {
+          const float incl = wave_incl_scan(w, lane);
+          const uint64_t hit = __ballot(w > 0.f && carry + incl > target);
+          const uint64_t nz = __ballot(w > 0.f);
+          const int l = hit ? __ffsll((unsigned long long)hit) - 1 : 63 - __clzll((long long)nz);
+          gsel = g0 + l;
+          rem = target - (carry + __shfl(incl - w, l));
+        }
+        carry += tot;
+      }
+      if (gsel < 0) {      // u * total rounded up to total: the last block with mass
+        for (int g = n_blocks - 1; g >= 0; --g)
+          if (part_s[g] > 0.f) { gsel = g; break; }
+      }
+      if (gsel < 0) gsel = 0;   // not reached: total > 0 means some block has mass
+      // inside the block: lane sums in lane order, then the lane's 4 entries
+      float r[4];
+      resid4(gsel, r);
+      const float ls = ((r[0] + r[1]) + r[2]) + r[3];
+      const float incl = wave_incl_scan(ls, lane);
+      const uint64_t hit = __ballot(ls > 0.f && incl > rem);
+      const uint64_t nz = __ballot(ls > 0.f);
+      const int l = hit ? __ffsll((unsigned long long)hit) - 1 : (nz ? 63 - __clzll((long long)nz) : 0);
+      if (lane == l) {
+        float acc = incl - ls;
+        int last = -1;
+        for (int e = 0; e < 4; ++e) {
+          if (r[e] > 0.f) last = e;
+          if (x_sel < 0 && hit && r[e] > 0.f && acc + r[e] > rem) x_sel = gsel * kResidBlock + 4 * lane + e;
+          acc += r[e];
+        }
+        if (x_sel < 0) x_sel = gsel * kResidBlock + 4 * lane + (last < 0 ? 0 : last);
+        pick_s[0] = x_sel;
+      }
+      if (!nz && lane == 0) pick_s[0] = -1;
+    } else if (lane == 0) {
+      pick_s[0] = -1;
     }
-    pick_s[0] = x_sel >= 0 ? x_sel : last;
   }
   __syncthreads();
   return pick_s[0];
@@ -795,7 +856,7 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
     // the step's last token from the residual (first rejection) or from the
     // bonus row (all kept)
     __shared__ float Ms[kMaxK + 1], Ss[kMaxK + 1];
-    __shared__ float scan_s[32];
+    __shared__ float part_s[kMaxResidBlocks];
     __shared__ int pick_s[2], a_s, tok_s;
     SeqState* st = p.states + ps.slot;
     const int draw = st->draw;
@@ -823,18 +884,20 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
       }
     } else {   // TAIL_VERIFY
       const int k = st->k;
-      if (tid == 0) {
+      if (wave == 0) {
+        // keep test of position j in lane j (k <= 32); a = the first position not kept
         const int2 dm = p.lm_map_draft[ps.slot];   // this slot's rows of the draft's last pass
-        int a = 0;
-        for (; a < k; ++a) {
-          const int x = st->cand[a];
-          const float pz = p.logits[(size_t)(ps.lm0 + a) * p.vocab + x];
-          const float qz = p.q_logits[(size_t)(dm.x + a) * p.vocab + x];
-          const float pp = __builtin_amdgcn_exp2f((pz - Ms[a]) * p.samp_k) / Ss[a];
-          const float qq = __builtin_amdgcn_exp2f((qz - st->qM[a]) * p.samp_k) / st->qS[a];
-          if (!(sample_uniform(p.seed, ps.slot, draw, a, PURPOSE_KEEP) * qq < pp)) break;
+        bool keep = true;
+        if (lane < k) {
+          const int x = st->cand[lane];
+          const float pz = p.logits[(size_t)(ps.lm0 + lane) * p.vocab + x];
+          const float qz = p.q_logits[(size_t)(dm.x + lane) * p.vocab + x];
+          const float pp = __builtin_amdgcn_exp2f((pz - Ms[lane]) * p.samp_k) / Ss[lane];
+          const float qq = __builtin_amdgcn_exp2f((qz - st->qM[lane]) * p.samp_k) / st->qS[lane];
+          keep = sample_uniform(p.seed, ps.slot, draw, lane, PURPOSE_KEEP) * qq < pp;
         }
-        a_s = a;
+        const uint64_t rejected = __ballot(!keep);
+        if (lane == 0) a_s = rejected ? __ffsll((unsigned long long)rejected) - 1 : k;
       }
       __syncthreads();
       const int a = a_s;
@@ -843,7 +906,7 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
       if (a < k) {
         const int2 dm = p.lm_map_draft[ps.slot];
         tok = block_sample_residual(p, p.logits + (size_t)(ps.lm0 + a) * p.vocab, Ms[a], Ss[a],
-                                    p.q_logits + (size_t)(dm.x + a) * p.vocab, st->qM[a], st->qS[a], u, scan_s,
+                                    p.q_logits + (size_t)(dm.x + a) * p.vocab, st->qM[a], st->qS[a], u, part_s,
                                     pick_s);
       }
       if (tok < 0) {                                // bonus row (or a residual without mass)

@@ -36,6 +36,7 @@
 namespace pard {
 
 constexpr int kMaxK = 32;
+constexpr int kMaxSampleVocab = 1 << 18;   // largest vocabulary speculative sampling supports
 constexpr int kMaxRows = 64;          // rows of a pass served by the skinny GEMM (prefill chunk)
 constexpr int kMaxPassRows = 512;     // rows of one forward pass over all of its sequences
 constexpr int kMaxPassSeqs = 64;      // sequences in one pass

@@ -83,6 +83,15 @@ typedef struct {
   int32_t dtype;             /* PARD_BF16 */
   uint32_t weight_stream;    /* generator stream id (target 0, draft 1 by convention) */
   uint64_t seed;
+  /* LLaMA-3.1-style rotary frequency scaling (rope_factor 0: plain RoPE).  A
+   * frequency w = rope_theta^(-2i/head_dim) whose wavelength 2 pi / w is below
+   * rope_original_max_pos / rope_high_freq_factor is kept, one above
+   * rope_original_max_pos / rope_low_freq_factor is divided by rope_factor,
+   * and in between w becomes (1 - s) w / rope_factor + s w with
+   * s = (rope_original_max_pos * w / (2 pi) - low) / (high - low).  Requires
+   * rope_factor >= 1, 0 < low < high, rope_original_max_pos >= 1 (ARG otherwise). */
+  float rope_factor, rope_low_freq_factor, rope_high_freq_factor;
+  int32_t rope_original_max_pos;
 } pard_model_spec;
 
 typedef struct pard_ctx pard_ctx;

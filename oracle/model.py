@@ -58,11 +58,28 @@ def silu(x: np.ndarray) -> np.ndarray:
     return x / (1.0 + np.exp(-x))
 
 
-def rope(x: np.ndarray, pos: np.ndarray, theta: float) -> np.ndarray:
+def rope_inv_freq(hd: int, theta: float, scaling=None) -> np.ndarray:
+    """Rotary frequencies theta^(-2i/hd), i < hd/2.  With LLaMA-3.1-style
+    scaling (factor, low_freq_factor, high_freq_factor, original length L):
+    a frequency whose wavelength 2 pi / w is shorter than L / high_freq_factor
+    is kept, one longer than L / low_freq_factor is divided by factor, and in
+    between w is blended as (1 - s) w / factor + s w with
+    s = (L / wavelength - low_freq_factor) / (high_freq_factor - low_freq_factor)."""
+    inv_freq = float(theta) ** (-(2.0 * np.arange(hd // 2, dtype=F64)) / hd)
+    if scaling is None:
+        return inv_freq
+    factor, low, high, orig = (float(v) for v in scaling)
+    wavelen = 2.0 * np.pi / inv_freq
+    s = (orig / wavelen - low) / (high - low)
+    blended = (1.0 - s) * inv_freq / factor + s * inv_freq
+    return np.where(wavelen < orig / high, inv_freq, np.where(wavelen > orig / low, inv_freq / factor, blended))
+
+
+def rope(x: np.ndarray, pos: np.ndarray, theta: float, scaling=None) -> np.ndarray:
     """Rotate-half rotary embedding of x [n, H, hd] at absolute positions pos [n]."""
     hd = x.shape[-1]
     half = hd // 2
-    inv_freq = float(theta) ** (-(2.0 * np.arange(half, dtype=F64)) / hd)
+    inv_freq = rope_inv_freq(hd, theta, scaling)
     ang = np.asarray(pos, F64)[:, None] * inv_freq[None, :]          # [n, half]
     c = np.cos(ang)[:, None, :]
     s = np.sin(ang)[:, None, :]
@@ -124,8 +141,8 @@ def _layer(spec, lw: dict, x: np.ndarray, pos: np.ndarray,
     q = linear(y, lw["wq"], lw.get("bq")).reshape(n, hq, hd)
     k = linear(y, lw["wk"], lw.get("bk")).reshape(n, hkv, hd)
     v = linear(y, lw["wv"], lw.get("bv")).reshape(n, hkv, hd)
-    q = rope(q, pos, spec.rope_theta)
-    k = rope(k, pos, spec.rope_theta)
+    q = rope(q, pos, spec.rope_theta, spec.rope_scaling)
+    k = rope(k, pos, spec.rope_theta, spec.rope_scaling)
     k_all = np.concatenate([k_prev, k], axis=0)
     v_all = np.concatenate([v_prev, v], axis=0)
     k_pos = np.arange(k_all.shape[0])

@@ -35,7 +35,9 @@ class pard_model_spec(C.Structure):
                 ("n_kv_heads", C.c_int32), ("head_dim", C.c_int32), ("ffn_dim", C.c_int32),
                 ("vocab", C.c_int32), ("rms_eps", C.c_float), ("rope_theta", C.c_float),
                 ("init_std", C.c_float), ("qkv_bias", C.c_int32), ("tied_embeddings", C.c_int32),
-                ("dtype", C.c_int32), ("weight_stream", C.c_uint32), ("seed", C.c_uint64)]
+                ("dtype", C.c_int32), ("weight_stream", C.c_uint32), ("seed", C.c_uint64),
+                ("rope_factor", C.c_float), ("rope_low_freq_factor", C.c_float),
+                ("rope_high_freq_factor", C.c_float), ("rope_original_max_pos", C.c_int32)]
 
 
 class pard_stats(C.Structure):
@@ -92,7 +94,16 @@ def spec_from(s) -> pard_model_spec:
         n_layers=s.n_layers, d_model=s.d_model, n_heads=s.n_heads, n_kv_heads=s.n_kv_heads,
         head_dim=s.head_dim, ffn_dim=s.ffn_dim, vocab=s.vocab, rms_eps=s.rms_eps,
         rope_theta=s.rope_theta, init_std=s.init_std, qkv_bias=int(s.qkv_bias),
-        tied_embeddings=int(s.tied), dtype=PARD_BF16, weight_stream=s.stream, seed=s.seed)
+        tied_embeddings=int(s.tied), dtype=PARD_BF16, weight_stream=s.stream, seed=s.seed,
+        **_rope_fields(s))
+
+
+def _rope_fields(s) -> dict:
+    if s.rope_scaling is None:
+        return {}
+    factor, low, high, orig = s.rope_scaling
+    return dict(rope_factor=float(factor), rope_low_freq_factor=float(low), rope_high_freq_factor=float(high),
+                rope_original_max_pos=int(orig))
 
 
 def _i32(a) -> Tuple[np.ndarray, object]:

@@ -22,7 +22,11 @@ hipError_t launch_gen_packed(const GenArgs& a, hipStream_t st);
 hipError_t launch_gen_bias(const GenArgs& a, float* dst, int n_total, hipStream_t st);
 hipError_t launch_fill_f32(float* p, size_t n, float v, hipStream_t st);
 hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st);
-hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStream_t st);
+// LLaMA-3.1-style rotary frequency scaling (factor 0: none).
+struct RopeScaling {
+  double factor = 0.0, low = 1.0, high = 1.0, orig = 1.0;
+};
+hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const RopeScaling& sc, hipStream_t st);
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, int act_rows, float* ss, int max_rows, hipStream_t st);
 hipError_t launch_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out, hipStream_t st);

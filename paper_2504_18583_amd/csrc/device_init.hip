@@ -128,12 +128,24 @@ __global__ void k_fill_u32(uint32_t* p, size_t n, uint32_t v) {
 }
 
 // cos/sin of position * theta^(-2i/hd), evaluated in double, stored fp32.
-__global__ void k_rope_table(float2* tab, int cap, int hd, double theta) {
+// cos/sin of pos * w_i, w_i = theta^(-2i/hd), optionally with LLaMA-3.1-style
+// frequency scaling: wavelengths 2 pi / w below orig / high are kept, above
+// orig / low divided by factor, blended in between.
+__global__ void k_rope_table(float2* tab, int cap, int hd, double theta, RopeScaling sc) {
   const int half = hd / 2;
   const size_t total = (size_t)cap * half;
   for (size_t t = (size_t)blockIdx.x * blockDim.x + threadIdx.x; t < total; t += (size_t)gridDim.x * blockDim.x) {
     const int pos = (int)(t / half), i = (int)(t % half);
-    const double inv_freq = pow(theta, -(2.0 * i) / hd);
+    double inv_freq = pow(theta, -(2.0 * i) / hd);
+    if (sc.factor > 0.0) {
+      const double wavelen = 6.283185307179586 / inv_freq;
+      if (wavelen > sc.orig / sc.low) {
+        inv_freq = inv_freq / sc.factor;
+      } else if (!(wavelen < sc.orig / sc.high)) {
+        const double s = (sc.orig / wavelen - sc.low) / (sc.high - sc.low);
+        inv_freq = (1.0 - s) * inv_freq / sc.factor + s * inv_freq;
+      }
+    }
     const double ang = (double)pos * inv_freq;
     tab[t] = make_float2((float)cos(ang), (float)sin(ang));
   }
@@ -209,8 +221,8 @@ hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t v, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, hipStream_t st) {
-  k_rope_table<<<blocks_for((size_t)cap * hd / 2, 256), 256, 0, st>>>(tab, cap, hd, theta);
+hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const RopeScaling& sc, hipStream_t st) {
+  k_rope_table<<<blocks_for((size_t)cap * hd / 2, 256), 256, 0, st>>>(tab, cap, hd, theta, sc);
   return hipGetLastError();
 }
 

@@ -250,6 +250,11 @@ pard_status check_spec(const pard_model_spec* s, const char* who, std::string* w
   if (s->n_heads % s->n_kv_heads) return bad(PARD_ERR_ARG, "n_heads not a multiple of n_kv_heads");
   if (!(s->rms_eps > 0.f) || !(s->rope_theta > 1.f) || !(s->init_std > 0.f))
     return bad(PARD_ERR_ARG, "rms_eps, rope_theta or init_std out of range");
+  if (s->rope_factor != 0.f &&
+      (!(s->rope_factor >= 1.f) || !std::isfinite(s->rope_factor) || !(s->rope_low_freq_factor > 0.f) ||
+       !(s->rope_high_freq_factor > s->rope_low_freq_factor) || !std::isfinite(s->rope_high_freq_factor) ||
+       s->rope_original_max_pos < 1))
+    return bad(PARD_ERR_ARG, "rope scaling: need factor >= 1, 0 < low < high, original length >= 1");
   if (s->seed >= (1ull << 44) || s->weight_stream >= 16) return bad(PARD_ERR_ARG, "seed or weight_stream out of range");
   if (s->dtype != PARD_BF16) return bad(PARD_ERR_UNSUPPORTED, "only bf16 weights are supported");
   if (s->head_dim != 64 && s->head_dim != 128) return bad(PARD_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
@@ -402,7 +407,14 @@ pard_status generate(pard_ctx* c, int w) {
   HIP_TRY(c, gen(M.embed, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(0), 0, 0));
   if (!s.tied_embeddings) HIP_TRY(c, gen(M.lm_head, s.vocab, M.d, s.vocab, M.d, MAP_IDENTITY, key(1), 0, 0));
   HIP_TRY(c, launch_fill_f32(M.g_final, M.d, 1.0f, c->stream));
-  HIP_TRY(c, launch_rope_table(M.rope, c->kv_cap, s.head_dim, (double)s.rope_theta, c->stream));
+  RopeScaling sc;
+  if (s.rope_factor != 0.f) {
+    sc.factor = s.rope_factor;
+    sc.low = s.rope_low_freq_factor;
+    sc.high = s.rope_high_freq_factor;
+    sc.orig = s.rope_original_max_pos;
+  }
+  HIP_TRY(c, launch_rope_table(M.rope, c->kv_cap, s.head_dim, (double)s.rope_theta, sc, c->stream));
   // zero KV caches: padded key tiles read stale slots, which must hold finite values
   HIP_TRY(c, launch_fill_u32(reinterpret_cast<uint32_t*>(M.kcache), c->kv_elems[w] / 2, 0u, c->stream));
   HIP_TRY(c, launch_fill_u32(reinterpret_cast<uint32_t*>(M.vcache), c->kv_elems[w] / 2, 0u, c->stream));

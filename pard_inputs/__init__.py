@@ -174,6 +174,9 @@ class ModelSpec:
     dtype: str = "bf16"          # rounding applied to generated weights
     seed: int = 0
     stream: int = 0              # weight stream id (target 0, draft 1)
+    # LLaMA-3.1-style rotary frequency scaling: (factor, low_freq_factor,
+    # high_freq_factor, original max positions); None = plain RoPE
+    rope_scaling: Optional[Tuple[float, float, float, int]] = None
 
     @property
     def q_dim(self) -> int:

@@ -54,12 +54,27 @@ def test_arena_bytes_covers_weights_and_cache(b):
 
 @pytest.mark.parametrize("field,value", [("head_dim", 96), ("dtype", 0), ("vocab", 1000),
                                          ("d_model", 100), ("n_kv_heads", 3), ("n_layers", 0),
-                                         ("rms_eps", 0.0)])
+                                         ("rms_eps", 0.0), ("rope_factor", 0.5)])
 def test_arena_bytes_rejects_bad_spec(b, field, value):
     _, t, d = _pair("tiny")
     ts = b.spec_from(t)
     setattr(ts, field, value)
     assert b.pard_arena_bytes(ts, b.spec_from(d), 1, 256, 4) == 0
+
+
+def test_rope_scaling_fields_cross_the_abi(b):
+    """The scaling fields sit after the seed in the C struct: a valid set is
+    accepted, each inconsistent one rejected."""
+    from dataclasses import replace
+    _, t, d = _pair("tiny")
+    good = b.spec_from(replace(t, rope_scaling=(8.0, 1.0, 4.0, 8192)))
+    assert (good.rope_factor, good.rope_original_max_pos) == (8.0, 8192)
+    assert b.pard_arena_bytes(good, b.spec_from(d), 1, 256, 4) > 0
+    for field, value in (("rope_low_freq_factor", 0.0), ("rope_high_freq_factor", 1.0),
+                         ("rope_original_max_pos", 0), ("rope_factor", float("inf"))):
+        bad = b.spec_from(replace(t, rope_scaling=(8.0, 1.0, 4.0, 8192)))
+        setattr(bad, field, value)
+        assert b.pard_arena_bytes(bad, b.spec_from(d), 1, 256, 4) == 0, field
 
 
 def test_arena_bytes_rejects_bad_capacity(b):

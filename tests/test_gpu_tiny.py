@@ -82,6 +82,47 @@ def test_lockstep_draft_verify(eng, models, k):
     say(f"    max |logit err| {worst:.3g}")
 
 
+@pytest.mark.parametrize("k", [16, 24, 32])
+def test_large_k_lockstep_and_fused(B, models, k):
+    """K past the trained range (the shared mask id extends the draft to any
+    K): draft passes of a+K rows up to 64, verify passes of K+1 rows over
+    two or three row tiles, the tail's K+1 lm rows; fused loop vs greedy."""
+    target, _ = models
+    e = B.Engine(T_SPEC, D_SPEC, WL.mask_id, max_ctx=1024, max_k=32)
+    try:
+        say(f"[gpu] tiny: large K={k}")
+        worst = lockstep(e, target, models[1], PROMPT, k, steps=5, mask_id=WL.mask_id, tag=f"K={k}")
+        say(f"    max |logit err| {worst:.3g}")
+        e.prefill(PROMPT)
+        toks, stats = e.generate(k, 40)
+        ref = oracle.greedy_ar(target, PROMPT, 40)
+        cache = oracle.KVCache(target)
+        lg = oracle.forward_cached(target, cache, PROMPT, logits_rows=[len(PROMPT) - 1])
+        for i in range(40):              # equal up to the first near-tie of the oracle
+            if margins(lg)[-1] <= MARGIN:
+                break
+            assert toks[i] == ref[i], f"K={k} token {i}"
+            lg = oracle.forward_cached(target, cache, [ref[i]])
+    finally:
+        e.close()
+
+
+def test_rope_scaled_pair_lockstep(B):
+    """LLaMA-3.1-style rotary scaling (original length 32, so the tiny head's
+    frequencies span the kept, blended and divided regimes) on both models."""
+    from dataclasses import replace
+    scaling = (8.0, 1.0, 4.0, 32)
+    t_spec, d_spec = replace(T_SPEC, rope_scaling=scaling), replace(D_SPEC, rope_scaling=scaling)
+    target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)
+    e = B.Engine(t_spec, d_spec, WL.mask_id, max_ctx=512, max_k=8)
+    try:
+        say("[gpu] tiny: rope-scaled pair, lock-step K=4")
+        worst = lockstep(e, target, draft, PROMPT, WL.k, steps=6, mask_id=WL.mask_id, tag="rope-scaled")
+        say(f"    max |logit err| {worst:.3g}")
+    finally:
+        e.close()
+
+
 def test_generate_matches_greedy(eng, models, B):
     say("[gpu] tiny: fused generate vs greedy")
     target, _ = models

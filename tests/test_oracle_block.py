@@ -10,9 +10,11 @@ import pytest
 import torch
 import torch.nn.functional as F
 
+from dataclasses import replace
+
 import oracle
 import pard_inputs as pi
-from oracle.model import attention, rms_norm, rope
+from oracle.model import attention, rms_norm, rope, rope_inv_freq
 
 transformers = pytest.importorskip("transformers")
 
@@ -23,6 +25,10 @@ def _hf_model(spec, weights, family):
                   num_attention_heads=spec.n_heads, num_key_value_heads=spec.n_kv_heads,
                   rms_norm_eps=spec.rms_eps, rope_theta=spec.rope_theta,
                   tie_word_embeddings=spec.tied, max_position_embeddings=4096)
+    if spec.rope_scaling is not None:
+        factor, low, high, orig = spec.rope_scaling
+        common["rope_scaling"] = {"rope_type": "llama3", "factor": factor, "low_freq_factor": low,
+                                  "high_freq_factor": high, "original_max_position_embeddings": orig}
     if family == "llama":
         cfg = transformers.LlamaConfig(head_dim=spec.head_dim, attention_bias=False,
                                        mlp_bias=False, **common)
@@ -68,10 +74,17 @@ def _tiny_qwen_like():
                         tied=True, dtype="bf16", seed=9, stream=0)
 
 
-@pytest.mark.parametrize("which", ["target", "draft", "qwen"])
+# LLaMA-3.1-style rotary scaling with an original length of 32 positions: at
+# head_dim 64 and theta 1e4 the wavelengths span the kept, blended and divided
+# regimes (below 8, 8..32, above 32)
+SCALING = (8.0, 1.0, 4.0, 32)
+
+
+@pytest.mark.parametrize("which", ["target", "draft", "qwen", "target_scaled"])
 def test_forward_full_matches_hf(which):
     wl = pi.WORKLOADS["tiny"]
-    spec = {"target": wl.target, "draft": wl.draft, "qwen": _tiny_qwen_like()}[which]
+    spec = {"target": wl.target, "draft": wl.draft, "qwen": _tiny_qwen_like(),
+            "target_scaled": replace(wl.target, rope_scaling=SCALING)}[which]
     family = "qwen" if which == "qwen" else "llama"
     model = oracle.build_model(spec)
     ids = pi.gen_prompt(5, spec.vocab, 48)
@@ -84,6 +97,24 @@ def test_forward_full_matches_hf(which):
     assert np.abs(ours - ref).max() <= 1e-5 * max(1.0, scale)
     assert np.array_equal(np.argmax(ours, -1), np.argmax(ref, -1)) or \
         np.abs(ours - ref).max() < 1e-6
+
+
+def test_rope_scaling_matches_hf_frequencies_and_regimes():
+    from transformers.modeling_rope_utils import ROPE_INIT_FUNCTIONS
+    cfg = transformers.LlamaConfig(hidden_size=256, num_attention_heads=4, head_dim=64, rope_theta=1e4,
+                                   rope_scaling={"rope_type": "llama3", "factor": 8.0, "low_freq_factor": 1.0,
+                                                 "high_freq_factor": 4.0, "original_max_position_embeddings": 32})
+    hf, _ = ROPE_INIT_FUNCTIONS["llama3"](cfg, "cpu")
+    ours = rope_inv_freq(64, 1e4, SCALING)
+    assert np.allclose(ours, hf.double().numpy(), rtol=1e-6, atol=0)
+    plain = rope_inv_freq(64, 1e4)
+    wavelen = 2 * np.pi / plain
+    kept, divided = wavelen < 8, wavelen > 32
+    assert kept.any() and divided.any() and (~kept & ~divided).any()
+    assert np.array_equal(ours[kept], plain[kept])
+    assert np.allclose(ours[divided], plain[divided] / 8, rtol=1e-15)
+    mid = ~kept & ~divided                                           # blended: between w / 8 and w
+    assert np.all((ours[mid] <= plain[mid]) & (ours[mid] >= plain[mid] / 8))
 
 
 def test_attention_matches_torch_sdpa_gqa():

@@ -13,6 +13,8 @@ Modules:
 * ``oracle.sampling`` -- speculative sampling at temperature T > 0 (the
   rejection rule Sec. 1 and Sec. 2.2 cite) on the PARD draft, with a
   counter-based SplitMix64 generator.
+* ``oracle.cod`` -- conditional drop-token training-data processing (Sec. 3.2,
+  Alg. 1, App. B).
 
 Pins (tests marked "not gpu"): the decoder against the independent
 Hugging Face Llama/Qwen2 implementations and torch's attention/normalisation
@@ -24,13 +26,15 @@ Sampling: SplitMix64's published outputs; inverse-CDF drawing against the
 weights; the keep / residual / bonus rule against the target distribution at
 every position (chi-square); the whole sampled loop against enumerated
 autoregressive marginals on a small vocabulary; vanishing temperature ==
-greedy.
+greedy.  COD: App. B's worked example, the kept-token closed form (App. A's
+3.37M), the integrity condition, and packed samples reproducing the eq. 7
+draft pass through the decoder.
 """
 from .model import (KVCache, Model, attention, forward_cached, forward_full, linear,
                     rms_norm, rope, silu)
 from .pard import (PardTrace, accept_prefix, argmax_rows, draft_step, greedy_ar,
                    pard_generate, prefill, vanilla_draft_step, vanilla_generate, verify_step)
-from . import sampling
+from . import cod, sampling
 
 
 def build_model(spec, layers=None) -> Model:

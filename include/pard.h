@@ -239,6 +239,48 @@ pard_status pard_read_weight(const pard_ctx *ctx, int32_t which, int32_t tensor,
 pard_status pard_timer_enable(pard_ctx *ctx, int32_t kernel_class, int32_t max_launches);
 pard_status pard_timer_read(pard_ctx *ctx, int32_t *launches, double *total_ms);
 
+/* COD training-data processing (Sec. 3.2 eqs. 9-11, Alg. 1, App. B): the
+ * conditional drop-token data of PARD's mask-token training, on the device.
+ * A sample of L tokens t_0..t_{L-1} has n = L-1 columns per subtask k = 1..K;
+ * column j of subtask k is labelled t_{j+1} at position j, with input t_j
+ * (k = 1) or mask_id (k >= 2).  Subtask 1 keeps every column.  Subtask k >= 2
+ * keeps min(#valid, floor(n * gamma_k + 1/2)) columns, gamma_k =
+ * max(r^(k-1), r_min) (float64), chosen among the valid ones -- j >= k-1 and
+ * column j-1 of subtask k-1 kept, so every kept token's context is kept --
+ * by the smallest (key, j), key = top 24 bits of output j of the SplitMix64
+ * stream seeded with output k of the stream seeded with output s (the sample
+ * index) of the stream seeded with `seed`.  Kept columns are packed in
+ * subtask order, each in column order.  Packed token (k, j) attends to the
+ * real tokens t_0..t_{j-k+1} and to the packed tokens (k', j-k+k'),
+ * 2 <= k' <= k (its diagonal up to itself): the context of eq. 8.
+ *
+ * pard_cod_capacity: packed rows a sample of n_tokens tokens may need
+ * (n + sum_{k>=2} floor(n * gamma_k + 1/2)); -1 if n_tokens is outside
+ * [2, 8193] or K (1..64), r (0, 1] or r_min [0, 1] is invalid.  Host only.
+ *
+ * pard_cod_build: tokens (device, int32) holds the samples back to back;
+ * tok_offsets (host, n_samples+1 entries) their bounds; out_offsets (host,
+ * n_samples+1) the bounds of each sample's packed region in the five device
+ * output arrays (ids, labels, positions, subtask k, column j; int32), each
+ * region at least pard_cod_capacity of its sample; out_len (device,
+ * n_samples) receives each sample's packed length.  Runs on hip_stream and
+ * returns after the results are complete.  The caller owns every buffer.
+ * Errors: ARG (null pointer, bad parameters, a sample outside [2, 8193]
+ * tokens), CAPACITY (an output region below its capacity), NOMEM, DEVICE. */
+int64_t pard_cod_capacity(int32_t n_tokens, int32_t K, double r, double r_min);
+/* pard_cod_layout: out_offsets (host, n_samples+1) = the prefix sums of the
+ * samples' capacities for tok_offsets (host, n_samples+1); returns the total,
+ * or -1 under the same conditions as pard_cod_capacity.  Host only. */
+int64_t pard_cod_layout(const int64_t *tok_offsets, int32_t n_samples, int32_t K, double r,
+                        double r_min, int64_t *out_offsets);
+/* kernel_ms (host, may be NULL) receives the kernel's device time, from HIP
+ * events recorded around its launch on hip_stream. */
+pard_status pard_cod_build(const int32_t *tokens, const int64_t *tok_offsets, int32_t n_samples,
+                           int32_t K, double r, double r_min, int32_t mask_id, uint64_t seed,
+                           const int64_t *out_offsets, int32_t *out_ids, int32_t *out_labels,
+                           int32_t *out_pos, int32_t *out_section, int32_t *out_column,
+                           int32_t *out_len, float *kernel_ms, void *hip_stream);
+
 /* Message of the last error on this context (never NULL; "" if none). */
 const char *pard_last_error(const pard_ctx *ctx);
 

@@ -63,6 +63,13 @@ _sig = {
     "pard_generate_ex": (C.c_int, [_CTX, C.c_int32, _I32P, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
                                    _I32P, C.POINTER(pard_stats)]),
     "pard_set_sampling": (C.c_int, [_CTX, C.c_float, C.c_uint64]),
+    "pard_cod_capacity": (C.c_int64, [C.c_int32, C.c_int32, C.c_double, C.c_double]),
+    "pard_cod_layout": (C.c_int64, [C.POINTER(C.c_int64), C.c_int32, C.c_int32, C.c_double, C.c_double,
+                                    C.POINTER(C.c_int64)]),
+    "pard_cod_build": (C.c_int, [C.c_void_p, C.POINTER(C.c_int64), C.c_int32, C.c_int32, C.c_double,
+                                 C.c_double, C.c_int32, C.c_uint64, C.POINTER(C.c_int64), C.c_void_p,
+                                 C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
+                                 C.POINTER(C.c_float), C.c_void_p]),
     "pard_read_logits": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                    C.c_int32]),
     "pard_read_weight": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -127,6 +134,43 @@ def pard_model_load(target, draft, mask_id, max_batch, max_ctx, max_k, dev_arena
     if st != PARD_OK:
         raise PardError(st, "pard_model_load failed")
     return ctx.value
+
+
+def cod_capacity(n_tokens: int, k: int, r: float, r_min: float) -> int:
+    return int(lib.pard_cod_capacity(int(n_tokens), int(k), float(r), float(r_min)))
+
+
+def cod_build(tokens, tok_offsets: Sequence[int], k: int, r: float, r_min: float, mask_id: int, seed: int,
+              stream=None, timing: bool = False):
+    """COD training-data processing on the device (pard_cod_build).
+
+    tokens: 1-D int32 device tensor of the samples back to back; tok_offsets:
+    host offsets (n_samples + 1).  Returns (out_offsets, dict of the five int32
+    device tensors ids/labels/pos/section/column, out_len device tensor), and
+    the kernel's device milliseconds when timing is set."""
+    import torch
+    offs = np.ascontiguousarray(np.asarray(tok_offsets, np.int64))
+    n = len(offs) - 1
+    out_offs = np.zeros(max(n, 0) + 1, np.int64)
+    total = lib.pard_cod_layout(offs.ctypes.data_as(C.POINTER(C.c_int64)), n, k, float(r), float(r_min),
+                                out_offs.ctypes.data_as(C.POINTER(C.c_int64))) if n >= 1 else -1
+    if total < 0:
+        raise PardError(PARD_ERR_ARG, "cod_build: empty batch, bad parameters or a sample outside the lengths")
+    dev = tokens.device
+    out = {name: torch.empty(total, dtype=torch.int32, device=dev)
+           for name in ("ids", "labels", "pos", "section", "column")}
+    out_len = torch.empty(n, dtype=torch.int32, device=dev)
+    ms = C.c_float(0.0)
+    st = stream if stream is not None else torch.cuda.current_stream(dev).cuda_stream
+    rc = lib.pard_cod_build(C.c_void_p(tokens.data_ptr()), offs.ctypes.data_as(C.POINTER(C.c_int64)), n, k,
+                            float(r), float(r_min), mask_id, int(seed) & ((1 << 64) - 1),
+                            out_offs.ctypes.data_as(C.POINTER(C.c_int64)),
+                            *[C.c_void_p(out[name].data_ptr()) for name in ("ids", "labels", "pos", "section",
+                                                                            "column")],
+                            C.c_void_p(out_len.data_ptr()), C.byref(ms) if timing else None, C.c_void_p(st))
+    if rc != PARD_OK:
+        raise PardError(rc, "pard_cod_build failed")
+    return (out_offs, out, out_len, ms.value) if timing else (out_offs, out, out_len)
 
 
 class Engine:

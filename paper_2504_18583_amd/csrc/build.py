@@ -21,8 +21,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpard.so")
 COUNTERS_EXE = os.path.join(PKG, "gemm_counters")
 
-SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "gemm_counters.hip"]
-LIB_SOURCES = SOURCES[:4]
+SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "cod.hip", "gemm_counters.hip"]
+LIB_SOURCES = SOURCES[:5]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -1261,6 +1261,98 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
   return PARD_OK;
 }
 
+// ----------------------------------------------------------------------------
+// COD training-data processing
+// ----------------------------------------------------------------------------
+
+namespace {
+
+bool cod_params_ok(int32_t K, double r, double r_min) {
+  return K >= 1 && K <= 64 && r > 0.0 && r <= 1.0 && r_min >= 0.0 && r_min <= 1.0 && std::isfinite(r) &&
+         std::isfinite(r_min);
+}
+
+// Packed rows a sample of n_tokens tokens can produce: n columns of subtask 1
+// plus each later subtask's keep target (the same float64 arithmetic as the kernel).
+int64_t cod_capacity(int64_t n_tokens, int32_t K, double r, double r_min) {
+  const int64_t n = n_tokens - 1;
+  int64_t total = n;
+  double gamma = 1.0;
+  for (int k = 2; k <= K; ++k) {
+    gamma *= r;
+    total += (int64_t)std::floor((double)n * std::fmax(gamma, r_min) + 0.5);
+  }
+  return total;
+}
+
+}  // namespace
+
+int64_t pard_cod_capacity(int32_t n_tokens, int32_t K, double r, double r_min) {
+  if (n_tokens < 2 || n_tokens - 1 > cod_max_columns() || !cod_params_ok(K, r, r_min)) return -1;
+  return cod_capacity(n_tokens, K, r, r_min);
+}
+
+int64_t pard_cod_layout(const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r, double r_min,
+                        int64_t* out_offsets) {
+  if (!tok_offsets || !out_offsets || n_samples < 1 || !cod_params_ok(K, r, r_min) || tok_offsets[0] < 0) return -1;
+  out_offsets[0] = 0;
+  for (int s = 0; s < n_samples; ++s) {
+    const int64_t len = tok_offsets[s + 1] - tok_offsets[s];
+    if (len < 2 || len - 1 > cod_max_columns()) return -1;
+    out_offsets[s + 1] = out_offsets[s] + cod_capacity(len, K, r, r_min);
+  }
+  return out_offsets[n_samples];
+}
+
+pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
+                           double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets, int32_t* out_ids,
+                           int32_t* out_labels, int32_t* out_pos, int32_t* out_section, int32_t* out_column,
+                           int32_t* out_len, float* kernel_ms, void* hip_stream) {
+  if (!tokens || !tok_offsets || !out_offsets || !out_ids || !out_labels || !out_pos || !out_section ||
+      !out_column || !out_len || n_samples < 1 || !cod_params_ok(K, r, r_min))
+    return PARD_ERR_ARG;
+  // every sample fits the kernel and its output region holds its capacity
+  if (tok_offsets[0] < 0 || out_offsets[0] < 0) return PARD_ERR_ARG;
+  int max_cols = 1;
+  for (int s = 0; s < n_samples; ++s) {
+    const int64_t len = tok_offsets[s + 1] - tok_offsets[s];
+    if (len < 2 || len - 1 > cod_max_columns()) return PARD_ERR_ARG;
+    if (out_offsets[s + 1] - out_offsets[s] < cod_capacity(len, K, r, r_min)) return PARD_ERR_CAPACITY;
+    max_cols = std::max(max_cols, (int)(len - 1));
+  }
+  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
+  int64_t* d_off = nullptr;
+  const size_t bytes = sizeof(int64_t) * (size_t)(n_samples + 1);
+  if (hipMalloc((void**)&d_off, 2 * bytes) != hipSuccess) return PARD_ERR_NOMEM;
+  CodArgs a;
+  a.k_max = K;
+  a.r = r;
+  a.r_min = r_min;
+  a.mask_id = mask_id;
+  a.seed = seed;
+  a.ids = out_ids;
+  a.labels = out_labels;
+  a.pos = out_pos;
+  a.section = out_section;
+  a.column = out_column;
+  a.out_len = out_len;
+  pard_status stt = PARD_OK;
+  hipEvent_t ev[2] = {nullptr, nullptr};
+  if (kernel_ms && (hipEventCreate(&ev[0]) != hipSuccess || hipEventCreate(&ev[1]) != hipSuccess)) stt = PARD_ERR_DEVICE;
+  if (stt == PARD_OK &&
+      (hipMemcpyAsync(d_off, tok_offsets, bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
+       hipMemcpyAsync(d_off + n_samples + 1, out_offsets, bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
+       (kernel_ms && hipEventRecord(ev[0], st) != hipSuccess) ||
+       launch_cod(tokens, d_off, d_off + n_samples + 1, n_samples, max_cols, a, st) != hipSuccess ||
+       (kernel_ms && hipEventRecord(ev[1], st) != hipSuccess) || hipStreamSynchronize(st) != hipSuccess))
+    stt = PARD_ERR_DEVICE;
+  if (stt == PARD_OK && kernel_ms && hipEventElapsedTime(kernel_ms, ev[0], ev[1]) != hipSuccess) stt = PARD_ERR_DEVICE;
+  for (hipEvent_t e : ev)
+    if (e) (void)hipEventDestroy(e);
+  (void)hipFree(d_off);
+  return stt;
+}
+
 pard_status pard_read_logits(const pard_ctx* cc, int32_t which, int32_t seq, float* out, int32_t rows,
                              int32_t vocab) {
   pard_ctx* c = const_cast<pard_ctx*>(cc);

@@ -234,6 +234,16 @@ struct LaunchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
 };
 
+// COD training-data processing (one workgroup per sample).
+struct CodArgs {
+  int k_max;
+  double r, r_min;         // retention decay and floor (float64: they decide the kept counts)
+  int mask_id;
+  uint64_t seed;
+  int32_t *ids, *labels, *pos, *section, *column;   // packed outputs
+  int32_t* out_len;                                 // packed length per sample
+};
+
 // Launchers (return hipSuccess or the launch error).
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st,
                        LaunchEvents ev = LaunchEvents{});
@@ -243,5 +253,8 @@ hipError_t launch_stage(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);
 size_t attn_part_floats(int head_dim, int nqt);
 int attn_max_q_tiles(int head_dim);
+hipError_t launch_cod(const int32_t* tokens, const int64_t* tok_off, const int64_t* out_off, int n_samples,
+                      int max_columns, const CodArgs& a, hipStream_t st);
+int cod_max_columns();
 
 }  // namespace pard

@@ -125,3 +125,37 @@ def test_null_context_calls_return_arg(b):
     assert b.lib.pard_last_error(None) == b"null context"
     b.lib.pard_free(None)
     assert b.lib.pard_status_string(b.PARD_ERR_CAPACITY) == b"PARD_ERR_CAPACITY"
+
+
+def test_cod_capacity_and_argument_checks(b):
+    """Host-side COD checks (no device work): the capacity equals subtask 1's
+    columns plus each later subtask's keep target; bad parameters, lengths and
+    undersized output regions are refused before any device call."""
+    import ctypes as C
+    from oracle import cod
+    for n_tok, k, r, r_min in ((5, 3, 0.5, 0.0), (1001, 8, 0.7, 0.2), (2, 8, 0.7, 0.2), (8193, 4, 0.9, 0.0)):
+        n = n_tok - 1
+        want = n + sum(cod.keep_target(n, kk, r, r_min) for kk in range(2, k + 1))
+        assert b.cod_capacity(n_tok, k, r, r_min) == want
+    assert b.cod_capacity(1, 4, 0.5, 0.0) == -1 and b.cod_capacity(8194, 4, 0.5, 0.0) == -1
+    assert b.cod_capacity(10, 0, 0.5, 0.0) == -1 and b.cod_capacity(10, 4, 0.0, 0.0) == -1
+    assert b.cod_capacity(10, 4, 1.5, 0.0) == -1 and b.cod_capacity(10, 4, 0.5, -0.1) == -1
+    dummy = C.c_void_p(16)                       # never dereferenced: the checks fail first
+    P64 = C.POINTER(C.c_int64)
+
+    def build(tok_offs, out_offs, k=4, r=0.5):
+        t = (C.c_int64 * len(tok_offs))(*tok_offs)
+        o = (C.c_int64 * len(out_offs))(*out_offs)
+        return b.lib.pard_cod_build(dummy, C.cast(t, P64), len(tok_offs) - 1, k, r, 0.0, 0, 0, C.cast(o, P64),
+                                    dummy, dummy, dummy, dummy, dummy, dummy, None, None)
+    cap = b.cod_capacity(10, 4, 0.5, 0.0)
+    assert build([0, 10], [0, cap - 1]) == b.PARD_ERR_CAPACITY
+    assert build([0, 1], [0, 100]) == b.PARD_ERR_ARG          # a one-token sample
+    assert build([0, 10], [0, cap], k=0) == b.PARD_ERR_ARG
+    assert build([0, 10], [0, cap], r=2.0) == b.PARD_ERR_ARG
+    # the layout is the capacities' prefix sum
+    offs = (C.c_int64 * 4)(0, 10, 12, 500)
+    lay = (C.c_int64 * 4)()
+    total = b.lib.pard_cod_layout(C.cast(offs, P64), 3, 4, 0.5, 0.0, C.cast(lay, P64))
+    caps = [b.cod_capacity(n, 4, 0.5, 0.0) for n in (10, 2, 488)]
+    assert list(lay) == [0, caps[0], caps[0] + caps[1], sum(caps)] and total == sum(caps)

@@ -82,17 +82,22 @@ __device__ __forceinline__ float sum4g(float x) {
   return r[0] + r[1];
 }
 
-template <int HD, int NQ>
-__global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
-  constexpr int NWA = kAttnWaves;
+// NW wavefronts per workgroup: kAttnWaves (4) for chunked passes, 2 * kAttnWaves
+// (8) for short contexts covered by one chunk -- there waves 4..7 first fold
+// their (m, l, o) into waves 0..3 through LDS (wave w + 4 into wave w), so
+// that the wave merge below and its LDS stay those of 4 waves.
+template <int HD, int NQ, int NW>
+__global__ __launch_bounds__(64 * NW) void k_attn(const AttnArgs p) {
+  constexpr int NWA = NW;
+  constexpr int MW = kAttnWaves;     // waves in the final LDS merge
   constexpr int QP = 16 * NQ;        // query pairs per workgroup
   constexpr int KS = HD / 32;        // 32-dim steps of Q.K
   constexpr int DB = HD / 16;        // 16-dim blocks of the output
   constexpr int OS = HD + 4;         // row stride of the per-wave output tiles in LDS
   constexpr int REC = QP * HD + 2 * QP;   // floats of one chunk record: o [QP][HD], m [QP], l [QP]
   __shared__ u32x4 q_lds[NQ * KS * 64];   // Q fragments in B-operand lane order
-  __shared__ __attribute__((aligned(16))) float o_lds[NWA][QP][OS];
-  __shared__ float m_lds[NWA][QP], l_lds[NWA][QP], sc_lds[NWA][QP], linv_lds[QP];
+  __shared__ __attribute__((aligned(16))) float o_lds[MW][QP][OS];
+  __shared__ float m_lds[MW][QP], l_lds[MW][QP], sc_lds[MW][QP], linv_lds[QP];
 
   const int kvh = blockIdx.x, qg = blockIdx.y;
   const int sj = blockIdx.z / p.n_splits, ch = blockIdx.z % p.n_splits;
@@ -272,27 +277,50 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
   }
 
   // ---- merge the wavefronts in wave order ----
-  if (g4 == 0) {
-#pragma unroll
-    for (int t = 0; t < NQ; ++t) {
-      m_lds[wave][t * 16 + c16] = m[t];
-      l_lds[wave][t * 16 + c16] = l[t];
-    }
-  }
   // lane (c16, g4) holds dims db*16 + 4*g4 .. +3 of pair t*16 + c16
+  auto publish = [&](int slot) {
+    if (g4 == 0) {
 #pragma unroll
-  for (int t = 0; t < NQ; ++t)
+      for (int t = 0; t < NQ; ++t) {
+        m_lds[slot][t * 16 + c16] = m[t];
+        l_lds[slot][t * 16 + c16] = l[t];
+      }
+    }
 #pragma unroll
-    for (int db = 0; db < DB; ++db)
-      *reinterpret_cast<f32x4*>(&o_lds[wave][t * 16 + c16][db * 16 + g4 * 4]) = o[t][db];
+    for (int t = 0; t < NQ; ++t)
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+        *reinterpret_cast<f32x4*>(&o_lds[slot][t * 16 + c16][db * 16 + g4 * 4]) = o[t][db];
+  };
+  if constexpr (NW > MW) {
+    static_assert(NW == 2 * MW, "the fold pairs wave w + MW with wave w");
+    if (wave >= MW) publish(wave - MW);
+    __syncthreads();
+    if (wave < MW) {
+#pragma unroll
+      for (int t = 0; t < NQ; ++t) {
+        const float mb = m_lds[wave][t * 16 + c16], lb = l_lds[wave][t * 16 + c16];
+        const float mn = fmaxf(m[t], mb);
+        const float mu = mn == -INFINITY ? 0.f : mn;
+        const float sa = __builtin_amdgcn_exp2f(m[t] - mu), sb = __builtin_amdgcn_exp2f(mb - mu);
+        l[t] = l[t] * sa + lb * sb;
+        m[t] = mn;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+          o[t][db] = o[t][db] * sa + *reinterpret_cast<const f32x4*>(&o_lds[wave][t * 16 + c16][db * 16 + g4 * 4]) * sb;
+      }
+    }
+    __syncthreads();
+  }
+  if (wave < MW) publish(wave);
   __syncthreads();
   float* rec = p.part + (((size_t)(sj * p.n_kv + kvh) * p.n_qblocks + qg) * p.n_splits + ch) * REC;   // this chunk's record
   if (tid < QP) {
     float M = m_lds[0][tid];
-    for (int w = 1; w < NWA; ++w) M = fmaxf(M, m_lds[w][tid]);
+    for (int w = 1; w < MW; ++w) M = fmaxf(M, m_lds[w][tid]);
     const float M_use = M == -INFINITY ? 0.f : M;
     float L = 0.f;
-    for (int w = 0; w < NWA; ++w) {
+    for (int w = 0; w < MW; ++w) {
       const float sc = __builtin_amdgcn_exp2f(m_lds[w][tid] - M_use);
       sc_lds[w][tid] = sc;
       L += l_lds[w][tid] * sc;
@@ -311,7 +339,7 @@ __global__ __launch_bounds__(64 * kAttnWaves) void k_attn(const AttnArgs p) {
     const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
     f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, b = a;
 #pragma unroll
-    for (int w = 0; w < NWA; ++w) {
+    for (int w = 0; w < MW; ++w) {
       const float sc = sc_lds[w][q];
       a += *reinterpret_cast<const f32x4*>(&o_lds[w][q][d0]) * sc;
       b += *reinterpret_cast<const f32x4*>(&o_lds[w][q][d0 + 4]) * sc;
@@ -410,7 +438,11 @@ __global__ __launch_bounds__(256) void k_attn_merge(const AttnArgs p) {
 
 template <int HD, int NQ>
 hipError_t launch_hd_nq(const AttnArgs& a, hipStream_t st) {
-  k_attn<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
+  if (a.wide) {                      // one chunk, 8 waves: no merge kernel
+    k_attn<HD, NQ, 2 * kAttnWaves><<<dim3(a.n_kv, a.n_qblocks, a.n_seq), dim3(128 * kAttnWaves), 0, st>>>(a);
+    return hipGetLastError();
+  }
+  k_attn<HD, NQ, kAttnWaves><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
   k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * kMergeParts), dim3(256), 0, st>>>(a);
@@ -438,6 +470,7 @@ hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st) {
   if (a.split_len % 128 || a.split_len <= 0) return hipErrorInvalidValue;
   if (a.nqt < 1 || a.nqt > attn_max_q_tiles(head_dim)) return hipErrorInvalidValue;
   if (a.n_seq < 1 || a.n_seq > kMaxPassSeqs || (size_t)a.n_seq * a.n_splits > 65535) return hipErrorInvalidValue;
+  if (a.wide && a.n_splits != 1) return hipErrorInvalidValue;
   if (head_dim == 64) return launch_hd<64>(a, st);
   if (head_dim == 128) return launch_hd<128>(a, st);
   return hipErrorInvalidValue;

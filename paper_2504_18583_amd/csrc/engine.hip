@@ -22,6 +22,7 @@ namespace {
 
 constexpr int kPrefillRows = kMaxPassRows;   // prefill chunks run the row-block GEMM
 constexpr int kDescRing = 128;
+constexpr int kStepsPerPlan = 32;            // fused steps between two host checks of the length class
 constexpr int kGatherMax = 4096;
 constexpr size_t kRowsPartBudget = 512;   // fp32 partial tiles of split row-block GEMMs (144 KiB each)
 static_assert(kRowsPartBudget * kRowsPartFloats >= kSplitPartFloats, "split partial tiles share the row-block buffer");
@@ -520,12 +521,17 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   // groups, use longer chunks to bound the partial records)
   const int seq_rows = ps.max_seq_rows > 0 ? std::min(ps.max_seq_rows, ps.max_rows) : ps.max_rows;
   const int qpairs = seq_rows * M.group;
-  const int nqt = std::min(attn_max_q_tiles(s.head_dim), ceil_div(qpairs, 16));
-  const int n_qblocks = ceil_div(qpairs, 16 * nqt);
   const int l_bound = std::min(std::max(ps.l_bound, 1), c->kv_cap);
+  // decode passes over a short context: one chunk per workgroup of 8 waves
+  // (no merge kernel), one query tile per workgroup (at head_dim 128 that keeps
+  // the 8-wave kernel within its registers; at 64 it measured fastest)
+  const bool wide = !rows && l_bound <= kAttnWideMaxKeys;
+  int nqt = std::min(attn_max_q_tiles(s.head_dim), ceil_div(qpairs, 16));
+  if (wide) nqt = std::min(nqt, s.head_dim == 128 ? 1 : kAttnWideQTiles64);
+  const int n_qblocks = ceil_div(qpairs, 16 * nqt);
   if (ps.n_seq * n_qblocks > kAttnRecords)
     return fail(c, PARD_ERR_CAPACITY, "attention plan: %d query blocks exceed the record budget", ps.n_seq * n_qblocks);
-  int split_len = kAttnChunk;
+  int split_len = wide ? ceil_div(l_bound, 128) * 128 : kAttnChunk;
   while ((int64_t)ps.n_seq * n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
   const int n_splits = ceil_div(l_bound, split_len);
   for (int l = 0; l < s.n_layers; ++l) {
@@ -571,6 +577,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
       a.n_seq = ps.n_seq;
       a.scale = 1.0f / std::sqrt((float)s.head_dim);
       a.part = c->attn_part;
+      a.wide = wide ? 1 : 0;
       Timed t(c, cls0 + 2);
       HIP_TRY(c, launch_attention(s.head_dim, a, c->stream));
     }
@@ -1199,6 +1206,9 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
     }
     int batch = ceil_div(min_left, K + 1);
     if (max_steps > 0) batch = std::min(batch, max_steps - steps);
+    // a bounded batch keeps the attention length class (and so the attention
+    // plan of the captured steps) close to the actual context
+    batch = std::min(batch, kStepsPerPlan);
     // L_t grows by at most K+1 per step: one attention plan covers the batch
     StepShape sh;
     sh.n_seq = (int)active.size();

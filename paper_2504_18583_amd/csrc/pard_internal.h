@@ -55,6 +55,8 @@ constexpr int kSplitCounters = 4096;
 constexpr size_t kSplitPartFloats = (size_t)4 << 20;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
 constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
+constexpr int kAttnWideMaxKeys = 1024;   // decode passes up to this context: one 8-wave workgroup covers all keys
+constexpr int kAttnWideQTiles64 = 1;     // query tiles per such workgroup at head_dim 64 (measured: 1 ahead of 2 and 4)
 constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head and sequence
 
 // Position of activation element (row, k) in a k-blocked buffer with `slots`
@@ -227,6 +229,7 @@ struct AttnArgs {
   int n_seq;                                  // sequences the grid covers (>= the pass's)
   float scale;
   float* part;                                // chunk records when n_splits > 1
+  int wide;                                   // 1: one chunk per workgroup of 8 waves (n_splits == 1)
 };
 
 // Optional timing events of one launch (recorded at the kernel's start and end).

@@ -55,7 +55,7 @@ constexpr int kSplitCounters = 4096;
 constexpr size_t kSplitPartFloats = (size_t)4 << 20;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
 constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
-constexpr int kAttnWideMaxKeys = 1024;   // decode passes up to this context: one 8-wave workgroup covers all keys
+constexpr int kAttnWideMaxKeys = 2048;   // decode passes up to this context: one 8-wave workgroup covers all keys
 constexpr int kAttnWideQTiles64 = 1;     // query tiles per such workgroup at head_dim 64 (measured: 1 ahead of 2 and 4)
 constexpr int kAttnRecords = 512;  // max (query group, key chunk) partial records per KV head and sequence
 

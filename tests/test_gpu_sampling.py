@@ -305,3 +305,39 @@ def test_llama_8b_1b_full_width_slice_sampling_lockstep(B):
         say(f"    oracle-decided {ls.decided}/{ls.compared}, max |logit err| {ls.worst:.3g}")
     finally:
         eng.close()
+
+
+def test_batched_sampling_decisions_per_slot(B):
+    """Five slots stepped together with sampling (multi-sequence skinny passes):
+    every slot's candidates, keep count and last token equal the rule applied
+    in fp64 to that slot's own GPU logits with its own uniforms (slot index),
+    away from decision boundaries; KV lengths grow by a + 1."""
+    wl, t_spec, d_spec = _tiny()
+    temp, seed, k = 0.2, 99, 4
+    slots = [1, 3, 4, 6, 7]
+    prompts = {s: [int(x) for x in pi.gen_prompt(40 + s, t_spec.vocab, 20 + 7 * s)] for s in slots}
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=256, max_k=8, max_batch=8)
+    try:
+        eng.set_sampling(temp, seed)
+        for s in slots:
+            eng.prefill(prompts[s], seq=s)
+        for step in range(4):
+            lt = {s: eng.kv_len(B.PARD_TARGET, seq=s) for s in slots}
+            res, stats = eng.generate_batch(slots, k, 64, max_steps=1)
+            say(f"[gpu] batched sampling: step {step}, tokens {[len(r) - 1 for r in res]}")
+            for s, toks in zip(slots, res):
+                g_dl = eng.read_logits(B.PARD_DRAFT, k, seq=s)
+                g_vl = eng.read_logits(B.PARD_TARGET, k + 1, seq=s)
+                qg, pg = S.probs(g_dl, temp), S.probs(g_vl, temp)
+                cands = [S.sample_index(qg[j], S.uniform(seed, s, step, j, S.PURPOSE_DRAFT)) for j in range(k)]
+                margins_ok = all(m >= SELF_TOL for m in draft_margins(qg, cands, seed, s, step))
+                a = eng.kv_len(B.PARD_TARGET, seq=s) - lt[s] - 1
+                emitted = toks[1:]
+                assert len(emitted) == a + 1 and 0 <= a <= k
+                if margins_ok:
+                    assert emitted[:a] == cands[:a], f"slot {s} step {step}: kept candidates"
+                    ra, rtok = S.keep_decisions(cands, pg, qg, seed, s, step)
+                    if verify_margin(cands, pg, qg, ra, rtok, seed, s, step) >= SELF_TOL:
+                        assert (a, emitted[a]) == (ra, rtok), f"slot {s} step {step}"
+    finally:
+        eng.close()

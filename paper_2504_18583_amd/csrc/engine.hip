@@ -23,6 +23,7 @@ namespace {
 constexpr int kPrefillRows = kMaxPassRows;   // prefill chunks run the row-block GEMM
 constexpr int kDescRing = 128;
 constexpr int kStepsPerPlan = 32;            // fused steps between two host checks of the length class
+constexpr int kLmStrips = 8;                 // strips per lm_head workgroup at up to 16 lm rows
 constexpr int kGatherMax = 4096;
 constexpr size_t kRowsPartBudget = 512;   // fp32 partial tiles of split row-block GEMMs (144 KiB each)
 static_assert(kRowsPartBudget * kRowsPartFloats >= kSplitPartFloats, "split partial tiles share the row-block buffer");
@@ -89,7 +90,7 @@ int pick_S(int epi, int n_strips, int mt) {
   // workgroups (measured faster for the 8B QKV shape: 384 strips)
   if ((epi == EPI_QKV || epi == EPI_RESID) && n_strips >= 384) s = 2;
   if (epi == EPI_SWIGLU) s = 2;
-  if (epi == EPI_LOGITS) s = (mt == 1) ? 4 : 2;
+  if (epi == EPI_LOGITS) s = (mt == 1) ? kLmStrips : 2;
   while (s > 1 && n_strips % s) s >>= 1;
   return s;
 }

@@ -703,15 +703,22 @@ __device__ int wave_sample(const TailArgs& p, int lmr, float M, float S, float u
     if (tsel < 0) return 0;
     rem = INFINITY;
   }
-  // columns of the chosen tile, one per lane
-  const int col = tsel * p.tile_w + lane;
-  float w = 0.f;
-  if (lane < p.tile_w && col < p.vocab)
-    w = __builtin_amdgcn_exp2f((p.logits[(size_t)lmr * p.vocab + col] - M) * k);
-  const float cincl = wave_incl_scan(w, lane);
-  const uint64_t chit = __ballot(cincl > rem && w > 0.f);
-  const uint64_t cnz = __ballot(w > 0.f);
-  const int x = chit ? __ffsll((unsigned long long)chit) - 1 : (cnz ? 63 - __clzll((long long)cnz) : 0);
+  // columns of the chosen tile, 64 at a time (one per lane), running sum in column order
+  int x = -1, last = -1;
+  float ccarry = 0.f;
+  for (int c0 = 0; c0 < p.tile_w && x < 0; c0 += 64) {
+    const int col = tsel * p.tile_w + c0 + lane;
+    float w = 0.f;
+    if (c0 + lane < p.tile_w && col < p.vocab)
+      w = __builtin_amdgcn_exp2f((p.logits[(size_t)lmr * p.vocab + col] - M) * k);
+    const float cincl = wave_incl_scan(w, lane);
+    const uint64_t chit = __ballot(w > 0.f && ccarry + cincl > rem);
+    const uint64_t cnz = __ballot(w > 0.f);
+    if (chit) x = c0 + __ffsll((unsigned long long)chit) - 1;
+    if (cnz) last = c0 + 63 - __clzll((long long)cnz);
+    ccarry += __shfl(cincl, 63);
+  }
+  if (x < 0) x = last < 0 ? 0 : last;   // rounding: the tile's last column with weight
   return tsel * p.tile_w + x;
 }
 
@@ -1366,6 +1373,7 @@ hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEven
     case 2: return launch_one<EPI, MT, 2>(nw, a, st, ev);
     case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st, ev); break;
     case 7: if constexpr (MT == 1 && EPI == EPI_SWIGLU) return launch_one<EPI, MT, 7>(nw, a, st, ev); break;
+    case 8: if constexpr (MT == 1 && EPI == EPI_LOGITS) return launch_one<EPI, MT, 8>(nw, a, st, ev); break;
   }
   return hipErrorInvalidValue;
 }

@@ -23,6 +23,7 @@ namespace {
 constexpr int kPrefillRows = kMaxPassRows;   // prefill chunks run the row-block GEMM
 constexpr int kDescRing = 128;
 constexpr int kStepsPerPlan = 32;            // fused steps between two host checks of the length class
+constexpr int kRowsSplitTarget = 224;       // workgroups a split row-block GEMM aims at (batch-32 step: 224 ahead of 192 and 256)
 constexpr int kLmStrips = 8;                 // strips per lm_head workgroup at up to 16 lm rows
 constexpr int kGatherMax = 4096;
 constexpr size_t kRowsPartBudget = 512;   // fp32 partial tiles of split row-block GEMMs (144 KiB each)
@@ -126,7 +127,7 @@ RowsPlan plan_rows(const GemmPlan& p, int max_rows, int typ_rows) {
   r.n_tiles = ceil_div(p.n_strips, kRowsTileStrips);
   r.m_blocks = ceil_div(max_rows, kRowTiles * 16);
   const int live = r.n_tiles * ceil_div(std::max(1, std::min(typ_rows, max_rows)), kRowTiles * 16);
-  if (live < 160) r.ksplit = ceil_div(256, live);
+  if (live < 160) r.ksplit = ceil_div(kRowsSplitTarget, live);
   r.ksplit = std::min({r.ksplit, 16, std::max(1, p.kb_total / 8)});
   while (r.ksplit > 1 && (size_t)r.ksplit * r.n_tiles * r.m_blocks > kRowsPartBudget) --r.ksplit;
   return r;

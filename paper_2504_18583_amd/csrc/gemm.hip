@@ -141,14 +141,91 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     }
   };
 
-  // The weight stream does not depend on the pass: its first stage is in
-  // flight before the pass descriptor is read.
-  if (n_it > 0) load_w(w0, 0);
+  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
+  constexpr bool NORM = EPI != EPI_RESID;             // A is RMS-normalised: rows need 1/rms
+
+  // 1/rms per row from the producer's per-tile sums of squares: 16 threads per
+  // row, fixed summation order.  For one row tile the loads of the first 256
+  // tiles are issued ahead of the weight stream (ss_issue) and summed just
+  // before the first MFMAs (ss_finish): loads complete in issue order, so
+  // waiting for them would otherwise also wait for every weight load in
+  // flight and empty the pipeline.
+  float ss_part[16];
+  auto ss_issue = [&](int row) {
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      // unconditional loads (a tile index past the end re-reads the last
+      // tile and is dropped when summed), so none waits behind a branch
+      const int q = (tid & 15) + 16 * u;
+      ss_part[u] = p.ss_in[(size_t)min(q, p.ss_tiles - 1) * kMaxPassRows + row];
+    }
+  };
+  auto ss_finish = [&](int row) {
+    float t = 0.f;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) t += (tid & 15) + 16 * u < p.ss_tiles ? ss_part[u] : 0.f;
+    for (int q0 = (tid & 15) + 256; q0 < p.ss_tiles; q0 += 256) {
+      float part[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int q = q0 + 16 * u;
+        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u) t += part[u];
+    }
+    t += __shfl_xor(t, 8);
+    t += __shfl_xor(t, 4);
+    t += __shfl_xor(t, 2);
+    t += __shfl_xor(t, 1);
+    if ((tid & 15) == 0) rs_s[tid >> 4] = 1.0f / sqrtf(t * p.inv_k + p.eps);
+  };
+  // thread tid (< 256) of the epilogue owns, for j = s*MT + mt, element
+  // (row, col) below; its epilogue operands are fetched while the weights stream
+  const bool epi = tid < 256;
+  const int ew = tid >> 6;
+  const int rsub = (lane >> 4) * 4 + ew;
+  const int csub = lane & 15;
+
+  // Per-lane reads of the pass descriptor are issued first, for the same
+  // reason: lm source rows (A fragment rows, row-scale rows) and, for QKV, the
+  // position and sequence slot of each epilogue row.  Entries past the pass
+  // are read (in bounds) but never used.
+  const FwdDesc* dp = p.desc;
+  int lm_a[MT], e_pos[MT], e_slot[MT];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    lm_a[mt] = LM ? dp->lm_src[mt * 16 + (lane & 15)] : 0;
+    e_pos[mt] = EPI == EPI_QKV ? dp->pos[mt * 16 + rsub] : 0;
+    e_slot[mt] = EPI == EPI_QKV ? dp->slot[mt * 16 + rsub] : 0;
+  }
+  const int lm_ss = LM ? dp->lm_src[(tid & 255) >> 4] : 0;
+  // rows of a pass's activations need no descriptor (rows past the pass read
+  // unused sums and are never stored)
+  if constexpr (NORM && !LM && MT == 1) {
+    if (tid < 256) ss_issue(tid >> 4);
+  }
   __builtin_amdgcn_sched_barrier(0);
 
-  constexpr bool LM = EPI == EPI_LOGITS;              // rows are the pass's lm rows
-  const FwdDesc* dp = p.desc;
+  // The weight stream does not depend on the pass: its first stage is in
+  // flight before the pass descriptor's scalar fields are read.  It is loaded
+  // unconditionally (a wave with no k-block of its own, n_it = 0, reads the
+  // range's last one and never uses it): a branch around it would make every
+  // later wait on an earlier load wait for the whole stage too.
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int kb = kb0 + min(wave + min(u, max(n_it - 1, 0)) * nw, kb_n - 1);
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+      w0[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
   const int row_count = LM ? dp->n_lm : dp->n_rows;
+  const int ss_row = LM ? ((tid & 255) >> 4 < row_count ? lm_ss : 0) : (tid & 255) >> 4;
+  if constexpr (LM && MT == 1) {
+    if (tid < 256) ss_issue(ss_row);              // lm rows read their source row's sums
+  }
 
   // A fragment of this lane: row (lane % 16) of each M tile, 8 columns at
   // 8*(lane/16); A is k-blocked, so k-block kb of all rows is one contiguous
@@ -162,7 +239,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
     const int r = mt * 16 + (lane & 15);
-    const int src = r < row_count ? (LM ? dp->lm_src[r] : r) : 0;
+    const int src = r < row_count ? (LM ? lm_a[mt] : r) : 0;
     a_voff[mt] = r < row_count ? src * 64 + (lane >> 4) * 16 : kOutOfRange;
   }
   auto load_a = [&](u32x4 (&a)[U][MT], int its) {
@@ -179,12 +256,6 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     load_a(a, its);
   };
 
-  // thread tid (< 256) of the epilogue owns, for j = s*MT + mt, element
-  // (row, col) below; its epilogue operands are fetched while the weights stream
-  const bool epi = tid < 256;
-  const int ew = tid >> 6;
-  const int rsub = (lane >> 4) * 4 + ew;
-  const int csub = lane & 15;
   float e0[NJ], e1[NJ];
   float2 e2[NJ];
   auto prefetch_epilogue = [&]() {
@@ -204,7 +275,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       } else if constexpr (EPI == EPI_QKV) {
         if (epi && p.bias) e0[j] = p.bias[n];
         if (epi && row < row_count && n < p.q_dim + p.kv_dim)
-          e2[j] = p.rope[(size_t)dp->pos[row] * (p.hd / 2) + ((n % p.hd) >> 1)];
+          e2[j] = p.rope[(size_t)e_pos[mt] * (p.hd / 2) + ((n % p.hd) >> 1)];
       }
     }
   };
@@ -223,8 +294,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     }
   };
 
-  // 1/rms per row from the producer's per-tile sums of squares: 16 threads per
-  // row, 16 independent loads each in flight together, fixed summation order
+  // several row tiles: the same sums, loaded and summed in one go
   auto row_scales = [&]() {
     if (tid < 256) {
       for (int r = tid >> 4; r < MT * 16; r += 16) {
@@ -254,10 +324,14 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     int its = 0;
     load_a(a0, its);
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (EPI != EPI_RESID) row_scales();   // overlaps the first weight loads
+    if constexpr (NORM && MT > 1) row_scales();     // overlaps the first weight loads
     load(w1, a1, its + U);
     __builtin_amdgcn_sched_barrier(0);
     prefetch_epilogue();
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (NORM && MT == 1) {
+      if (tid < 256) ss_finish(ss_row);
+    }
     __builtin_amdgcn_sched_barrier(0);
     while (true) {
       compute(w0, a0, its);
@@ -274,7 +348,10 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       __builtin_amdgcn_sched_barrier(0);
     }
   } else {
-    if constexpr (EPI != EPI_RESID) row_scales();
+    if constexpr (NORM && MT > 1) row_scales();
+    if constexpr (NORM && MT == 1) {
+      if (tid < 256) ss_finish(ss_row);
+    }
     prefetch_epilogue();
   }
 
@@ -343,8 +420,8 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       float y = v[j] * rs_s[row] + e0[j];            // + bias
       const float partner = __shfl_xor(y, 1);
       if (row < row_count) {
-        const int pos = dp->pos[row];
-        const size_t cache = (size_t)dp->slot[row] * p.kv_seq_stride;
+        const int pos = e_pos[mt];
+        const size_t cache = (size_t)e_slot[mt] * p.kv_seq_stride;
         if (n < p.q_dim + p.kv_dim) {
           const float2 cs = e2[j];                     // rotary (cos, sin) of (pos, pair)
           y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);

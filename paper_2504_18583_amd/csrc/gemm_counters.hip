@@ -1,7 +1,7 @@
 // Stand-alone launches of one skinny GEMM shape, for hardware counters and
 // launch-shape timing.
 //
-// Launches k_gemm<MT=1, S, EPI> (EPI_SWIGLU or EPI_RESID) over `rows` decode
+// Launches k_gemm<MT=1, S, EPI> (EPI_SWIGLU, EPI_RESID or EPI_QKV) over `rows` decode
 // rows of a weight of `strips` 16-column strips x `kb` 32-column k-blocks,
 // with the input dimension split into P ranges, 20 times untimed and 100 times
 // timed, and prints the mean launch time.  The defaults are the LLaMA3.1-8B
@@ -13,9 +13,14 @@
 // = 1 it then runs, for every weight copy in turn, the same launch unsplit and
 // split and compares the two outputs (they differ only by summation order), a
 // test of the split's partial-tile exchange; the numerics of the kernel itself
-// are tested against the oracle through the library.
+// are tested against the oracle through the library.  The QKV epilogue
+// writes a grouped-query layout of head_dim 128 (query width 4 x the key
+// width) at positions 512.. of one sequence's cache.  `ss_tiles` is the number
+// of per-tile sums of squares each row scale adds (256 after the 8B down
+// projection).
 //
-// usage: gemm_counters [rows 9] [S 7] [P 1] [strips 1792] [kb 128] [epi swiglu|resid] [copies 1] [check 0]
+// usage: gemm_counters [rows 9] [S 7] [P 1] [strips 1792] [kb 128] [epi swiglu|resid|qkv] [copies 1] [check 0]
+//                      [ss_tiles 1]
 #include <cstdio>
 #include <cstdlib>
 #include <cmath>
@@ -55,15 +60,20 @@ int main(int argc, char** argv) {
   const int n_strips = argc > 4 ? atoi(argv[4]) : 2 * 14336 / 16;
   const int kb_total = argc > 5 ? atoi(argv[5]) : 4096 / 32;
   const bool resid = argc > 6 && strcmp(argv[6], "resid") == 0;
+  const bool qkv = argc > 6 && strcmp(argv[6], "qkv") == 0;
   const int copies = argc > 7 ? atoi(argv[7]) : 1;
   const bool check = argc > 8 && atoi(argv[8]) != 0;
-  const int epi = resid ? EPI_RESID : EPI_SWIGLU;
+  const int ss_tiles = argc > 9 ? atoi(argv[9]) : 1;
+  const int epi = resid ? EPI_RESID : qkv ? EPI_QKV : EPI_SWIGLU;
+  constexpr int kHd = 128, kCap = 1024, kPos0 = 512;
   const int kb_split = P > 0 ? (kb_total + P - 1) / P : 0;
-  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || (S == 7 && !resid)) || n_strips < 1 ||
-      n_strips % S != 0 || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 || copies > 64 ||
-      (size_t)n_strips * kb_total * 1024 * copies > ((size_t)8 << 30)) {
+  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || (S == 7 && epi == EPI_SWIGLU)) ||
+      n_strips < 1 || n_strips % S != 0 || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 ||
+      copies > 64 || (size_t)n_strips * kb_total * 1024 * copies > ((size_t)8 << 30) || ss_tiles < 1 ||
+      ss_tiles > n_strips || (qkv && ((n_strips * 16) % (6 * kHd) != 0 || check))) {
     fprintf(stderr, "bad shape: rows 1..%d, S in {1, 2, 4, 7 (swiglu)}, S | strips, every input range non-empty, "
-            "copies 1..64 of at most 8 GiB in all\n", kMaxRows);
+            "copies 1..64 of at most 8 GiB in all, 1 <= ss_tiles <= strips; qkv: 6 x 128 | columns, no check\n",
+            kMaxRows);
     return 2;
   }
   const int hidden = kb_total * 32;
@@ -75,10 +85,16 @@ int main(int argc, char** argv) {
   float *ss, *x, *g, *ss_out, *part;
   int* counters;
   FwdDesc* desc;
+  uint16_t *kc, *vc;
+  float2* rope;
+  const int kv_dim = out_cols / 6, q_dim = out_cols - 2 * kv_dim;
+  CHECK(hipMalloc(&kc, sizeof(uint16_t) * kv_dim * kCap));
+  CHECK(hipMalloc(&vc, sizeof(uint16_t) * kv_dim * kCap));
+  CHECK(hipMalloc(&rope, sizeof(float2) * kCap * kHd / 2));
   CHECK(hipMalloc(&W, w_elems * 2 * copies));
   CHECK(hipMalloc(&A, a_elems * 2));
   CHECK(hipMalloc(&out, o_elems * 2));
-  CHECK(hipMalloc(&ss, sizeof(float) * kMaxPassRows));
+  CHECK(hipMalloc(&ss, sizeof(float) * kMaxPassRows * ss_tiles));
   CHECK(hipMalloc(&x, sizeof(float) * kMaxRows * out_cols));
   CHECK(hipMalloc(&g, sizeof(float) * out_cols));
   CHECK(hipMalloc(&ss_out, sizeof(float) * (size_t)kMaxPassRows * n_strips));
@@ -88,7 +104,8 @@ int main(int argc, char** argv) {
   CHECK(hipMemset(counters, 0, sizeof(int) * kSplitCounters));
   k_fill_f16<<<1024, 256>>>(W, w_elems * copies, 1u);
   k_fill_f16<<<64, 256>>>(A, a_elems, 2u);
-  k_fill_value<<<64, 256>>>(ss, kMaxPassRows, (float)hidden / 3072.0f);   // rms ~ 1/sqrt(3072)
+  k_fill_value<<<64, 256>>>(ss, (size_t)kMaxPassRows * ss_tiles, (float)hidden / 3072.0f / ss_tiles);
+  k_fill_value<<<64, 256>>>(reinterpret_cast<float*>(rope), (size_t)kCap * kHd, 0.5f);
   k_fill_value<<<64, 256>>>(x, (size_t)kMaxRows * out_cols, 0.5f);
   k_fill_value<<<64, 256>>>(g, out_cols, 1.0f);
   CHECK(hipGetLastError());
@@ -97,15 +114,21 @@ int main(int argc, char** argv) {
   hd.n_seq = 1;
   hd.seq[0].n_rows = rows;
   hd.seq[0].n_real = rows;
+  for (int r = 0; r < rows; ++r) {
+    hd.pos[r] = kPos0 + r;
+    hd.slot[r] = 0;
+  }
   CHECK(hipMemcpy(desc, &hd, sizeof hd, hipMemcpyHostToDevice));
 
   GemmArgs a{};
   a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = n_strips / S;
   a.ksplit = P; a.kb_split = kb_split; a.part = part; a.counters = counters;
   a.A = A; a.lda = hidden; a.act_rows = kMaxRows; a.desc = desc;
-  a.ss_in = ss; a.ss_tiles = 1; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
+  a.ss_in = ss; a.ss_tiles = ss_tiles; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
   a.out = out; a.ld_out = out_cols;
   a.x = x; a.ldx = out_cols; a.g_next = g; a.xg = out; a.ss_out = ss_out;
+  a.kc = kc; a.vc = vc; a.cap = kCap; a.kv_seq_stride = (size_t)kv_dim * kCap; a.rope = rope;
+  a.q_dim = q_dim; a.kv_dim = kv_dim; a.hd = kHd;
 
   hipEvent_t e0, e1;
   CHECK(hipEventCreate(&e0));
@@ -126,7 +149,7 @@ int main(int argc, char** argv) {
   CHECK(hipEventElapsedTime(&ms, e0, e1));
   const double us = ms * 1e3 / n;
   printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups, %d weight copies: "
-         "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : "swiglu", n_strips, kb_total, rows,
+         "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : qkv ? "qkv" : "swiglu", n_strips, kb_total, rows,
          n_strips / S, P, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
   if (check) {
     // unsplit reference and split launch per copy, x reset before each (the
@@ -164,5 +187,6 @@ int main(int argc, char** argv) {
   }
   CHECK(hipFree(W)); CHECK(hipFree(A)); CHECK(hipFree(out)); CHECK(hipFree(ss)); CHECK(hipFree(x));
   CHECK(hipFree(g)); CHECK(hipFree(ss_out)); CHECK(hipFree(part)); CHECK(hipFree(counters)); CHECK(hipFree(desc));
+  CHECK(hipFree(kc)); CHECK(hipFree(vc)); CHECK(hipFree(rope));
   return 0;
 }

@@ -517,10 +517,10 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
   // attention plan: one workgroup per (sequence, KV head, query group, key
   // chunk); a query group holds every (row, head) pair of the KV head for
-  // decode passes (up to 48 / 64 pairs); chunks of kAttnChunk keys start at
-  // fixed multiples whatever the pass, so a query's result does not depend on
-  // the other rows of its pass (only very long prefill chunks, with many query
-  // groups, use longer chunks to bound the partial records)
+  // decode passes (up to 48 / 64 pairs); chunks start at fixed multiples of
+  // the chunk length, which depends only on the pass's shape and context
+  // bound, never on its rows' contents (kAttnChunk keys; decode passes over
+  // long contexts and very long prefill chunks use longer ones)
   const int seq_rows = ps.max_seq_rows > 0 ? std::min(ps.max_seq_rows, ps.max_rows) : ps.max_rows;
   const int qpairs = seq_rows * M.group;
   const int l_bound = std::min(std::max(ps.l_bound, 1), c->kv_cap);
@@ -534,6 +534,13 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   if (ps.n_seq * n_qblocks > kAttnRecords)
     return fail(c, PARD_ERR_CAPACITY, "attention plan: %d query blocks exceed the record budget", ps.n_seq * n_qblocks);
   int split_len = wide ? ceil_div(l_bound, 128) * 128 : kAttnChunk;
+  // decode passes over long contexts: chunks double while the grid holds more
+  // than one workgroup per CU (16k keys, 8B/1B step: 5.33 ms with 256-key
+  // chunks, 5.08 with 512, 5.05 with 1024)
+  if (!rows && !wide)
+    while (split_len < kAttnLongChunkMax &&
+           (int64_t)ps.n_seq * s.n_kv_heads * n_qblocks * ceil_div(l_bound, split_len) > kAttnDecodeWGs)
+      split_len *= 2;
   while ((int64_t)ps.n_seq * n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
   const int n_splits = ceil_div(l_bound, split_len);
   for (int l = 0; l < s.n_layers; ++l) {

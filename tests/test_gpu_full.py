@@ -11,6 +11,9 @@
   granular calls token for token, bitwise determinism of both models' logits.
 * 16k-token context: the attention chunk/merge path at the long-context
   workload's length, on a narrow pair the oracle can follow.
+* Long key chunks: one-layer targets with as many KV heads as query heads, at
+  contexts where 256-key chunks would give the decode pass's attention more
+  than one workgroup per CU, so the plan takes 512- and 1024-key chunks.
 """
 from dataclasses import replace
 
@@ -139,6 +142,30 @@ def test_16k_context_chunked_attention_lockstep(B):
     try:
         say(f"[gpu] {n}-token context: lock-step K=8")
         worst = lockstep(eng, target, draft, prompt, 8, steps=2, mask_id=wl.mask_id, tag="16k")
+        say(f"    max |logit err| {worst:.3g}")
+    finally:
+        eng.close()
+
+
+@pytest.mark.parametrize("heads,hd,ctx,chunk", [(16, 128, 4200, 512), (32, 64, 4200, 1024)])
+def test_long_key_chunks_lockstep(B, heads, hd, ctx, chunk):
+    wl = pi.WORKLOADS["tiny"]
+    t_spec = replace(pi.with_dtype(wl.target, "bf16"), n_layers=1, d_model=heads * hd, n_heads=heads,
+                     n_kv_heads=heads, head_dim=hd, ffn_dim=512)
+    d_spec = pi.with_dtype(wl.draft, "bf16")
+    # the plan's chunk for the verify pass: doubled from 256 while the grid
+    # (KV heads x chunks, one query group) exceeds 256 workgroups
+    n_chunks = lambda c: -(-(ctx + 9) // c)
+    c = 256
+    while c < 1024 and heads * n_chunks(c) > 256:
+        c *= 2
+    assert c == chunk
+    prompt = [int(x) for x in pi.gen_prompt(23, t_spec.vocab, ctx)]
+    say(f"[gpu] {heads}x{hd} KV heads, {ctx}-token context ({chunk}-key chunks): oracle build")
+    target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=ctx + 64, max_k=8)
+    try:
+        worst = lockstep(eng, target, draft, prompt, 8, steps=2, mask_id=wl.mask_id, tag=f"chunk{chunk}")
         say(f"    max |logit err| {worst:.3g}")
     finally:
         eng.close()

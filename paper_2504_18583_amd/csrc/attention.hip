@@ -7,8 +7,9 @@
 // A workgroup serves one sequence of the pass, one KV head, one group of 16*NQ
 // (row, head-in-group) query pairs -- for decode passes every pair of the KV
 // head, so each key is read once per pass -- and one chunk of split_len keys
-// (256 keys, two 32-key tiles per wavefront; up to 1024 for decode passes over
-// long contexts, so that their grid stays near one workgroup per CU).  Its four wavefronts take the
+// (256 keys, two 32-key tiles per wavefront; decode passes over long contexts
+// take longer chunks, multiples of 128 keys, so that their grid stays within
+// one workgroup per CU).  Its four wavefronts take the
 // chunk's tiles round-robin; per tile a wavefront computes
 //   S^T[key][q] = K[key] . Q[q]          (v_mfma_f32_16x16x32_f16, K as A,
 //                                          Q as B, accumulated over head_dim)

@@ -534,13 +534,13 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   if (ps.n_seq * n_qblocks > kAttnRecords)
     return fail(c, PARD_ERR_CAPACITY, "attention plan: %d query blocks exceed the record budget", ps.n_seq * n_qblocks);
   int split_len = wide ? ceil_div(l_bound, 128) * 128 : kAttnChunk;
-  // decode passes over long contexts: chunks double while the grid holds more
-  // than one workgroup per CU (16k keys, 8B/1B step: 5.33 ms with 256-key
-  // chunks, 5.08 with 512, 5.05 with 1024)
-  if (!rows && !wide)
-    while (split_len < kAttnLongChunkMax &&
-           (int64_t)ps.n_seq * s.n_kv_heads * n_qblocks * ceil_div(l_bound, split_len) > kAttnDecodeWGs)
-      split_len *= 2;
+  // decode passes over long contexts: the shortest chunk (a multiple of 128
+  // keys) that keeps the grid within one workgroup per CU (16k keys, 8B/1B
+  // step: 5.33 ms with 256-key chunks, 5.06 with 1024, 4.91 with 640)
+  if (!rows && !wide) {
+    const int per = std::max(1, kAttnDecodeWGs / (ps.n_seq * s.n_kv_heads * n_qblocks));
+    split_len = std::min(kAttnLongChunkMax, std::max(split_len, ceil_div(ceil_div(l_bound, per), 128) * 128));
+  }
   while ((int64_t)ps.n_seq * n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
   const int n_splits = ceil_div(l_bound, split_len);
   for (int l = 0; l < s.n_layers; ++l) {

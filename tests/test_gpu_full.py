@@ -13,7 +13,9 @@
   workload's length, on a narrow pair the oracle can follow.
 * Long key chunks: one-layer targets with as many KV heads as query heads, at
   contexts where 256-key chunks would give the decode pass's attention more
-  than one workgroup per CU, so the plan takes 512- and 1024-key chunks.
+  than one workgroup per CU, so the plan takes longer chunks (384 and 640
+  keys here: not powers of two, several tiles per wavefront, a ragged last
+  chunk).
 """
 from dataclasses import replace
 
@@ -147,19 +149,16 @@ def test_16k_context_chunked_attention_lockstep(B):
         eng.close()
 
 
-@pytest.mark.parametrize("heads,hd,ctx,chunk", [(16, 128, 4200, 512), (32, 64, 4200, 1024)])
+@pytest.mark.parametrize("heads,hd,ctx,chunk", [(16, 128, 4200, 384), (32, 64, 4200, 640)])
 def test_long_key_chunks_lockstep(B, heads, hd, ctx, chunk):
     wl = pi.WORKLOADS["tiny"]
     t_spec = replace(pi.with_dtype(wl.target, "bf16"), n_layers=1, d_model=heads * hd, n_heads=heads,
                      n_kv_heads=heads, head_dim=hd, ffn_dim=512)
     d_spec = pi.with_dtype(wl.draft, "bf16")
-    # the plan's chunk for the verify pass: doubled from 256 while the grid
-    # (KV heads x chunks, one query group) exceeds 256 workgroups
-    n_chunks = lambda c: -(-(ctx + 9) // c)
-    c = 256
-    while c < 1024 and heads * n_chunks(c) > 256:
-        c *= 2
-    assert c == chunk
+    # the plan's chunk for the verify pass: the shortest multiple of 128 keys
+    # that keeps KV heads x chunks (one query group) within 256 workgroups
+    per = 256 // heads
+    assert chunk == -(-(-(-(ctx + 9) // per)) // 128) * 128 and heads * -(-(ctx + 9) // chunk) <= 256
     prompt = [int(x) for x in pi.gen_prompt(23, t_spec.vocab, ctx)]
     say(f"[gpu] {heads}x{hd} KV heads, {ctx}-token context ({chunk}-key chunks): oracle build")
     target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)

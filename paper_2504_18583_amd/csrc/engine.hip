@@ -66,6 +66,15 @@ struct GemmPlan {
 
 int pick_S(int epi, int n_strips, int mt) {
   if (epi == EPI_SWIGLU && mt == 1) {
+    // one workgroup per CU when 7-10 strips each fill at least 7/8 of the
+    // CUs in one round (from 8 strips on, the last workgroup may hold fewer):
+    // every activation row is then read once per CU (Qwen2.5-7B shape, 2368
+    // strips x 112 k-blocks: 43.5 us at 10 strips per workgroup against 57.1
+    // at 2, 50.0 at 4, 56.0 at 8 and 60.5 at 9, which take two rounds)
+    for (int s : {7, 8, 9, 10}) {
+      const int tiles = ceil_div(n_strips, s);
+      if ((s >= 8 || n_strips % s == 0) && tiles <= 256 && tiles >= 224) return s;
+    }
     // the strips-per-workgroup count that divides the strips and fills the 256
     // CUs most evenly; among equally even ones, the one closest to two rounds
     // of workgroups (measured: 8B shape 7 strips = one workgroup per CU, 41 us,
@@ -489,7 +498,7 @@ hipError_t run_gemm(pard_ctx* c, int cls, int epi, int max_rows, int typ_rows, G
   }
   const int mt = ceil_div(max_rows, 16);
   const int S = pick_S(epi, p.n_strips, mt);
-  a.n_tiles = p.n_strips / S;
+  a.n_tiles = ceil_div(p.n_strips, S);
   a.ksplit = p.ksplit;
   a.kb_split = ceil_div(p.kb_total, p.ksplit);
   a.part = c->rows_part;

@@ -122,7 +122,12 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   // arithmetic (which would otherwise force waits on in-flight loads), and
   // every access is bounds-checked by the hardware.
   // W is k-block-major: block (kb, strip) sits at (kb * n_strips + strip) KiB.
-  const int n_strips = p.n_tiles * S;
+  // A gate/up workgroup of 8 or more strips may be the grid's last, with
+  // fewer strips than S (ragged): its missing strips re-read its last strip
+  // (cache hits) and store nothing.
+  constexpr bool RAGGED = EPI == EPI_SWIGLU && MT == 1 && S >= 8;
+  const int n_strips = p.n_strips;
+  const int s_last = RAGGED ? min(S - 1, n_strips - 1 - tile * S) : S - 1;
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.W), 0, (int)min((size_t)n_strips * p.kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
   const int w_voff = (tile * S * 64 + lane) * 16;
@@ -137,7 +142,8 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       const int kb = kb0 + wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
       for (int s = 0; s < S; ++s)
-        w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
+        w[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + (RAGGED ? min(s, s_last) : s)) * 1024,
+                                                        kCachePolicyNT);
     }
   };
 
@@ -217,7 +223,8 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
     const int kb = kb0 + min(wave + min(u, max(n_it - 1, 0)) * nw, kb_n - 1);
 #pragma unroll
     for (int s = 0; s < S; ++s)
-      w0[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + s) * 1024, kCachePolicyNT);
+      w0[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + (RAGGED ? min(s, s_last) : s)) * 1024,
+                                                       kCachePolicyNT);
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -475,7 +482,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         const float up = __shfl_xor(gt, 8);
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * S + s) * 8 + csub;
-        if (csub < 8 && row < row_count) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
+        if (csub < 8 && row < row_count && s <= s_last) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
       }
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;
@@ -1450,7 +1457,9 @@ hipError_t launch_s(int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEven
     case 2: return launch_one<EPI, MT, 2>(nw, a, st, ev);
     case 4: if constexpr (MT <= 2) return launch_one<EPI, MT, 4>(nw, a, st, ev); break;
     case 7: if constexpr (MT == 1 && EPI == EPI_SWIGLU) return launch_one<EPI, MT, 7>(nw, a, st, ev); break;
-    case 8: if constexpr (MT == 1 && EPI == EPI_LOGITS) return launch_one<EPI, MT, 8>(nw, a, st, ev); break;
+    case 8: if constexpr (MT == 1 && (EPI == EPI_LOGITS || EPI == EPI_SWIGLU)) return launch_one<EPI, MT, 8>(nw, a, st, ev); break;
+    case 9: if constexpr (MT == 1 && EPI == EPI_SWIGLU) return launch_one<EPI, MT, 9>(nw, a, st, ev); break;
+    case 10: if constexpr (MT == 1 && EPI == EPI_SWIGLU) return launch_one<EPI, MT, 10>(nw, a, st, ev); break;
   }
   return hipErrorInvalidValue;
 }
@@ -1469,7 +1478,11 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, L
 }  // namespace
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
-  if (nw < 4 || nw > 8 || (size_t)nw * S * mt * 1024 > 32 * 1024) return hipErrorInvalidValue;
+  if (nw < 4 || nw > 8 || S < 1 || (size_t)nw * S * mt * 1024 > 64 * 1024) return hipErrorInvalidValue;
+  // the tiles cover the strips; only gate/up workgroups of 8+ strips may be ragged
+  if (a.n_tiles < 1 || (size_t)a.n_tiles * S < (size_t)a.n_strips || (size_t)(a.n_tiles - 1) * S >= (size_t)a.n_strips)
+    return hipErrorInvalidValue;
+  if (a.n_tiles * S != a.n_strips && !(epi == EPI_SWIGLU && mt == 1 && S >= 8)) return hipErrorInvalidValue;
   // split input: every range non-empty, partial tiles and counters supplied
   if (a.ksplit < 1 || a.kb_split < 1 || (a.ksplit - 1) * a.kb_split >= a.kb_total ||
       a.ksplit * a.kb_split < a.kb_total)

@@ -67,11 +67,12 @@ int main(int argc, char** argv) {
   const int epi = resid ? EPI_RESID : qkv ? EPI_QKV : EPI_SWIGLU;
   constexpr int kHd = 128, kCap = 1024, kPos0 = 512;
   const int kb_split = P > 0 ? (kb_total + P - 1) / P : 0;
-  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || (S == 7 && epi == EPI_SWIGLU)) ||
-      n_strips < 1 || n_strips % S != 0 || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 ||
+  const bool wide_s = epi == EPI_SWIGLU && S >= 7 && S <= 10;
+  if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || wide_s) ||
+      n_strips < 1 || (n_strips % S != 0 && S < 8) || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 ||
       copies > 64 || (size_t)n_strips * kb_total * 1024 * copies > ((size_t)8 << 30) || ss_tiles < 1 ||
       ss_tiles > n_strips || (qkv && ((n_strips * 16) % (6 * kHd) != 0 || check))) {
-    fprintf(stderr, "bad shape: rows 1..%d, S in {1, 2, 4, 7 (swiglu)}, S | strips, every input range non-empty, "
+    fprintf(stderr, "bad shape: rows 1..%d, S in {1, 2, 4, 7-10 (swiglu)}, S | strips (S < 8), every input range non-empty, "
             "copies 1..64 of at most 8 GiB in all, 1 <= ss_tiles <= strips; qkv: 6 x 128 | columns, no check\n",
             kMaxRows);
     return 2;
@@ -121,7 +122,7 @@ int main(int argc, char** argv) {
   CHECK(hipMemcpy(desc, &hd, sizeof hd, hipMemcpyHostToDevice));
 
   GemmArgs a{};
-  a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = n_strips / S;
+  a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = (n_strips + S - 1) / S;
   a.ksplit = P; a.kb_split = kb_split; a.part = part; a.counters = counters;
   a.A = A; a.lda = hidden; a.act_rows = kMaxRows; a.desc = desc;
   a.ss_in = ss; a.ss_tiles = ss_tiles; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
@@ -150,7 +151,7 @@ int main(int argc, char** argv) {
   const double us = ms * 1e3 / n;
   printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups, %d weight copies: "
          "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : qkv ? "qkv" : "swiglu", n_strips, kb_total, rows,
-         n_strips / S, P, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
+         a.n_tiles, P, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
   if (check) {
     // unsplit reference and split launch per copy, x reset before each (the
     // residual epilogue updates it in place); outputs compared as fp16

@@ -65,21 +65,25 @@ struct GemmPlan {
 };
 
 int pick_S(int epi, int n_strips, int mt) {
-  if (epi == EPI_SWIGLU && mt == 1) {
-    // one workgroup per CU when 7-10 strips each fill at least 7/8 of the
-    // CUs in one round (from 8 strips on, the last workgroup may hold fewer):
-    // every activation row is then read once per CU (Qwen2.5-7B shape, 2368
-    // strips x 112 k-blocks: 43.5 us at 10 strips per workgroup against 57.1
-    // at 2, 50.0 at 4, 56.0 at 8 and 60.5 at 9, which take two rounds)
-    for (int s : {7, 8, 9, 10}) {
-      const int tiles = ceil_div(n_strips, s);
-      if ((s >= 8 || n_strips % s == 0) && tiles <= 256 && tiles >= 224) return s;
+  if (mt == 1 && epi != EPI_LOGITS) {
+    // decode rows: the fewest strips per workgroup that cover the weight in
+    // one round of at most 256 workgroups (one per CU), so each CU reads the
+    // activation rows once; from 8 strips on the last workgroup may hold
+    // fewer.  Measured (gemm_counters, 9 rows): gate/up 8B 1792 strips 7 per
+    // workgroup, 37.7 us (54 at 1); Qwen2.5-7B 2368 strips 10, 43.5 us
+    // against 57.1 at 2, 50.0 at 4, 56.0 at 8 and 60.5 at 9; 1B 1024 strips
+    // 4, 13.7 us against 14.7 at 2 and 19.7 at 1; Qwen2.5-0.5B 608 strips 4,
+    // 7.2 us against 8.1 at 2 and 9.3 at 1; QKV 8B 384 strips 2 (12.4 us
+    // against 14.1 at 1), Qwen2.5-7B 288 strips 2 (12.2 against 14.8).
+    for (int s : {1, 2, 4, 7, 8, 9, 10}) {
+      if (s >= 7 && epi != EPI_SWIGLU) break;
+      if ((s >= 8 || n_strips % s == 0) && ceil_div(n_strips, s) <= 256) return s;
     }
-    // the strips-per-workgroup count that divides the strips and fills the 256
-    // CUs most evenly; among equally even ones, the one closest to two rounds
-    // of workgroups (measured: 8B shape 7 strips = one workgroup per CU, 41 us,
-    // against 54 us at 1 strip; 1B shape 2 strips, two rounds, slightly ahead
-    // of 4 strips)
+  }
+  if (epi == EPI_SWIGLU && mt == 1) {
+    // wider weights: the strips-per-workgroup count that divides the strips
+    // and fills the 256 CUs most evenly; among equally even ones, the one
+    // closest to two rounds of workgroups
     int best = 1, best_d = 1 << 30;
     double best_u = 0.0;
     for (int s : {7, 4, 2, 1}) {
@@ -97,7 +101,7 @@ int pick_S(int epi, int n_strips, int mt) {
   }
   int s = 1;
   // two strips share one activation stream once that still leaves >= 192
-  // workgroups (measured faster for the 8B QKV shape: 384 strips)
+  // workgroups
   if ((epi == EPI_QKV || epi == EPI_RESID) && n_strips >= 384) s = 2;
   if (epi == EPI_SWIGLU) s = 2;
   if (epi == EPI_LOGITS) s = (mt == 1) ? kLmStrips : 2;

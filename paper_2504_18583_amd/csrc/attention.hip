@@ -359,9 +359,90 @@ __global__ __launch_bounds__(64 * NW) void k_attn(const AttnArgs p) {
   }
 }
 
-// Combine the key chunks of k_attn.  One workgroup per (KV head, query group,
-// sequence, 16 output vectors of 8 dims), so long contexts with many chunks
-// still spread over many workgroups.  The chunks are dealt round-robin over
+// Combine a few key chunks of k_attn (passes with many sequences or query
+// groups and short contexts) in chunk order.  Grid (kv head, query group,
+// sequence x kMergeParts): per-query (max, sum) first, then each thread merges
+// 8 consecutive dims of one pair with the loads of 4 chunks in flight at a
+// time.
+constexpr int kMergeParts = 8;
+
+template <int HD, int NQ>
+__global__ __launch_bounds__(256) void k_attn_merge_few(const AttnArgs p) {
+  constexpr int QP = 16 * NQ;
+  constexpr int REC = QP * HD + 2 * QP;
+  __shared__ float Ms[QP], Linv[QP];
+  const int kvh = blockIdx.x, qg = blockIdx.y, tid = threadIdx.x;
+  const int sj = blockIdx.z / kMergeParts, part = blockIdx.z % kMergeParts;
+  const int group = p.n_heads / p.n_kv;
+  if (sj >= p.desc->n_seq) return;                 // uniform
+  const PassSeq d = p.desc->seq[sj];
+  const int L_end = d.pos0 + d.n_rows;
+  const int n_qh = d.n_rows * group;
+  if (qg * QP >= n_qh) return;                     // uniform
+  const int n_act = min(p.n_splits, (L_end + p.split_len - 1) / p.split_len);
+  const float* base = p.part + ((size_t)(sj * p.n_kv + kvh) * p.n_qblocks + qg) * p.n_splits * REC;
+  if (tid < QP) {
+    // the (m, l) of up to 8 chunks are requested together
+    float mv[8], lv[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int sx = min(u, n_act - 1);
+      mv[u] = base[(size_t)sx * REC + QP * HD + tid];
+      lv[u] = base[(size_t)sx * REC + QP * HD + QP + tid];
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n_act) M = fmaxf(M, mv[u]);
+    for (int s = 8; s < n_act; ++s) M = fmaxf(M, base[(size_t)s * REC + QP * HD + tid]);
+    const float M_use = M == -INFINITY ? 0.f : M;
+    float L = 0.f;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (u < n_act) L += lv[u] * __builtin_amdgcn_exp2f(mv[u] - M_use);
+    for (int s = 8; s < n_act; ++s)
+      L += base[(size_t)s * REC + QP * HD + QP + tid] *
+           __builtin_amdgcn_exp2f(base[(size_t)s * REC + QP * HD + tid] - M_use);
+    Ms[tid] = M_use;
+    Linv[tid] = 1.0f / L;
+  }
+  __syncthreads();
+  constexpr int NV = QP * HD / 8;                  // 8-dim vectors of the group
+  constexpr int PER = (NV + kMergeParts - 1) / kMergeParts;
+  for (int e = part * PER + tid; e < min(NV, (part + 1) * PER); e += 256) {
+    const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
+    const int qh = qg * QP + q;
+    if (qh >= n_qh) continue;
+    const float M = Ms[q];
+    f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, b = a;
+    for (int s0 = 0; s0 < n_act; s0 += 4) {
+      f32x4 va[4], vb[4];
+      float mv[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int sx = min(s0 + u, n_act - 1);
+        const float* r = base + (size_t)sx * REC;
+        va[u] = *reinterpret_cast<const f32x4*>(r + q * HD + d0);
+        vb[u] = *reinterpret_cast<const f32x4*>(r + q * HD + d0 + 4);
+        mv[u] = r[QP * HD + q];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (s0 + u < n_act) {
+          const float sc = __builtin_amdgcn_exp2f(mv[u] - M);
+          a += va[u] * sc;
+          b += vb[u] * sc;
+        }
+    }
+    const int row = qh / group, head = kvh * group + qh % group;
+    store_f16x8(p.out + act_index(d.row0 + row, head * HD + d0, p.act_rows), a * Linv[q], b * Linv[q]);
+  }
+}
+
+// Combine many key chunks of k_attn (long contexts).  One workgroup per (KV
+// head, query group, sequence, 16 output vectors of 8 dims), so that the
+// chunks spread over many workgroups and lanes.  (With few chunks its many
+// small workgroups cost more than they save: batch-32 step 15.8 -> 16.7 ms.)  The chunks are dealt round-robin over
 // lanes, every lane folds its chunks in chunk order with all of its loads in
 // flight together, and lanes are combined in a fixed tree order: the result
 // is deterministic and no lane waits on more than one round of loads for
@@ -371,6 +452,7 @@ __global__ __launch_bounds__(64 * NW) void k_attn(const AttnArgs p) {
 //       shuffles, then the wavefronts in order);
 //   (2) per output vector: 16 lanes add o_chunk * 2^(m_chunk - M), then a
 //       shuffle tree; lane 0 stores o / L.
+constexpr int kMergeFewChunks = 16;   // up to this many chunks: k_attn_merge_few
 constexpr int kMergeVecs = 16;     // 8-dim output vectors per workgroup
 constexpr int kMergeLanes = 16;    // lanes (chunk subsets) per vector
 
@@ -497,7 +579,10 @@ hipError_t launch_hd_nq(const AttnArgs& a, hipStream_t st) {
   k_attn<HD, NQ, kAttnWaves><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * a.n_splits), dim3(64 * kAttnWaves), 0, st>>>(a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.n_splits == 1) return e;
-  k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * merge_parts<HD, NQ>()), dim3(256), 0, st>>>(a);
+  if (a.n_splits <= kMergeFewChunks)
+    k_attn_merge_few<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * kMergeParts), dim3(256), 0, st>>>(a);
+  else
+    k_attn_merge<HD, NQ><<<dim3(a.n_kv, a.n_qblocks, a.n_seq * merge_parts<HD, NQ>()), dim3(256), 0, st>>>(a);
   return hipGetLastError();
 }
 

@@ -11,11 +11,12 @@
   granular calls token for token, bitwise determinism of both models' logits.
 * 16k-token context: the attention chunk/merge path at the long-context
   workload's length, on a narrow pair the oracle can follow.
-* Long key chunks: one-layer targets with as many KV heads as query heads, at
-  contexts where 256-key chunks would give the decode pass's attention more
-  than one workgroup per CU, so the plan takes longer chunks (384 and 640
-  keys here: not powers of two, several tiles per wavefront, a ragged last
-  chunk).
+* Long-context plans: one-layer targets with as many KV heads as query heads,
+  at contexts where 256-key chunks would give the decode pass's attention
+  more than one workgroup per CU, so the plan takes longer chunks (384 and
+  640 keys here: not powers of two, several tiles per wavefront, a ragged
+  last chunk); and a head_dim-128 case with more than 16 chunks, which the
+  many-chunk merge combines (the 16k test covers it at head_dim 64).
 """
 from dataclasses import replace
 
@@ -149,7 +150,7 @@ def test_16k_context_chunked_attention_lockstep(B):
         eng.close()
 
 
-@pytest.mark.parametrize("heads,hd,ctx,chunk", [(16, 128, 4200, 384), (32, 64, 4200, 640)])
+@pytest.mark.parametrize("heads,hd,ctx,chunk", [(16, 128, 4200, 384), (32, 64, 4200, 640), (8, 128, 4200, 256)])
 def test_long_key_chunks_lockstep(B, heads, hd, ctx, chunk):
     wl = pi.WORKLOADS["tiny"]
     t_spec = replace(pi.with_dtype(wl.target, "bf16"), n_layers=1, d_model=heads * hd, n_heads=heads,
@@ -158,7 +159,9 @@ def test_long_key_chunks_lockstep(B, heads, hd, ctx, chunk):
     # the plan's chunk for the verify pass: the shortest multiple of 128 keys
     # that keeps KV heads x chunks (one query group) within 256 workgroups
     per = 256 // heads
-    assert chunk == -(-(-(-(ctx + 9) // per)) // 128) * 128 and heads * -(-(ctx + 9) // chunk) <= 256
+    assert chunk == max(256, -(-(-(-(ctx + 9) // per)) // 128) * 128) and heads * -(-(ctx + 9) // chunk) <= 256
+    if chunk == 256:
+        assert -(-(ctx + 9) // chunk) > 16          # the many-chunk merge
     prompt = [int(x) for x in pi.gen_prompt(23, t_spec.vocab, ctx)]
     say(f"[gpu] {heads}x{hd} KV heads, {ctx}-token context ({chunk}-key chunks): oracle build")
     target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)

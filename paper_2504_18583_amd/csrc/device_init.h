@@ -28,7 +28,7 @@ struct RopeScaling {
 };
 hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const RopeScaling& sc, hipStream_t st);
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
-                        uint16_t* xg, int act_rows, float* ss, int max_rows, hipStream_t st);
+                        uint16_t* xg, int act_rows, float* ss, int ss_stride, int max_rows, hipStream_t st);
 hipError_t launch_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out, hipStream_t st);
 
 }  // namespace pard

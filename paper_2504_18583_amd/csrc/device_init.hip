@@ -154,7 +154,8 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta, RopeSca
 // x[r, :] = E[ids[r], :] (fp32) from the strip-packed embedding, plus the
 // first normalised GEMM's operand xg = fp16(x * g) and the row's sum of squares.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc,
-                                               float* x, const float* g, uint16_t* xg, int act_rows, float* ss) {
+                                               float* x, const float* g, uint16_t* xg, int act_rows, float* ss,
+                                               int ss_stride) {
   __shared__ float wsum[4];
   const int r = blockIdx.x;
   if (r >= desc->n_rows) return;
@@ -184,7 +185,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
   for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
   __syncthreads();
-  if (threadIdx.x == 0) ss[r] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
+  if (threadIdx.x == 0) ss[(size_t)r * ss_stride] = ((wsum[0] + wsum[1]) + wsum[2]) + wsum[3];
 }
 
 __global__ void k_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out) {
@@ -227,8 +228,8 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const R
 }
 
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
-                        uint16_t* xg, int act_rows, float* ss, int max_rows, hipStream_t st) {
-  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss);
+                        uint16_t* xg, int act_rows, float* ss, int ss_stride, int max_rows, hipStream_t st) {
+  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss, ss_stride);
   return hipGetLastError();
 }
 

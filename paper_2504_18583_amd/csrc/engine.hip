@@ -65,6 +65,12 @@ struct GemmPlan {
 };
 
 int pick_S(int epi, int n_strips, int mt) {
+  if (epi == EPI_RESID) {
+    // residual GEMMs also write the per-tile row sums that the next
+    // normalised GEMM adds up, so their tile count must not depend on the
+    // pass: one strip per workgroup up to 256 strips (one round), two beyond
+    return (n_strips > 256 && n_strips % 2 == 0) ? 2 : 1;
+  }
   if (mt == 1 && epi != EPI_LOGITS) {
     // decode rows: the fewest strips per workgroup that cover the weight in
     // one round of at most 256 workgroups (one per CU), so each CU reads the
@@ -102,7 +108,7 @@ int pick_S(int epi, int n_strips, int mt) {
   int s = 1;
   // two strips share one activation stream once that still leaves >= 192
   // workgroups
-  if ((epi == EPI_QKV || epi == EPI_RESID) && n_strips >= 384) s = 2;
+  if (epi == EPI_QKV && n_strips >= 384) s = 2;
   if (epi == EPI_SWIGLU) s = 2;
   if (epi == EPI_LOGITS) s = (mt == 1) ? kLmStrips : 2;
   while (s > 1 && n_strips % s) s >>= 1;
@@ -173,7 +179,7 @@ struct ModelDev {
   float2* rope = nullptr;
   float* x = nullptr;                 // residual stream, fp32 [kMaxPassRows][d]
   uint16_t* xg = nullptr;             // x * g of the next normalised GEMM (fp16, k-blocked)
-  float* ss = nullptr;                // per-tile row sums of squares of x [tiles][kMaxPassRows]
+  float* ss = nullptr;                // per-tile row sums of squares of x [kMaxPassRows][ss_tiles_max]
   int ss_tiles_max = 1;               // ss buffer tiles
   uint16_t *q = nullptr, *attn = nullptr, *h = nullptr;
   float* logits = nullptr;            // lm rows of the last pass [kMaxLmRows][vocab]
@@ -464,6 +470,7 @@ GemmArgs gemm_base(const ModelDev& M, const uint16_t* W, int act_rows) {
   a.desc = M.desc;
   a.eps = M.spec.rms_eps;
   a.inv_k = 1.0f / (float)M.d;
+  a.ss_stride = std::max(1, M.ss_tiles_max);
   return a;
 }
 
@@ -525,7 +532,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   {
     Timed t(c, cls0 + 0);
     HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, act_rows, M.ss,
-                            ps.max_rows, c->stream));
+                            std::max(1, M.ss_tiles_max), ps.max_rows, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
   // attention plan: one workgroup per (sequence, KV head, query group, key

@@ -163,7 +163,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       // unconditional loads (a tile index past the end re-reads the last
       // tile and is dropped when summed), so none waits behind a branch
       const int q = (tid & 15) + 16 * u;
-      ss_part[u] = p.ss_in[(size_t)min(q, p.ss_tiles - 1) * kMaxPassRows + row];
+      ss_part[u] = p.ss_in[(size_t)row * p.ss_stride + min(q, p.ss_tiles - 1)];
     }
   };
   auto ss_finish = [&](int row) {
@@ -175,7 +175,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int q = q0 + 16 * u;
-        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
+        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) t += part[u];
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
           for (int u = 0; u < 16; ++u) {
             const int q = q0 + 16 * u;
-            part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
+            part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
           }
 #pragma unroll
           for (int u = 0; u < 16; ++u) t += part[u];
@@ -467,7 +467,7 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       const float t = sum16(sq[mt]);
-      if (csub == 0) p.ss_out[(size_t)tile * kMaxPassRows + mt * 16 + rsub] = t;
+      if (csub == 0) p.ss_out[(size_t)(mt * 16 + rsub) * p.ss_stride + tile] = t;
     }
   } else if constexpr (EPI == EPI_SWIGLU) {
     // a strip holds 8 gate columns then the 8 up columns of the same features:
@@ -1074,7 +1074,7 @@ __device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int q = q0 + 16 * u;
-        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)q * kMaxPassRows + row] : 0.f;
+        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) t += part[u];
@@ -1133,7 +1133,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
       }
     });
   } else if constexpr (EPI == EPI_RESID) {
-    float* ss = p.ss_out + (size_t)(tile * kRowsWaves + wave) * kMaxPassRows;
+    float* ss = p.ss_out + (tile * kRowsWaves + wave);
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
       constexpr int mt = decltype(mtc)::value;
       if (mt < mt_lo || mt >= mt_live) return;       // uniform
@@ -1159,7 +1159,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
       for (int i = 0; i < 4; ++i) {
         const float t = sum16(sq[i]);
         const int r = row0 + mt * 16 + g4 * 4 + i;
-        if (c16 == 0 && r < row_count) ss[r] = t;
+        if (c16 == 0 && r < row_count) ss[(size_t)r * p.ss_stride] = t;
       }
     });
   } else if constexpr (EPI == EPI_SWIGLU) {

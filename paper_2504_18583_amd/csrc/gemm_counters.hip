@@ -95,17 +95,18 @@ int main(int argc, char** argv) {
   CHECK(hipMalloc(&W, w_elems * 2 * copies));
   CHECK(hipMalloc(&A, a_elems * 2));
   CHECK(hipMalloc(&out, o_elems * 2));
-  CHECK(hipMalloc(&ss, sizeof(float) * kMaxPassRows * ss_tiles));
+  const int ss_stride = std::max(ss_tiles, (n_strips + S - 1) / S);   // [row][tile] sums, in and out
+  CHECK(hipMalloc(&ss, sizeof(float) * kMaxPassRows * ss_stride));
   CHECK(hipMalloc(&x, sizeof(float) * kMaxRows * out_cols));
   CHECK(hipMalloc(&g, sizeof(float) * out_cols));
-  CHECK(hipMalloc(&ss_out, sizeof(float) * (size_t)kMaxPassRows * n_strips));
+  CHECK(hipMalloc(&ss_out, sizeof(float) * (size_t)kMaxPassRows * ss_stride));
   CHECK(hipMalloc(&part, sizeof(float) * kSplitPartFloats));
   CHECK(hipMalloc(&counters, sizeof(int) * kSplitCounters));
   CHECK(hipMalloc(&desc, sizeof(FwdDesc)));
   CHECK(hipMemset(counters, 0, sizeof(int) * kSplitCounters));
   k_fill_f16<<<1024, 256>>>(W, w_elems * copies, 1u);
   k_fill_f16<<<64, 256>>>(A, a_elems, 2u);
-  k_fill_value<<<64, 256>>>(ss, (size_t)kMaxPassRows * ss_tiles, (float)hidden / 3072.0f / ss_tiles);
+  k_fill_value<<<64, 256>>>(ss, (size_t)kMaxPassRows * ss_stride, (float)hidden / 3072.0f / ss_tiles);
   k_fill_value<<<64, 256>>>(reinterpret_cast<float*>(rope), (size_t)kCap * kHd, 0.5f);
   k_fill_value<<<64, 256>>>(x, (size_t)kMaxRows * out_cols, 0.5f);
   k_fill_value<<<64, 256>>>(g, out_cols, 1.0f);
@@ -125,7 +126,7 @@ int main(int argc, char** argv) {
   a.kb_total = kb_total; a.n_strips = n_strips; a.n_tiles = (n_strips + S - 1) / S;
   a.ksplit = P; a.kb_split = kb_split; a.part = part; a.counters = counters;
   a.A = A; a.lda = hidden; a.act_rows = kMaxRows; a.desc = desc;
-  a.ss_in = ss; a.ss_tiles = ss_tiles; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
+  a.ss_in = ss; a.ss_tiles = ss_tiles; a.ss_stride = ss_stride; a.eps = 1e-5f; a.inv_k = 1.0f / hidden;
   a.out = out; a.ld_out = out_cols;
   a.x = x; a.ldx = out_cols; a.g_next = g; a.xg = out; a.ss_out = ss_out;
   a.kc = kc; a.vc = vc; a.cap = kCap; a.kv_seq_stride = (size_t)kv_dim * kCap; a.rope = rope;

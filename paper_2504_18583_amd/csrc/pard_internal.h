@@ -165,9 +165,10 @@ struct GemmArgs {
   // RMSNorm of the A operand (QKV, SWIGLU, LOGITS): A already holds x*g in
   // fp16; 1/rms comes from the producer's per-tile sums of squares.
   const float* ss_in; int ss_tiles;
+  int ss_stride;          // floats between two rows' tile sums ([row][tile] layout, in and out)
   float eps, inv_k;
   // EPI_RESID: x += Y, and for the next consumer xg = fp16(x * g_next) and
-  // per-tile sums of squares of x ([tile][kMaxPassRows]).
+  // per-tile sums of squares of x ([row][tile], ss_stride per row).
   float* x; int ldx;
   const float* g_next; uint16_t* xg; float* ss_out;
   // EPI_QKV / EPI_SWIGLU

@@ -28,7 +28,9 @@
 // prefix and the k-1 mask tokens before it).
 //
 // The wavefronts are merged in LDS in wave order.  With several chunks each
-// workgroup writes (o, m, l) and k_attn_merge combines them in a fixed order.
+// workgroup writes (o, m, l) and a merge kernel combines them in a fixed order
+// (k_attn_merge_few in chunk order for up to 16 chunks, k_attn_merge over lanes
+// for more).
 // All reductions have a fixed order, chunk boundaries sit at fixed multiples
 // of split_len and a query's arithmetic does not depend on which other pairs
 // share its workgroup: results are deterministic and a query's result does

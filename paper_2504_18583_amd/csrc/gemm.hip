@@ -5,7 +5,9 @@
 // Decode streams every weight once per forward (Sec. 2.1: decoding is bound by
 // reloading the weights), so the kernel is organised around the weight
 // stream.  A workgroup owns S strips (16 output columns each) over the whole
-// input dimension; its NW wavefronts split the input dimension, each one
+// input dimension (the grid's last gate/up workgroup of 8-10 strips may own
+// fewer, so that one round of workgroups covers the weight); its NW wavefronts
+// split the input dimension, each one
 // streaming its slice of the strips' 1 KiB blocks (one 16-byte load per lane,
 // directly in the 16x16x32 MFMA B-operand layout) through a double-buffered
 // register pipeline and accumulating MT 16x16 fp32 tiles.  Activation rows

@@ -123,6 +123,27 @@ def test_rope_scaled_pair_lockstep(B):
         e.close()
 
 
+@pytest.mark.parametrize("ffn,S", [(14368, 8), (16480, 9)])
+def test_wide_gate_up_ragged_last_workgroup_lockstep(B, ffn, S):
+    """Gate/up weights of 1796 and 2060 strips: too many for 7 strips per
+    workgroup in one round of 256 workgroups, so the plan takes 8 and 9 strips
+    per workgroup and the last workgroup holds 4 and 8 strips (the 10-strip
+    case runs in the Qwen full-width slices)."""
+    from dataclasses import replace
+    n_strips = 2 * ffn // 16
+    assert n_strips % 7 and -(-n_strips // 7) > 256 and -(-n_strips // S) <= 256 and n_strips % S
+    assert S == 8 or -(-n_strips // 8) > 256
+    t_spec = replace(T_SPEC, n_layers=1, ffn_dim=ffn)
+    target, draft = oracle.build_model(t_spec), oracle.build_model(D_SPEC)
+    e = B.Engine(t_spec, D_SPEC, WL.mask_id, max_ctx=512, max_k=8)
+    try:
+        say(f"[gpu] tiny: target ffn {ffn} ({n_strips} gate/up strips, {S} per workgroup), lock-step K=4")
+        worst = lockstep(e, target, draft, PROMPT, WL.k, steps=3, mask_id=WL.mask_id, tag=f"ffn{ffn}")
+        say(f"    max |logit err| {worst:.3g}")
+    finally:
+        e.close()
+
+
 def test_generate_matches_greedy(eng, models, B):
     say("[gpu] tiny: fused generate vs greedy")
     target, _ = models

@@ -129,37 +129,56 @@ __global__ __launch_bounds__(64 * NW) void k_attn(const AttnArgs p) {
 
   // K and V fragments of two tiles (a pair of tiles shares one softmax max)
   u32x4 kf[2][2][KS], vf[2][DB];
-  auto load = [&](int tt, int it) {
-    const int key0 = k_begin + (wave + NWA * min(it, n_my - 1)) * 32;   // in bounds: key0 + 31 < cap
+  // a wave with no tile of its own (n_my = 0) reads the chunk's first tile
+  // and never uses it; in bounds: key0 + 31 < cap
+  auto tile_key = [&](int it) { return k_begin + (n_my > 0 ? wave + NWA * min(it, n_my - 1) : 0) * 32; };
+  auto load_k = [&](int tt, int it) {
+    const int key0 = tile_key(it);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       const uint16_t* kp = kbase + ((size_t)((key0 >> 4) + kb) * KS * 64 + lane) * 8;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) kf[tt][kb][ks] = *reinterpret_cast<const u32x4*>(kp + ks * 64 * 8);
     }
+  };
+  auto load_v = [&](int tt, int it) {
+    const int key0 = tile_key(it);
     const uint16_t* vp = vbase + ((size_t)(key0 >> 5) * HD + c16) * 32 + g4 * 8;
 #pragma unroll
     for (int db = 0; db < DB; ++db) vf[tt][db] = *reinterpret_cast<const u32x4*>(vp + db * 16 * 32);
   };
+  auto load = [&](int tt, int it) {
+    load_k(tt, it);
+    load_v(tt, it);
+  };
 
   // stage the Q fragments: entry (t, ks, l) = pair t*16 + l%16, dims ks*32 + 8*(l/16) .. +7.
   // Their loads go out before the K/V loads (returns are in order per wavefront).
+  // All of these loads are unconditional (entries past the group re-read a
+  // valid one and are zeroed; a wave without tiles reads the chunk's first):
+  // a branch around any of them would make the wait for Q below also wait for
+  // every K/V load in flight.
   constexpr int QE = (NQ * KS * 64 + 64 * NWA - 1) / (64 * NWA);   // entries per thread
   u32x4 qv[QE];
 #pragma unroll
   for (int j = 0; j < QE; ++j) {
     const int e = tid + j * 64 * NWA;
-    const int t = e / (KS * 64), ks = (e / 64) % KS, l = e & 63;
+    const int ec = min(e, NQ * KS * 64 - 1);
+    const int t = ec / (KS * 64), ks = (ec / 64) % KS, l = ec & 63;
     const int qh = qg * QP + t * 16 + (l & 15);
-    qv[j] = u32x4{0u, 0u, 0u, 0u};
-    if (e < NQ * KS * 64 && qh < n_qh) {
-      const int row = qh / group, head = kvh * group + qh % group;
-      qv[j] = *reinterpret_cast<const u32x4*>(p.q + (size_t)(d.row0 + row) * p.ldq + head * HD + ks * 32 +
-                                              (l >> 4) * 8);
-    }
+    const int qhc = min(qh, n_qh - 1);
+    const int row = qhc / group, head = kvh * group + qhc % group;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(p.q + (size_t)(d.row0 + row) * p.ldq + head * HD + ks * 32 +
+                                                    (l >> 4) * 8);
+    qv[j] = (e < NQ * KS * 64 && qh < n_qh) ? v : u32x4{0u, 0u, 0u, 0u};
   }
-  if (n_my > 0) load(0, 0);
-  if (n_my > 1) load(1, 1);
+  __builtin_amdgcn_sched_barrier(0);                // Q's loads, then both tiles' K, then V
+  load_k(0, 0);
+  load_k(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
+  load_v(0, 0);
+  load_v(1, 1);
+  __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int j = 0; j < QE; ++j) {
     const int e = tid + j * 64 * NWA;

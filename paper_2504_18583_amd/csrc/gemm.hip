@@ -342,20 +342,22 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       if (tid < 256) ss_finish(ss_row);
     }
     __builtin_amdgcn_sched_barrier(0);
-    while (true) {
+    // One exit per pair of stages: with an exit between the two halves the
+    // compiler's wait at the top of the loop covered every load in flight
+    // (draining the pipeline once per pair); with one exit it waits only for
+    // the stage it computes.  A last stage past the range computes zeros
+    // (its A fragments are zeroed) and the loads past the range are clamped.
+    do {
       compute(w0, a0, its);
       __builtin_amdgcn_sched_barrier(0);
-      its += U;
-      if (its >= n_it) break;
-      load(w0, a0, its + U);
+      load(w0, a0, its + 2 * U);
       __builtin_amdgcn_sched_barrier(0);
-      compute(w1, a1, its);
+      compute(w1, a1, its + U);
       __builtin_amdgcn_sched_barrier(0);
-      its += U;
-      if (its >= n_it) break;
-      load(w1, a1, its + U);
+      load(w1, a1, its + 3 * U);
       __builtin_amdgcn_sched_barrier(0);
-    }
+      its += 2 * U;
+    } while (its < n_it);
   } else {
     if constexpr (NORM && MT > 1) row_scales();
     if constexpr (NORM && MT == 1) {

@@ -342,12 +342,12 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       if (tid < 256) ss_finish(ss_row);
     }
     __builtin_amdgcn_sched_barrier(0);
-    // One exit per pair of stages: with an exit between the two halves the
-    // compiler's wait at the top of the loop covered every load in flight
-    // (draining the pipeline once per pair); with one exit it waits only for
-    // the stage it computes.  A last stage past the range computes zeros
-    // (its A fragments are zeroed) and the loads past the range are clamped.
-    do {
+    // One exit per pair of stages, at the loop's top: with an exit between
+    // the two halves the compiler's wait at the top covered every load in
+    // flight (draining the pipeline once per pair); with one exit it waits
+    // only for the stage it computes.  The last two stages are computed after
+    // the loop (loads past the range are clamped: at most one stage of them).
+    while (its + 2 * U < n_it) {
       compute(w0, a0, its);
       __builtin_amdgcn_sched_barrier(0);
       load(w0, a0, its + 2 * U);
@@ -357,7 +357,9 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
       load(w1, a1, its + 3 * U);
       __builtin_amdgcn_sched_barrier(0);
       its += 2 * U;
-    } while (its < n_it);
+    }
+    compute(w0, a0, its);
+    if (its + U < n_it) compute(w1, a1, its + U);     // uniform
   } else {
     if constexpr (NORM && MT > 1) row_scales();
     if constexpr (NORM && MT == 1) {

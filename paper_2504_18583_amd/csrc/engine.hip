@@ -554,11 +554,14 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   if (ps.n_seq * n_qblocks > kAttnRecords)
     return fail(c, PARD_ERR_CAPACITY, "attention plan: %d query blocks exceed the record budget", ps.n_seq * n_qblocks);
   int split_len = wide ? ceil_div(l_bound, 128) * 128 : kAttnChunk;
+  // row-block passes over several sequences (batched decode): 1024-key
+  // chunks (batch-32 step 15.5 ms with 256, 15.4 with 512, 15.2 with 1024;
+  // whole contexts, up to 2048 keys, 16.3)
+  if (rows && ps.n_seq > 1) split_len = kAttnBatchChunk;
   // decode passes over long contexts and single-sequence prefill chunks: the
   // shortest chunk (a multiple of 128 keys) that keeps the grid within one
   // workgroup per CU (16k keys, 8B/1B step: 5.33 ms with 256-key chunks, 5.06
-  // with 1024, 4.91 with 640; 16k-token prefill 839 -> 807 ms).  Batched
-  // row-block passes keep 256-key chunks (batch-32 step 15.7 ms against 16.3).
+  // with 1024, 4.91 with 640; 16k-token prefill 839 -> 807 ms)
   if (!wide && (!rows || ps.n_seq == 1)) {
     const int per = std::max(1, kAttnDecodeWGs / (ps.n_seq * s.n_kv_heads * n_qblocks));
     split_len = std::min(kAttnLongChunkMax, std::max(split_len, ceil_div(ceil_div(l_bound, per), 128) * 128));

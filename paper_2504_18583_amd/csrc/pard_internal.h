@@ -56,6 +56,7 @@ constexpr size_t kSplitPartFloats = (size_t)4 << 20;
 constexpr int kAttnWaves = 4;      // wavefronts per attention workgroup
 constexpr int kAttnChunk = 256;    // keys per attention workgroup (decode passes): two tiles per wavefront
 constexpr int kAttnWideMaxKeys = 2048;   // decode passes up to this context: one 8-wave workgroup covers all keys
+constexpr int kAttnBatchChunk = 1024;    // keys per chunk, row-block passes over several sequences
 constexpr int kAttnLongChunkMax = 2048;   // longest key chunk of a decode pass over a long context
 constexpr int kAttnDecodeWGs = 256;       // decode passes: chunks grow while the grid exceeds this
 constexpr int kAttnWideQTiles64 = 1;     // query tiles per such workgroup at head_dim 64 (measured: 1 ahead of 2 and 4)

@@ -30,7 +30,7 @@ greedy.  COD: App. B's worked example, the kept-token closed form (App. A's
 3.37M), the integrity condition, and packed samples reproducing the eq. 7
 draft pass through the decoder.
 """
-from .model import (KVCache, Model, attention, forward_cached, forward_full, linear,
+from .model import (KVCache, Model, attention, fill_cache, forward_cached, forward_full, linear,
                     rms_norm, rope, silu)
 from .pard import (PardTrace, accept_prefix, argmax_rows, draft_step, greedy_ar,
                    pard_generate, prefill, vanilla_draft_step, vanilla_generate, verify_step)

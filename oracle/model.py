@@ -163,7 +163,7 @@ def forward_full(model: Model, ids: Sequence[int]) -> np.ndarray:
     s, w = model.spec, model.weights
     ids = np.asarray(ids, dtype=np.int64)
     pos = np.arange(len(ids))
-    x = np.asarray(w["embed"], F64)[ids]
+    x = np.asarray(np.asarray(w["embed"])[ids], F64)
     empty = np.zeros((0, s.n_kv_heads, s.head_dim), F64)
     for l in range(s.n_layers):
         x, _, _ = _layer(s, w["layers"][l], x, pos, empty, empty)
@@ -180,10 +180,35 @@ def forward_cached(model: Model, cache: KVCache, ids: Sequence[int],
     ids = np.asarray(ids, dtype=np.int64)
     start = cache.length
     pos = np.arange(start, start + len(ids))
-    x = np.asarray(w["embed"], F64)[ids]
+    x = np.asarray(np.asarray(w["embed"])[ids], F64)
     for l in range(s.n_layers):
         x, cache.k[l], cache.v[l] = _layer(s, w["layers"][l], x, pos, cache.k[l], cache.v[l])
     rows = np.arange(len(ids)) if logits_rows is None else np.asarray(list(logits_rows), int)
     if rows.size == 0:
         return np.zeros((0, s.vocab), F64)
     return _head(model, x[rows])
+
+
+def fill_cache(model: Model, cache: KVCache, ids: Sequence[int]) -> None:
+    """Append the K/V of ``ids`` (positions cache.length ..) without any logits.
+
+    The same layer arithmetic as ``forward_cached``, except that in the last
+    layer only the keys and values are formed: the attention output and MLP
+    of that layer feed nothing the cache holds.  Used to ingest long prompts
+    whose outputs are not compared (a 1-layer model then needs no attention
+    over the prompt at all)."""
+    s, w = model.spec, model.weights
+    ids = np.asarray(ids, dtype=np.int64)
+    start = cache.length
+    pos = np.arange(start, start + len(ids))
+    x = np.asarray(np.asarray(w["embed"])[ids], F64)
+    last = s.n_layers - 1
+    for l in range(last):
+        x, cache.k[l], cache.v[l] = _layer(s, w["layers"][l], x, pos, cache.k[l], cache.v[l])
+    lw = w["layers"][last]
+    n, hkv, hd = x.shape[0], s.n_kv_heads, s.head_dim
+    y = rms_norm(x, lw["attn_norm"], s.rms_eps)
+    k = rope(linear(y, lw["wk"], lw.get("bk")).reshape(n, hkv, hd), pos, s.rope_theta, s.rope_scaling)
+    v = linear(y, lw["wv"], lw.get("bv")).reshape(n, hkv, hd)
+    cache.k[last] = np.concatenate([cache.k[last], k], axis=0)
+    cache.v[last] = np.concatenate([cache.v[last], v], axis=0)

@@ -43,6 +43,23 @@ def test_cached_matches_uncached_position_by_position(tiny, prompt):
         assert np.abs(cached[t] - full).max() < 1e-12
 
 
+@pytest.mark.parametrize("n_layers", [1, 2])
+def test_fill_cache_equals_forward_cached(tiny, prompt, n_layers):
+    """The logit-free ingest leaves exactly the cache the full cached forward
+    leaves (every layer, every position), so later passes see the same keys."""
+    from dataclasses import replace
+    target = oracle.build_model(replace(WL.target, n_layers=n_layers))
+    a, b = KVCache(target), KVCache(target)
+    forward_cached(target, a, prompt[:20])
+    forward_cached(target, a, prompt[20:])
+    oracle.fill_cache(target, b, prompt[:20])
+    oracle.fill_cache(target, b, prompt[20:])
+    assert a.length == b.length == len(prompt)
+    for l in range(n_layers):
+        assert np.array_equal(a.k[l], b.k[l]) and np.array_equal(a.v[l], b.v[l])
+    assert np.array_equal(forward_cached(target, a, [9, 1023]), forward_cached(target, b, [9, 1023]))
+
+
 def test_truncate_then_refeed_reproduces_logits(tiny, prompt):
     target, _ = tiny
     cache = KVCache(target)

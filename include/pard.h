@@ -63,7 +63,10 @@ enum { PARD_MODE_PARALLEL = 0, PARD_MODE_VANILLA = 1 };
  * cores (the same value when |w| >= 2^-14; smaller weights round to fp16
  * subnormals, within 2^-25).  Q/K/V biases stay fp32 holding the bf16 value.
  * Constraints: d_model % 32 == 0, head_dim in {64, 128},
- * n_heads % n_kv_heads == 0, vocab % 16 == 0, dtype == PARD_BF16.
+ * n_heads % n_kv_heads == 0, vocab % 16 == 0, dtype == PARD_BF16, and every
+ * weight matrix (rows padded to 16, columns to 32) below 2 GiB in its 2-byte
+ * encoding (UNSUPPORTED otherwise: the kernels address a matrix with 32-bit
+ * byte offsets).
  *
  * Generator (both this library and the test inputs implement it):
  * SplitMix64 (Steele, Lea, Flood 2014) stream with state
@@ -96,10 +99,28 @@ typedef struct {
 
 typedef struct pard_ctx pard_ctx;
 
+/* Statistics of one pard_generate call.  The phase times follow the time
+ * model of Sec. 2.2 (eqs. 3-4: a step costs the draft's forward passes plus
+ * one target forward): they are read on the device from its constant-rate
+ * clock at the pass boundaries of every step (the first kernel of a pass, the
+ * end of its step tail), so they cover the whole call, graph replays
+ * included.
+ *   draft_ms  -- every draft pass, from its first kernel to the end of its
+ *                tail (candidates stored, verify pass staged);
+ *   verify_ms -- every target pass up to and including its lm_head (the
+ *                verification forward and the per-tile argmax);
+ *   accept_ms -- every verify tail: the vocab argmax reduction, greedy prefix
+ *                acceptance (eq. 2), KV commit/rollback and the staging of the
+ *                next draft pass.
+ * step_ms_p50 / step_ms_p90: median and 90th percentile of the step latency,
+ * the time between the ends of consecutive verify tails (0 with fewer than two
+ * steps; the last 4096 steps of the call). */
 typedef struct {
   int64_t steps;             /* draft+verify steps executed */
   int64_t tokens;            /* tokens written to out_tokens */
   double elapsed_ms;         /* device time between the first and last step */
+  double draft_ms, verify_ms, accept_ms;
+  double step_ms_p50, step_ms_p90;
   int64_t accept_hist[33];   /* accept_hist[a] = steps that accepted a candidates */
 } pard_stats;
 
@@ -151,8 +172,15 @@ pard_status pard_verify(pard_ctx *ctx, int32_t seq, const int32_t *cand, int32_t
                         int32_t *n_accepted, int32_t *bonus);
 
 /* Roll the KV cache of `which` (PARD_TARGET / PARD_DRAFT) back to new_len
- * (0 <= new_len <= current length).  O(1): a length update.
- * Errors: ARG, STATE. */
+ * (0 <= new_len <= current length).  This is the rollback of Sec. 2.2's
+ * verification stage (candidates the target does not accept are dropped, so
+ * their cache rows are discarded) on a static, preallocated KV cache (the
+ * setting of App. F): O(1), a length update; later passes overwrite the
+ * dropped rows.  pard_verify already rolls the target back by itself; this
+ * call serves rewinds and tests.  For the target, the token history the
+ * library keeps is cut to the first new_len tokens and the pending token is
+ * kept.  Errors: ARG (bad which, new_len outside [0, length]), STATE (slot
+ * not prefilled), CAPACITY (seq outside [0, max_batch)), DEVICE. */
 pard_status pard_kv_truncate(pard_ctx *ctx, int32_t seq, int32_t which, int32_t new_len);
 
 /* Current committed KV length of `which` for slot `seq`. */
@@ -263,23 +291,31 @@ pard_status pard_timer_read(pard_ctx *ctx, int32_t *launches, double *total_ms);
  * n_samples+1) the bounds of each sample's packed region in the five device
  * output arrays (ids, labels, positions, subtask k, column j; int32), each
  * region at least pard_cod_capacity of its sample; out_len (device,
- * n_samples) receives each sample's packed length.  Runs on hip_stream and
- * returns after the results are complete.  The caller owns every buffer.
+ * n_samples) receives each sample's packed length; workspace (device, at
+ * least pard_cod_workspace_bytes(n_samples) bytes, 256-byte aligned) holds the
+ * device copy of both offset arrays during the call.  Runs on hip_stream and
+ * returns after the results are complete.  The caller owns every buffer; the
+ * call allocates no device memory.
  * Errors: ARG (null pointer, bad parameters, a sample outside [2, 8193]
- * tokens), CAPACITY (an output region below its capacity), NOMEM, DEVICE. */
+ * tokens, misaligned workspace), CAPACITY (an output region below its
+ * capacity), NOMEM (workspace too small), DEVICE. */
 int64_t pard_cod_capacity(int32_t n_tokens, int32_t K, double r, double r_min);
 /* pard_cod_layout: out_offsets (host, n_samples+1) = the prefix sums of the
  * samples' capacities for tok_offsets (host, n_samples+1); returns the total,
  * or -1 under the same conditions as pard_cod_capacity.  Host only. */
 int64_t pard_cod_layout(const int64_t *tok_offsets, int32_t n_samples, int32_t K, double r,
                         double r_min, int64_t *out_offsets);
+/* pard_cod_workspace_bytes: device workspace pard_cod_build needs for
+ * n_samples samples (0 if n_samples < 1).  Host only. */
+size_t pard_cod_workspace_bytes(int32_t n_samples);
 /* kernel_ms (host, may be NULL) receives the kernel's device time, from HIP
  * events recorded around its launch on hip_stream. */
 pard_status pard_cod_build(const int32_t *tokens, const int64_t *tok_offsets, int32_t n_samples,
                            int32_t K, double r, double r_min, int32_t mask_id, uint64_t seed,
                            const int64_t *out_offsets, int32_t *out_ids, int32_t *out_labels,
                            int32_t *out_pos, int32_t *out_section, int32_t *out_column,
-                           int32_t *out_len, float *kernel_ms, void *hip_stream);
+                           int32_t *out_len, void *workspace, size_t workspace_bytes,
+                           float *kernel_ms, void *hip_stream);
 
 /* Message of the last error on this context (never NULL; "" if none). */
 const char *pard_last_error(const pard_ctx *ctx);

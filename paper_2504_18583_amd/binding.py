@@ -42,6 +42,8 @@ class pard_model_spec(C.Structure):
 
 class pard_stats(C.Structure):
     _fields_ = [("steps", C.c_int64), ("tokens", C.c_int64), ("elapsed_ms", C.c_double),
+                ("draft_ms", C.c_double), ("verify_ms", C.c_double), ("accept_ms", C.c_double),
+                ("step_ms_p50", C.c_double), ("step_ms_p90", C.c_double),
                 ("accept_hist", C.c_int64 * 33)]
 
 
@@ -66,10 +68,11 @@ _sig = {
     "pard_cod_capacity": (C.c_int64, [C.c_int32, C.c_int32, C.c_double, C.c_double]),
     "pard_cod_layout": (C.c_int64, [C.POINTER(C.c_int64), C.c_int32, C.c_int32, C.c_double, C.c_double,
                                     C.POINTER(C.c_int64)]),
+    "pard_cod_workspace_bytes": (C.c_size_t, [C.c_int32]),
     "pard_cod_build": (C.c_int, [C.c_void_p, C.POINTER(C.c_int64), C.c_int32, C.c_int32, C.c_double,
                                  C.c_double, C.c_int32, C.c_uint64, C.POINTER(C.c_int64), C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
-                                 C.POINTER(C.c_float), C.c_void_p]),
+                                 C.c_void_p, C.c_size_t, C.POINTER(C.c_float), C.c_void_p]),
     "pard_read_logits": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                    C.c_int32]),
     "pard_read_weight": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -160,6 +163,9 @@ def cod_build(tokens, tok_offsets: Sequence[int], k: int, r: float, r_min: float
     out = {name: torch.empty(total, dtype=torch.int32, device=dev)
            for name in ("ids", "labels", "pos", "section", "column")}
     out_len = torch.empty(n, dtype=torch.int32, device=dev)
+    ws_bytes = int(lib.pard_cod_workspace_bytes(n))
+    ws = torch.empty(ws_bytes + 256, dtype=torch.uint8, device=dev)
+    ws_ptr = ws.data_ptr() + (-ws.data_ptr()) % 256
     ms = C.c_float(0.0)
     st = stream if stream is not None else torch.cuda.current_stream(dev).cuda_stream
     rc = lib.pard_cod_build(C.c_void_p(tokens.data_ptr()), offs.ctypes.data_as(C.POINTER(C.c_int64)), n, k,
@@ -167,7 +173,8 @@ def cod_build(tokens, tok_offsets: Sequence[int], k: int, r: float, r_min: float
                             out_offs.ctypes.data_as(C.POINTER(C.c_int64)),
                             *[C.c_void_p(out[name].data_ptr()) for name in ("ids", "labels", "pos", "section",
                                                                             "column")],
-                            C.c_void_p(out_len.data_ptr()), C.byref(ms) if timing else None, C.c_void_p(st))
+                            C.c_void_p(out_len.data_ptr()), C.c_void_p(ws_ptr), ws_bytes,
+                            C.byref(ms) if timing else None, C.c_void_p(st))
     if rc != PARD_OK:
         raise PardError(rc, "pard_cod_build failed")
     return (out_offs, out, out_len, ms.value) if timing else (out_offs, out, out_len)

@@ -219,6 +219,10 @@ struct pard_ctx {
   float* h_gather_out = nullptr;
   int* h_out = nullptr;
   hipEvent_t ev_start = nullptr, ev_stop = nullptr;
+  // pass-boundary clock of the fused loop (device) and its host copy
+  PhaseClock* clock_dev = nullptr;
+  PhaseClock* h_clock = nullptr;
+  double clock_khz = 0.0;
   // captured fused steps (draft pass + verify pass), replayed on `stream`
   struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
@@ -283,6 +287,15 @@ pard_status check_spec(const pard_model_spec* s, const char* who, std::string* w
   if (s->d_model % 32) return bad(PARD_ERR_UNSUPPORTED, "d_model must be a multiple of 32");
   if (s->vocab % 16) return bad(PARD_ERR_UNSUPPORTED, "vocab must be a multiple of 16");
   if ((int64_t)s->vocab * s->d_model >= (1ll << 40)) return bad(PARD_ERR_ARG, "vocab too large");
+  // every strip-packed matrix is addressed with 32-bit byte offsets (buffer
+  // descriptors, k-block offsets): rows padded to 16, columns to 32, 2 bytes each
+  auto pad = [](int64_t v, int64_t m) { return (v + m - 1) / m * m; };
+  const int64_t d = s->d_model, q = (int64_t)s->n_heads * s->head_dim, kv = (int64_t)s->n_kv_heads * s->head_dim;
+  const int64_t f = pad(s->ffn_dim, 32);
+  const int64_t mats[5][2] = {{q + 2 * kv, d}, {d, q}, {2 * f, d}, {d, f}, {s->vocab, d}};
+  for (const auto& m : mats)
+    if (pad(m[0], 16) * pad(m[1], 32) * 2 >= (1ll << 31))
+      return bad(PARD_ERR_UNSUPPORTED, "a weight matrix reaches 2 GiB (32-bit byte offsets)");
   return PARD_OK;
 }
 
@@ -373,6 +386,7 @@ size_t layout(pard_ctx* c, char* base) {
   c->out_dev = b.take<int>((size_t)c->max_batch * c->max_ctx);
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
   c->gather_out_dev = b.take<float>(kGatherMax);
+  c->clock_dev = b.take<PhaseClock>(1);
   return align256(b.off);
 }
 
@@ -532,7 +546,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   {
     Timed t(c, cls0 + 0);
     HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, act_rows, M.ss,
-                            std::max(1, M.ss_tiles_max), ps.max_rows, c->stream));
+                            std::max(1, M.ss_tiles_max), ps.max_rows, &c->clock_dev->pass_start[w], c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
   // attention plan: one workgroup per (sequence, KV head, query group, key
@@ -683,6 +697,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     ta.logits = M.logits;
     ta.q_logits = c->m[PARD_DRAFT].logits;
     ta.tile_w = lm_rows ? kRowsWaveStrips * 16 : pick_S(EPI_LOGITS, M.p_lm.n_strips, mt_lm) * 16;
+    ta.clock = c->clock_dev;
     Timed t(c, cls0 + 7);
     HIP_TRY(c, launch_tail(ta, ps.n_seq, c->stream));
     if (ps.n_seq > 1 && ps.next_desc) HIP_TRY(c, launch_stage(ta, c->stream));
@@ -942,8 +957,16 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
       hipHostMalloc((void**)&c->h_seq, sizeof(SeqState) * max_batch, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_gather_idx, sizeof(size_t) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_gather_out, sizeof(float) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_out, sizeof(int) * max_ctx, hipHostMallocDefault) != hipSuccess)
+      hipHostMalloc((void**)&c->h_out, sizeof(int) * max_ctx, hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_clock, sizeof(PhaseClock), hipHostMallocDefault) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
+  {
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+        khz <= 0)
+      return bail(PARD_ERR_DEVICE);
+    c->clock_khz = khz;
+  }
   memset(c->h_seq, 0, sizeof(SeqState) * max_batch);
   if (hipEventCreate(&c->ev_start) != hipSuccess || hipEventCreate(&c->ev_stop) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
@@ -954,6 +977,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
       hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[1].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->split_counters, 0, sizeof(int) * kSplitCounters, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->clock_dev, 0, sizeof(PhaseClock), c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   *out = c;
@@ -968,6 +992,7 @@ void pard_free(pard_ctx* c) {
   if (c->h_gather_idx) (void)hipHostFree(c->h_gather_idx);
   if (c->h_gather_out) (void)hipHostFree(c->h_gather_out);
   if (c->h_out) (void)hipHostFree(c->h_out);
+  if (c->h_clock) (void)hipHostFree(c->h_clock);
   if (c->ev_start) (void)hipEventDestroy(c->ev_start);
   if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
   for (hipEvent_t e : c->timer_ev) (void)hipEventDestroy(e);
@@ -1226,6 +1251,7 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
     }
   }
   if ((st = stage_desc(c, K > 0 ? PARD_DRAFT : PARD_TARGET, first)) != PARD_OK) return restore(st);
+  HIP_TRY(c, hipMemsetAsync(c->clock_dev, 0, sizeof(PhaseClock), c->stream));
   HIP_TRY(c, hipEventRecord(c->ev_start, c->stream));
   // active: sequences that still need tokens (a finished one leaves the
   // batch when the device stages the next draft pass)
@@ -1274,6 +1300,8 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
   }
   float ms = 0.f;
   if (steps > 0) HIP_TRY(c, hipEventElapsedTime(&ms, c->ev_start, c->ev_stop));
+  HIP_TRY(c, hipMemcpyAsync(c->h_clock, c->clock_dev, sizeof(PhaseClock), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipStreamSynchronize(c->stream));
   int64_t total_written = 0;
   int64_t hist_sum[kMaxK + 1] = {0};
   for (int i = 0; i < n_seq; ++i) {
@@ -1300,6 +1328,24 @@ pard_status pard_generate_ex(pard_ctx* c, int32_t n_seq, const int32_t* seqs, in
     stats->steps = steps;
     stats->tokens = total_written;
     stats->elapsed_ms = ms;
+    const PhaseClock& ck = *c->h_clock;
+    const double per_ms = c->clock_khz;   // clock ticks per millisecond
+    stats->draft_ms = ck.draft_ticks / per_ms;
+    stats->verify_ms = ck.verify_ticks / per_ms;
+    stats->accept_ms = ck.accept_ticks / per_ms;
+    // step latencies: gaps between consecutive verify-tail ends in the ring
+    const uint64_t n_end = std::min<uint64_t>(ck.n_steps, kStepRing);
+    std::vector<double> lat;
+    for (uint64_t i = 1; i < n_end; ++i) {
+      const uint64_t j = ck.n_steps - n_end + i;
+      lat.push_back((ck.step_end[j % kStepRing] - ck.step_end[(j - 1) % kStepRing]) / per_ms);
+    }
+    if (!lat.empty()) {
+      std::sort(lat.begin(), lat.end());
+      auto rank = [&](double q) { return lat[(size_t)std::max(0.0, std::ceil(q * lat.size()) - 1)]; };
+      stats->step_ms_p50 = rank(0.5);
+      stats->step_ms_p90 = rank(0.9);
+    }
     for (int i = 0; i <= kMaxK; ++i) stats->accept_hist[i] = hist_sum[i];
   }
   return PARD_OK;
@@ -1348,13 +1394,20 @@ int64_t pard_cod_layout(const int64_t* tok_offsets, int32_t n_samples, int32_t K
   return out_offsets[n_samples];
 }
 
+size_t pard_cod_workspace_bytes(int32_t n_samples) {
+  return n_samples < 1 ? 0 : align256(2 * sizeof(int64_t) * ((size_t)n_samples + 1));
+}
+
 pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
                            double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets, int32_t* out_ids,
                            int32_t* out_labels, int32_t* out_pos, int32_t* out_section, int32_t* out_column,
-                           int32_t* out_len, float* kernel_ms, void* hip_stream) {
+                           int32_t* out_len, void* workspace, size_t workspace_bytes, float* kernel_ms,
+                           void* hip_stream) {
   if (!tokens || !tok_offsets || !out_offsets || !out_ids || !out_labels || !out_pos || !out_section ||
-      !out_column || !out_len || n_samples < 1 || !cod_params_ok(K, r, r_min))
+      !out_column || !out_len || !workspace || n_samples < 1 || !cod_params_ok(K, r, r_min) ||
+      (reinterpret_cast<uintptr_t>(workspace) & 255))
     return PARD_ERR_ARG;
+  if (workspace_bytes < pard_cod_workspace_bytes(n_samples)) return PARD_ERR_NOMEM;
   // every sample fits the kernel and its output region holds its capacity
   if (tok_offsets[0] < 0 || out_offsets[0] < 0) return PARD_ERR_ARG;
   int max_cols = 1;
@@ -1365,9 +1418,8 @@ pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, in
     max_cols = std::max(max_cols, (int)(len - 1));
   }
   hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  int64_t* d_off = nullptr;
+  int64_t* d_off = static_cast<int64_t*>(workspace);   // tok_offsets, then out_offsets
   const size_t bytes = sizeof(int64_t) * (size_t)(n_samples + 1);
-  if (hipMalloc((void**)&d_off, 2 * bytes) != hipSuccess) return PARD_ERR_NOMEM;
   CodArgs a;
   a.k_max = K;
   a.r = r;
@@ -1393,7 +1445,6 @@ pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, in
   if (stt == PARD_OK && kernel_ms && hipEventElapsedTime(kernel_ms, ev[0], ev[1]) != hipSuccess) stt = PARD_ERR_DEVICE;
   for (hipEvent_t e : ev)
     if (e) (void)hipEventDestroy(e);
-  (void)hipFree(d_off);
   return stt;
 }
 

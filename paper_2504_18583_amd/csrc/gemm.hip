@@ -905,12 +905,38 @@ __device__ int block_sample_residual(const TailArgs& p, const float* zp, float M
   return pick_s[0];
 }
 
+// Phase clock of the fused loop (one thread): at the start of a step tail the
+// verify phase ends (target pass up to its lm_head); at the end of the tail --
+// after the next pass is staged -- the draft phase (draft pass and tail) or the
+// accept phase (verify tail) ends, and a verify tail records the step's end.
+__device__ void clock_tail_start(const TailArgs& p) {
+  if (p.tail != TAIL_VERIFY) return;
+  const unsigned long long t = wall_clock64();
+  p.clock->tail_start = t;
+  p.clock->verify_ticks += t - p.clock->pass_start[0];
+}
+__device__ void clock_tail_end(const TailArgs& p) {
+  const unsigned long long t = wall_clock64();
+  PhaseClock* c = p.clock;
+  if (p.tail == TAIL_DRAFT || p.tail == TAIL_VSD_DRAFT) {
+    c->draft_ticks += t - c->pass_start[1];
+  } else if (p.tail == TAIL_VERIFY) {
+    c->accept_ticks += t - c->tail_start;
+    c->step_end[c->n_steps % kStepRing] = t;
+    ++c->n_steps;
+  }
+}
+
 __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
   __shared__ int res_s[kMaxK + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const FwdDesc* dp = p.desc;
   const int sj = blockIdx.x;
   if (sj >= dp->n_seq) return;                    // uniform: the whole block leaves
+  // block 0 keeps the clock; with several sequences k_stage (the kernel after
+  // this one) ends the phase
+  const bool clock = p.clock && blockIdx.x == 0;
+  if (clock && tid == 0) clock_tail_start(p);
   const PassSeq ps = dp->seq[sj];
   const int rows = min(ps.lm_rows, kMaxK + 1);
   for (int r = wave; r < rows; r += 16) {
@@ -1026,9 +1052,19 @@ __global__ __launch_bounds__(1024) void k_lm_tail(const TailArgs p) {
     __syncthreads();
     stage_next(p, false);
   }
+  if (clock && (gridDim.x == 1 || !p.next_desc)) {
+    __syncthreads();
+    if (tid == 0) clock_tail_end(p);
+  }
 }
 
-__global__ __launch_bounds__(256) void k_stage(const TailArgs p) { stage_next(p, true); }
+__global__ __launch_bounds__(256) void k_stage(const TailArgs p) {
+  stage_next(p, true);
+  if (p.clock) {
+    __syncthreads();
+    if (threadIdx.x == 0) clock_tail_end(p);
+  }
+}
 
 // ============================================================================
 // Row-block GEMM: passes of more than kMaxRows rows (batched decode passes,

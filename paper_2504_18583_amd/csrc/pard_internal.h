@@ -152,6 +152,18 @@ struct SeqState {
   float qM[kMaxK], qS[kMaxK];   // sampling: max logit and softmax normaliser of the draft's rows
 };
 
+// Device clock readings of the fused loop's pass boundaries (wall_clock64,
+// constant rate): the first kernel of a pass stores its start, the step tails
+// accumulate the draft, verify and accept phases and record each step's end.
+constexpr int kStepRing = 4096;
+struct PhaseClock {
+  unsigned long long pass_start[2];   // [model]: start of its current pass
+  unsigned long long tail_start;      // start of the current verify tail
+  unsigned long long draft_ticks, verify_ticks, accept_ticks;
+  unsigned long long n_steps;         // verify tails ended since the reset
+  unsigned long long step_end[kStepRing];
+};
+
 enum Epi { EPI_QKV = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_LOGITS = 3 };
 enum Tail { TAIL_NONE = 0, TAIL_PREFILL = 1, TAIL_DRAFT = 2, TAIL_VERIFY = 3, TAIL_VSD_DRAFT = 4 };
 
@@ -217,6 +229,7 @@ struct TailArgs {
   const float* logits;
   const float* q_logits;
   int tile_w;
+  PhaseClock* clock;      // pass-boundary clock (phase times of the fused loop)
 };
 
 struct AttnArgs {

@@ -143,12 +143,21 @@ def test_cod_capacity_and_argument_checks(b):
     dummy = C.c_void_p(16)                       # never dereferenced: the checks fail first
     P64 = C.POINTER(C.c_int64)
 
-    def build(tok_offs, out_offs, k=4, r=0.5):
+    def build(tok_offs, out_offs, k=4, r=0.5, ws=256, ws_bytes=None):
         t = (C.c_int64 * len(tok_offs))(*tok_offs)
         o = (C.c_int64 * len(out_offs))(*out_offs)
-        return b.lib.pard_cod_build(dummy, C.cast(t, P64), len(tok_offs) - 1, k, r, 0.0, 0, 0, C.cast(o, P64),
-                                    dummy, dummy, dummy, dummy, dummy, dummy, None, None)
+        n = len(tok_offs) - 1
+        if ws_bytes is None:
+            ws_bytes = b.lib.pard_cod_workspace_bytes(n)
+        return b.lib.pard_cod_build(dummy, C.cast(t, P64), n, k, r, 0.0, 0, 0, C.cast(o, P64),
+                                    dummy, dummy, dummy, dummy, dummy, dummy, C.c_void_p(ws), ws_bytes, None, None)
     cap = b.cod_capacity(10, 4, 0.5, 0.0)
+    # the device workspace holds both offset arrays (int64, n_samples + 1 each)
+    assert b.lib.pard_cod_workspace_bytes(1) >= 32 and b.lib.pard_cod_workspace_bytes(1000) >= 16 * 1001
+    assert b.lib.pard_cod_workspace_bytes(0) == 0
+    assert build([0, 10], [0, cap], ws=0) == b.PARD_ERR_ARG                 # no workspace
+    assert build([0, 10], [0, cap], ws=256 + 8) == b.PARD_ERR_ARG           # misaligned
+    assert build([0, 10], [0, cap], ws_bytes=31) == b.PARD_ERR_NOMEM        # too small
     assert build([0, 10], [0, cap - 1]) == b.PARD_ERR_CAPACITY
     assert build([0, 1], [0, 100]) == b.PARD_ERR_ARG          # a one-token sample
     assert build([0, 10], [0, cap], k=0) == b.PARD_ERR_ARG
@@ -159,3 +168,23 @@ def test_cod_capacity_and_argument_checks(b):
     total = b.lib.pard_cod_layout(C.cast(offs, P64), 3, 4, 0.5, 0.0, C.cast(lay, P64))
     caps = [b.cod_capacity(n, 4, 0.5, 0.0) for n in (10, 2, 488)]
     assert list(lay) == [0, caps[0], caps[0] + caps[1], sum(caps)] and total == sum(caps)
+
+
+def test_matrices_of_2gib_or_more_are_refused(b):
+    """The kernels address a strip-packed weight with 32-bit byte offsets: a
+    spec whose largest matrix (here a 152 064 x 8192 lm_head, 2.49 GB in two
+    bytes per weight) reaches 2 GiB is refused, one just below is accepted."""
+    from dataclasses import replace
+    _, t, d = _pair("tiny")
+    big = replace(t, n_layers=1, d_model=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=1024,
+                  vocab=152064)
+    drf = replace(d, vocab=152064)
+    ts, ds = b.spec_from(big), b.spec_from(drf)
+    assert b.pard_arena_bytes(ts, ds, 1, 256, 4) == 0
+    assert _load(b, ts, ds, 152063, 0x1000, 1 << 40)[0] == b.PARD_ERR_UNSUPPORTED
+    # 131 056 x 8192 x 2 = 2 147 221 504 bytes < 2^31: accepted
+    ok = replace(big, vocab=131056)
+    assert b.pard_arena_bytes(b.spec_from(ok), b.spec_from(replace(d, vocab=131056)), 1, 256, 4) > 0
+    # gate/up: 2 x 65 536 x 8192 x 2 bytes = 2 GiB exactly
+    ffn = replace(t, n_layers=1, d_model=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=65536)
+    assert b.pard_arena_bytes(b.spec_from(ffn), b.spec_from(d), 1, 256, 4) == 0

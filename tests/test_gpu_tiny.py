@@ -167,6 +167,27 @@ def test_generate_matches_greedy(eng, models, B):
     assert eng.kv_len(B.PARD_TARGET) == len(PROMPT) + committed
 
 
+@pytest.mark.parametrize("k,mode", [(4, 0), (0, 0), (3, 1)])
+def test_generate_phase_times(eng, B, k, mode):
+    """pard_stats' phase times come from the device clock at pass boundaries:
+    draft + verify + accept cover the timed steps (the gaps between passes are
+    a few kernel launches), a plain target step has no draft phase, and the
+    step-latency percentiles are ordered and match the mean step."""
+    say(f"[gpu] tiny: phase times K={k} mode={mode}")
+    eng.prefill(PROMPT)
+    toks, st = eng.generate(k, 48, mode=mode)
+    assert st.steps >= 8
+    phases = st.draft_ms + st.verify_ms + st.accept_ms
+    say(f"    steps {st.steps}: elapsed {st.elapsed_ms:.3f} ms, draft {st.draft_ms:.3f} verify {st.verify_ms:.3f} "
+        f"accept {st.accept_ms:.3f}, step p50 {st.step_ms_p50:.4f} p90 {st.step_ms_p90:.4f}")
+    assert st.verify_ms > 0 and st.accept_ms > 0
+    assert (st.draft_ms > 0) == (k > 0)
+    assert 0.5 * st.elapsed_ms < phases <= 1.02 * st.elapsed_ms
+    assert 0 < st.step_ms_p50 <= st.step_ms_p90
+    mean = st.elapsed_ms / st.steps
+    assert 0.5 * mean < st.step_ms_p50 < 2.0 * mean
+
+
 def test_k1_draft_is_plain_draft_decode(eng, models, B):
     say("[gpu] tiny: K=1 draft")
     target, draft = models

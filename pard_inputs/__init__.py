@@ -269,11 +269,13 @@ def with_dtype(spec: ModelSpec, dtype: str) -> ModelSpec:
 # Model weights (canonical layout) and prompts
 # --------------------------------------------------------------------------
 
-def gen_model_weights(spec: ModelSpec, layers: Optional[List[int]] = None) -> dict:
+def gen_model_weights(spec: ModelSpec, layers: Optional[List[int]] = None,
+                      progress=None) -> dict:
     """All weights of one model as float32 arrays in canonical [out, in] layout.
 
     ``layers`` restricts generation to a subset of layer indices (each layer's
-    values do not depend on which other layers are generated).
+    values do not depend on which other layers are generated).  ``progress``
+    (optional) is called with a short message after each generated layer.
     """
     s, d, f = spec, spec.d_model, spec.ffn_dim
 
@@ -302,6 +304,8 @@ def gen_model_weights(spec: ModelSpec, layers: Optional[List[int]] = None) -> di
             lw["bk"] = g(layer_tensor(l, T_BK), (s.kv_dim,))
             lw["bv"] = g(layer_tensor(l, T_BV), (s.kv_dim,))
         w["layers"][l] = lw
+        if progress is not None:
+            progress(f"layer {l + 1}/{s.n_layers}")
     return w
 
 

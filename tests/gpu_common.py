@@ -59,11 +59,21 @@ class Lockstep:
         self.worst = 0.0
         self.step_no = 0
 
-    def prefill(self):
+    def prefill(self, cache_only_prefix: bool = False):
+        """Both prefills.  With cache_only_prefix the oracle ingests the prompt
+        but its last token with oracle.fill_cache (no logits; for long prompts)
+        and runs the last token through the cached forward: the same caches and
+        last-row logits as oracle.prefill."""
         from paper_2504_18583_amd.binding import PARD_TARGET
         eng, seq, tag = self.eng, self.seq, self.tag
         first = eng.prefill(self.prompt, seq=seq)
-        self.cache_t, self.cache_d, _, lg = oracle.prefill(self.target, self.draft, self.prompt)
+        if cache_only_prefix:
+            self.cache_t, self.cache_d = oracle.KVCache(self.target), oracle.KVCache(self.draft)
+            oracle.fill_cache(self.target, self.cache_t, self.prompt[:-1])
+            lg = oracle.forward_cached(self.target, self.cache_t, self.prompt[-1:])
+            oracle.fill_cache(self.draft, self.cache_d, self.prompt)
+        else:
+            self.cache_t, self.cache_d, _, lg = oracle.prefill(self.target, self.draft, self.prompt)
         self.worst = max(self.worst, assert_logits_close(eng.read_logits(PARD_TARGET, 1, seq=seq), lg,
                                                          f"{tag} prefill logits"))
         assert_tokens_match([first], lg, f"{tag} first token")

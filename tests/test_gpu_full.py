@@ -134,6 +134,81 @@ def test_llama_8b_1b_full_depth_properties(B):
         eng.close()
 
 
+FULL_DEPTH_PROMPT = 64     # tokens of the benchmark prompt the full-depth lock-step uses
+
+
+@pytest.fixture(scope="module")
+def full_depth(B):
+    """The 32-layer 8B-shaped target and 16-layer 1B-shaped draft, on the GPU
+    and in the oracle (float32 weights held on the host, ~37 GB)."""
+    from gpu_common import Lockstep
+    wl = pi.WORKLOADS["llama8b_1b"]
+    t_spec, d_spec = pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0][:FULL_DEPTH_PROMPT]]
+    models = []
+    for name, spec in (("target", t_spec), ("draft", d_spec)):
+        say(f"[gpu] 8B/1B full depth: oracle {name} weights")
+        models.append(oracle.Model(spec, pi.gen_model_weights(spec, progress=lambda m, n=name: say(f"    {n} {m}"))))
+    say("[gpu] 8B/1B full depth: engine load")
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=len(prompt) + 64, max_k=wl.k)
+    ls = Lockstep(eng, models[0], models[1], prompt, wl.k, wl.mask_id, tag="8B/1B full depth")
+    try:
+        yield ls
+    finally:
+        eng.close()
+
+
+def test_llama_8b_1b_full_depth_prefill_lockstep(full_depth):
+    """The headline pair at its full 32/16 layers: prefill logits and first
+    token against the float64 oracle at the stated tolerance."""
+    say("[gpu] 8B/1B full depth: prefill lock-step")
+    full_depth.prefill()
+    say(f"    max |logit err| after prefill {full_depth.worst:.4g}")
+
+
+def test_llama_8b_1b_full_depth_steps_lockstep(full_depth):
+    """Two draft/verify steps (K = 8) of the full-depth pair in lock-step: draft
+    and verify logits, candidates, accept counts and KV lengths."""
+    if not hasattr(full_depth, "cache_t"):
+        full_depth.prefill()
+    for i in range(2):
+        say(f"[gpu] 8B/1B full depth: step {i + 1}")
+        full_depth.step()
+    say(f"    max |logit err| at full depth {full_depth.worst:.4g}")
+
+
+def test_16k_context_8b_width_slice_lockstep(B):
+    """The long-context workload's attention plan at its real shape: one
+    layer of the 8B-shaped target (32 query / 8 KV heads of 128, group 4) and
+    of the 1B-shaped draft over a 16 384-token prompt; the decode passes take
+    640-key chunks (26 of them, one query group per KV head) combined by the
+    many-chunk merge.  The oracle ingests the prompt's keys and values without
+    logits (oracle.fill_cache) and runs the last token, then two steps."""
+    from gpu_common import Lockstep
+    wl = pi.WORKLOADS["llama8b_1b_long"]
+    t_spec, d_spec = _slice(wl.target, 1), _slice(wl.draft, 1)
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0]]
+    n = len(prompt)
+    # the verify pass's plan: 8 KV heads x 1 query group, chunks the shortest
+    # multiple of 128 keys that keeps the grid within 256 workgroups
+    per = 256 // t_spec.n_kv_heads
+    chunk = -(-(-(-(n + wl.k + 1) // per)) // 128) * 128
+    assert (chunk, -(-(n + wl.k + 1) // chunk)) == (640, 26)
+    say(f"[gpu] {n}-token context, 8B/1B width, 1 layer each: oracle build")
+    target, draft = oracle.build_model(t_spec), oracle.build_model(d_spec)
+    eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=n + 64, max_k=wl.k)
+    try:
+        ls = Lockstep(eng, target, draft, prompt, wl.k, wl.mask_id, tag="16k 8B width")
+        say("[gpu] 16k 8B width: prefill")
+        ls.prefill(cache_only_prefix=True)
+        for i in range(2):
+            say(f"[gpu] 16k 8B width: step {i + 1}")
+            ls.step()
+        say(f"    max |logit err| {ls.worst:.4g}")
+    finally:
+        eng.close()
+
+
 def test_16k_context_chunked_attention_lockstep(B):
     wl = pi.WORKLOADS["tiny"]
     t_spec, d_spec = pi.with_dtype(wl.target, "bf16"), pi.with_dtype(wl.draft, "bf16")

@@ -223,6 +223,11 @@ struct pard_ctx {
   PhaseClock* clock_dev = nullptr;
   PhaseClock* h_clock = nullptr;
   double clock_khz = 0.0;
+  // QKV GEMM + decode attention in one launch: its counters and wait-error flag
+  int* fuse_cnt = nullptr;
+  int* fuse_err = nullptr;
+  int* h_fuse_err = nullptr;
+  bool use_fused = true;
   // captured fused steps (draft pass + verify pass), replayed on `stream`
   struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
@@ -387,6 +392,8 @@ size_t layout(pard_ctx* c, char* base) {
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
   c->gather_out_dev = b.take<float>(kGatherMax);
   c->clock_dev = b.take<PhaseClock>(1);
+  c->fuse_cnt = b.take<int>(kFuseInts);
+  c->fuse_err = b.take<int>(64);
   return align256(b.off);
 }
 
@@ -582,11 +589,39 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   }
   while ((int64_t)ps.n_seq * n_qblocks * ceil_div(l_bound, split_len) > kAttnRecords) split_len *= 2;
   const int n_splits = ceil_div(l_bound, split_len);
+  // decode passes over one attention chunk: QKV GEMM and attention in one
+  // launch when its grid fits the device at once
+  const int mt_q = ceil_div(ps.max_rows, 16);
+  const int S_q = rows ? 0 : pick_S(EPI_QKV, M.p_qkv.n_strips, mt_q);
+  const int n_attn_wg = s.n_kv_heads * n_qblocks * ps.n_seq;
+  const bool fused = c->use_fused && !rows && wide && nqt == 1 && M.p_qkv.ksplit == 1 && S_q > 0 &&
+                     M.p_qkv.n_strips % S_q == 0 &&
+                     M.p_qkv.n_strips / S_q + n_attn_wg <= qkv_attn_capacity(mt_q, S_q, s.head_dim);
   for (int l = 0; l < s.n_layers; ++l) {
     const Layer& L = M.layers[l];
     uint16_t* kc = M.kcache + layer_kv * l;
     uint16_t* vc = M.vcache + layer_kv * l;
-    {  // norm + QKV + bias + RoPE + KV append
+    AttnArgs aa{};
+    aa.q = M.q;
+    aa.ldq = M.q_dim;
+    aa.kc = kc;
+    aa.vc = vc;
+    aa.kv_seq_stride = c->kv_seq_stride[w];
+    aa.cap = c->kv_cap;
+    aa.out = M.attn;
+    aa.act_rows = act_rows;
+    aa.desc = M.desc;
+    aa.n_heads = s.n_heads;
+    aa.n_kv = s.n_kv_heads;
+    aa.nqt = nqt;
+    aa.n_qblocks = n_qblocks;
+    aa.split_len = split_len;
+    aa.n_splits = n_splits;
+    aa.n_seq = ps.n_seq;
+    aa.scale = 1.0f / std::sqrt((float)s.head_dim);
+    aa.part = c->attn_part;
+    aa.wide = wide ? 1 : 0;
+    {  // norm + QKV + bias + RoPE + KV append (and, fused, the attention)
       GemmArgs a = gemm_base(M, L.wqkv, act_rows);
       a.A = M.xg;
       a.lda = M.d;
@@ -603,31 +638,32 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
       a.q_dim = M.q_dim;
       a.kv_dim = M.kv_dim;
       a.hd = s.head_dim;
-      HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
+      if (fused) {
+        a.kb_total = M.p_qkv.kb_total;
+        a.n_strips = M.p_qkv.n_strips;
+        a.n_tiles = M.p_qkv.n_strips / S_q;
+        a.ksplit = 1;
+        a.kb_split = M.p_qkv.kb_total;
+        FuseCtl f;
+        f.counters = c->fuse_cnt;
+        f.err = c->fuse_err;
+        f.n_prod = a.n_tiles;
+        f.n_cons = n_attn_wg;
+        // the kernel timer's QKV class covers the fused launch (attention included)
+        LaunchEvents ev;
+        if (c->timer_class == cls0 + 1 && c->timer_used < c->timer_max) {
+          ev.start = c->timer_ev[2 * c->timer_used];
+          ev.stop = c->timer_ev[2 * c->timer_used + 1];
+          ++c->timer_used;
+        }
+        HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, c->stream, ev));
+      } else {
+        HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
+      }
     }
-    {  // attention
-      AttnArgs a{};
-      a.q = M.q;
-      a.ldq = M.q_dim;
-      a.kc = kc;
-      a.vc = vc;
-      a.kv_seq_stride = c->kv_seq_stride[w];
-      a.cap = c->kv_cap;
-      a.out = M.attn;
-      a.act_rows = act_rows;
-      a.desc = M.desc;
-      a.n_heads = s.n_heads;
-      a.n_kv = s.n_kv_heads;
-      a.nqt = nqt;
-      a.n_qblocks = n_qblocks;
-      a.split_len = split_len;
-      a.n_splits = n_splits;
-      a.n_seq = ps.n_seq;
-      a.scale = 1.0f / std::sqrt((float)s.head_dim);
-      a.part = c->attn_part;
-      a.wide = wide ? 1 : 0;
+    if (!fused) {  // attention
       Timed t(c, cls0 + 2);
-      HIP_TRY(c, launch_attention(s.head_dim, a, c->stream));
+      HIP_TRY(c, launch_attention(s.head_dim, aa, c->stream));
     }
     {  // O-projection + residual
       GemmArgs a = gemm_base(M, L.wo, act_rows);
@@ -726,8 +762,11 @@ pard_status pull_seqs_sync(pard_ctx* c, const int* seqs, int n) {
   for (int i = 0; i < n; ++i)
     HIP_TRY(c, hipMemcpyAsync(c->h_seq + seqs[i], c->seq_dev + seqs[i], sizeof(SeqState), hipMemcpyDeviceToHost,
                               c->stream));
+  HIP_TRY(c, hipMemcpyAsync(c->h_fuse_err, c->fuse_err, sizeof(int), hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   c->desc_slot = 0;
+  if (*c->h_fuse_err)
+    return fail(c, PARD_ERR_DEVICE, "a QKV+attention launch's wait exceeded its spin limit: results are invalid");
   return PARD_OK;
 }
 
@@ -946,6 +985,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   layout(c, c->arena);
   c->hist.assign(max_batch, {});
   if (const char* e = getenv("PARD_NO_GRAPH")) c->use_graphs = e[0] == '0';
+  if (const char* e = getenv("PARD_NO_FUSE")) c->use_fused = e[0] == '0';
   c->prefilled.assign(max_batch, 0);
   c->draft_k.assign(max_batch, 0);
 
@@ -958,7 +998,8 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
       hipHostMalloc((void**)&c->h_gather_idx, sizeof(size_t) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_gather_out, sizeof(float) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_out, sizeof(int) * max_ctx, hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_clock, sizeof(PhaseClock), hipHostMallocDefault) != hipSuccess)
+      hipHostMalloc((void**)&c->h_clock, sizeof(PhaseClock), hipHostMallocDefault) != hipSuccess ||
+      hipHostMalloc((void**)&c->h_fuse_err, sizeof(int), hipHostMallocDefault) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   {
     int dev = 0, khz = 0;
@@ -973,11 +1014,18 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
 
   for (int w = 0; w < 2; ++w)
     if (generate(c, w) != PARD_OK) return bail(PARD_ERR_DEVICE);
+  // occupancy of the fused QKV+attention kernels, asked once here rather than
+  // during a graph capture
+  for (int w = 0; w < 2; ++w)
+    for (int mt = 1; mt <= 4; ++mt)
+      for (int S = 1; S <= 2; ++S) (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim);
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[1].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->split_counters, 0, sizeof(int) * kSplitCounters, c->stream) != hipSuccess ||
       hipMemsetAsync(c->clock_dev, 0, sizeof(PhaseClock), c->stream) != hipSuccess ||
+      hipMemsetAsync(c->fuse_cnt, 0, sizeof(int) * kFuseInts, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->fuse_err, 0, sizeof(int) * 64, c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   *out = c;
@@ -993,6 +1041,7 @@ void pard_free(pard_ctx* c) {
   if (c->h_gather_out) (void)hipHostFree(c->h_gather_out);
   if (c->h_out) (void)hipHostFree(c->h_out);
   if (c->h_clock) (void)hipHostFree(c->h_clock);
+  if (c->h_fuse_err) (void)hipHostFree(c->h_fuse_err);
   if (c->ev_start) (void)hipEventDestroy(c->ev_start);
   if (c->ev_stop) (void)hipEventDestroy(c->ev_stop);
   for (hipEvent_t e : c->timer_ev) (void)hipEventDestroy(e);

@@ -41,6 +41,7 @@
 // k_lm_tail then reduces the tiles per row (lowest id on ties) and runs the
 // step tail: candidates for a draft pass; greedy prefix acceptance, KV
 // rollback and next-pass staging for a verify pass.
+#include "attn_tile.h"
 #include "pard_internal.h"
 
 #include <hip/hip_ext.h>
@@ -92,22 +93,26 @@ __device__ __forceinline__ float wave_incl_scan(float v, int lane) {
   return v;
 }
 
-template <int MT, int S, int EPI>
-__global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
+// One workgroup tile of the skinny GEMM: strips [tile*S, tile*S + S) over the
+// input range `split` of n_split, computed by the first nw wavefronts of the
+// workgroup; red is the [nw][S*MT*256] float LDS of the wave reduction.  With
+// FUSED (the QKV GEMM of a launch that also carries the attention reading its
+// output) the Q / K / V stores are device-scope, so that workgroups on other
+// XCDs of the same launch read them after the count-in.
+template <int MT, int S, int EPI, bool FUSED = false>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, const unsigned split, const int n_split,
+                                          const int nw, float* red) {
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
   constexpr int NJ = S * MT;         // elements per thread in the epilogue (first 256 threads)
   // k-blocks per pipeline stage: 8 KiB of W per wave (smaller for prefill-sized row counts)
   constexpr int U = MT >= 3 ? 2 : ((8 / S) > 0 ? 8 / S : 1);
-  extern __shared__ float red[];     // [NW][NE]
   __shared__ float rs_s[MT * 16];
 
-  const int tile = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
-  const int nw = blockDim.x >> 6;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // uniform per wavefront
 
   // input range of this workgroup: k-blocks [kb0, kb0 + kb_n)
-  const int kb0 = blockIdx.y * p.kb_split;
+  const int kb0 = split * p.kb_split;
   const int kb_n = min(p.kb_split, p.kb_total - kb0);
   // wave w streams k-blocks kb0 + w, kb0 + w + nw, ...: at any time the
   // workgroup reads nw consecutive k-blocks of each strip
@@ -394,14 +399,13 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   // read from, the level shared by all XCDs), so the count needs no cache
   // write-back or invalidation: each wavefront waits until its stores are
   // complete before the workgroup counts itself in.
-  const int n_split = gridDim.y;
   if (n_split > 1) {
     __shared__ int last_s;
     float* part = p.part + (size_t)tile * n_split * NE;
     if (epi) {
 #pragma unroll
       for (int j = 0; j < NJ; ++j)
-        __hip_atomic_store(part + (size_t)blockIdx.y * NE + j * 256 + tid, v[j], __ATOMIC_RELAXED,
+        __hip_atomic_store(part + (size_t)split * NE + j * 256 + tid, v[j], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
@@ -440,16 +444,21 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
           y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
         }
         const uint16_t b = f16_bits(y);
+        uint16_t* dst;
         if (n < p.q_dim) {
-          p.out[(size_t)row * p.ld_out + n] = b;
+          dst = p.out + (size_t)row * p.ld_out + n;
         } else if (n < p.q_dim + p.kv_dim) {
           const int c = n - p.q_dim;
-          p.kc[cache + (size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd)] = b;
+          dst = p.kc + cache + (size_t)(c / p.hd) * p.cap * p.hd + k_index(pos, c % p.hd, p.hd);
         } else {
           const int c = n - p.q_dim - p.kv_dim;
           const size_t blk = (size_t)(c / p.hd) * (p.cap / 32) + (pos >> 5);
-          p.vc[cache + (blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31)] = b;
+          dst = p.vc + cache + (blk * p.hd + (c % p.hd)) * 32 + v_slot(pos & 31);
         }
+        if constexpr (FUSED)
+          __hip_atomic_store(dst, b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else
+          *dst = b;
       }
     }
   } else if constexpr (EPI == EPI_RESID) {
@@ -528,6 +537,59 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
         sw = wave_sum(sw);
         if (lane == 0) p.amax_sum[(size_t)r * p.amax_stride + tile] = sw;
       }
+    }
+  }
+}
+
+template <int MT, int S, int EPI>
+__global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
+  extern __shared__ float red[];     // [NW][NE]
+  gemm_tile<MT, S, EPI>(p, blockIdx.x, blockIdx.y, gridDim.y, blockDim.x >> 6, red);
+}
+
+// Decode passes over contexts of one attention chunk: the QKV GEMM and the
+// attention that reads its output in one launch.  Workgroups [0, n_tiles)
+// are GEMM tiles (wavefronts 0-3 compute, 4-7 only take part in the
+// workgroup's two barriers); each stores its Q / K / V at device scope, waits
+// for its stores, and counts itself in.  The remaining workgroups are the
+// attention workgroups of k_attn's single-chunk plan (KV head, query group,
+// sequence): the first pair of key tiles, when it precedes the pass, is
+// requested before they wait for every GEMM tile; Q and the keys of the pass
+// are then read at device scope.  Attention workgroups depart on the second
+// counter and the last one resets them all (every wait is bounded; see
+// attn::fuse_wait).  All workgroups of the launch are co-resident (the host
+// checks the grid against the device's occupancy), and GEMM tiles never wait,
+// so the attention workgroups' waits end.
+template <int MT, int S, int HD>
+__global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnArgs a, const FuseCtl f) {
+  extern __shared__ float red[];     // [4][S * MT * 256] of the GEMM tiles
+  const int tid = threadIdx.x;
+  if ((int)blockIdx.x < g.n_tiles) {
+    if (tid < 256) {
+      gemm_tile<MT, S, EPI_QKV, true>(g, blockIdx.x, 0, 1, 4, red);
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's stores are complete
+    } else {
+      __syncthreads();                              // the tile's reduction barrier
+    }
+    __syncthreads();
+    if (tid == 0)
+      __hip_atomic_fetch_add(f.counters + (blockIdx.x % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
+                             __HIP_MEMORY_SCOPE_AGENT);
+    return;
+  }
+  const int i = blockIdx.x - g.n_tiles;
+  const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
+  const unsigned z = i / (a.n_kv * a.n_qblocks);
+  attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f);
+  attn::fuse_wait(f);                               // a workgroup that left early has waited too
+  __syncthreads();
+  if (tid == 0) {
+    int* out = f.counters + kFuseLanes * kFuseStride;
+    const int prev = __hip_atomic_fetch_add(out, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (prev == f.n_cons - 1) {
+      for (int j = 0; j < kFuseLanes; ++j)
+        __hip_atomic_store(f.counters + j * kFuseStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_store(out, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -1517,7 +1579,79 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, L
   return hipErrorInvalidValue;
 }
 
+template <int MT, int S, int HD>
+hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, hipStream_t st,
+                               LaunchEvents ev, int* capacity) {
+  const size_t lds = (size_t)4 * S * MT * 256 * sizeof(float);
+  if (capacity) {
+    int per_cu = 0, dev = 0;
+    hipDeviceProp_t prop;
+    if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_qkv_attn<MT, S, HD>, 512, lds) != hipSuccess)
+      return hipErrorInvalidValue;
+    *capacity = per_cu * prop.multiProcessorCount;
+    return hipSuccess;
+  }
+  const int grid = g.n_tiles + f.n_cons;
+  if (ev.start) {
+    hipExtLaunchKernelGGL(k_qkv_attn<MT, S, HD>, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, f);
+  } else {
+    k_qkv_attn<MT, S, HD><<<grid, 512, lds, st>>>(g, a, f);
+  }
+  return hipGetLastError();
+}
+
+template <int MT, int S>
+hipError_t launch_qkv_attn_hd(int hd, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, hipStream_t st,
+                              LaunchEvents ev, int* capacity) {
+  if (hd == 64) return launch_qkv_attn_one<MT, S, 64>(g, a, f, st, ev, capacity);
+  if (hd == 128) return launch_qkv_attn_one<MT, S, 128>(g, a, f, st, ev, capacity);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_qkv_attn_any(int mt, int S, int hd, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                               hipStream_t st, LaunchEvents ev, int* capacity) {
+  switch (mt * 4 + S) {
+    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, g, a, f, st, ev, capacity);
+    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, g, a, f, st, ev, capacity);
+    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, g, a, f, st, ev, capacity);
+    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, g, a, f, st, ev, capacity);
+    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, g, a, f, st, ev, capacity);
+    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, g, a, f, st, ev, capacity);
+    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, g, a, f, st, ev, capacity);
+    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, g, a, f, st, ev, capacity);
+  }
+  return hipErrorInvalidValue;
+}
+
 }  // namespace
+
+int qkv_attn_capacity(int mt, int S, int head_dim) {
+  static int cache[5][3][2];   // [mt][S][hd 64 / 128]: co-resident workgroups (0: not yet asked, -1: unsupported)
+  if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128)) return 0;
+  int& c = cache[mt][S][head_dim == 128];
+  if (c == 0) {
+    int n = 0;
+    c = launch_qkv_attn_any(mt, S, head_dim, GemmArgs{}, AttnArgs{}, FuseCtl{}, nullptr, LaunchEvents{}, &n) ==
+                hipSuccess && n > 0 ? n : -1;
+  }
+  return c > 0 ? c : 0;
+}
+
+hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                           hipStream_t st, LaunchEvents ev) {
+  // the GEMM tiles cover the strips exactly, one input range; the attention
+  // part is the single-chunk plan with one query tile per workgroup
+  if (g.n_tiles < 1 || g.ksplit != 1 || g.kb_split < g.kb_total || (size_t)g.n_tiles * S != (size_t)g.n_strips)
+    return hipErrorInvalidValue;
+  if (!a.wide || a.n_splits != 1 || a.nqt != 1 || a.split_len % 128 || a.n_seq < 1 || a.n_seq > kMaxPassSeqs)
+    return hipErrorInvalidValue;
+  if (!f.counters || !f.err || f.n_prod != g.n_tiles || f.n_cons != a.n_kv * a.n_qblocks * a.n_seq)
+    return hipErrorInvalidValue;
+  const int cap = qkv_attn_capacity(mt, S, head_dim);
+  if (cap <= 0 || g.n_tiles + f.n_cons > cap) return hipErrorInvalidValue;
+  return launch_qkv_attn_any(mt, S, head_dim, g, a, f, st, ev, nullptr);
+}
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {
   if (nw < 4 || nw > 8 || S < 1 || (size_t)nw * S * mt * 1024 > 64 * 1024) return hipErrorInvalidValue;

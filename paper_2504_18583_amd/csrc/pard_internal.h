@@ -249,6 +249,21 @@ struct AttnArgs {
   int wide;                                   // 1: one chunk per workgroup of 8 waves (n_splits == 1)
 };
 
+// A launch that carries a producer phase and a consumer phase (the QKV GEMM
+// and the decode attention that reads its output): producer workgroup b
+// counts itself in on counter b % kFuseLanes once its stores are complete;
+// consumers wait for n_prod arrivals in all, then count themselves out on the
+// last counter, and the last of them resets every counter to zero for the
+// next launch.  err is set if a wait exceeds its bounded spin.
+constexpr int kFuseLanes = 8;      // producer counters (spread over XCDs and memory channels)
+constexpr int kFuseStride = 64;    // ints between two counters
+constexpr int kFuseInts = (kFuseLanes + 1) * kFuseStride;   // producer counters, then the consumer counter
+struct FuseCtl {
+  int* counters = nullptr;         // kFuseInts ints, zero between launches
+  int n_prod = 0, n_cons = 0;
+  int* err = nullptr;
+};
+
 // Optional timing events of one launch (recorded at the kernel's start and end).
 struct LaunchEvents {
   hipEvent_t start = nullptr, stop = nullptr;
@@ -268,6 +283,13 @@ struct CodArgs {
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st,
                        LaunchEvents ev = LaunchEvents{});
 hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEvents ev = LaunchEvents{});
+// QKV GEMM (mt row tiles, S strips per workgroup, one input range) and the
+// single-chunk decode attention reading its output, in one launch; only when
+// every workgroup of it is co-resident (qkv_attn_capacity: workgroups the
+// device holds at once, 0 if the shape has no fused kernel).
+int qkv_attn_capacity(int mt, int S, int head_dim);
+hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                           hipStream_t st, LaunchEvents ev = LaunchEvents{});
 hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st);
 hipError_t launch_stage(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);

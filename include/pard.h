@@ -317,6 +317,26 @@ pard_status pard_cod_build(const int32_t *tokens, const int64_t *tok_offsets, in
                            int32_t *out_len, void *workspace, size_t workspace_bytes,
                            float *kernel_ms, void *hip_stream);
 
+/* pard_cod_build without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, serving loops,
+ * harnesses that forbid hipMalloc).  The device copy of the two offset arrays
+ * lives in a fixed scratch array that the library holds on every GPU it runs
+ * on (1 MiB each, until the process ends), so n_samples is limited to
+ * PARD_COD_NOALLOC_MAX_SAMPLES (CAPACITY above it, before any device work).
+ * The call allocates no device memory and reports no kernel time; the current
+ * device must be the one hip_stream belongs to (the scratch of that device is
+ * used; its address is looked up on the first call on each device).  Every
+ * call on a GPU shares that GPU's scratch: calls that overlap on one GPU (other
+ * threads, other streams) race and must be serialised by the caller.  Nothing
+ * in the scratch needs clearing: each call writes both arrays before its
+ * kernel reads them.  Other arguments, outputs and errors as pard_cod_build. */
+#define PARD_COD_NOALLOC_MAX_SAMPLES 65535
+pard_status pard_cod_build_noalloc(const int32_t *tokens, const int64_t *tok_offsets, int32_t n_samples,
+                                   int32_t K, double r, double r_min, int32_t mask_id, uint64_t seed,
+                                   const int64_t *out_offsets, int32_t *out_ids, int32_t *out_labels,
+                                   int32_t *out_pos, int32_t *out_section, int32_t *out_column,
+                                   int32_t *out_len, void *hip_stream);
+
 /* Message of the last error on this context (never NULL; "" if none). */
 const char *pard_last_error(const pard_ctx *ctx);
 

@@ -73,6 +73,9 @@ _sig = {
                                  C.c_double, C.c_int32, C.c_uint64, C.POINTER(C.c_int64), C.c_void_p,
                                  C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p,
                                  C.c_void_p, C.c_size_t, C.POINTER(C.c_float), C.c_void_p]),
+    "pard_cod_build_noalloc": (C.c_int, [C.c_void_p, C.POINTER(C.c_int64), C.c_int32, C.c_int32, C.c_double,
+                                         C.c_double, C.c_int32, C.c_uint64, C.POINTER(C.c_int64), C.c_void_p,
+                                         C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p, C.c_void_p]),
     "pard_read_logits": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.POINTER(C.c_float), C.c_int32,
                                    C.c_int32]),
     "pard_read_weight": (C.c_int, [_CTX, C.c_int32, C.c_int32, C.c_int32, C.c_int32, C.c_int32,
@@ -178,6 +181,38 @@ def cod_build(tokens, tok_offsets: Sequence[int], k: int, r: float, r_min: float
     if rc != PARD_OK:
         raise PardError(rc, "pard_cod_build failed")
     return (out_offs, out, out_len, ms.value) if timing else (out_offs, out, out_len)
+
+
+PARD_COD_NOALLOC_MAX_SAMPLES = 65535
+
+
+def cod_build_noalloc(tokens, tok_offsets: Sequence[int], k: int, r: float, r_min: float, mask_id: int, seed: int,
+                      stream=None):
+    """pard_cod_build_noalloc: as cod_build, with the offsets staged in the
+    library's fixed device scratch instead of a workspace.  The output tensors
+    are allocated here (by the caller of the C function)."""
+    import torch
+    offs = np.ascontiguousarray(np.asarray(tok_offsets, np.int64))
+    n = len(offs) - 1
+    out_offs = np.zeros(max(n, 0) + 1, np.int64)
+    total = lib.pard_cod_layout(offs.ctypes.data_as(C.POINTER(C.c_int64)), n, k, float(r), float(r_min),
+                                out_offs.ctypes.data_as(C.POINTER(C.c_int64))) if n >= 1 else -1
+    if total < 0:
+        raise PardError(PARD_ERR_ARG, "cod_build_noalloc: empty batch, bad parameters or a sample outside the lengths")
+    dev = tokens.device
+    out = {name: torch.empty(total, dtype=torch.int32, device=dev)
+           for name in ("ids", "labels", "pos", "section", "column")}
+    out_len = torch.empty(n, dtype=torch.int32, device=dev)
+    st = stream if stream is not None else torch.cuda.current_stream(dev).cuda_stream
+    rc = lib.pard_cod_build_noalloc(C.c_void_p(tokens.data_ptr()), offs.ctypes.data_as(C.POINTER(C.c_int64)), n, k,
+                                    float(r), float(r_min), mask_id, int(seed) & ((1 << 64) - 1),
+                                    out_offs.ctypes.data_as(C.POINTER(C.c_int64)),
+                                    *[C.c_void_p(out[name].data_ptr()) for name in ("ids", "labels", "pos", "section",
+                                                                                    "column")],
+                                    C.c_void_p(out_len.data_ptr()), C.c_void_p(st))
+    if rc != PARD_OK:
+        raise PardError(rc, "pard_cod_build_noalloc failed")
+    return out_offs, out, out_len
 
 
 class Engine:

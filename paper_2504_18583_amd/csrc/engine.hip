@@ -8,6 +8,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
@@ -1447,27 +1448,36 @@ size_t pard_cod_workspace_bytes(int32_t n_samples) {
   return n_samples < 1 ? 0 : align256(2 * sizeof(int64_t) * ((size_t)n_samples + 1));
 }
 
-pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
-                           double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets, int32_t* out_ids,
-                           int32_t* out_labels, int32_t* out_pos, int32_t* out_section, int32_t* out_column,
-                           int32_t* out_len, void* workspace, size_t workspace_bytes, float* kernel_ms,
-                           void* hip_stream) {
-  if (!tokens || !tok_offsets || !out_offsets || !out_ids || !out_labels || !out_pos || !out_section ||
-      !out_column || !out_len || !workspace || n_samples < 1 || !cod_params_ok(K, r, r_min) ||
-      (reinterpret_cast<uintptr_t>(workspace) & 255))
+}  // extern "C"
+
+namespace {
+
+// Host-side checks of a COD batch (no device work): every sample's length fits
+// the kernel and its output region holds its capacity.  *max_cols receives the
+// longest sample's column count.
+pard_status cod_check(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
+                      double r_min, const int64_t* out_offsets, int32_t* const* outs, int32_t* out_len,
+                      int* max_cols) {
+  if (!tokens || !tok_offsets || !out_offsets || !out_len || n_samples < 1 || !cod_params_ok(K, r, r_min))
     return PARD_ERR_ARG;
-  if (workspace_bytes < pard_cod_workspace_bytes(n_samples)) return PARD_ERR_NOMEM;
-  // every sample fits the kernel and its output region holds its capacity
+  for (int i = 0; i < 5; ++i)
+    if (!outs[i]) return PARD_ERR_ARG;
   if (tok_offsets[0] < 0 || out_offsets[0] < 0) return PARD_ERR_ARG;
-  int max_cols = 1;
+  *max_cols = 1;
   for (int s = 0; s < n_samples; ++s) {
     const int64_t len = tok_offsets[s + 1] - tok_offsets[s];
     if (len < 2 || len - 1 > cod_max_columns()) return PARD_ERR_ARG;
     if (out_offsets[s + 1] - out_offsets[s] < cod_capacity(len, K, r, r_min)) return PARD_ERR_CAPACITY;
-    max_cols = std::max(max_cols, (int)(len - 1));
+    *max_cols = std::max(*max_cols, (int)(len - 1));
   }
-  hipStream_t st = reinterpret_cast<hipStream_t>(hip_stream);
-  int64_t* d_off = static_cast<int64_t*>(workspace);   // tok_offsets, then out_offsets
+  return PARD_OK;
+}
+
+// Copies both offset arrays to d_off (2 * (n_samples + 1) int64 of device
+// memory), runs the kernel on st and waits for it.
+pard_status cod_run(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
+                    double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets, int32_t* const* outs,
+                    int32_t* out_len, int max_cols, int64_t* d_off, float* kernel_ms, hipStream_t st) {
   const size_t bytes = sizeof(int64_t) * (size_t)(n_samples + 1);
   CodArgs a;
   a.k_max = K;
@@ -1475,11 +1485,11 @@ pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, in
   a.r_min = r_min;
   a.mask_id = mask_id;
   a.seed = seed;
-  a.ids = out_ids;
-  a.labels = out_labels;
-  a.pos = out_pos;
-  a.section = out_section;
-  a.column = out_column;
+  a.ids = outs[0];
+  a.labels = outs[1];
+  a.pos = outs[2];
+  a.section = outs[3];
+  a.column = outs[4];
   a.out_len = out_len;
   pard_status stt = PARD_OK;
   hipEvent_t ev[2] = {nullptr, nullptr};
@@ -1495,6 +1505,66 @@ pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, in
   for (hipEvent_t e : ev)
     if (e) (void)hipEventDestroy(e);
   return stt;
+}
+
+// Device scratch of pard_cod_build_noalloc: the device copy of its two offset
+// arrays, (n_samples + 1) int64 each, for at most PARD_COD_NOALLOC_MAX_SAMPLES
+// samples (1 MiB; every GPU the library runs on holds one until the process
+// ends).  Host code never passes `scratch` itself to the device: its name is a
+// host-side stand-in, and each GPU's copy has its own device address, looked
+// up once per device and kept in g_scratch_dev.
+static __device__ __align__(256) int64_t scratch[2 * (PARD_COD_NOALLOC_MAX_SAMPLES + 1)];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int64_t* g_scratch_dev[kMaxDevices];
+
+// Device address of the current device's scratch, looked up on the first call
+// on that device (with it current) and kept.
+pard_status scratch_address(int64_t** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return PARD_ERR_DEVICE;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_dev[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return PARD_ERR_DEVICE;
+    g_scratch_dev[dev] = static_cast<int64_t*>(p);
+  }
+  *out = g_scratch_dev[dev];
+  return PARD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+pard_status pard_cod_build(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K, double r,
+                           double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets, int32_t* out_ids,
+                           int32_t* out_labels, int32_t* out_pos, int32_t* out_section, int32_t* out_column,
+                           int32_t* out_len, void* workspace, size_t workspace_bytes, float* kernel_ms,
+                           void* hip_stream) {
+  int32_t* const outs[5] = {out_ids, out_labels, out_pos, out_section, out_column};
+  int max_cols = 1;
+  if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255) || n_samples < 1) return PARD_ERR_ARG;
+  if (workspace_bytes < pard_cod_workspace_bytes(n_samples)) return PARD_ERR_NOMEM;
+  const pard_status st = cod_check(tokens, tok_offsets, n_samples, K, r, r_min, out_offsets, outs, out_len, &max_cols);
+  if (st != PARD_OK) return st;
+  return cod_run(tokens, tok_offsets, n_samples, K, r, r_min, mask_id, seed, out_offsets, outs, out_len, max_cols,
+                 static_cast<int64_t*>(workspace), kernel_ms, reinterpret_cast<hipStream_t>(hip_stream));
+}
+
+pard_status pard_cod_build_noalloc(const int32_t* tokens, const int64_t* tok_offsets, int32_t n_samples, int32_t K,
+                                   double r, double r_min, int32_t mask_id, uint64_t seed, const int64_t* out_offsets,
+                                   int32_t* out_ids, int32_t* out_labels, int32_t* out_pos, int32_t* out_section,
+                                   int32_t* out_column, int32_t* out_len, void* hip_stream) {
+  int32_t* const outs[5] = {out_ids, out_labels, out_pos, out_section, out_column};
+  int max_cols = 1;
+  if (n_samples > PARD_COD_NOALLOC_MAX_SAMPLES) return PARD_ERR_CAPACITY;
+  const pard_status st = cod_check(tokens, tok_offsets, n_samples, K, r, r_min, out_offsets, outs, out_len, &max_cols);
+  if (st != PARD_OK) return st;
+  int64_t* d_off = nullptr;
+  if (scratch_address(&d_off) != PARD_OK) return PARD_ERR_DEVICE;
+  return cod_run(tokens, tok_offsets, n_samples, K, r, r_min, mask_id, seed, out_offsets, outs, out_len, max_cols, d_off,
+                 nullptr, reinterpret_cast<hipStream_t>(hip_stream));
 }
 
 pard_status pard_read_logits(const pard_ctx* cc, int32_t which, int32_t seq, float* out, int32_t rows,

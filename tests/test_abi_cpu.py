@@ -188,3 +188,22 @@ def test_matrices_of_2gib_or_more_are_refused(b):
     # gate/up: 2 x 65 536 x 8192 x 2 bytes = 2 GiB exactly
     ffn = replace(t, n_layers=1, d_model=8192, n_heads=64, n_kv_heads=8, head_dim=128, ffn_dim=65536)
     assert b.pard_arena_bytes(b.spec_from(ffn), b.spec_from(d), 1, 256, 4) == 0
+
+
+def test_cod_noalloc_refuses_batches_above_its_scratch(b):
+    """The allocation-free COD call stages its offsets in a fixed device
+    scratch of PARD_COD_NOALLOC_MAX_SAMPLES samples: a larger batch is refused
+    with CAPACITY before any device work (nothing is dereferenced)."""
+    import numpy as np
+    P64 = C.POINTER(C.c_int64)
+    dummy = C.c_void_p(16)
+    n = b.PARD_COD_NOALLOC_MAX_SAMPLES + 1
+    offs = np.arange(0, 3 * (n + 1), 3, dtype=np.int64)
+    out = np.zeros(n + 1, np.int64)
+    rc = b.lib.pard_cod_build_noalloc(dummy, offs.ctypes.data_as(P64), n, 4, 0.5, 0.0, 0, 0, out.ctypes.data_as(P64),
+                                      dummy, dummy, dummy, dummy, dummy, dummy, None)
+    assert rc == b.PARD_ERR_CAPACITY
+    # bad parameters are refused the same way as by pard_cod_build
+    rc = b.lib.pard_cod_build_noalloc(dummy, offs.ctypes.data_as(P64), 3, 0, 0.5, 0.0, 0, 0, out.ctypes.data_as(P64),
+                                      dummy, dummy, dummy, dummy, dummy, dummy, None)
+    assert rc == b.PARD_ERR_ARG

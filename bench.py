@@ -83,6 +83,102 @@ def copy_calibration() -> int:
     return 0
 
 
+DTYPE = "bf16 weights (fp16 encoding), fp16 activations/KV, fp16 MFMA, fp32 accumulate"
+
+
+def host_description() -> str:
+    """CPU model and numpy's BLAS, for the CPU-baseline record."""
+    model = "unknown CPU"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = "unknown BLAS"
+    try:
+        b = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{b.get('name', '?')} {b.get('version', '')}".strip()
+    except Exception:
+        pass
+    return f"{model}; numpy {np.__version__} with {blas}"
+
+
+def cpu_baseline_full(wl, tokens_per_step: float, context: int, steps: int = 2) -> dict:
+    """The oracle, as it is, timed on the host for whole steps at full depth.
+
+    The oracle's float32 weights of both models are generated first (not
+    timed), the KV caches hold `context` positions of random keys and values
+    (the step's arithmetic does not depend on their values), and `steps`
+    steps -- one draft pass over 1 pending token and K-1 masks, one verify pass
+    over K+1 rows -- are timed; the median step is reported."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    k = wl.k
+    rng = np.random.default_rng(0)
+    t0 = time.perf_counter()
+    target, draft = oracle.build_model(wl.target), oracle.build_model(wl.draft)
+    gen_s = time.perf_counter() - t0
+    log(f"cpu_baseline: oracle weights generated in {gen_s:.1f} s")
+    caches = []
+    for model in (target, draft):
+        s_ = model.spec
+        cache = oracle.KVCache(model)
+        for l in range(s_.n_layers):
+            cache.k[l] = rng.standard_normal((context, s_.n_kv_heads, s_.head_dim))
+            cache.v[l] = rng.standard_normal((context, s_.n_kv_heads, s_.head_dim))
+        caches.append(cache)
+    times = []
+    for i in range(steps):
+        t0 = time.perf_counter()
+        oracle.draft_step(draft, caches[1], [1], k, wl.mask_id)
+        oracle.verify_step(target, caches[0], 1, list(range(2, 2 + k)))
+        times.append(time.perf_counter() - t0)
+        log(f"cpu_baseline: full-depth step {i + 1}: {times[-1]:.2f} s")
+        caches[0].truncate(context)
+        caches[1].truncate(context)
+    step = statistics.median(times)
+    return {"value": round(tokens_per_step / step, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"{steps} whole steps at full depth ({wl.target.n_layers}/{wl.draft.n_layers} layers): one "
+                       f"draft pass over 1 pending + {k - 1} mask rows and one verify pass over {k + 1} rows, "
+                       f"context {context}, float64 numpy on {threads} threads; median step {step:.2f} s "
+                       f"(steps {', '.join(f'{t:.2f}' for t in times)} s; weights generated beforehand in "
+                       f"{gen_s:.0f} s, not timed); {tokens_per_step:.3f} tokens/step as measured on the GPU; "
+                       f"host: {host_description()}")}
+
+
+def copy_ceiling(nbytes: int = 2 << 30, reps: int = 10):
+    """Plain device bandwidths this box reaches, in GB/s: a device-to-device
+    copy (bytes read + written) and a read-dominated reduction (torch.sum over
+    fp16 values, bytes read); practical references beside the 8 TB/s peak."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1)
+    dst.copy_(src)
+    halves = src.view(torch.float16)
+    torch.sum(halves, dtype=torch.float32)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    ev1.record()
+    torch.cuda.synchronize()
+    copy_ms = ev0.elapsed_time(ev1) / reps
+    ev0.record()
+    for _ in range(reps):
+        torch.sum(halves, dtype=torch.float32)
+    ev1.record()
+    torch.cuda.synchronize()
+    read_ms = ev0.elapsed_time(ev1) / reps
+    del src, dst, halves
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (copy_ms * 1e-3) / 1e9, nbytes / (read_ms * 1e-3) / 1e9
+
+
 def cpu_baseline(wl, tokens_per_step: float, context: int) -> dict:
     """The oracle, as it is, timed on the host for one step at this workload's shapes.
 
@@ -273,7 +369,7 @@ def bench_batched(args, wl) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.target.n_layers}-layer d{wl.target.d_model} target / "
                                f"{wl.draft.n_layers}-layer d{wl.draft.d_model} draft, batch {n}, prompts "
@@ -418,6 +514,10 @@ def main() -> int:
     log(f"prefill ({len(prompt)} tokens, both models): {ttft_ms:.1f} ms")
 
     big = max_ctx  # n_tokens bound; max_steps decides
+    # capture every step graph the timed steps will replay (one per attention
+    # length class the context passes through), then start again from the prompt
+    eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2, max_steps=args.warmup + args.steps)
+    eng.prefill(prompt)
     if args.warmup:
         eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2, max_steps=args.warmup)
     l_t0 = eng.kv_len(B.PARD_TARGET)
@@ -443,6 +543,14 @@ def main() -> int:
         tot_bytes += bm.step_bytes(t_spec, d_spec, k, round(mean_acc), int(lt), int(lt) + 1)
     step_gbps = tot_bytes / wall / 1e9
 
+    phases = {"draft_ms_per_step": round(stats.draft_ms / steps, 4),
+              "verify_ms_per_step": round(stats.verify_ms / steps, 4),
+              "accept_ms_per_step": round(stats.accept_ms / steps, 4),
+              "note": ("device clock at pass boundaries inside the timed steps: draft pass incl. its tail; "
+                       "target pass through its lm_head; verify tail (argmax, acceptance, rollback, staging)")}
+    latency = {"p50_ms": round(stats.step_ms_p50, 4), "p90_ms": round(stats.step_ms_p90, 4),
+               "mean_ms": round(step_s * 1e3, 4)}
+
     # dominant kernel: the target's gate/up GEMM, timed with HIP events around
     # each launch on the engine's stream over a second run of the same steps
     kclass = B.PARD_TARGET * 8 + B.OP_GATEUP
@@ -467,6 +575,10 @@ def main() -> int:
                 "bytes_per_launch": gu_bytes}
 
     baselines = None if args.no_baselines else measure_baselines(eng, B, prompt, k, wall / steps, emitted / wall)
+    eng.close()
+    del eng
+    copy_gbps, read_gbps = copy_ceiling()
+    log(f"device copy: {copy_gbps:.0f} GB/s (read + write); torch.sum read: {read_gbps:.0f} GB/s")
 
     result = {
         "metric": METRIC,
@@ -479,7 +591,7 @@ def main() -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": DTYPE,
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {wl.target.n_layers}-layer d{wl.target.d_model} target / "
                                f"{wl.draft.n_layers}-layer d{wl.draft.d_model} draft, batch 1, "
@@ -489,17 +601,20 @@ def main() -> int:
         "accept_hist": hist[:k + 1],
         "step_hbm_gbps": round(step_gbps, 1),
         "step_hbm_frac": round(step_gbps / PEAK_HBM_GBPS, 4),
+        "copy_gbps": round(copy_gbps, 1),
+        "read_gbps": round(read_gbps, 1),
+        "step_frac_of_copy": round(step_gbps / copy_gbps, 4),
         "bytes_per_step": round(tot_bytes / steps),
         "context": [l_t0, l_t1],
         "ttft_ms": round(ttft_ms, 2),
         "device_ms_per_step": round(stats.elapsed_ms / steps, 4),
+        "step_latency": latency,
+        "phases": phases,
         "roofline": roofline,
         "baselines": baselines,
     }
-    eng.close()
-    del eng
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, tokens_per_step, len(prompt))
+        result["cpu_baseline"] = cpu_baseline_full(wl, tokens_per_step, len(prompt))
     print(json.dumps(result), flush=True)
     return 0
 

@@ -91,8 +91,10 @@ __device__ __forceinline__ void fuse_wait(const FuseCtl& f) {
   __builtin_amdgcn_s_barrier();
 }
 
+// Returns whether the tile went through the fused wait (FUSED only): a
+// workgroup with no work leaves before it.
 template <int HD, int NQ, int NW, bool FUSED>
-__device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,
+__device__ __forceinline__ bool attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,
                                           const FuseCtl& fc) {
   constexpr int NWA = NW;
   constexpr int MW = kAttnWaves;     // waves in the final LDS merge
@@ -109,13 +111,13 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int group = p.n_heads / p.n_kv;
-  if (sj >= p.desc->n_seq) return;                 // uniform: the whole block leaves
+  if (sj >= p.desc->n_seq) return false;           // uniform: the whole block leaves
   const PassSeq d = p.desc->seq[sj];
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
-  if (qg * QP >= n_qh) return;                     // uniform
+  if (qg * QP >= n_qh) return false;               // uniform
   const int k_begin = ch * p.split_len;            // multiple of 128
-  if (k_begin >= L_end) return;                    // uniform: chunk beyond the context
+  if (k_begin >= L_end) return false;              // uniform: chunk beyond the context
   const int k_end = min(L_end, k_begin + p.split_len);
   // wave w takes tiles w, w+NWA, ... of the chunk: the assignment does not
   // depend on where the pass ends, so tiles beyond a query's position add
@@ -426,6 +428,7 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
       *reinterpret_cast<f32x4*>(rec + q * HD + d0 + 4) = b;
     }
   }
+  return FUSED;
 }
 
 }  // namespace attn

@@ -580,8 +580,8 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
   const int i = blockIdx.x - g.n_tiles;
   const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
   const unsigned z = i / (a.n_kv * a.n_qblocks);
-  attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f);
-  attn::fuse_wait(f);                               // a workgroup that left early has waited too
+  if (!attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f))
+    attn::fuse_wait(f);                             // a workgroup with no work waits here instead
   __syncthreads();
   if (tid == 0) {
     int* out = f.counters + kFuseLanes * kFuseStride;

@@ -61,9 +61,9 @@ constexpr int kRsrcWord3 = 0x00020000;     // buffer descriptor word 3 for gfx9-
 constexpr int kCachePolicyDevice = 16;     // sc1: device scope, coherent across XCDs
 constexpr int kFuseSpinLimit = 1 << 20;    // polls before a fused wait gives up (and flags an error)
 
-// Wait until every producer workgroup of this launch has counted itself in.
-// Producers count in on kFuseLanes counters (one per XCD when workgroups are
-// dealt round-robin over the XCDs, kFuseStride ints apart), so that their
+// Wait until n workgroups of this launch have counted themselves in on the
+// kFuseLanes counters at `lanes` (one per XCD when workgroups are dealt
+// round-robin over the XCDs, kFuseStride ints apart), so that their
 // device-scope atomics and the pollers' loads do not all meet on one address.
 // Wavefront 0 polls (lane j reads counter j, the lanes add them up); the
 // other wavefronts wait at the workgroup barrier with their loads still in
@@ -71,18 +71,18 @@ constexpr int kFuseSpinLimit = 1 << 20;    // polls before a fused wait gives up
 // bounded: past kFuseSpinLimit polls the wait sets *err and returns (the
 // results are then invalid and the host reports an error), so no wavefront
 // waits forever.
-__device__ __forceinline__ void fuse_wait(const FuseCtl& f) {
+__device__ __forceinline__ void fuse_wait_on(const int* lanes, const int n, int* err) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     for (int spins = 0;; ++spins) {
-      int v = lane < kFuseLanes ? __hip_atomic_load(f.counters + lane * kFuseStride, __ATOMIC_RELAXED,
+      int v = lane < kFuseLanes ? __hip_atomic_load(lanes + lane * kFuseStride, __ATOMIC_RELAXED,
                                                     __HIP_MEMORY_SCOPE_AGENT) : 0;
       v += __shfl_xor(v, 4);
       v += __shfl_xor(v, 2);
       v += __shfl_xor(v, 1);
-      if (__shfl(v, 0) >= f.n_prod) break;
+      if (__shfl(v, 0) >= n) break;
       if (spins >= kFuseSpinLimit) {
-        if (lane == 0) __hip_atomic_store(f.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;
       }
       __builtin_amdgcn_s_sleep(4);
@@ -91,10 +91,11 @@ __device__ __forceinline__ void fuse_wait(const FuseCtl& f) {
   __builtin_amdgcn_s_barrier();
 }
 
-// Returns whether the tile went through the fused wait (FUSED only): a
-// workgroup with no work leaves before it.
+// Wait for every QKV workgroup of the launch.
+__device__ __forceinline__ void fuse_wait(const FuseCtl& f) { fuse_wait_on(f.counters, f.n_prod, f.err); }
+
 template <int HD, int NQ, int NW, bool FUSED>
-__device__ __forceinline__ bool attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,
+__device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,
                                           const FuseCtl& fc) {
   constexpr int NWA = NW;
   constexpr int MW = kAttnWaves;     // waves in the final LDS merge
@@ -111,13 +112,13 @@ __device__ __forceinline__ bool attn_tile(const AttnArgs& p, const int kvh, cons
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int group = p.n_heads / p.n_kv;
-  if (sj >= p.desc->n_seq) return false;           // uniform: the whole block leaves
+  if (sj >= p.desc->n_seq) return;                 // uniform: the whole block leaves
   const PassSeq d = p.desc->seq[sj];
   const int L_end = d.pos0 + d.n_rows;
   const int n_qh = d.n_rows * group;
-  if (qg * QP >= n_qh) return false;               // uniform
+  if (qg * QP >= n_qh) return;                     // uniform
   const int k_begin = ch * p.split_len;            // multiple of 128
-  if (k_begin >= L_end) return false;              // uniform: chunk beyond the context
+  if (k_begin >= L_end) return;                    // uniform: chunk beyond the context
   const int k_end = min(L_end, k_begin + p.split_len);
   // wave w takes tiles w, w+NWA, ... of the chunk: the assignment does not
   // depend on where the pass ends, so tiles beyond a query's position add
@@ -408,6 +409,8 @@ __device__ __forceinline__ bool attn_tile(const AttnArgs& p, const int kvh, cons
   __syncthreads();
   // each thread finishes 8 consecutive dims of one pair: one 16-byte fp16
   // store (or two 16-byte fp32 stores of the chunk record)
+  const __amdgpu_buffer_rsrc_t ors = __builtin_amdgcn_make_buffer_rsrc(
+      p.out, 0, p.act_rows * p.n_heads * HD * 2, kRsrcWord3);
   for (int e = tid; e < QP * HD / 8; e += 64 * NWA) {
     const int q = e / (HD / 8), d0 = (e % (HD / 8)) * 8;
     f32x4 a = f32x4{0.f, 0.f, 0.f, 0.f}, b = a;
@@ -421,14 +424,21 @@ __device__ __forceinline__ bool attn_tile(const AttnArgs& p, const int kvh, cons
       const int qh = qg * QP + q;
       if (qh < n_qh) {
         const int row = qh / group, head = kvh * group + qh % group;
-        store_f16x8(p.out + act_index(d.row0 + row, head * HD + d0, p.act_rows), a * linv_lds[q], b * linv_lds[q]);
+        const f32x4 a1 = a * linv_lds[q], b1 = b * linv_lds[q];
+        if constexpr (FUSED) {   // read in this launch by the O-projection workers: device scope
+          const u32x4 v = u32x4{pack_f16x2(a1[0], a1[1]), pack_f16x2(a1[2], a1[3]), pack_f16x2(b1[0], b1[1]),
+                                pack_f16x2(b1[2], b1[3])};
+          __builtin_amdgcn_raw_buffer_store_b128(v, ors, (int)act_index(d.row0 + row, head * HD + d0, p.act_rows) * 2, 0,
+                                                 kCachePolicyDevice);
+        } else {
+          store_f16x8(p.out + act_index(d.row0 + row, head * HD + d0, p.act_rows), a1, b1);
+        }
       }
     } else {
       *reinterpret_cast<f32x4*>(rec + q * HD + d0) = a;
       *reinterpret_cast<f32x4*>(rec + q * HD + d0 + 4) = b;
     }
   }
-  return FUSED;
 }
 
 }  // namespace attn

@@ -155,10 +155,18 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta, RopeSca
 // first normalised GEMM's operand xg = fp16(x * g) and the row's sum of squares.
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc,
                                                float* x, const float* g, uint16_t* xg, int act_rows, float* ss,
-                                               int ss_stride, unsigned long long* t_start) {
+                                               int ss_stride, unsigned long long* t_start, int* fuse_cnt,
+                                               int n_sets) {
   __shared__ float wsum[4];
   const int r = blockIdx.x;
   if (r == 0 && threadIdx.x == 0 && t_start) *t_start = wall_clock64();
+  // the pass's fused-launch counters start at zero (their last use was in an
+  // earlier launch)
+  if (r == 0 && fuse_cnt) {
+    for (int i = threadIdx.x; i < n_sets * 2 * kFuseLanes; i += blockDim.x)
+      __hip_atomic_store(fuse_cnt + (size_t)(i / (2 * kFuseLanes)) * kFuseInts + (i % (2 * kFuseLanes)) * kFuseStride, 0,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   if (r >= desc->n_rows) return;
   const int id = desc->ids[r];
   const size_t strip = (size_t)(id >> 4);
@@ -230,8 +238,9 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const R
 
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, int act_rows, float* ss, int ss_stride, int max_rows,
-                        unsigned long long* t_start, hipStream_t st) {
-  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss, ss_stride, t_start);
+                        unsigned long long* t_start, int* fuse_cnt, int n_sets, hipStream_t st) {
+  k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss, ss_stride, t_start, fuse_cnt,
+                                    n_sets);
   return hipGetLastError();
 }
 

@@ -224,11 +224,14 @@ struct pard_ctx {
   PhaseClock* clock_dev = nullptr;
   PhaseClock* h_clock = nullptr;
   double clock_khz = 0.0;
-  // QKV GEMM + decode attention in one launch: its counters and wait-error flag
+  // QKV GEMM + decode attention (+ O-projection) in one launch: one counter
+  // set per layer of each model (the target's layers, then the draft's) and
+  // the wait-error flag
   int* fuse_cnt = nullptr;
   int* fuse_err = nullptr;
   int* h_fuse_err = nullptr;
   bool use_fused = true;
+  bool use_fused_o = true;
   // captured fused steps (draft pass + verify pass), replayed on `stream`
   struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
@@ -329,6 +332,12 @@ void derive(ModelDev& M, const pard_model_spec& s, int max_ctx) {
   M.group = s.n_heads / s.n_kv_heads;
   M.p_qkv = plan_gemm(EPI_QKV, M.nqkv, M.d);
   M.p_o = plan_gemm(EPI_RESID, M.d, M.q_dim);
+  // one strip per workgroup: eight wavefronts over the input (at every row
+  // tile count), as the O units fused into the QKV + attention launch use,
+  // so a row's O-projection is summed in the same order whether or not its
+  // pass runs fused (the unfused launch measured 8.3 -> 10.9 us at the 8B
+  // shape for it; 16k-context 8B/1B step 4.53 -> 4.57 ms)
+  if (pick_S(EPI_RESID, M.p_o.n_strips, 1) == 1) M.p_o.nw = 8;
   M.p_gu = plan_gemm(EPI_SWIGLU, 2 * M.f_pad, M.d);
   M.p_d = plan_gemm(EPI_RESID, M.d, M.f_pad);
   M.p_lm = plan_gemm(EPI_LOGITS, s.vocab, M.d);
@@ -393,7 +402,7 @@ size_t layout(pard_ctx* c, char* base) {
   c->gather_idx_dev = b.take<size_t>(kGatherMax);
   c->gather_out_dev = b.take<float>(kGatherMax);
   c->clock_dev = b.take<PhaseClock>(1);
-  c->fuse_cnt = b.take<int>(kFuseInts);
+  c->fuse_cnt = b.take<int>((size_t)kFuseInts * (c->m[0].spec.n_layers + c->m[1].spec.n_layers));
   c->fuse_err = b.take<int>(64);
   return align256(b.off);
 }
@@ -496,6 +505,30 @@ GemmArgs gemm_base(const ModelDev& M, const uint16_t* W, int act_rows) {
   return a;
 }
 
+// The fused launches' counter sets of model w (one per layer).
+int* fuse_counters(pard_ctx* c, int w) {
+  return c->fuse_cnt + (w == 0 ? 0 : (size_t)kFuseInts * c->m[0].spec.n_layers);
+}
+
+// O-projection + residual: x += attn W_o^T, then fp16(x * g_mlp) and the row
+// sums of squares for the gate/up GEMM.
+GemmArgs o_args(const ModelDev& M, const Layer& L, int act_rows) {
+  GemmArgs a = gemm_base(M, L.wo, act_rows);
+  a.A = M.attn;
+  a.lda = M.q_dim;
+  a.x = M.x;
+  a.ldx = M.d;
+  a.g_next = L.g_mlp;
+  a.xg = M.xg;
+  a.ss_out = M.ss;
+  a.kb_total = M.p_o.kb_total;
+  a.n_strips = M.p_o.n_strips;
+  a.n_tiles = M.p_o.n_strips;
+  a.ksplit = 1;
+  a.kb_split = M.p_o.kb_total;
+  return a;
+}
+
 struct PassSpec {
   int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
   int typ_rows = 0;       // row count the split plan is tuned for (0: max_rows)
@@ -554,7 +587,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   {
     Timed t(c, cls0 + 0);
     HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, act_rows, M.ss,
-                            std::max(1, M.ss_tiles_max), ps.max_rows, &c->clock_dev->pass_start[w], c->stream));
+                            std::max(1, M.ss_tiles_max), ps.max_rows, &c->clock_dev->pass_start[w],
+                            fuse_counters(c, w), s.n_layers, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
   // attention plan: one workgroup per (sequence, KV head, query group, key
@@ -598,6 +632,22 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   const bool fused = c->use_fused && !rows && wide && nqt == 1 && M.p_qkv.ksplit == 1 && S_q > 0 &&
                      M.p_qkv.n_strips % S_q == 0 &&
                      M.p_qkv.n_strips / S_q + n_attn_wg <= qkv_attn_capacity(mt_q, S_q, s.head_dim);
+  // one row tile: the O-projection joins the launch too, its weights
+  // streaming while the attention runs.  Workers are the QKV workgroups plus
+  // extra ones in the room the device has left; the extras start with the
+  // launch and take two units where the strips outnumber the workers.  The
+  // units sum over eight wavefronts, as the unfused O-projection does.
+  FuseCtl fo;
+  bool fused_o = false;
+  if (fused && c->use_fused_o && mt_q == 1 && M.p_o.ksplit == 1 && M.p_o.nw == 8) {
+    const int n_qkv = M.p_qkv.n_strips / S_q;
+    const int cap = qkv_attn_capacity(1, S_q, s.head_dim, M.p_o.kb_total);
+    const int room = cap - n_qkv - n_attn_wg;
+    fo.o_units = M.p_o.n_strips;
+    fo.o_extra = std::max(0, std::min(room, fo.o_units - n_qkv));
+    fo.o_two = std::max(0, fo.o_units - n_qkv - fo.o_extra);
+    fused_o = cap > 0 && room >= 0 && fo.o_two <= fo.o_extra;
+  }
   for (int l = 0; l < s.n_layers; ++l) {
     const Layer& L = M.layers[l];
     uint16_t* kc = M.kcache + layer_kv * l;
@@ -645,11 +695,13 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
         a.n_tiles = M.p_qkv.n_strips / S_q;
         a.ksplit = 1;
         a.kb_split = M.p_qkv.kb_total;
-        FuseCtl f;
-        f.counters = c->fuse_cnt;
+        FuseCtl f = fused_o ? fo : FuseCtl{};
+        f.counters = fuse_counters(c, w) + (size_t)l * kFuseInts;
         f.err = c->fuse_err;
         f.n_prod = a.n_tiles;
         f.n_cons = n_attn_wg;
+        GemmArgs o{};
+        if (fused_o) o = o_args(M, L, act_rows);
         // the kernel timer's QKV class covers the fused launch (attention included)
         LaunchEvents ev;
         if (c->timer_class == cls0 + 1 && c->timer_used < c->timer_max) {
@@ -657,7 +709,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
           ev.stop = c->timer_ev[2 * c->timer_used + 1];
           ++c->timer_used;
         }
-        HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, c->stream, ev));
+        HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, fused_o ? &o : nullptr, c->stream, ev));
       } else {
         HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
       }
@@ -666,16 +718,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
       Timed t(c, cls0 + 2);
       HIP_TRY(c, launch_attention(s.head_dim, aa, c->stream));
     }
-    {  // O-projection + residual
-      GemmArgs a = gemm_base(M, L.wo, act_rows);
-      a.A = M.attn;
-      a.lda = M.q_dim;
-      a.x = M.x;
-      a.ldx = M.d;
-      a.g_next = L.g_mlp;
-      a.xg = M.xg;
-      a.ss_out = M.ss;
-      HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, ps.max_rows, typ, a, M.p_o));
+    if (!fused_o) {  // O-projection + residual
+      HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, ps.max_rows, typ, o_args(M, L, act_rows), M.p_o));
     }
     {  // norm + gate/up + SiLU * up
       GemmArgs a = gemm_base(M, L.wgu, act_rows);
@@ -987,6 +1031,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   c->hist.assign(max_batch, {});
   if (const char* e = getenv("PARD_NO_GRAPH")) c->use_graphs = e[0] == '0';
   if (const char* e = getenv("PARD_NO_FUSE")) c->use_fused = e[0] == '0';
+  if (const char* e = getenv("PARD_NO_FUSE_O")) c->use_fused_o = e[0] == '0';
   c->prefilled.assign(max_batch, 0);
   c->draft_k.assign(max_batch, 0);
 
@@ -1019,13 +1064,17 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   // during a graph capture
   for (int w = 0; w < 2; ++w)
     for (int mt = 1; mt <= 4; ++mt)
-      for (int S = 1; S <= 2; ++S) (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim);
+      for (int S = 1; S <= 2; ++S) {
+        (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim);
+        if (mt == 1) (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim, c->m[w].p_o.kb_total);
+      }
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[1].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->split_counters, 0, sizeof(int) * kSplitCounters, c->stream) != hipSuccess ||
       hipMemsetAsync(c->clock_dev, 0, sizeof(PhaseClock), c->stream) != hipSuccess ||
-      hipMemsetAsync(c->fuse_cnt, 0, sizeof(int) * kFuseInts, c->stream) != hipSuccess ||
+      hipMemsetAsync(c->fuse_cnt, 0, sizeof(int) * kFuseInts * (c->m[0].spec.n_layers + c->m[1].spec.n_layers),
+                     c->stream) != hipSuccess ||
       hipMemsetAsync(c->fuse_err, 0, sizeof(int) * 64, c->stream) != hipSuccess ||
       hipStreamSynchronize(c->stream) != hipSuccess)
     return bail(PARD_ERR_DEVICE);

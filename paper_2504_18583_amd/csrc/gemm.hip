@@ -46,6 +46,7 @@
 
 #include <hip/hip_ext.h>
 
+#include <algorithm>
 #include <climits>
 #include <type_traits>
 
@@ -547,51 +548,149 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
   gemm_tile<MT, S, EPI>(p, blockIdx.x, blockIdx.y, gridDim.y, blockDim.x >> 6, red);
 }
 
-// Decode passes over contexts of one attention chunk: the QKV GEMM and the
-// attention that reads its output in one launch.  Workgroups [0, n_tiles)
-// are GEMM tiles (wavefronts 0-3 compute, 4-7 only take part in the
-// workgroup's two barriers); each stores its Q / K / V at device scope, waits
-// for its stores, and counts itself in.  The remaining workgroups are the
-// attention workgroups of k_attn's single-chunk plan (KV head, query group,
-// sequence): the first pair of key tiles, when it precedes the pass, is
-// requested before they wait for every GEMM tile; Q and the keys of the pass
-// are then read at device scope.  Attention workgroups depart on the second
-// counter and the last one resets them all (every wait is bounded; see
-// attn::fuse_wait).  All workgroups of the launch are co-resident (the host
-// checks the grid against the device's occupancy), and GEMM tiles never wait,
-// so the attention workgroups' waits end.
-template <int MT, int S, int HD>
-__global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnArgs a, const FuseCtl f) {
-  extern __shared__ float red[];     // [4][S * MT * 256] of the GEMM tiles
+// O-projection units of a fused decode-layer launch (one row tile, EPI_RESID,
+// one strip per unit, the whole input range): NU units of this worker
+// starting at strip u0.  Wavefront v of the eight holds k-blocks v, v + 8, ...
+// (KI of them; past the input range it re-reads the last one and never uses
+// it).  Every weight block is requested before the wait for the attention
+// workgroups, so the weights stream while the attention runs; the attention
+// output (written in this launch) is then read at device scope.  The eight
+// wavefront partials are summed in wave order, then the residual epilogue of
+// gemm_tile: x += Y, fp16(x * g_next) and the strip's row sums of squares.
+template <int KI, int NU>
+__device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, const int u0, float* red) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n_strips = p.n_strips, kb_total = p.kb_total;
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.W), 0, (int)min((size_t)n_strips * kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
+  u32x4 wv[NU][KI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int kb = min(wave + 8 * i, kb_total - 1);
+#pragma unroll
+    for (int j = 0; j < NU; ++j)
+      wv[j][i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, ((u0 + j) * 64 + lane) * 16, kb * n_strips * 1024,
+                                                       kCachePolicyNT);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  // epilogue element of this thread: unit ej, row rsub, column csub of the
+  // strip (the MFMA output layout; threads < 256 * NU)
+  const int row_count = p.desc->n_rows;
+  const bool epi = tid < 256 * NU;
+  const int ej = min(tid >> 8, NU - 1);
+  const int rsub = (lane >> 4) * 4 + ((tid & 255) >> 6), csub = lane & 15;
+  const int n = (u0 + ej) * 16 + csub;
+  float x_old = 0.f, g = 0.f;
+  if (epi && rsub < row_count) {
+    x_old = p.x[(size_t)rsub * p.ldx + n];
+    g = p.g_next[n];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  attn::fuse_wait_on(f.counters + kFuseLanes * kFuseStride, f.n_cons, f.err);
+  __builtin_amdgcn_sched_barrier(0);
+  // A fragment of this lane: row lane % 16, 8 columns at 8 * (lane / 16) of
+  // each k-block; rows past the pass read zeros without a memory access
+  constexpr int kOutOfRange = 0x7FFFFFF0;
+  const __amdgpu_buffer_rsrc_t ars = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.A), 0, p.act_rows * p.lda * 2, kRsrcWord3);
+  const int a_voff = (lane & 15) < row_count ? (lane & 15) * 64 + (lane >> 4) * 16 : kOutOfRange;
+  u32x4 av[KI];
+#pragma unroll
+  for (int i = 0; i < KI; ++i)
+    av[i] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff, min(wave + 8 * i, kb_total - 1) * (p.act_rows * 64),
+                                                  attn::kCachePolicyDevice);
+  f32x4 acc[NU];
+#pragma unroll
+  for (int j = 0; j < NU; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const u32x4 a = wave + 8 * i < kb_total ? av[i] : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < NU; ++j)
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, wv[j][i]),
+                                                      acc[j], 0, 0, 0);
+  }
+#pragma unroll
+  for (int j = 0; j < NU; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[(wave * NU + j) * 256 + i * 64 + lane] = acc[j][i];
+  __syncthreads();
+  if (!epi) return;   // whole wavefronts; no barrier follows
+  float v = red[ej * 256 + (tid & 255)];
+  for (int w = 1; w < 8; ++w) v += red[(w * NU + ej) * 256 + (tid & 255)];
+  float sq = 0.f;
+  if (rsub < row_count) {
+    const float xn = x_old + v;                      // residual + projection
+    p.x[(size_t)rsub * p.ldx + n] = xn;
+    p.xg[act_index(rsub, n, p.act_rows)] = f16_bits(xn * g);
+    sq = xn * xn;
+  }
+  const float t = sum16(sq);
+  if (csub == 0) p.ss_out[(size_t)rsub * p.ss_stride + u0 + ej] = t;
+}
+
+// The O units of worker w (see FuseCtl), if it has any.
+template <int KI>
+__device__ __forceinline__ void o_part(const GemmArgs& p, const FuseCtl& f, const int w, float* red) {
+  if (w < f.o_two)
+    o_units<KI, 2>(p, f, 2 * w, red);
+  else if (f.o_two + w < f.o_units)
+    o_units<KI, 1>(p, f, f.o_two + w, red);
+}
+
+// Decode passes over contexts of one attention chunk: the QKV GEMM, the
+// attention that reads its output and (OKI > 0) the O-projection of the
+// attention output in one launch.  Workgroups [0, n_tiles) are GEMM tiles
+// (wavefronts 0-3 compute, 4-7 only take part in the workgroup's barriers);
+// each stores its Q / K / V at device scope, waits for its stores, and counts
+// itself in.  The next n_cons workgroups are the attention workgroups of
+// k_attn's single-chunk plan (KV head, query group, sequence): the first pair
+// of key tiles, when it precedes the pass, is requested before they wait for
+// every GEMM tile; Q and the keys of the pass are then read at device scope.
+// With O units their output is stored at device scope and they count
+// themselves in; O-projection workers (the QKV workgroups once their tile is
+// done, and o_extra workgroups after the attention ones) request their
+// weights, wait for every attention workgroup and finish their units
+// (o_part).  The counters: FuseCtl.  All workgroups of the launch are
+// co-resident (the host checks the grid against the device's occupancy), a
+// phase waits only for earlier phases, and every wait is bounded
+// (attn::fuse_wait_on), so every wait ends.
+template <int MT, int S, int HD, int OKI>
+__global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnArgs a, const FuseCtl f,
+                                                  const GemmArgs o) {
+  extern __shared__ float red[];     // GEMM tiles: [4][S * MT * 256]; O units: [8][2][256]
   const int tid = threadIdx.x;
-  if ((int)blockIdx.x < g.n_tiles) {
+  const int b = blockIdx.x;
+  if (b < g.n_tiles) {
     if (tid < 256) {
-      gemm_tile<MT, S, EPI_QKV, true>(g, blockIdx.x, 0, 1, 4, red);
+      gemm_tile<MT, S, EPI_QKV, true>(g, b, 0, 1, 4, red);
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's stores are complete
     } else {
       __syncthreads();                              // the tile's reduction barrier
     }
     __syncthreads();
     if (tid == 0)
-      __hip_atomic_fetch_add(f.counters + (blockIdx.x % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
+      __hip_atomic_fetch_add(f.counters + (b % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
+    if constexpr (OKI > 0) o_part<OKI>(o, f, f.o_extra + b, red);
     return;
   }
-  const int i = blockIdx.x - g.n_tiles;
-  const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
-  const unsigned z = i / (a.n_kv * a.n_qblocks);
-  if (!attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f))
-    attn::fuse_wait(f);                             // a workgroup with no work waits here instead
-  __syncthreads();
-  if (tid == 0) {
-    int* out = f.counters + kFuseLanes * kFuseStride;
-    const int prev = __hip_atomic_fetch_add(out, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (prev == f.n_cons - 1) {
-      for (int j = 0; j < kFuseLanes; ++j)
-        __hip_atomic_store(f.counters + j * kFuseStride, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(out, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  const int i = b - g.n_tiles;
+  if (i < f.n_cons) {
+    const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
+    const unsigned z = i / (a.n_kv * a.n_qblocks);
+    attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f);
+    if constexpr (OKI > 0) {
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's output stores are complete
+      __syncthreads();
+      if (tid == 0)
+        __hip_atomic_fetch_add(f.counters + (kFuseLanes + i % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
     }
+    return;
   }
+  if constexpr (OKI > 0) o_part<OKI>(o, f, i - f.n_cons, red);
 }
 
 __device__ void commit_verify(const TailArgs& p, const PassSeq& ps, int a, int bonus, const int* res);
@@ -1579,67 +1678,87 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, L
   return hipErrorInvalidValue;
 }
 
-template <int MT, int S, int HD>
-hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, hipStream_t st,
-                               LaunchEvents ev, int* capacity) {
-  const size_t lds = (size_t)4 * S * MT * 256 * sizeof(float);
+template <int MT, int S, int HD, int OKI>
+hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, const GemmArgs& o,
+                               hipStream_t st, LaunchEvents ev, int* capacity) {
+  const size_t lds = std::max((size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0) * sizeof(float);
   if (capacity) {
     int per_cu = 0, dev = 0;
     hipDeviceProp_t prop;
     if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_qkv_attn<MT, S, HD>, 512, lds) != hipSuccess)
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_qkv_attn<MT, S, HD, OKI>, 512, lds) != hipSuccess)
       return hipErrorInvalidValue;
     *capacity = per_cu * prop.multiProcessorCount;
     return hipSuccess;
   }
-  const int grid = g.n_tiles + f.n_cons;
+  const int grid = g.n_tiles + f.n_cons + f.o_extra;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_qkv_attn<MT, S, HD>, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, f);
+    hipExtLaunchKernelGGL(k_qkv_attn<MT, S, HD, OKI>, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u,
+                          g, a, f, o);
   } else {
-    k_qkv_attn<MT, S, HD><<<grid, 512, lds, st>>>(g, a, f);
+    k_qkv_attn<MT, S, HD, OKI><<<grid, 512, lds, st>>>(g, a, f, o);
   }
   return hipGetLastError();
 }
 
-template <int MT, int S>
-hipError_t launch_qkv_attn_hd(int hd, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, hipStream_t st,
-                              LaunchEvents ev, int* capacity) {
-  if (hd == 64) return launch_qkv_attn_one<MT, S, 64>(g, a, f, st, ev, capacity);
-  if (hd == 128) return launch_qkv_attn_one<MT, S, 128>(g, a, f, st, ev, capacity);
-  return hipErrorInvalidValue;
-}
-
-hipError_t launch_qkv_attn_any(int mt, int S, int hd, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+template <int MT, int S, int HD>
+hipError_t launch_qkv_attn_oki(int oki, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, const GemmArgs& o,
                                hipStream_t st, LaunchEvents ev, int* capacity) {
-  switch (mt * 4 + S) {
-    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, g, a, f, st, ev, capacity);
-    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, g, a, f, st, ev, capacity);
-    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, g, a, f, st, ev, capacity);
-    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, g, a, f, st, ev, capacity);
-    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, g, a, f, st, ev, capacity);
-    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, g, a, f, st, ev, capacity);
-    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, g, a, f, st, ev, capacity);
-    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, g, a, f, st, ev, capacity);
+  if (oki == 0) return launch_qkv_attn_one<MT, S, HD, 0>(g, a, f, o, st, ev, capacity);
+  if constexpr (MT == 1) {
+    if (oki == 8) return launch_qkv_attn_one<MT, S, HD, 8>(g, a, f, o, st, ev, capacity);
+    if (oki == 16) return launch_qkv_attn_one<MT, S, HD, 16>(g, a, f, o, st, ev, capacity);
   }
   return hipErrorInvalidValue;
 }
 
+template <int MT, int S>
+hipError_t launch_qkv_attn_hd(int hd, int oki, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                              const GemmArgs& o, hipStream_t st, LaunchEvents ev, int* capacity) {
+  if (hd == 64) return launch_qkv_attn_oki<MT, S, 64>(oki, g, a, f, o, st, ev, capacity);
+  if (hd == 128) return launch_qkv_attn_oki<MT, S, 128>(oki, g, a, f, o, st, ev, capacity);
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_qkv_attn_any(int mt, int S, int hd, int oki, const GemmArgs& g, const AttnArgs& a,
+                               const FuseCtl& f, const GemmArgs& o, hipStream_t st, LaunchEvents ev, int* capacity) {
+  switch (mt * 4 + S) {
+    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, oki, g, a, f, o, st, ev, capacity);
+  }
+  return hipErrorInvalidValue;
+}
+
+// k-blocks per wavefront of the fused O units for an O weight of kb k-blocks
+// (0: no fused O; -1: unsupported)
+int o_ki(int kb) { return kb == 0 ? 0 : kb <= 64 ? 8 : kb <= kFuseOMaxKb ? 16 : -1; }
+
 }  // namespace
 
-int qkv_attn_capacity(int mt, int S, int head_dim) {
-  static int cache[5][3][2];   // [mt][S][hd 64 / 128]: co-resident workgroups (0: not yet asked, -1: unsupported)
-  if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128)) return 0;
-  int& c = cache[mt][S][head_dim == 128];
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb) {
+  // [mt][S][hd 64 / 128][no O, 8, 16 k-blocks per wavefront]: co-resident
+  // workgroups (0: not yet asked, -1: unsupported)
+  static int cache[5][3][2][3];
+  const int oki = o_ki(o_kb);
+  if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki < 0 || (oki > 0 && mt != 1))
+    return 0;
+  int& c = cache[mt][S][head_dim == 128][oki / 8];
   if (c == 0) {
     int n = 0;
-    c = launch_qkv_attn_any(mt, S, head_dim, GemmArgs{}, AttnArgs{}, FuseCtl{}, nullptr, LaunchEvents{}, &n) ==
-                hipSuccess && n > 0 ? n : -1;
+    c = launch_qkv_attn_any(mt, S, head_dim, oki, GemmArgs{}, AttnArgs{}, FuseCtl{}, GemmArgs{}, nullptr,
+                            LaunchEvents{}, &n) == hipSuccess && n > 0 ? n : -1;
   }
   return c > 0 ? c : 0;
 }
 
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           hipStream_t st, LaunchEvents ev) {
+                           const GemmArgs* o, hipStream_t st, LaunchEvents ev) {
   // the GEMM tiles cover the strips exactly, one input range; the attention
   // part is the single-chunk plan with one query tile per workgroup
   if (g.n_tiles < 1 || g.ksplit != 1 || g.kb_split < g.kb_total || (size_t)g.n_tiles * S != (size_t)g.n_strips)
@@ -1648,9 +1767,22 @@ hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const
     return hipErrorInvalidValue;
   if (!f.counters || !f.err || f.n_prod != g.n_tiles || f.n_cons != a.n_kv * a.n_qblocks * a.n_seq)
     return hipErrorInvalidValue;
-  const int cap = qkv_attn_capacity(mt, S, head_dim);
-  if (cap <= 0 || g.n_tiles + f.n_cons > cap) return hipErrorInvalidValue;
-  return launch_qkv_attn_any(mt, S, head_dim, g, a, f, st, ev, nullptr);
+  int oki = 0;
+  if (o) {
+    // one row tile; O units: one strip each over one input range, every
+    // worker with two units an extra workgroup
+    oki = o_ki(o->kb_total);
+    const int workers = f.o_extra + f.n_prod;
+    if (mt != 1 || oki <= 0 || o->n_strips != f.o_units || f.o_units < 1 || f.o_extra < 0 || f.o_two < 0 ||
+        f.o_two > f.o_extra || f.o_units > workers + f.o_two || o->act_rows != a.act_rows || !o->A || !o->x ||
+        !o->xg || !o->g_next || !o->ss_out || o->desc != a.desc)
+      return hipErrorInvalidValue;
+  } else if (f.o_units != 0 || f.o_extra != 0) {
+    return hipErrorInvalidValue;
+  }
+  const int cap = qkv_attn_capacity(mt, S, head_dim, o ? o->kb_total : 0);
+  if (cap <= 0 || g.n_tiles + f.n_cons + f.o_extra > cap) return hipErrorInvalidValue;
+  return launch_qkv_attn_any(mt, S, head_dim, oki, g, a, f, o ? *o : GemmArgs{}, st, ev, nullptr);
 }
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {

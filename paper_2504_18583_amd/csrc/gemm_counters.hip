@@ -20,7 +20,7 @@
 // projection).
 //
 // usage: gemm_counters [rows 9] [S 7] [P 1] [strips 1792] [kb 128] [epi swiglu|resid|qkv] [copies 1] [check 0]
-//                      [ss_tiles 1]
+//                      [ss_tiles 1] [wavefronts 4|8]
 #include <cstdio>
 #include <cstdlib>
 #include <cmath>
@@ -64,6 +64,7 @@ int main(int argc, char** argv) {
   const int copies = argc > 7 ? atoi(argv[7]) : 1;
   const bool check = argc > 8 && atoi(argv[8]) != 0;
   const int ss_tiles = argc > 9 ? atoi(argv[9]) : 1;
+  const int nw = argc > 10 ? atoi(argv[10]) : 4;
   const int epi = resid ? EPI_RESID : qkv ? EPI_QKV : EPI_SWIGLU;
   constexpr int kHd = 128, kCap = 1024, kPos0 = 512;
   const int kb_split = P > 0 ? (kb_total + P - 1) / P : 0;
@@ -71,9 +72,10 @@ int main(int argc, char** argv) {
   if (rows < 1 || rows > kMaxRows || !(S == 1 || S == 2 || S == 4 || wide_s) ||
       n_strips < 1 || (n_strips % S != 0 && S < 8) || kb_total < 1 || P < 1 || (P - 1) * kb_split >= kb_total || copies < 1 ||
       copies > 64 || (size_t)n_strips * kb_total * 1024 * copies > ((size_t)8 << 30) || ss_tiles < 1 ||
-      ss_tiles > n_strips || (qkv && ((n_strips * 16) % (6 * kHd) != 0 || check))) {
+      ss_tiles > n_strips || (qkv && ((n_strips * 16) % (6 * kHd) != 0 || check)) || (nw != 4 && nw != 8)) {
     fprintf(stderr, "bad shape: rows 1..%d, S in {1, 2, 4, 7-10 (swiglu)}, S | strips (S < 8), every input range non-empty, "
-            "copies 1..64 of at most 8 GiB in all, 1 <= ss_tiles <= strips; qkv: 6 x 128 | columns, no check\n",
+            "copies 1..64 of at most 8 GiB in all, 1 <= ss_tiles <= strips; qkv: 6 x 128 | columns, no check; "
+            "4 or 8 wavefronts\n",
             kMaxRows);
     return 2;
   }
@@ -138,7 +140,7 @@ int main(int argc, char** argv) {
   int launch = 0;
   auto run = [&]() {
     a.W = W + w_elems * (launch++ % copies);
-    return launch_gemm(epi, 1, S, 4, a, 0);
+    return launch_gemm(epi, 1, S, nw, a, 0);
   };
   for (int i = 0; i < 20; ++i) CHECK(run());
   CHECK(hipDeviceSynchronize());
@@ -150,9 +152,9 @@ int main(int argc, char** argv) {
   float ms = 0.f;
   CHECK(hipEventElapsedTime(&ms, e0, e1));
   const double us = ms * 1e3 / n;
-  printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups, %d weight copies: "
+  printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups of %d wavefronts, %d weight copies: "
          "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : qkv ? "qkv" : "swiglu", n_strips, kb_total, rows,
-         a.n_tiles, P, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
+         a.n_tiles, P, nw, copies, us, (double)w_elems * 2 / (us * 1e-6) / 1e12);
   if (check) {
     // unsplit reference and split launch per copy, x reset before each (the
     // residual epilogue updates it in place); outputs compared as fp16
@@ -169,7 +171,7 @@ int main(int argc, char** argv) {
         q.W = W + w_elems * c;
         k_fill_value<<<64, 256>>>(x, (size_t)kMaxRows * out_cols, 0.5f);
         CHECK(hipMemset(out, 0, o_elems * 2));
-        CHECK(launch_gemm(epi, 1, S, 4, q, 0));
+        CHECK(launch_gemm(epi, 1, S, nw, q, 0));
         CHECK(hipMemcpy(pass == 0 ? ref.data() : got.data(), out, o_elems * 2, hipMemcpyDeviceToHost));
       }
       const int cols = resid ? out_cols : out_cols / 2;

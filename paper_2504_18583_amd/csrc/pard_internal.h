@@ -249,19 +249,30 @@ struct AttnArgs {
   int wide;                                   // 1: one chunk per workgroup of 8 waves (n_splits == 1)
 };
 
-// A launch that carries a producer phase and a consumer phase (the QKV GEMM
-// and the decode attention that reads its output): producer workgroup b
-// counts itself in on counter b % kFuseLanes once its stores are complete;
-// consumers wait for n_prod arrivals in all, then count themselves out on the
-// last counter, and the last of them resets every counter to zero for the
-// next launch.  err is set if a wait exceeds its bounded spin.
-constexpr int kFuseLanes = 8;      // producer counters (spread over XCDs and memory channels)
+// A launch that carries the dependent phases of one decode layer: the QKV
+// GEMM, the decode attention that reads its output and, optionally, the
+// O-projection that reads the attention's output.  QKV workgroup b counts
+// itself in on counter b % kFuseLanes once its stores are complete; attention
+// workgroups wait for n_prod such arrivals in all and, when O units follow,
+// count themselves in on counter kFuseLanes + i % kFuseLanes once their own
+// output stores are complete; O-projection workers wait for n_cons of those.
+// Each layer of a model has its own set of counters, zeroed by the pass's
+// embedding launch (k_embed), so no workgroup has to reset them at the end of
+// a launch.  err is set if a wait exceeds its bounded spin.
+//
+// O units (o_units > 0): strip j of the O weight over its whole input range.
+// Workers are the o_extra workgroups placed after the attention ones (they do
+// nothing else, so their weight requests start with the launch), then the
+// QKV workgroups; worker w < o_two takes units 2w and 2w + 1, a later worker
+// unit o_two + w (if any).
+constexpr int kFuseLanes = 8;      // arrival counters per phase (spread over XCDs and memory channels)
 constexpr int kFuseStride = 64;    // ints between two counters
-constexpr int kFuseInts = (kFuseLanes + 1) * kFuseStride;   // producer counters, then the consumer counter
+constexpr int kFuseInts = 2 * kFuseLanes * kFuseStride;   // one layer's set: QKV arrivals, attention arrivals
 struct FuseCtl {
-  int* counters = nullptr;         // kFuseInts ints, zero between launches
-  int n_prod = 0, n_cons = 0;
+  int* counters = nullptr;         // this layer's kFuseInts ints, zero at the launch
+  int n_prod = 0, n_cons = 0;      // QKV workgroups, attention workgroups
   int* err = nullptr;
+  int o_units = 0, o_extra = 0, o_two = 0;
 };
 
 // Optional timing events of one launch (recorded at the kernel's start and end).
@@ -287,9 +298,13 @@ hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEv
 // single-chunk decode attention reading its output, in one launch; only when
 // every workgroup of it is co-resident (qkv_attn_capacity: workgroups the
 // device holds at once, 0 if the shape has no fused kernel).
-int qkv_attn_capacity(int mt, int S, int head_dim);
+// With o (non-null, one row tile only) the launch also carries the
+// O-projection + residual of the attention output (EPI_RESID, one strip per
+// tile, one input range of at most kFuseOMaxKb k-blocks; f's O fields set).
+constexpr int kFuseOMaxKb = 128;
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb = 0);
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           hipStream_t st, LaunchEvents ev = LaunchEvents{});
+                           const GemmArgs* o, hipStream_t st, LaunchEvents ev = LaunchEvents{});
 hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st);
 hipError_t launch_stage(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);

@@ -18,6 +18,11 @@
  *     the context has changed and pard_last_error() describes the problem.
  *     Validation of arguments, state and capacity happens on the host before
  *     any device work.  Nothing aborts, prints or allocates device memory.
+ *     The one exception is PARD_ERR_RANGE: activations and the KV cache are
+ *     held in fp16, and a call whose passes produced a value fp16 cannot hold
+ *     (|x| >= 65520, or NaN) runs to its end and then returns PARD_ERR_RANGE;
+ *     its outputs and the caches of its sequences are invalid (prefill them
+ *     again).  Weights whose activations stay within fp16's range never see it.
  *   - Host pointers (prompt, prefix, cand, outputs) are owned by the caller and
  *     are only accessed during the call.  Granular calls return after their
  *     outputs are valid (one device->host copy and a stream synchronisation).
@@ -45,7 +50,8 @@ typedef enum {
   PARD_ERR_CAPACITY = -3,    /* would exceed max_ctx / max_k / max_batch */
   PARD_ERR_NOMEM = -4,       /* arena smaller than pard_arena_bytes() */
   PARD_ERR_DEVICE = -5,      /* a HIP runtime call failed */
-  PARD_ERR_UNSUPPORTED = -6  /* valid request this build does not implement */
+  PARD_ERR_UNSUPPORTED = -6, /* valid request this build does not implement */
+  PARD_ERR_RANGE = -7        /* the call ran, but an activation exceeded fp16's range (see below) */
 } pard_status;
 
 enum { PARD_F32 = 0, PARD_BF16 = 1 };

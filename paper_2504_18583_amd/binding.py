@@ -23,7 +23,7 @@ if not os.path.exists(LIB_PATH):
 lib = C.CDLL(LIB_PATH)
 
 PARD_OK, PARD_ERR_ARG, PARD_ERR_STATE, PARD_ERR_CAPACITY = 0, -1, -2, -3
-PARD_ERR_NOMEM, PARD_ERR_DEVICE, PARD_ERR_UNSUPPORTED = -4, -5, -6
+PARD_ERR_NOMEM, PARD_ERR_DEVICE, PARD_ERR_UNSUPPORTED, PARD_ERR_RANGE = -4, -5, -6, -7
 PARD_F32, PARD_BF16 = 0, 1
 PARD_TARGET, PARD_DRAFT = 0, 1
 PARD_MODE_PARALLEL, PARD_MODE_VANILLA = 0, 1

@@ -29,10 +29,10 @@ struct RopeScaling {
 hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const RopeScaling& sc, hipStream_t st);
 // t_start (may be null): receives the device clock at the kernel's start (the
 // start of the pass).  fuse_cnt (may be null): n_sets fused-launch counter
-// sets (kFuseInts ints each) to zero.
+// sets (kFuseInts ints each) to zero.  ovf: fp16 range flag (f16_flagged).
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, int act_rows, float* ss, int ss_stride, int max_rows,
-                        unsigned long long* t_start, int* fuse_cnt, int n_sets, hipStream_t st);
+                        unsigned long long* t_start, int* fuse_cnt, int n_sets, int* ovf, hipStream_t st);
 hipError_t launch_gather_u16(const uint16_t* src, const size_t* idx, int n, float* out, hipStream_t st);
 
 }  // namespace pard

@@ -156,7 +156,7 @@ __global__ void k_rope_table(float2* tab, int cap, int hd, double theta, RopeSca
 __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc,
                                                float* x, const float* g, uint16_t* xg, int act_rows, float* ss,
                                                int ss_stride, unsigned long long* t_start, int* fuse_cnt,
-                                               int n_sets) {
+                                               int n_sets, int* ovf) {
   __shared__ float wsum[4];
   const int r = blockIdx.x;
   if (r == 0 && threadIdx.x == 0 && t_start) *t_start = wall_clock64();
@@ -171,6 +171,7 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
   const int id = desc->ids[r];
   const size_t strip = (size_t)(id >> 4);
   float sq = 0.f;
+  bool bad = false;
   for (int c8 = threadIdx.x; c8 < d / 8; c8 += blockDim.x) {
     const int k0 = c8 * 8, kb = k0 >> 5;
     const int lane = (id & 15) + 16 * ((k0 & 31) >> 3);
@@ -186,11 +187,13 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
     dst[1] = make_float4(v[4], v[5], v[6], v[7]);
     uint32_t o[4];
     for (int i = 0; i < 4; ++i) {
-      o[i] = (uint32_t)f16_bits(v[2 * i] * g[k0 + 2 * i]) | ((uint32_t)f16_bits(v[2 * i + 1] * g[k0 + 2 * i + 1]) << 16);
+      o[i] = (uint32_t)f16_flagged(v[2 * i] * g[k0 + 2 * i], bad) |
+             ((uint32_t)f16_flagged(v[2 * i + 1] * g[k0 + 2 * i + 1], bad) << 16);
       sq += v[2 * i] * v[2 * i] + v[2 * i + 1] * v[2 * i + 1];
     }
     *reinterpret_cast<uint4*>(xg + act_index(r, k0, act_rows)) = make_uint4(o[0], o[1], o[2], o[3]);
   }
+  flag_range(bad, ovf);
   for (int off = 32; off > 0; off >>= 1) sq += __shfl_xor(sq, off);
   if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = sq;
   __syncthreads();
@@ -238,9 +241,9 @@ hipError_t launch_rope_table(float2* tab, int cap, int hd, double theta, const R
 
 hipError_t launch_embed(const uint16_t* E, int n_strips, int d, const FwdDesc* desc, float* x, const float* g,
                         uint16_t* xg, int act_rows, float* ss, int ss_stride, int max_rows,
-                        unsigned long long* t_start, int* fuse_cnt, int n_sets, hipStream_t st) {
+                        unsigned long long* t_start, int* fuse_cnt, int n_sets, int* ovf, hipStream_t st) {
   k_embed<<<max_rows, 256, 0, st>>>(E, n_strips, d, desc, x, g, xg, act_rows, ss, ss_stride, t_start, fuse_cnt,
-                                    n_sets);
+                                    n_sets, ovf);
   return hipGetLastError();
 }
 

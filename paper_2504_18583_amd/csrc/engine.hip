@@ -171,6 +171,7 @@ struct Layer {
 
 struct ModelDev {
   pard_model_spec spec{};
+  int* ovf = nullptr;                 // fp16 range flag of this model's activations (the context's)
   int d = 0, q_dim = 0, kv_dim = 0, nqkv = 0, f_pad = 0, group = 0;
   GemmPlan p_qkv, p_o, p_gu, p_d, p_lm;
   std::vector<Layer> layers;
@@ -404,6 +405,8 @@ size_t layout(pard_ctx* c, char* base) {
   c->clock_dev = b.take<PhaseClock>(1);
   c->fuse_cnt = b.take<int>((size_t)kFuseInts * (c->m[0].spec.n_layers + c->m[1].spec.n_layers));
   c->fuse_err = b.take<int>(64);
+  // ints 0: a fused launch's wait gave up; 32: an fp16 activation overflowed
+  c->m[0].ovf = c->m[1].ovf = c->fuse_err ? c->fuse_err + 32 : nullptr;
   return align256(b.off);
 }
 
@@ -502,6 +505,7 @@ GemmArgs gemm_base(const ModelDev& M, const uint16_t* W, int act_rows) {
   a.eps = M.spec.rms_eps;
   a.inv_k = 1.0f / (float)M.d;
   a.ss_stride = std::max(1, M.ss_tiles_max);
+  a.ovf = M.ovf;
   return a;
 }
 
@@ -588,7 +592,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     Timed t(c, cls0 + 0);
     HIP_TRY(c, launch_embed(M.embed, M.p_lm.n_strips, M.d, M.desc, M.x, M.layers[0].g_attn, M.xg, act_rows, M.ss,
                             std::max(1, M.ss_tiles_max), ps.max_rows, &c->clock_dev->pass_start[w],
-                            fuse_counters(c, w), s.n_layers, c->stream));
+                            fuse_counters(c, w), s.n_layers, M.ovf, c->stream));
   }
   const size_t layer_kv = (size_t)s.n_kv_heads * c->kv_cap * s.head_dim;
   // attention plan: one workgroup per (sequence, KV head, query group, key
@@ -807,11 +811,18 @@ pard_status pull_seqs_sync(pard_ctx* c, const int* seqs, int n) {
   for (int i = 0; i < n; ++i)
     HIP_TRY(c, hipMemcpyAsync(c->h_seq + seqs[i], c->seq_dev + seqs[i], sizeof(SeqState), hipMemcpyDeviceToHost,
                               c->stream));
-  HIP_TRY(c, hipMemcpyAsync(c->h_fuse_err, c->fuse_err, sizeof(int), hipMemcpyDeviceToHost, c->stream));
+  HIP_TRY(c, hipMemcpyAsync(c->h_fuse_err, c->fuse_err, sizeof(int) * 64, hipMemcpyDeviceToHost, c->stream));
   HIP_TRY(c, hipStreamSynchronize(c->stream));
   c->desc_slot = 0;
-  if (*c->h_fuse_err)
+  if (c->h_fuse_err[0])
     return fail(c, PARD_ERR_DEVICE, "a QKV+attention launch's wait exceeded its spin limit: results are invalid");
+  if (c->h_fuse_err[32]) {
+    // reported once: the flag is cleared for the calls that follow
+    HIP_TRY(c, hipMemsetAsync(c->fuse_err + 32, 0, sizeof(int), c->stream));
+    HIP_TRY(c, hipStreamSynchronize(c->stream));
+    return fail(c, PARD_ERR_RANGE, "an activation exceeded fp16's range (or was NaN): this call's tokens and the "
+                "sequences' caches are invalid; prefill them again");
+  }
   return PARD_OK;
 }
 
@@ -984,6 +995,7 @@ const char* pard_status_string(pard_status s) {
     case PARD_ERR_NOMEM: return "PARD_ERR_NOMEM";
     case PARD_ERR_DEVICE: return "PARD_ERR_DEVICE";
     case PARD_ERR_UNSUPPORTED: return "PARD_ERR_UNSUPPORTED";
+    case PARD_ERR_RANGE: return "PARD_ERR_RANGE";
   }
   return "PARD_UNKNOWN";
 }
@@ -1045,7 +1057,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
       hipHostMalloc((void**)&c->h_gather_out, sizeof(float) * kGatherMax, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_out, sizeof(int) * max_ctx, hipHostMallocDefault) != hipSuccess ||
       hipHostMalloc((void**)&c->h_clock, sizeof(PhaseClock), hipHostMallocDefault) != hipSuccess ||
-      hipHostMalloc((void**)&c->h_fuse_err, sizeof(int), hipHostMallocDefault) != hipSuccess)
+      hipHostMalloc((void**)&c->h_fuse_err, sizeof(int) * 64, hipHostMallocDefault) != hipSuccess)
     return bail(PARD_ERR_DEVICE);
   {
     int dev = 0, khz = 0;

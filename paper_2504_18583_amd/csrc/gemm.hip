@@ -428,6 +428,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
     }
   }
 
+  [[maybe_unused]] bool bad = false;
   if constexpr (EPI == EPI_QKV) {
     if (!epi) return;   // no barrier follows in this epilogue
 #pragma unroll
@@ -444,7 +445,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
           const float2 cs = e2[j];                     // rotary (cos, sin) of (pos, pair)
           y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
         }
-        const uint16_t b = f16_bits(y);
+        const uint16_t b = f16_flagged(y, bad);
         uint16_t* dst;
         if (n < p.q_dim) {
           dst = p.out + (size_t)row * p.ld_out + n;
@@ -462,6 +463,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
           *dst = b;
       }
     }
+    flag_range(bad, p.ovf);
   } else if constexpr (EPI == EPI_RESID) {
     if (!epi) return;   // no barrier follows in this epilogue
     float sq[MT];
@@ -476,7 +478,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
         const size_t o = (size_t)row * p.ldx + n;
         const float xn = e0[j] + v[j];                 // residual + projection
         p.x[o] = xn;
-        p.xg[act_index(row, n, p.act_rows)] = f16_bits(xn * e1[j]);
+        p.xg[act_index(row, n, p.act_rows)] = f16_flagged(xn * e1[j], bad);
         sq[mt] += xn * xn;
       }
     }
@@ -485,6 +487,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       const float t = sum16(sq[mt]);
       if (csub == 0) p.ss_out[(size_t)(mt * 16 + rsub) * p.ss_stride + tile] = t;
     }
+    flag_range(bad, p.ovf);
   } else if constexpr (EPI == EPI_SWIGLU) {
     // a strip holds 8 gate columns then the 8 up columns of the same features:
     // the up value of column csub < 8 is in lane ^ 8 (same row)
@@ -498,8 +501,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
         const float up = __shfl_xor(gt, 8);
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * S + s) * 8 + csub;
-        if (csub < 8 && row < row_count && s <= s_last) p.out[act_index(row, f, p.act_rows)] = f16_bits(h);
+        if (csub < 8 && row < row_count && s <= s_last) p.out[act_index(row, f, p.act_rows)] = f16_flagged(h, bad);
       }
+    flag_range(bad, p.ovf);
   } else {  // EPI_LOGITS
     constexpr int TW = S * 16;
     __syncthreads();   // everyone is done reading red; it becomes the [row][col] tile
@@ -620,14 +624,16 @@ __device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, con
   float v = red[ej * 256 + (tid & 255)];
   for (int w = 1; w < 8; ++w) v += red[(w * NU + ej) * 256 + (tid & 255)];
   float sq = 0.f;
+  bool bad = false;
   if (rsub < row_count) {
     const float xn = x_old + v;                      // residual + projection
     p.x[(size_t)rsub * p.ldx + n] = xn;
-    p.xg[act_index(rsub, n, p.act_rows)] = f16_bits(xn * g);
+    p.xg[act_index(rsub, n, p.act_rows)] = f16_flagged(xn * g, bad);
     sq = xn * xn;
   }
   const float t = sum16(sq);
   if (csub == 0) p.ss_out[(size_t)rsub * p.ss_stride + u0 + ej] = t;
+  flag_range(bad, p.ovf);
 }
 
 // The O units of worker w (see FuseCtl), if it has any.
@@ -1299,6 +1305,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
                                               const float* rs_s) {
   const int c16 = lane & 15, g4 = lane >> 4;
   const int strip0 = tile * kRowsTileStrips + wave * kRowsWaveStrips;
+  [[maybe_unused]] bool bad = false;
   if constexpr (EPI == EPI_QKV) {
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
       constexpr int mt = decltype(mtc)::value;
@@ -1320,7 +1327,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
               const float2 cs = p.rope[(size_t)pos * (p.hd / 2) + ((n % p.hd) >> 1)];
               y = (n & 1) ? (y * cs.x + partner * cs.y) : (y * cs.x - partner * cs.y);
             }
-            const uint16_t b = f16_bits(y);
+            const uint16_t b = f16_flagged(y, bad);
             if (n < p.q_dim) {
               p.out[(size_t)r * p.ld_out + n] = b;
             } else if (n < p.q_dim + p.kv_dim) {
@@ -1335,6 +1342,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
         }
       }
     });
+    flag_range(bad, p.ovf);
   } else if constexpr (EPI == EPI_RESID) {
     float* ss = p.ss_out + (tile * kRowsWaves + wave);
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
@@ -1353,7 +1361,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
             const size_t o = (size_t)r * p.ldx + n;
             const float xn = p.x[o] + acc[mt][s][i];   // residual + projection
             p.x[o] = xn;
-            p.xg[act_index(r, n, p.act_rows)] = f16_bits(xn * g);
+            p.xg[act_index(r, n, p.act_rows)] = f16_flagged(xn * g, bad);
             sq[i] += xn * xn;
           }
         }
@@ -1365,6 +1373,7 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
         if (c16 == 0 && r < row_count) ss[(size_t)r * p.ss_stride] = t;
       }
     });
+    flag_range(bad, p.ovf);
   } else if constexpr (EPI == EPI_SWIGLU) {
     // 8 gate columns then the 8 up columns of the same features per strip
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
@@ -1380,10 +1389,11 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
           const float gt = acc[mt][s][i] * rs_s[rl];
           const float up = __shfl_xor(gt, 8);
           const float h = gt / (1.0f + expf(-gt)) * up;
-          if (c16 < 8 && r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_bits(h);
+          if (c16 < 8 && r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_flagged(h, bad);
         }
       }
     });
+    flag_range(bad, p.ovf);
   } else {  // EPI_LOGITS
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
       constexpr int mt = decltype(mtc)::value;

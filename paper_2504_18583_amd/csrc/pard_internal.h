@@ -106,6 +106,17 @@ __host__ __device__ inline float sample_uniform(uint64_t seed, int slot, int dra
 
 // fp16 bits of v, nearest even.
 __device__ inline uint16_t f16_bits(float v) { return __builtin_bit_cast(uint16_t, (_Float16)v); }
+// fp16 bits of an activation that feeds a GEMM or the KV cache.  A value that
+// fp16 cannot hold (|v| >= 65520 rounds to infinity) or a NaN sets `bad`; the
+// caller then sets the pass's range flag (flag_range), and the host reports
+// the pass's results as invalid.
+__device__ inline uint16_t f16_flagged(float v, bool& bad) {
+  bad |= !(fabsf(v) < 65520.0f);
+  return f16_bits(v);
+}
+__device__ inline void flag_range(bool bad, int* ovf) {
+  if (bad && ovf) *ovf = 1;
+}
 
 // One sequence's share of a forward pass: rows [row0, row0 + n_rows) at
 // positions pos0.., of which the first n_real carry real tokens (committed
@@ -205,6 +216,7 @@ struct GemmArgs {
   float* part;
   int kb_split;
   int* counters;
+  int* ovf;               // fp16 range flag of the activations this GEMM writes (f16_flagged), or null
 };
 
 // Second argmax pass over the lm_head tiles and the step tail: one workgroup

@@ -125,6 +125,7 @@ def test_null_context_calls_return_arg(b):
     assert b.lib.pard_last_error(None) == b"null context"
     b.lib.pard_free(None)
     assert b.lib.pard_status_string(b.PARD_ERR_CAPACITY) == b"PARD_ERR_CAPACITY"
+    assert b.lib.pard_status_string(b.PARD_ERR_RANGE) == b"PARD_ERR_RANGE"
 
 
 def test_cod_capacity_and_argument_checks(b):

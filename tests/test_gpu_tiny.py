@@ -279,6 +279,34 @@ def test_errors_leave_state_unchanged(eng, B):
         assert (eng.kv_len(B.PARD_TARGET), eng.kv_len(B.PARD_DRAFT)) == (lt, ld)
 
 
+def test_fp16_range_overflow_is_reported(B):
+    """Activations and the KV cache are fp16: a pass whose values leave fp16's
+    range must fail loudly (PARD_ERR_RANGE), not return silently wrong tokens.
+    Weights at init_std 5 take the tiny target's residual stream past 65520
+    in its first layer (the oracle shows it below), far beyond what the
+    benchmark weights do (|x| < 1)."""
+    import dataclasses
+    from oracle import model as om
+    say("[gpu] tiny: fp16 overflow flag")
+    t_big = dataclasses.replace(T_SPEC, init_std=5.0)
+    m = oracle.build_model(t_big)
+    ids = np.asarray(PROMPT)
+    x = np.asarray(np.asarray(m.weights["embed"])[ids], np.float64)
+    assert np.abs(x).max() < 65520
+    empty = np.zeros((0, t_big.n_kv_heads, t_big.head_dim))
+    with np.errstate(over="ignore"):
+        x1, _, _ = om._layer(t_big, m.weights["layers"][0], x, np.arange(len(ids)), empty, empty)
+    assert np.abs(x1).max() >= 65520
+    eng = B.Engine(t_big, D_SPEC, WL.mask_id, max_ctx=256, max_k=8)
+    try:
+        for _ in range(2):                              # reported by every call that overflows
+            with pytest.raises(B.PardError) as e:
+                eng.prefill(PROMPT)
+            assert e.value.status == B.PARD_ERR_RANGE
+    finally:
+        eng.close()
+
+
 def test_self_draft_accepts_every_step(B):
     say("[gpu] tiny: draft == target")
     eng = B.Engine(T_SPEC, T_SPEC, WL.mask_id, max_ctx=256, max_k=8)

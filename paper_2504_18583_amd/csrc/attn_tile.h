@@ -65,22 +65,26 @@ constexpr int kFuseSpinLimit = 1 << 20;    // polls before a fused wait gives up
 // kFuseLanes counters at `lanes` (one per XCD when workgroups are dealt
 // round-robin over the XCDs, kFuseStride ints apart), so that their
 // device-scope atomics and the pollers' loads do not all meet on one address.
-// Wavefront 0 polls (lane j reads counter j, the lanes add them up); the
-// other wavefronts wait at the workgroup barrier with their loads still in
-// flight.  Every wavefront of the workgroup must call this.  The spin is
-// bounded: past kFuseSpinLimit polls the wait sets *err and returns (the
-// results are then invalid and the host reports an error), so no wavefront
-// waits forever.
+// Wavefront 0 polls (lane j reads counter j, the lanes add them up with DPP
+// moves); the other wavefronts wait at the workgroup barrier with their loads
+// still in flight.  One poll at a time: keeping four in flight per poller
+// measured slower (their loads delay the arrivals' atomics on the same lines).
+// Every wavefront of the workgroup must call this.  The spin is bounded: past
+// kFuseSpinLimit polls the wait sets *err and returns (the results are then
+// invalid and the host reports an error), so no wavefront waits forever.
 __device__ __forceinline__ void fuse_wait_on(const int* lanes, const int n, int* err) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
+    // every lane loads (lanes past the counters re-read the last one and are
+    // not counted): no branch around the load
+    const int* addr = lanes + min(lane, kFuseLanes - 1) * kFuseStride;
     for (int spins = 0;; ++spins) {
-      int v = lane < kFuseLanes ? __hip_atomic_load(lanes + lane * kFuseStride, __ATOMIC_RELAXED,
-                                                    __HIP_MEMORY_SCOPE_AGENT) : 0;
-      v += __shfl_xor(v, 4);
-      v += __shfl_xor(v, 2);
-      v += __shfl_xor(v, 1);
-      if (__shfl(v, 0) >= n) break;
+      int v = __hip_atomic_load(addr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      v = lane < kFuseLanes ? v : 0;
+      v += __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);    // quad_perm 1 0 3 2
+      v += __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);    // quad_perm 2 3 0 1
+      v += __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);   // half-row mirror: the other quad
+      if (__builtin_amdgcn_readfirstlane(v) >= n) break;
       if (spins >= kFuseSpinLimit) {
         if (lane == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         break;

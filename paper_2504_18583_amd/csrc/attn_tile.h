@@ -61,10 +61,13 @@ constexpr int kRsrcWord3 = 0x00020000;     // buffer descriptor word 3 for gfx9-
 constexpr int kCachePolicyDevice = 16;     // sc1: device scope, coherent across XCDs
 constexpr int kFuseSpinLimit = 1 << 20;    // polls before a fused wait gives up (and flags an error)
 
-// Wait until n workgroups of this launch have counted themselves in on the
-// kFuseLanes counters at `lanes` (one per XCD when workgroups are dealt
-// round-robin over the XCDs, kFuseStride ints apart), so that their
-// device-scope atomics and the pollers' loads do not all meet on one address.
+// Wait until the LANES (at most kFuseLanes) counters at `lanes`, kFuseStride
+// ints apart, add up to n: many arrivals are spread over the counters (one
+// per XCD when workgroups are dealt round-robin over the XCDs) so that their
+// device-scope atomics do not all meet on one address; few arrivals awaited
+// by many pollers go to every counter and each poller reads one (measured:
+// one shared counter for all pollers is slower, as are arrivals on every
+// counter for the QKV workgroups).
 // Wavefront 0 polls (lane j reads counter j, the lanes add them up with DPP
 // moves); the other wavefronts wait at the workgroup barrier with their loads
 // still in flight.  One poll at a time: keeping four in flight per poller
@@ -72,15 +75,16 @@ constexpr int kFuseSpinLimit = 1 << 20;    // polls before a fused wait gives up
 // Every wavefront of the workgroup must call this.  The spin is bounded: past
 // kFuseSpinLimit polls the wait sets *err and returns (the results are then
 // invalid and the host reports an error), so no wavefront waits forever.
+template <int LANES>
 __device__ __forceinline__ void fuse_wait_on(const int* lanes, const int n, int* err) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
     // every lane loads (lanes past the counters re-read the last one and are
     // not counted): no branch around the load
-    const int* addr = lanes + min(lane, kFuseLanes - 1) * kFuseStride;
+    const int* addr = lanes + min(lane, LANES - 1) * kFuseStride;
     for (int spins = 0;; ++spins) {
       int v = __hip_atomic_load(addr, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      v = lane < kFuseLanes ? v : 0;
+      v = lane < LANES ? v : 0;
       v += __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);    // quad_perm 1 0 3 2
       v += __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, false);    // quad_perm 2 3 0 1
       v += __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, false);   // half-row mirror: the other quad
@@ -96,7 +100,7 @@ __device__ __forceinline__ void fuse_wait_on(const int* lanes, const int n, int*
 }
 
 // Wait for every QKV workgroup of the launch.
-__device__ __forceinline__ void fuse_wait(const FuseCtl& f) { fuse_wait_on(f.counters, f.n_prod, f.err); }
+__device__ __forceinline__ void fuse_wait(const FuseCtl& f) { fuse_wait_on<kFuseLanes>(f.counters, f.n_prod, f.err); }
 
 template <int HD, int NQ, int NW, bool FUSED>
 __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,

@@ -591,7 +591,7 @@ __device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, con
     g = p.g_next[n];
   }
   __builtin_amdgcn_sched_barrier(0);
-  attn::fuse_wait_on(f.counters + kFuseLanes * kFuseStride, f.n_cons, f.err);
+  attn::fuse_wait_on<1>(f.counters + (kFuseLanes + blockIdx.x % kFuseLanes) * kFuseStride, f.n_cons, f.err);
   __builtin_amdgcn_sched_barrier(0);
   // A fragment of this lane: row lane % 16, 8 columns at 8 * (lane / 16) of
   // each k-block; rows past the pass read zeros without a memory access
@@ -690,8 +690,8 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     if constexpr (OKI > 0) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's output stores are complete
       __syncthreads();
-      if (tid == 0)
-        __hip_atomic_fetch_add(f.counters + (kFuseLanes + i % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
+      if (tid < kFuseLanes)   // every counter: each poller reads the one of its XCD
+        __hip_atomic_fetch_add(f.counters + (kFuseLanes + tid) * kFuseStride, 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     }
     return;

@@ -265,9 +265,12 @@ struct AttnArgs {
 // GEMM, the decode attention that reads its output and, optionally, the
 // O-projection that reads the attention's output.  QKV workgroup b counts
 // itself in on counter b % kFuseLanes once its stores are complete; attention
-// workgroups wait for n_prod such arrivals in all and, when O units follow,
-// count themselves in on counter kFuseLanes + i % kFuseLanes once their own
-// output stores are complete; O-projection workers wait for n_cons of those.
+// workgroups wait for n_prod such arrivals in all (summing the kFuseLanes
+// counters) and, when O units follow, count themselves in on each of the
+// counters kFuseLanes .. 2 kFuseLanes - 1 once their own output stores are
+// complete; O-projection worker b waits for n_cons arrivals on counter
+// kFuseLanes + b % kFuseLanes alone (a few dozen arrivals awaited by hundreds
+// of pollers: one line per poll, the pollers spread over the counters).
 // Each layer of a model has its own set of counters, zeroed by the pass's
 // embedding launch (k_embed), so no workgroup has to reset them at the end of
 // a launch.  err is set if a wait exceeds its bounded spin.

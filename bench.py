@@ -551,28 +551,39 @@ def main() -> int:
     latency = {"p50_ms": round(stats.step_ms_p50, 4), "p90_ms": round(stats.step_ms_p90, 4),
                "mean_ms": round(step_s * 1e3, 4)}
 
-    # dominant kernel: the target's gate/up GEMM, timed with HIP events around
-    # each launch on the engine's stream over a second run of the same steps
-    kclass = B.PARD_TARGET * 8 + B.OP_GATEUP
-    n_launch = steps * t_spec.n_layers
-    eng.timer_enable(kclass, min(n_launch, 1 << 16))
-    eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2,
-                 max_steps=max(1, min(steps, (max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2) // (k + 1))))
-    launches, total_ms = eng.timer_read()
-    eng.timer_enable(-1, 1)
-    avg_s = total_ms / 1e3 / max(launches, 1)
+    # dominant kernel, timed with HIP events around each launch on the engine's
+    # stream over a second run of the same steps: the target's gate/up GEMM,
+    # or, where the engine runs gate/up inside the decode layer's launch (QKV,
+    # attention, O-projection and gate/up), that launch
+    def time_class(op):
+        eng.timer_enable(B.PARD_TARGET * 8 + op, min(steps * t_spec.n_layers, 1 << 16))
+        eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2,
+                     max_steps=max(1, min(steps, (max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2) // (k + 1))))
+        n, ms = eng.timer_read()
+        eng.timer_enable(-1, 1)
+        return n, ms
+
     f_pad = (t_spec.ffn_dim + 31) // 32 * 32
-    # bf16 weights [2*F, d] once, bf16 activations in, bf16 h = silu(gate)*up out
-    gu_bytes = 2 * (2 * f_pad * t_spec.d_model) + (k + 1) * t_spec.d_model * 2 + (k + 1) * f_pad * 2
-    achieved = gu_bytes / avg_s / 1e9
-    # the counter summary covers the 8B-shaped gate/up launch with 9 rows only
-    counted = (t_spec.d_model, t_spec.ffn_dim, k) == (4096, 14336, 8)
+    launches, total_ms = time_class(B.OP_GATEUP)
+    if launches > 0:
+        # bf16 weights [2*F, d] once, fp16 activations in, fp16 h = silu(gate)*up out
+        kbytes = 2 * (2 * f_pad * t_spec.d_model) + (k + 1) * t_spec.d_model * 2 + (k + 1) * f_pad * 2
+        kname = f"k_gemm<MT=1,EPI_SWIGLU> (target gate/up, [{2 * f_pad}, {t_spec.d_model}] weight, {k + 1} rows)"
+        # the counter summary covers the 8B-shaped gate/up launch with 9 rows only
+        traffic = measured_traffic() if (t_spec.d_model, t_spec.ffn_dim, k) == (4096, 14336, 8) else None
+    else:
+        launches, total_ms = time_class(B.OP_QKV)
+        # the timer run's mean committed target length (it continues after the timed steps)
+        kbytes = bm.layer_launch_bytes(t_spec, k + 1, int(round(l_t1 + steps * tokens_per_step / 2)))
+        kname = (f"k_qkv_attn (target decode layer: QKV GEMM, attention, O-projection and gate/up GEMM, "
+                 f"{k + 1} rows)")
+        traffic = None                               # no counter summary of this launch
+    avg_s = total_ms / 1e3 / max(launches, 1)
+    achieved = kbytes / avg_s / 1e9 if launches > 0 else 0.0
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": measured_traffic() if counted else None,
-                "kernel": f"k_gemm<MT=1,EPI_SWIGLU> (target gate/up, [{2 * f_pad}, {t_spec.d_model}] weight, "
-                          f"{k + 1} rows)",
-                "launches": launches, "avg_us": round(avg_s * 1e6, 2),
-                "bytes_per_launch": gu_bytes}
+                "frac": round(achieved / PEAK_HBM_GBPS, 4), "traffic": traffic,
+                "kernel": kname, "launches": launches, "avg_us": round(avg_s * 1e6, 2),
+                "bytes_per_launch": kbytes}
 
     baselines = None if args.no_baselines else measure_baselines(eng, B, prompt, k, wall / steps, emitted / wall)
     eng.close()

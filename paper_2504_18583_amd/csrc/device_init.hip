@@ -163,9 +163,10 @@ __global__ __launch_bounds__(256) void k_embed(const uint16_t* E, int n_strips, 
   // the pass's fused-launch counters start at zero (their last use was in an
   // earlier launch)
   if (r == 0 && fuse_cnt) {
-    for (int i = threadIdx.x; i < n_sets * 2 * kFuseLanes; i += blockDim.x)
-      __hip_atomic_store(fuse_cnt + (size_t)(i / (2 * kFuseLanes)) * kFuseInts + (i % (2 * kFuseLanes)) * kFuseStride, 0,
-                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    constexpr int per = kFuseInts / kFuseStride;   // counters per set
+    for (int i = threadIdx.x; i < n_sets * per; i += blockDim.x)
+      __hip_atomic_store(fuse_cnt + (size_t)(i / per) * kFuseInts + (i % per) * kFuseStride, 0, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
   }
   if (r >= desc->n_rows) return;
   const int id = desc->ids[r];

@@ -233,6 +233,8 @@ struct pard_ctx {
   int* h_fuse_err = nullptr;
   bool use_fused = true;
   bool use_fused_o = true;
+  bool use_fused_gu = true;
+  int gu_pre = -1, gu_pre_q = -1;   // preloaded gate/up iterations (-1: as many as the LDS holds)
   // captured fused steps (draft pass + verify pass), replayed on `stream`
   struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
   std::vector<StepGraph> graphs;
@@ -533,6 +535,25 @@ GemmArgs o_args(const ModelDev& M, const Layer& L, int act_rows) {
   return a;
 }
 
+// Norm + gate/up + SiLU * up: h = silu(x g W_gate^T / rms) * (x g W_up^T / rms).
+// S > 0: the tile plan of a fused launch (S strips per tile, one input range).
+GemmArgs gu_args(const ModelDev& M, const Layer& L, int act_rows, int ss_tiles, int S) {
+  GemmArgs a = gemm_base(M, L.wgu, act_rows);
+  a.A = M.xg;
+  a.lda = M.d;
+  a.ss_in = M.ss;
+  a.ss_tiles = ss_tiles;
+  a.out = M.h;
+  if (S > 0) {
+    a.kb_total = M.p_gu.kb_total;
+    a.n_strips = M.p_gu.n_strips;
+    a.n_tiles = M.p_gu.n_strips / S;
+    a.ksplit = 1;
+    a.kb_split = M.p_gu.kb_total;
+  }
+  return a;
+}
+
 struct PassSpec {
   int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
   int typ_rows = 0;       // row count the split plan is tuned for (0: max_rows)
@@ -652,6 +673,31 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     fo.o_two = std::max(0, fo.o_units - n_qkv - fo.o_extra);
     fused_o = cap > 0 && room >= 0 && fo.o_two <= fo.o_extra;
   }
+  // with O units, the gate/up GEMM joins as well: every workgroup of the grid
+  // runs one gate/up tile, whose first weight blocks it loads into LDS while
+  // the attention runs (extras are added until the grid covers the tiles)
+  const int S_gu = pick_S(EPI_SWIGLU, M.p_gu.n_strips, 1);
+  bool fused_gu = false;
+  if (fused_o && c->use_fused_gu && (S_gu == 4 || S_gu == 7) && M.p_gu.ksplit == 1 &&
+      M.p_gu.n_strips % S_gu == 0 && plan_nw(M.p_gu, S_gu, 1) == 4) {
+    const int n_qkv = M.p_qkv.n_strips / S_q;
+    const int gu_tiles = M.p_gu.n_strips / S_gu;
+    const int pre_max = std::min(qkv_attn_gu_pre_max(S_q, s.head_dim, M.p_o.kb_total, S_gu), M.p_gu.kb_total / 4);
+    const int pre = c->gu_pre >= 0 ? std::min(c->gu_pre, pre_max) : pre_max;
+    const int pre_q = c->gu_pre_q >= 0 ? std::min(c->gu_pre_q, pre) : pre;
+    const int cap = pre >= 1 ? qkv_attn_capacity(1, S_q, s.head_dim, M.p_o.kb_total, S_gu, pre) : 0;
+    FuseCtl t = fo;
+    t.o_extra = std::max(fo.o_extra, gu_tiles - n_qkv - n_attn_wg);
+    t.o_two = std::max(0, t.o_units - n_qkv - t.o_extra);
+    if (cap > 0 && gu_tiles <= cap && n_qkv + n_attn_wg + t.o_extra <= cap && t.o_two <= t.o_extra) {
+      fused_gu = true;
+      t.gu_tiles = gu_tiles;
+      t.gu_pre = pre;
+      t.gu_pre_q = pre_q;
+      t.n_odone = std::min(n_qkv + t.o_extra, t.o_units - t.o_two);
+      fo = t;
+    }
+  }
   for (int l = 0; l < s.n_layers; ++l) {
     const Layer& L = M.layers[l];
     uint16_t* kc = M.kcache + layer_kv * l;
@@ -704,8 +750,9 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
         f.err = c->fuse_err;
         f.n_prod = a.n_tiles;
         f.n_cons = n_attn_wg;
-        GemmArgs o{};
+        GemmArgs o{}, gu{};
         if (fused_o) o = o_args(M, L, act_rows);
+        if (fused_gu) gu = gu_args(M, L, act_rows, ss_tiles, S_gu);
         // the kernel timer's QKV class covers the fused launch (attention included)
         LaunchEvents ev;
         if (c->timer_class == cls0 + 1 && c->timer_used < c->timer_max) {
@@ -713,7 +760,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
           ev.stop = c->timer_ev[2 * c->timer_used + 1];
           ++c->timer_used;
         }
-        HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, fused_o ? &o : nullptr, c->stream, ev));
+        HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, fused_o ? &o : nullptr, fused_gu ? &gu : nullptr,
+                                   S_gu, c->stream, ev));
       } else {
         HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
       }
@@ -725,14 +773,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     if (!fused_o) {  // O-projection + residual
       HIP_TRY(c, run_gemm(c, cls0 + 3, EPI_RESID, ps.max_rows, typ, o_args(M, L, act_rows), M.p_o));
     }
-    {  // norm + gate/up + SiLU * up
-      GemmArgs a = gemm_base(M, L.wgu, act_rows);
-      a.A = M.xg;
-      a.lda = M.d;
-      a.ss_in = M.ss;
-      a.ss_tiles = ss_tiles;
-      a.out = M.h;
-      HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, ps.max_rows, typ, a, M.p_gu));
+    if (!fused_gu) {  // norm + gate/up + SiLU * up
+      HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, ps.max_rows, typ, gu_args(M, L, act_rows, ss_tiles, 0), M.p_gu));
     }
     {  // down + residual
       GemmArgs a = gemm_base(M, L.wd, act_rows);
@@ -1044,6 +1086,9 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   if (const char* e = getenv("PARD_NO_GRAPH")) c->use_graphs = e[0] == '0';
   if (const char* e = getenv("PARD_NO_FUSE")) c->use_fused = e[0] == '0';
   if (const char* e = getenv("PARD_NO_FUSE_O")) c->use_fused_o = e[0] == '0';
+  if (const char* e = getenv("PARD_NO_FUSE_GU")) c->use_fused_gu = e[0] == '0';
+  if (const char* e = getenv("PARD_GU_PRE")) c->gu_pre = atoi(e);
+  if (const char* e = getenv("PARD_GU_PRE_Q")) c->gu_pre_q = atoi(e);
   c->prefilled.assign(max_batch, 0);
   c->draft_k.assign(max_batch, 0);
 
@@ -1078,7 +1123,14 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
     for (int mt = 1; mt <= 4; ++mt)
       for (int S = 1; S <= 2; ++S) {
         (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim);
-        if (mt == 1) (void)qkv_attn_capacity(mt, S, c->m[w].spec.head_dim, c->m[w].p_o.kb_total);
+        if (mt == 1) {
+          const ModelDev& M = c->m[w];
+          (void)qkv_attn_capacity(mt, S, M.spec.head_dim, M.p_o.kb_total);
+          const int S_gu = pick_S(EPI_SWIGLU, M.p_gu.n_strips, 1);
+          const int pre_max = qkv_attn_gu_pre_max(S, M.spec.head_dim, M.p_o.kb_total, S_gu);
+          for (int pre = 1; pre <= pre_max; ++pre)
+            (void)qkv_attn_capacity(mt, S, M.spec.head_dim, M.p_o.kb_total, S_gu, pre);
+        }
       }
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||
       hipMemsetAsync(c->m[0].lm_map, 0, sizeof(int2) * max_batch, c->stream) != hipSuccess ||

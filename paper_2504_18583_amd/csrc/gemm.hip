@@ -48,6 +48,7 @@
 
 #include <algorithm>
 #include <climits>
+#include <map>
 #include <type_traits>
 
 namespace pard {
@@ -94,15 +95,28 @@ __device__ __forceinline__ float wave_incl_scan(float v, int lane) {
   return v;
 }
 
+// Input iterations per wavefront that a fused gate/up tile may take from LDS.
+constexpr int kGuPreMax = 8;
+
 // One workgroup tile of the skinny GEMM: strips [tile*S, tile*S + S) over the
 // input range `split` of n_split, computed by the first nw wavefronts of the
 // workgroup; red is the [nw][S*MT*256] float LDS of the wave reduction.  With
 // FUSED (the QKV GEMM of a launch that also carries the attention reading its
 // output) the Q / K / V stores are device-scope, so that workgroups on other
-// XCDs of the same launch read them after the count-in.
-template <int MT, int S, int EPI, bool FUSED = false>
+// XCDs of the same launch read them after the count-in.  With PM (the gate/up
+// tile of such a launch: one row tile, one input range, four wavefronts) the
+// first `pre` iterations of each wavefront take their weights from pre_lds
+// (gu_preload put them there; the caller has waited for its loads), the
+// first global weight stages are requested before the tile waits for the O
+// workers (fc), and the activations and row sums they wrote in this launch
+// are read at device scope (one acquire fence per workgroup measured 8B/1B
+// 3.511 ms against 3.456, one per wavefront 3.757).  The arithmetic and its
+// order are those of the unfused tile.
+template <int MT, int S, int EPI, bool FUSED = false, bool PM = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, const unsigned split, const int n_split,
-                                          const int nw, float* red) {
+                                          const int nw, float* red, const FuseCtl* fc = nullptr,
+                                          const uint32_t* pre_lds = nullptr, const int pre = 0) {
+  static_assert(!PM || (MT == 1 && EPI == EPI_SWIGLU && S < 8), "preloaded tiles: one row tile of gate/up, not ragged");
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
   constexpr int NJ = S * MT;         // elements per thread in the epilogue (first 256 threads)
   // k-blocks per pipeline stage: 8 KiB of W per wave (smaller for prefill-sized row counts)
@@ -171,7 +185,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       // unconditional loads (a tile index past the end re-reads the last
       // tile and is dropped when summed), so none waits behind a branch
       const int q = (tid & 15) + 16 * u;
-      ss_part[u] = p.ss_in[(size_t)row * p.ss_stride + min(q, p.ss_tiles - 1)];
+      if constexpr (PM)   // written by the O workers of this launch: device scope
+        ss_part[u] = __hip_atomic_load(p.ss_in + (size_t)row * p.ss_stride + min(q, p.ss_tiles - 1), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+      else
+        ss_part[u] = p.ss_in[(size_t)row * p.ss_stride + min(q, p.ss_tiles - 1)];
     }
   };
   auto ss_finish = [&](int row) {
@@ -183,7 +201,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
 #pragma unroll
       for (int u = 0; u < 16; ++u) {
         const int q = q0 + 16 * u;
-        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
+        if constexpr (PM)
+          part[u] = q < p.ss_tiles ? __hip_atomic_load(p.ss_in + (size_t)row * p.ss_stride + q, __ATOMIC_RELAXED,
+                                                       __HIP_MEMORY_SCOPE_AGENT) : 0.f;
+        else
+          part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
       }
 #pragma unroll
       for (int u = 0; u < 16; ++u) t += part[u];
@@ -216,7 +238,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   const int lm_ss = LM ? dp->lm_src[(tid & 255) >> 4] : 0;
   // rows of a pass's activations need no descriptor (rows past the pass read
   // unused sums and are never stored)
-  if constexpr (NORM && !LM && MT == 1) {
+  if constexpr (NORM && !LM && MT == 1 && !PM) {
     if (tid < 256) ss_issue(tid >> 4);
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -226,9 +248,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   // unconditionally (a wave with no k-block of its own, n_it = 0, reads the
   // range's last one and never uses it): a branch around it would make every
   // later wait on an earlier load wait for the whole stage too.
+  const int its0 = PM ? pre : 0;   // the first iteration streamed from memory
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const int kb = kb0 + min(wave + min(u, max(n_it - 1, 0)) * nw, kb_n - 1);
+    const int kb = kb0 + min(wave + min(its0 + u, max(n_it - 1, 0)) * nw, kb_n - 1);
 #pragma unroll
     for (int s = 0; s < S; ++s)
       w0[u][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * n_strips + (RAGGED ? min(s, s_last) : s)) * 1024,
@@ -263,7 +286,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       const int kb = kb0 + wave + min(its + u, n_it - 1) * nw;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
-        a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (p.act_rows * 64), 0);
+        a[u][mt] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[mt], kb * (p.act_rows * 64),
+                                                         PM ? attn::kCachePolicyDevice : 0);
     }
   };
   auto load = [&](u32x4 (&w)[U][S], u32x4 (&a)[U][MT], int its) {
@@ -335,7 +359,50 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   };
 
   // sched_barrier keeps the compiler from sinking the prefetch next to its use
-  if (n_it > 0) {
+  if constexpr (PM) {
+    int its = pre;
+    load_w(w1, its + U);                                // the second stage, before the wait
+    __builtin_amdgcn_sched_barrier(0);
+    attn::fuse_wait_on<kFuseLanes>(fc->counters + 2 * kFuseLanes * kFuseStride, fc->n_odone, fc->err);
+    if (tid < 256) ss_issue(tid >> 4);
+    load_a(a0, its);
+    load_a(a1, its + U);
+    // A of the preloaded iterations (iterations past `pre` re-read the last
+    // one and are never used)
+    u32x4 ap[kGuPreMax];
+#pragma unroll
+    for (int i = 0; i < kGuPreMax; ++i)
+      ap[i] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[0], (kb0 + wave + min(i, max(pre - 1, 0)) * nw) *
+                                                    (p.act_rows * 64), attn::kCachePolicyDevice);
+    __builtin_amdgcn_sched_barrier(0);
+    if (tid < 256) ss_finish(ss_row);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < kGuPreMax; ++i) {
+      if (i < pre) {                                    // uniform
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+          const u32x4 wl = *reinterpret_cast<const u32x4*>(pre_lds + ((wave * pre + i) * S + s) * 256 + lane * 4);
+          acc[s][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, ap[i]),
+                                                             __builtin_bit_cast(f16x8, wl), acc[s][0], 0, 0, 0);
+        }
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+    while (its + 2 * U < n_it) {
+      compute(w0, a0, its);
+      __builtin_amdgcn_sched_barrier(0);
+      load(w0, a0, its + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(w1, a1, its + U);
+      __builtin_amdgcn_sched_barrier(0);
+      load(w1, a1, its + 3 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      its += 2 * U;
+    }
+    compute(w0, a0, its);
+    if (its + U < n_it) compute(w1, a1, its + U);     // uniform
+  } else if (n_it > 0) {
     int its = 0;
     load_a(a0, its);
     __builtin_amdgcn_sched_barrier(0);
@@ -561,8 +628,8 @@ __global__ __launch_bounds__(512) void k_gemm(const GemmArgs p) {
 // output (written in this launch) is then read at device scope.  The eight
 // wavefront partials are summed in wave order, then the residual epilogue of
 // gemm_tile: x += Y, fp16(x * g_next) and the strip's row sums of squares.
-template <int KI, int NU>
-__device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, const int u0, float* red) {
+template <int KI, int NU, bool GUF, class Pre>
+__device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, const int u0, float* red, Pre&& preload) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n_strips = p.n_strips, kb_total = p.kb_total;
@@ -577,6 +644,8 @@ __device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, con
       wv[j][i] = __builtin_amdgcn_raw_buffer_load_b128(wrs, ((u0 + j) * 64 + lane) * 16, kb * n_strips * 1024,
                                                        kCachePolicyNT);
   }
+  __builtin_amdgcn_sched_barrier(0);
+  preload();                                         // gate/up weights into LDS, behind the O weights
   __builtin_amdgcn_sched_barrier(0);
   // epilogue element of this thread: unit ej, row rsub, column csub of the
   // strip (the MFMA output layout; threads < 256 * NU)
@@ -628,21 +697,65 @@ __device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, con
   if (rsub < row_count) {
     const float xn = x_old + v;                      // residual + projection
     p.x[(size_t)rsub * p.ldx + n] = xn;
-    p.xg[act_index(rsub, n, p.act_rows)] = f16_flagged(xn * g, bad);
+    const uint16_t h = f16_flagged(xn * g, bad);
+    if constexpr (GUF)   // read by the gate/up tiles of this launch: device scope
+      __hip_atomic_store(p.xg + act_index(rsub, n, p.act_rows), h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      p.xg[act_index(rsub, n, p.act_rows)] = h;
     sq = xn * xn;
   }
   const float t = sum16(sq);
-  if (csub == 0) p.ss_out[(size_t)rsub * p.ss_stride + u0 + ej] = t;
+  if (csub == 0) {
+    if constexpr (GUF)
+      __hip_atomic_store(p.ss_out + (size_t)rsub * p.ss_stride + u0 + ej, t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      p.ss_out[(size_t)rsub * p.ss_stride + u0 + ej] = t;
+  }
   flag_range(bad, p.ovf);
 }
 
-// The O units of worker w (see FuseCtl), if it has any.
-template <int KI>
-__device__ __forceinline__ void o_part(const GemmArgs& p, const FuseCtl& f, const int w, float* red) {
-  if (w < f.o_two)
-    o_units<KI, 2>(p, f, 2 * w, red);
-  else if (f.o_two + w < f.o_units)
-    o_units<KI, 1>(p, f, f.o_two + w, red);
+// The O units of worker w (see FuseCtl), if it has any; `preload` runs once
+// in any case (after the O weight requests when there are units).  With GUF
+// (gate/up in the launch) a worker with units counts itself in once its
+// stores are complete.
+template <int KI, bool GUF, class Pre>
+__device__ __forceinline__ void o_part(const GemmArgs& p, const FuseCtl& f, const int w, float* red, Pre&& preload) {
+  if (w < f.o_two) {
+    o_units<KI, 2, GUF>(p, f, 2 * w, red, preload);
+  } else if (f.o_two + w < f.o_units) {
+    o_units<KI, 1, GUF>(p, f, f.o_two + w, red, preload);
+  } else {
+    preload();
+    return;
+  }
+  if constexpr (GUF) {
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);          // this wavefront's stores are complete
+    __syncthreads();
+    if (threadIdx.x == 0)
+      __hip_atomic_fetch_add(f.counters + (2 * kFuseLanes + blockIdx.x % kFuseLanes) * kFuseStride, 1,
+                             __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+// Gate/up weights of tile `tile` for the first `pre` input iterations of
+// wavefronts 0-3 (k-blocks w + 4i, as gemm_tile streams them), loaded
+// straight into LDS at [w][i][strip] (1 KiB blocks, lane-ordered) with no
+// registers held; called by wavefronts 0-3, each for its own blocks.
+template <int S>
+__device__ __forceinline__ void gu_preload(const GemmArgs& p, const int tile, const int pre, uint32_t* lds) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(p.W), 0, (int)min((size_t)p.n_strips * p.kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
+  const int voff = (tile * S * 64 + lane) * 16;
+  for (int i = 0; i < pre; ++i) {
+    const int kb = wave + 4 * i;                     // < kb_total: pre <= kb_total / 4 (host)
+#pragma unroll
+    for (int s = 0; s < S; ++s)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          wrs, (__attribute__((address_space(3))) void*)(lds + ((wave * pre + i) * S + s) * 256), 16, voff,
+          (kb * p.n_strips + s) * 1024, 0, kCachePolicyNT);
+  }
 }
 
 // Decode passes over contexts of one attention chunk: the QKV GEMM, the
@@ -662,12 +775,23 @@ __device__ __forceinline__ void o_part(const GemmArgs& p, const FuseCtl& f, cons
 // co-resident (the host checks the grid against the device's occupancy), a
 // phase waits only for earlier phases, and every wait is bounded
 // (attn::fuse_wait_on), so every wait ends.
-template <int MT, int S, int HD, int OKI>
+template <int MT, int S, int HD, int OKI, int SG>
 __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnArgs a, const FuseCtl f,
-                                                  const GemmArgs o) {
-  extern __shared__ float red[];     // GEMM tiles: [4][S * MT * 256]; O units: [8][2][256]
+                                                  const GemmArgs o, const GemmArgs gu) {
+  static_assert(SG == 0 || (MT == 1 && OKI > 0), "gate/up joins only launches with O units");
+  // [0, gu_lds): reductions (GEMM tiles [4][S * MT * 256], O units [8][2][256],
+  // gate/up [4][SG * 256]); from gu_lds: preloaded gate/up weights
+  extern __shared__ float red[];
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
+  uint32_t* pre_lds = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(red) + f.gu_lds);
+  const bool gu_tile = SG > 0 && b < f.gu_tiles;          // uniform
+  const int pre = b < g.n_tiles ? f.gu_pre_q : f.gu_pre;
+  auto preload = [&]() {
+    if constexpr (SG > 0) {
+      if (gu_tile && tid < 256) gu_preload<SG>(gu, b, pre, pre_lds);
+    }
+  };
   if (b < g.n_tiles) {
     if (tid < 256) {
       gemm_tile<MT, S, EPI_QKV, true>(g, b, 0, 1, 4, red);
@@ -679,13 +803,12 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     if (tid == 0)
       __hip_atomic_fetch_add(f.counters + (b % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
                              __HIP_MEMORY_SCOPE_AGENT);
-    if constexpr (OKI > 0) o_part<OKI>(o, f, f.o_extra + b, red);
-    return;
-  }
-  const int i = b - g.n_tiles;
-  if (i < f.n_cons) {
+    if constexpr (OKI > 0) o_part<OKI, (SG > 0)>(o, f, f.o_extra + b, red, preload);
+  } else if (b - g.n_tiles < f.n_cons) {
+    const int i = b - g.n_tiles;
     const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
     const unsigned z = i / (a.n_kv * a.n_qblocks);
+    preload();                                      // behind nothing: the attention waits long anyway
     attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f);
     if constexpr (OKI > 0) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's output stores are complete
@@ -694,9 +817,20 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
         __hip_atomic_fetch_add(f.counters + (kFuseLanes + tid) * kFuseStride, 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     }
-    return;
+  } else {
+    if constexpr (OKI > 0) o_part<OKI, (SG > 0)>(o, f, b - g.n_tiles - f.n_cons, red, preload);
   }
-  if constexpr (OKI > 0) o_part<OKI>(o, f, i - f.n_cons, red);
+  if constexpr (SG > 0) {
+    if (gu_tile) {
+      __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's preloaded weights are in LDS
+      if (tid < 256) {
+        gemm_tile<1, SG, EPI_SWIGLU, false, true>(gu, b, 0, 1, 4, red, &f, pre_lds, pre);
+      } else {                                      // the tile's two barriers
+        attn::fuse_wait_on<kFuseLanes>(f.counters + 2 * kFuseLanes * kFuseStride, f.n_odone, f.err);
+        __syncthreads();
+      }
+    }
+  }
 }
 
 __device__ void commit_verify(const TailArgs& p, const PassSeq& ps, int a, int bonus, const int* res);
@@ -1688,59 +1822,99 @@ hipError_t launch_mt(int mt, int S, int nw, const GemmArgs& a, hipStream_t st, L
   return hipErrorInvalidValue;
 }
 
-template <int MT, int S, int HD, int OKI>
+// What launch_qkv_attn_any does for a shape: launch it, or report its
+// co-resident workgroups (at `pre` preloaded gate/up iterations) or the
+// largest `pre` its LDS holds.
+struct FuseQuery {
+  enum { LAUNCH, CAPACITY, PRE_MAX } what = LAUNCH;
+  int pre = 0;
+  int result = 0;
+};
+
+template <int MT, int S, int OKI, int SG>
+constexpr size_t fuse_red_bytes() {
+  return std::max({(size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0,
+                   SG > 0 ? (size_t)4 * SG * 256 : (size_t)0}) * sizeof(float);
+}
+
+template <int MT, int S, int HD, int OKI, int SG>
 hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, const GemmArgs& o,
-                               hipStream_t st, LaunchEvents ev, int* capacity) {
-  const size_t lds = std::max((size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0) * sizeof(float);
-  if (capacity) {
-    int per_cu = 0, dev = 0;
+                               const GemmArgs& gu, hipStream_t st, LaunchEvents ev, FuseQuery& q) {
+  constexpr size_t red = fuse_red_bytes<MT, S, OKI, SG>();
+  auto kern = k_qkv_attn<MT, S, HD, OKI, SG>;
+  const int pre = q.what == FuseQuery::LAUNCH ? std::max(f.gu_pre, f.gu_pre_q) : q.pre;
+  const size_t lds = red + (SG > 0 ? (size_t)4 * pre * SG * 1024 : 0);
+  if (q.what != FuseQuery::LAUNCH) {
+    int dev = 0;
     hipDeviceProp_t prop;
+    hipFuncAttributes attr;
     if (hipGetDevice(&dev) != hipSuccess || hipGetDeviceProperties(&prop, dev) != hipSuccess ||
-        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_qkv_attn<MT, S, HD, OKI>, 512, lds) != hipSuccess)
+        hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(kern)) != hipSuccess)
       return hipErrorInvalidValue;
-    *capacity = per_cu * prop.multiProcessorCount;
+    const size_t room = (size_t)prop.maxSharedMemoryPerMultiProcessor;
+    if (q.what == FuseQuery::PRE_MAX) {
+      const size_t used = attr.sharedSizeBytes + red;
+      q.result = SG > 0 && room > used ? (int)std::min<size_t>(kGuPreMax, (room - used) / ((size_t)4 * SG * 1024)) : 0;
+      return hipSuccess;
+    }
+    if (attr.sharedSizeBytes + lds > room) return hipErrorInvalidValue;
+    int per_cu = 0;
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)(room - attr.sharedSizeBytes)) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, 512, lds) != hipSuccess)
+      return hipErrorInvalidValue;
+    q.result = per_cu * prop.multiProcessorCount;
     return hipSuccess;
   }
+  FuseCtl fl = f;
+  fl.gu_lds = (int)red;
   const int grid = g.n_tiles + f.n_cons + f.o_extra;
   if (ev.start) {
-    hipExtLaunchKernelGGL(k_qkv_attn<MT, S, HD, OKI>, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u,
-                          g, a, f, o);
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, fl, o, gu);
   } else {
-    k_qkv_attn<MT, S, HD, OKI><<<grid, 512, lds, st>>>(g, a, f, o);
+    kern<<<grid, 512, lds, st>>>(g, a, fl, o, gu);
   }
   return hipGetLastError();
 }
 
 template <int MT, int S, int HD>
-hipError_t launch_qkv_attn_oki(int oki, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, const GemmArgs& o,
-                               hipStream_t st, LaunchEvents ev, int* capacity) {
-  if (oki == 0) return launch_qkv_attn_one<MT, S, HD, 0>(g, a, f, o, st, ev, capacity);
+hipError_t launch_qkv_attn_oki(int oki, int sg, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                               const GemmArgs& o, const GemmArgs& gu, hipStream_t st, LaunchEvents ev,
+                               FuseQuery& q) {
+  if (oki == 0 && sg == 0) return launch_qkv_attn_one<MT, S, HD, 0, 0>(g, a, f, o, gu, st, ev, q);
   if constexpr (MT == 1) {
-    if (oki == 8) return launch_qkv_attn_one<MT, S, HD, 8>(g, a, f, o, st, ev, capacity);
-    if (oki == 16) return launch_qkv_attn_one<MT, S, HD, 16>(g, a, f, o, st, ev, capacity);
+    switch (oki * 100 + sg) {
+      case 800: return launch_qkv_attn_one<MT, S, HD, 8, 0>(g, a, f, o, gu, st, ev, q);
+      case 804: return launch_qkv_attn_one<MT, S, HD, 8, 4>(g, a, f, o, gu, st, ev, q);
+      case 807: return launch_qkv_attn_one<MT, S, HD, 8, 7>(g, a, f, o, gu, st, ev, q);
+      case 1600: return launch_qkv_attn_one<MT, S, HD, 16, 0>(g, a, f, o, gu, st, ev, q);
+      case 1604: return launch_qkv_attn_one<MT, S, HD, 16, 4>(g, a, f, o, gu, st, ev, q);
+      case 1607: return launch_qkv_attn_one<MT, S, HD, 16, 7>(g, a, f, o, gu, st, ev, q);
+    }
   }
   return hipErrorInvalidValue;
 }
 
 template <int MT, int S>
-hipError_t launch_qkv_attn_hd(int hd, int oki, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                              const GemmArgs& o, hipStream_t st, LaunchEvents ev, int* capacity) {
-  if (hd == 64) return launch_qkv_attn_oki<MT, S, 64>(oki, g, a, f, o, st, ev, capacity);
-  if (hd == 128) return launch_qkv_attn_oki<MT, S, 128>(oki, g, a, f, o, st, ev, capacity);
+hipError_t launch_qkv_attn_hd(int hd, int oki, int sg, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                              const GemmArgs& o, const GemmArgs& gu, hipStream_t st, LaunchEvents ev, FuseQuery& q) {
+  if (hd == 64) return launch_qkv_attn_oki<MT, S, 64>(oki, sg, g, a, f, o, gu, st, ev, q);
+  if (hd == 128) return launch_qkv_attn_oki<MT, S, 128>(oki, sg, g, a, f, o, gu, st, ev, q);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_qkv_attn_any(int mt, int S, int hd, int oki, const GemmArgs& g, const AttnArgs& a,
-                               const FuseCtl& f, const GemmArgs& o, hipStream_t st, LaunchEvents ev, int* capacity) {
+hipError_t launch_qkv_attn_any(int mt, int S, int hd, int oki, int sg, const GemmArgs& g, const AttnArgs& a,
+                               const FuseCtl& f, const GemmArgs& o, const GemmArgs& gu, hipStream_t st,
+                               LaunchEvents ev, FuseQuery& q) {
   switch (mt * 4 + S) {
-    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, oki, g, a, f, o, st, ev, capacity);
-    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, oki, g, a, f, o, st, ev, capacity);
+    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
   }
   return hipErrorInvalidValue;
 }
@@ -1751,24 +1925,46 @@ int o_ki(int kb) { return kb == 0 ? 0 : kb <= 64 ? 8 : kb <= kFuseOMaxKb ? 16 : 
 
 }  // namespace
 
-int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb) {
-  // [mt][S][hd 64 / 128][no O, 8, 16 k-blocks per wavefront]: co-resident
-  // workgroups (0: not yet asked, -1: unsupported)
-  static int cache[5][3][2][3];
+// Shape key of the fused launch queries (cached: the answers do not change,
+// and nothing is asked during a graph capture once the engine has warmed up).
+static int64_t fuse_key(int kind, int mt, int S, int head_dim, int oki, int sg, int pre) {
+  return ((((((int64_t)kind * 8 + mt) * 4 + S) * 256 + head_dim) * 32 + oki) * 16 + sg) * 16 + pre;
+}
+
+static int fuse_query(int kind, int mt, int S, int head_dim, int oki, int sg, int pre) {
+  static std::map<int64_t, int> cache;   // 0 or more: the answer; -1: unsupported
+  const int64_t key = fuse_key(kind, mt, S, head_dim, oki, sg, pre);
+  auto it = cache.find(key);
+  if (it != cache.end()) return it->second;
+  FuseQuery q;
+  q.what = kind == 0 ? FuseQuery::CAPACITY : FuseQuery::PRE_MAX;
+  q.pre = pre;
+  int r = -1;
+  if (launch_qkv_attn_any(mt, S, head_dim, oki, sg, GemmArgs{}, AttnArgs{}, FuseCtl{}, GemmArgs{}, GemmArgs{},
+                          nullptr, LaunchEvents{}, q) == hipSuccess)
+    r = q.result;
+  cache[key] = r;
+  return r;
+}
+
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb, int gu_S, int gu_pre) {
   const int oki = o_ki(o_kb);
-  if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki < 0 || (oki > 0 && mt != 1))
+  if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki < 0 || (oki > 0 && mt != 1) ||
+      (gu_S != 0 && gu_S != 4 && gu_S != 7) || (gu_S > 0 && (oki == 0 || gu_pre < 1 || gu_pre > kGuPreMax)))
     return 0;
-  int& c = cache[mt][S][head_dim == 128][oki / 8];
-  if (c == 0) {
-    int n = 0;
-    c = launch_qkv_attn_any(mt, S, head_dim, oki, GemmArgs{}, AttnArgs{}, FuseCtl{}, GemmArgs{}, nullptr,
-                            LaunchEvents{}, &n) == hipSuccess && n > 0 ? n : -1;
-  }
-  return c > 0 ? c : 0;
+  const int r = fuse_query(0, mt, S, head_dim, oki, gu_S, gu_S > 0 ? gu_pre : 0);
+  return r > 0 ? r : 0;
+}
+
+int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S) {
+  const int oki = o_ki(o_kb);
+  if (S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki <= 0 || (gu_S != 4 && gu_S != 7)) return 0;
+  const int r = fuse_query(1, 1, S, head_dim, oki, gu_S, 0);
+  return r > 0 ? r : 0;
 }
 
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           const GemmArgs* o, hipStream_t st, LaunchEvents ev) {
+                           const GemmArgs* o, const GemmArgs* gu, int gu_S, hipStream_t st, LaunchEvents ev) {
   // the GEMM tiles cover the strips exactly, one input range; the attention
   // part is the single-chunk plan with one query tile per workgroup
   if (g.n_tiles < 1 || g.ksplit != 1 || g.kb_split < g.kb_total || (size_t)g.n_tiles * S != (size_t)g.n_strips)
@@ -1778,11 +1974,11 @@ hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const
   if (!f.counters || !f.err || f.n_prod != g.n_tiles || f.n_cons != a.n_kv * a.n_qblocks * a.n_seq)
     return hipErrorInvalidValue;
   int oki = 0;
+  const int workers = f.o_extra + f.n_prod;
   if (o) {
     // one row tile; O units: one strip each over one input range, every
     // worker with two units an extra workgroup
     oki = o_ki(o->kb_total);
-    const int workers = f.o_extra + f.n_prod;
     if (mt != 1 || oki <= 0 || o->n_strips != f.o_units || f.o_units < 1 || f.o_extra < 0 || f.o_two < 0 ||
         f.o_two > f.o_extra || f.o_units > workers + f.o_two || o->act_rows != a.act_rows || !o->A || !o->x ||
         !o->xg || !o->g_next || !o->ss_out || o->desc != a.desc)
@@ -1790,9 +1986,25 @@ hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const
   } else if (f.o_units != 0 || f.o_extra != 0) {
     return hipErrorInvalidValue;
   }
-  const int cap = qkv_attn_capacity(mt, S, head_dim, o ? o->kb_total : 0);
-  if (cap <= 0 || g.n_tiles + f.n_cons + f.o_extra > cap) return hipErrorInvalidValue;
-  return launch_qkv_attn_any(mt, S, head_dim, oki, g, a, f, o ? *o : GemmArgs{}, st, ev, nullptr);
+  const int grid = g.n_tiles + f.n_cons + f.o_extra;
+  if (gu) {
+    // gate/up: needs the O units; tiles of gu_S strips cover the weight
+    // exactly, one per workgroup of the grid at most; four wavefronts;
+    // preloaded iterations within every wavefront's range
+    if (!o || (gu_S != 4 && gu_S != 7) || gu->n_tiles != f.gu_tiles || f.gu_tiles < 1 || f.gu_tiles > grid ||
+        (size_t)gu->n_tiles * gu_S != (size_t)gu->n_strips || gu->ksplit != 1 || gu->kb_split < gu->kb_total ||
+        f.gu_pre < 1 || f.gu_pre_q < 0 || f.gu_pre > kGuPreMax || f.gu_pre_q > f.gu_pre || f.gu_pre > gu->kb_total / 4 ||
+        f.n_odone != std::min(workers, f.o_units - f.o_two) || gu->act_rows != a.act_rows || gu->desc != a.desc ||
+        gu->A != o->xg || gu->ss_in != o->ss_out)
+      return hipErrorInvalidValue;
+  } else if (f.gu_tiles != 0) {
+    return hipErrorInvalidValue;
+  }
+  const int cap = qkv_attn_capacity(mt, S, head_dim, o ? o->kb_total : 0, gu ? gu_S : 0, gu ? f.gu_pre : 0);
+  if (cap <= 0 || grid > cap) return hipErrorInvalidValue;
+  FuseQuery q;
+  return launch_qkv_attn_any(mt, S, head_dim, oki, gu ? gu_S : 0, g, a, f, o ? *o : GemmArgs{}, gu ? *gu : GemmArgs{},
+                             st, ev, q);
 }
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {

@@ -20,7 +20,7 @@
 // projection).
 //
 // usage: gemm_counters [rows 9] [S 7] [P 1] [strips 1792] [kb 128] [epi swiglu|resid|qkv] [copies 1] [check 0]
-//                      [ss_tiles 1] [wavefronts 4|8]
+//                      [ss_tiles 1] [wavefronts 4|8] [touch -1|0|2]
 #include <cstdio>
 #include <cstdlib>
 #include <cmath>
@@ -49,6 +49,20 @@ __global__ void k_fill_f16(uint16_t* p, size_t n, uint32_t seed) {
   }
 }
 
+// Reads n 16-byte words of p with the given buffer cache policy (a stand-in
+// for a prefetch into the last-level cache); the XOR of what it read is
+// stored only when it equals a value no seeded fill produces.
+__global__ void k_touch(const uint16_t* p, size_t n16, int policy, unsigned* sink) {
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(p), 0, 0x7fffffff, 0x00020000);
+  unsigned x = 0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += (size_t)gridDim.x * blockDim.x) {
+    const auto v = policy == 2 ? __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, 2)
+                               : __builtin_amdgcn_raw_buffer_load_b128(rs, (int)(i * 16), 0, 0);
+    x ^= v[0] ^ v[1] ^ v[2] ^ v[3];
+  }
+  if (x == 0x9E3779B9u && sink) *sink = x;
+}
+
 __global__ void k_fill_value(float* p, size_t n, float v) {
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) p[i] = v;
 }
@@ -65,6 +79,10 @@ int main(int argc, char** argv) {
   const bool check = argc > 8 && atoi(argv[8]) != 0;
   const int ss_tiles = argc > 9 ? atoi(argv[9]) : 1;
   const int nw = argc > 10 ? atoi(argv[10]) : 4;
+  // touch >= 0: before each timed launch, read its weight copy with cache
+  // policy `touch` (0 default, 2 non-temporal; 10 + policy: read the next
+  // copy instead, the control) and time the launch alone
+  const int touch = argc > 11 ? atoi(argv[11]) : -1;
   const int epi = resid ? EPI_RESID : qkv ? EPI_QKV : EPI_SWIGLU;
   constexpr int kHd = 128, kCap = 1024, kPos0 = 512;
   const int kb_split = P > 0 ? (kb_total + P - 1) / P : 0;
@@ -145,12 +163,27 @@ int main(int argc, char** argv) {
   for (int i = 0; i < 20; ++i) CHECK(run());
   CHECK(hipDeviceSynchronize());
   const int n = 100;
-  CHECK(hipEventRecord(e0, 0));
-  for (int i = 0; i < n; ++i) CHECK(run());
-  CHECK(hipEventRecord(e1, 0));
-  CHECK(hipEventSynchronize(e1));
   float ms = 0.f;
-  CHECK(hipEventElapsedTime(&ms, e0, e1));
+  if (touch < 0) {
+    CHECK(hipEventRecord(e0, 0));
+    for (int i = 0; i < n; ++i) CHECK(run());
+    CHECK(hipEventRecord(e1, 0));
+    CHECK(hipEventSynchronize(e1));
+    CHECK(hipEventElapsedTime(&ms, e0, e1));
+  } else {
+    for (int i = 0; i < n; ++i) {
+      // touch >= 10: the control, which reads another copy (policy touch - 10)
+      const int cp = touch >= 10 ? (launch + 1) % copies : launch % copies;
+      k_touch<<<1024, 256>>>(W + w_elems * cp, w_elems * 2 / 16, touch % 10, nullptr);
+      CHECK(hipEventRecord(e0, 0));
+      CHECK(run());
+      CHECK(hipEventRecord(e1, 0));
+      CHECK(hipEventSynchronize(e1));
+      float t = 0.f;
+      CHECK(hipEventElapsedTime(&t, e0, e1));
+      ms += t;
+    }
+  }
   const double us = ms * 1e3 / n;
   printf("k_gemm<1, %d, %d> %s, %d strips x %d k-blocks, %d rows, %d x %d workgroups of %d wavefronts, %d weight copies: "
          "%.2f us per launch, weights %.2f TB/s\n", S, epi, resid ? "resid" : qkv ? "qkv" : "swiglu", n_strips, kb_total, rows,

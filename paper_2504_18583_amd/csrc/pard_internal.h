@@ -280,14 +280,26 @@ struct AttnArgs {
 // nothing else, so their weight requests start with the launch), then the
 // QKV workgroups; worker w < o_two takes units 2w and 2w + 1, a later worker
 // unit o_two + w (if any).
+//
+// Gate/up units (gu_tiles > 0, with O units): workgroup b < gu_tiles runs
+// gate/up tile b.  Its first gu_pre (gu_pre_q for QKV workgroups, which load
+// theirs only once their tile is done) input iterations of weights are loaded
+// straight into LDS early, while the attention runs; O workers count
+// themselves in on counter 2 kFuseLanes + w % kFuseLanes once their
+// epilogue's device-scope stores are complete, and the gate/up tiles wait for
+// n_odone such arrivals before reading the O-projection's output (at device
+// scope).
 constexpr int kFuseLanes = 8;      // arrival counters per phase (spread over XCDs and memory channels)
 constexpr int kFuseStride = 64;    // ints between two counters
-constexpr int kFuseInts = 2 * kFuseLanes * kFuseStride;   // one layer's set: QKV arrivals, attention arrivals
+constexpr int kFuseInts = 3 * kFuseLanes * kFuseStride;   // one layer's set: QKV, attention and O arrivals
 struct FuseCtl {
   int* counters = nullptr;         // this layer's kFuseInts ints, zero at the launch
   int n_prod = 0, n_cons = 0;      // QKV workgroups, attention workgroups
   int* err = nullptr;
   int o_units = 0, o_extra = 0, o_two = 0;
+  int gu_tiles = 0, gu_pre = 0, gu_pre_q = 0;
+  int n_odone = 0;                 // O workers with units
+  int gu_lds = 0;                  // byte offset of the preloaded weights in the dynamic LDS (set by the launcher)
 };
 
 // Optional timing events of one launch (recorded at the kernel's start and end).
@@ -316,10 +328,16 @@ hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEv
 // With o (non-null, one row tile only) the launch also carries the
 // O-projection + residual of the attention output (EPI_RESID, one strip per
 // tile, one input range of at most kFuseOMaxKb k-blocks; f's O fields set).
+// With gu as well (o required; f's gate/up fields set) it carries the
+// gate/up GEMM (EPI_SWIGLU, gu_S strips per tile, one input range, four
+// wavefronts), its first weight blocks preloaded into LDS.
 constexpr int kFuseOMaxKb = 128;
-int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb = 0);
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb = 0, int gu_S = 0, int gu_pre = 0);
+// largest gu_pre the LDS holds for this launch shape (0: none)
+int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S);
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           const GemmArgs* o, hipStream_t st, LaunchEvents ev = LaunchEvents{});
+                           const GemmArgs* o, const GemmArgs* gu, int gu_S, hipStream_t st,
+                           LaunchEvents ev = LaunchEvents{});
 hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st);
 hipError_t launch_stage(const TailArgs& a, hipStream_t st);
 hipError_t launch_attention(int head_dim, const AttnArgs& a, hipStream_t st);

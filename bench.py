@@ -555,10 +555,10 @@ def main() -> int:
     # stream over a second run of the same steps: the target's gate/up GEMM,
     # or, where the engine runs gate/up inside the decode layer's launch (QKV,
     # attention, O-projection and gate/up), that launch
-    def time_class(op):
-        eng.timer_enable(B.PARD_TARGET * 8 + op, min(steps * t_spec.n_layers, 1 << 16))
+    def time_class(op, n_steps=steps):
+        eng.timer_enable(B.PARD_TARGET * 8 + op, min(n_steps * t_spec.n_layers, 1 << 16))
         eng.generate(k, big - eng.kv_len(B.PARD_TARGET) - 2 * k - 2,
-                     max_steps=max(1, min(steps, (max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2) // (k + 1))))
+                     max_steps=max(1, min(n_steps, (max_ctx - eng.kv_len(B.PARD_TARGET) - 2 * k - 2) // (k + 1))))
         n, ms = eng.timer_read()
         eng.timer_enable(-1, 1)
         return n, ms
@@ -572,11 +572,13 @@ def main() -> int:
         # the counter summary covers the 8B-shaped gate/up launch with 9 rows only
         traffic = measured_traffic() if (t_spec.d_model, t_spec.ffn_dim, k) == (4096, 14336, 8) else None
     else:
+        with_down = time_class(B.OP_DOWN, 1)[0] == 0   # the down projection runs inside the launch too
+        l_mean = eng.kv_len(B.PARD_TARGET) + steps * tokens_per_step / 2
         launches, total_ms = time_class(B.OP_QKV)
         # the timer run's mean committed target length (it continues after the timed steps)
-        kbytes = bm.layer_launch_bytes(t_spec, k + 1, int(round(l_t1 + steps * tokens_per_step / 2)))
-        kname = (f"k_qkv_attn (target decode layer: QKV GEMM, attention, O-projection and gate/up GEMM, "
-                 f"{k + 1} rows)")
+        kbytes = bm.layer_launch_bytes(t_spec, k + 1, int(round(l_mean)), with_down)
+        kname = (f"k_qkv_attn (target decode layer: QKV GEMM, attention, O-projection, gate/up"
+                 f"{' and down' if with_down else ''} GEMMs, {k + 1} rows)")
         traffic = None                               # no counter summary of this launch
     avg_s = total_ms / 1e3 / max(launches, 1)
     achieved = kbytes / avg_s / 1e9 if launches > 0 else 0.0

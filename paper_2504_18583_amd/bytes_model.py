@@ -57,20 +57,20 @@ def step_bytes(target, draft, k: int, accepted_prev: int, l_t: int, l_d: int) ->
             + verify_pass_bytes(target, k, l_t))
 
 
-def layer_launch_bytes(spec, rows: int, context: int) -> int:
+def layer_launch_bytes(spec, rows: int, context: int, with_down: bool = False) -> int:
     """One decode layer's launch that carries the QKV GEMM (+ bias), the
-    attention, the O-projection and the gate/up GEMM: those weights once, the
-    layer's KV cache read over the context + rows positions and its new rows
-    written, the rows' fp16 activations in and h out (the down projection is
-    the next launch)."""
+    attention, the O-projection, the gate/up GEMM and (with_down) the down
+    projection: those weights once, the layer's KV cache read over the context
+    + rows positions and its new rows written, the rows' fp16 activations in
+    and out (h out, or the next layer's fp16 input with the down projection)."""
     d, hd = spec.d_model, spec.head_dim
     q_dim, kv_dim = spec.n_heads * hd, spec.n_kv_heads * hd
     f_pad = (spec.ffn_dim + 31) // 32 * 32
-    w = (d * (q_dim + 2 * kv_dim) + q_dim * d + 2 * f_pad * d) * BF16
+    w = (d * (q_dim + 2 * kv_dim) + q_dim * d + 2 * f_pad * d + (f_pad * d if with_down else 0)) * BF16
     if spec.qkv_bias:
         w += (q_dim + 2 * kv_dim) * BF16
     kv = 2 * kv_dim * BF16 * (context + rows) + 2 * kv_dim * BF16 * rows
-    return w + kv + rows * d * 2 + rows * f_pad * 2
+    return w + kv + rows * d * 2 + rows * (d if with_down else f_pad) * 2
 
 
 def gemm_bytes(n: int, k: int, rows: int, a_bytes: int = 4, out_bytes: int = 4) -> int:

@@ -234,6 +234,7 @@ struct pard_ctx {
   bool use_fused = true;
   bool use_fused_o = true;
   bool use_fused_gu = true;
+  bool use_fused_d = true;
   int gu_pre = -1, gu_pre_q = -1;   // preloaded gate/up iterations (-1: as many as the LDS holds)
   // captured fused steps (draft pass + verify pass), replayed on `stream`
   struct StepGraph { int n_seq, k, l_class; bool vsd; hipGraphExec_t exec; };
@@ -554,6 +555,28 @@ GemmArgs gu_args(const ModelDev& M, const Layer& L, int act_rows, int ss_tiles, 
   return a;
 }
 
+// Down projection + residual of layer l: x += h W_down^T, then fp16(x * g)
+// for the next layer's (or the final) norm and the row sums of squares.
+// fused: the tile plan of a fused launch (one strip per tile, one input range).
+GemmArgs d_args(const ModelDev& M, int l, int act_rows, bool fused) {
+  GemmArgs a = gemm_base(M, M.layers[l].wd, act_rows);
+  a.A = M.h;
+  a.lda = M.f_pad;
+  a.x = M.x;
+  a.ldx = M.d;
+  a.g_next = (l + 1 < M.spec.n_layers) ? M.layers[l + 1].g_attn : M.g_final;
+  a.xg = M.xg;
+  a.ss_out = M.ss;
+  if (fused) {
+    a.kb_total = M.p_d.kb_total;
+    a.n_strips = M.p_d.n_strips;
+    a.n_tiles = M.p_d.n_strips;
+    a.ksplit = 1;
+    a.kb_split = M.p_d.kb_total;
+  }
+  return a;
+}
+
 struct PassSpec {
   int max_rows = 1;       // upper bound of n_rows (sets the M tiles)
   int typ_rows = 0;       // row count the split plan is tuned for (0: max_rows)
@@ -677,24 +700,30 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
   // runs one gate/up tile, whose first weight blocks it loads into LDS while
   // the attention runs (extras are added until the grid covers the tiles)
   const int S_gu = pick_S(EPI_SWIGLU, M.p_gu.n_strips, 1);
-  bool fused_gu = false;
+  bool fused_gu = false, fused_d = false;
   if (fused_o && c->use_fused_gu && (S_gu == 4 || S_gu == 7) && M.p_gu.ksplit == 1 &&
       M.p_gu.n_strips % S_gu == 0 && plan_nw(M.p_gu, S_gu, 1) == 4) {
     const int n_qkv = M.p_qkv.n_strips / S_q;
     const int gu_tiles = M.p_gu.n_strips / S_gu;
-    const int pre_max = std::min(qkv_attn_gu_pre_max(S_q, s.head_dim, M.p_o.kb_total, S_gu), M.p_gu.kb_total / 4);
+    // and the down projection (one strip per tile, one input range), whose
+    // workgroups wait for every gate/up tile
+    const int d_S = c->use_fused_d && M.p_d.ksplit == 1 && pick_S(EPI_RESID, M.p_d.n_strips, 1) == 1 &&
+                    plan_nw(M.p_d, 1, 1) == 4 ? 1 : 0;
+    const int pre_max = std::min(qkv_attn_gu_pre_max(S_q, s.head_dim, M.p_o.kb_total, S_gu, d_S), M.p_gu.kb_total / 4);
     const int pre = c->gu_pre >= 0 ? std::min(c->gu_pre, pre_max) : pre_max;
     const int pre_q = c->gu_pre_q >= 0 ? std::min(c->gu_pre_q, pre) : pre;
-    const int cap = pre >= 1 ? qkv_attn_capacity(1, S_q, s.head_dim, M.p_o.kb_total, S_gu, pre) : 0;
+    const int cap = pre >= 1 ? qkv_attn_capacity(1, S_q, s.head_dim, M.p_o.kb_total, S_gu, pre, d_S) : 0;
     FuseCtl t = fo;
-    t.o_extra = std::max(fo.o_extra, gu_tiles - n_qkv - n_attn_wg);
+    t.o_extra = std::max({fo.o_extra, gu_tiles - n_qkv - n_attn_wg, d_S ? M.p_d.n_strips - n_qkv - n_attn_wg : 0});
     t.o_two = std::max(0, t.o_units - n_qkv - t.o_extra);
     if (cap > 0 && gu_tiles <= cap && n_qkv + n_attn_wg + t.o_extra <= cap && t.o_two <= t.o_extra) {
       fused_gu = true;
+      fused_d = d_S == 1;
       t.gu_tiles = gu_tiles;
       t.gu_pre = pre;
       t.gu_pre_q = pre_q;
       t.n_odone = std::min(n_qkv + t.o_extra, t.o_units - t.o_two);
+      t.d_tiles = fused_d ? M.p_d.n_strips : 0;
       fo = t;
     }
   }
@@ -750,9 +779,10 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
         f.err = c->fuse_err;
         f.n_prod = a.n_tiles;
         f.n_cons = n_attn_wg;
-        GemmArgs o{}, gu{};
+        GemmArgs o{}, gu{}, dn{};
         if (fused_o) o = o_args(M, L, act_rows);
         if (fused_gu) gu = gu_args(M, L, act_rows, ss_tiles, S_gu);
+        if (fused_d) dn = d_args(M, l, act_rows, true);
         // the kernel timer's QKV class covers the fused launch (attention included)
         LaunchEvents ev;
         if (c->timer_class == cls0 + 1 && c->timer_used < c->timer_max) {
@@ -761,7 +791,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
           ++c->timer_used;
         }
         HIP_TRY(c, launch_qkv_attn(mt_q, S_q, s.head_dim, a, aa, f, fused_o ? &o : nullptr, fused_gu ? &gu : nullptr,
-                                   S_gu, c->stream, ev));
+                                   S_gu, fused_d ? &dn : nullptr, c->stream, ev));
       } else {
         HIP_TRY(c, run_gemm(c, cls0 + 1, EPI_QKV, ps.max_rows, typ, a, M.p_qkv));
       }
@@ -776,16 +806,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     if (!fused_gu) {  // norm + gate/up + SiLU * up
       HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, ps.max_rows, typ, gu_args(M, L, act_rows, ss_tiles, 0), M.p_gu));
     }
-    {  // down + residual
-      GemmArgs a = gemm_base(M, L.wd, act_rows);
-      a.A = M.h;
-      a.lda = M.f_pad;
-      a.x = M.x;
-      a.ldx = M.d;
-      a.g_next = (l + 1 < s.n_layers) ? M.layers[l + 1].g_attn : M.g_final;
-      a.xg = M.xg;
-      a.ss_out = M.ss;
-      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, ps.max_rows, typ, a, M.p_d));
+    if (!fused_d) {  // down + residual
+      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, ps.max_rows, typ, d_args(M, l, act_rows, false), M.p_d));
     }
   }
   if (ps.max_lm_rows > 0) {
@@ -1087,6 +1109,7 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
   if (const char* e = getenv("PARD_NO_FUSE")) c->use_fused = e[0] == '0';
   if (const char* e = getenv("PARD_NO_FUSE_O")) c->use_fused_o = e[0] == '0';
   if (const char* e = getenv("PARD_NO_FUSE_GU")) c->use_fused_gu = e[0] == '0';
+  if (const char* e = getenv("PARD_NO_FUSE_D")) c->use_fused_d = e[0] == '0';
   if (const char* e = getenv("PARD_GU_PRE")) c->gu_pre = atoi(e);
   if (const char* e = getenv("PARD_GU_PRE_Q")) c->gu_pre_q = atoi(e);
   c->prefilled.assign(max_batch, 0);
@@ -1127,9 +1150,11 @@ pard_status pard_model_load(const pard_model_spec* target, const pard_model_spec
           const ModelDev& M = c->m[w];
           (void)qkv_attn_capacity(mt, S, M.spec.head_dim, M.p_o.kb_total);
           const int S_gu = pick_S(EPI_SWIGLU, M.p_gu.n_strips, 1);
-          const int pre_max = qkv_attn_gu_pre_max(S, M.spec.head_dim, M.p_o.kb_total, S_gu);
-          for (int pre = 1; pre <= pre_max; ++pre)
-            (void)qkv_attn_capacity(mt, S, M.spec.head_dim, M.p_o.kb_total, S_gu, pre);
+          for (int d_S = 0; d_S <= 1; ++d_S) {
+            const int pre_max = qkv_attn_gu_pre_max(S, M.spec.head_dim, M.p_o.kb_total, S_gu, d_S);
+            for (int pre = 1; pre <= pre_max; ++pre)
+              (void)qkv_attn_capacity(mt, S, M.spec.head_dim, M.p_o.kb_total, S_gu, pre, d_S);
+          }
         }
       }
   if (hipMemsetAsync(c->seq_dev, 0, sizeof(SeqState) * max_batch, c->stream) != hipSuccess ||

@@ -103,20 +103,25 @@ constexpr int kGuPreMax = 8;
 // workgroup; red is the [nw][S*MT*256] float LDS of the wave reduction.  With
 // FUSED (the QKV GEMM of a launch that also carries the attention reading its
 // output) the Q / K / V stores are device-scope, so that workgroups on other
-// XCDs of the same launch read them after the count-in.  With PM (the gate/up
+// XCDs of the same launch read them after the count-in.  With PM = 1 (the gate/up
 // tile of such a launch: one row tile, one input range, four wavefronts) the
 // first `pre` iterations of each wavefront take their weights from pre_lds
 // (gu_preload put them there; the caller has waited for its loads), the
 // first global weight stages are requested before the tile waits for the O
 // workers (fc), and the activations and row sums they wrote in this launch
 // are read at device scope (one acquire fence per workgroup measured 8B/1B
-// 3.511 ms against 3.456, one per wavefront 3.757).  The arithmetic and its
-// order are those of the unfused tile.
-template <int MT, int S, int EPI, bool FUSED = false, bool PM = false>
+// 3.511 ms against 3.456, one per wavefront 3.757), and h is stored at device
+// scope.  With PM = 2 (the down projection of such a launch, one strip per
+// tile) the first weight stages are requested before the tile waits for every
+// gate/up tile (fc), and h and the residual x, written in this launch, are
+// read at device scope.  The arithmetic and its order are those of the
+// unfused tile.
+template <int MT, int S, int EPI, bool FUSED = false, int PM = 0>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, const unsigned split, const int n_split,
                                           const int nw, float* red, const FuseCtl* fc = nullptr,
                                           const uint32_t* pre_lds = nullptr, const int pre = 0) {
-  static_assert(!PM || (MT == 1 && EPI == EPI_SWIGLU && S < 8), "preloaded tiles: one row tile of gate/up, not ragged");
+  static_assert(PM != 1 || (MT == 1 && EPI == EPI_SWIGLU && S < 8), "preloaded tiles: one row tile of gate/up, not ragged");
+  static_assert(PM != 2 || (MT == 1 && EPI == EPI_RESID && S == 1), "fused down tiles: one row tile, one strip");
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
   constexpr int NJ = S * MT;         // elements per thread in the epilogue (first 256 threads)
   // k-blocks per pipeline stage: 8 KiB of W per wave (smaller for prefill-sized row counts)
@@ -248,7 +253,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   // unconditionally (a wave with no k-block of its own, n_it = 0, reads the
   // range's last one and never uses it): a branch around it would make every
   // later wait on an earlier load wait for the whole stage too.
-  const int its0 = PM ? pre : 0;   // the first iteration streamed from memory
+  const int its0 = PM == 1 ? pre : 0;   // the first iteration streamed from memory
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int kb = kb0 + min(wave + min(its0 + u, max(n_it - 1, 0)) * nw, kb_n - 1);
@@ -308,7 +313,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       e2[j] = float2{1.f, 0.f};
       if constexpr (EPI == EPI_RESID) {
         if (epi && row < row_count) {
-          e0[j] = p.x[(size_t)row * p.ldx + n];
+          if constexpr (PM == 2)   // written by the O workers of this launch
+            e0[j] = __hip_atomic_load(p.x + (size_t)row * p.ldx + n, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          else
+            e0[j] = p.x[(size_t)row * p.ldx + n];
           e1[j] = p.g_next[n];
         }
       } else if constexpr (EPI == EPI_QKV) {
@@ -359,7 +367,30 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   };
 
   // sched_barrier keeps the compiler from sinking the prefetch next to its use
-  if constexpr (PM) {
+  if constexpr (PM == 2) {
+    int its = 0;
+    load_w(w1, its + U);                                // the second stage, before the wait
+    __builtin_amdgcn_sched_barrier(0);
+    attn::fuse_wait_on<kFuseLanes>(fc->counters + 3 * kFuseLanes * kFuseStride, fc->gu_tiles, fc->err);
+    load_a(a0, its);
+    load_a(a1, its + U);
+    __builtin_amdgcn_sched_barrier(0);
+    prefetch_epilogue();
+    __builtin_amdgcn_sched_barrier(0);
+    while (its + 2 * U < n_it) {
+      compute(w0, a0, its);
+      __builtin_amdgcn_sched_barrier(0);
+      load(w0, a0, its + 2 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      compute(w1, a1, its + U);
+      __builtin_amdgcn_sched_barrier(0);
+      load(w1, a1, its + 3 * U);
+      __builtin_amdgcn_sched_barrier(0);
+      its += 2 * U;
+    }
+    compute(w0, a0, its);
+    if (its + U < n_it) compute(w1, a1, its + U);     // uniform
+  } else if constexpr (PM == 1) {
     int its = pre;
     load_w(w1, its + U);                                // the second stage, before the wait
     __builtin_amdgcn_sched_barrier(0);
@@ -568,7 +599,13 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
         const float up = __shfl_xor(gt, 8);
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * S + s) * 8 + csub;
-        if (csub < 8 && row < row_count && s <= s_last) p.out[act_index(row, f, p.act_rows)] = f16_flagged(h, bad);
+        if (csub < 8 && row < row_count && s <= s_last) {
+          if constexpr (PM == 1)   // read by the down tiles of this launch: device scope
+            __hip_atomic_store(p.out + act_index(row, f, p.act_rows), f16_flagged(h, bad), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+          else
+            p.out[act_index(row, f, p.act_rows)] = f16_flagged(h, bad);
+        }
       }
     flag_range(bad, p.ovf);
   } else {  // EPI_LOGITS
@@ -696,7 +733,10 @@ __device__ __forceinline__ void o_units(const GemmArgs& p, const FuseCtl& f, con
   bool bad = false;
   if (rsub < row_count) {
     const float xn = x_old + v;                      // residual + projection
-    p.x[(size_t)rsub * p.ldx + n] = xn;
+    if constexpr (GUF)   // read by the down tiles of this launch: device scope
+      __hip_atomic_store(p.x + (size_t)rsub * p.ldx + n, xn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else
+      p.x[(size_t)rsub * p.ldx + n] = xn;
     const uint16_t h = f16_flagged(xn * g, bad);
     if constexpr (GUF)   // read by the gate/up tiles of this launch: device scope
       __hip_atomic_store(p.xg + act_index(rsub, n, p.act_rows), h, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -775,10 +815,11 @@ __device__ __forceinline__ void gu_preload(const GemmArgs& p, const int tile, co
 // co-resident (the host checks the grid against the device's occupancy), a
 // phase waits only for earlier phases, and every wait is bounded
 // (attn::fuse_wait_on), so every wait ends.
-template <int MT, int S, int HD, int OKI, int SG>
+template <int MT, int S, int HD, int OKI, int SG, int SD>
 __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnArgs a, const FuseCtl f,
-                                                  const GemmArgs o, const GemmArgs gu) {
+                                                  const GemmArgs o, const GemmArgs gu, const GemmArgs dn) {
   static_assert(SG == 0 || (MT == 1 && OKI > 0), "gate/up joins only launches with O units");
+  static_assert(SD == 0 || (SD == 1 && SG > 0), "the down projection joins only launches with gate/up");
   // [0, gu_lds): reductions (GEMM tiles [4][S * MT * 256], O units [8][2][256],
   // gate/up [4][SG * 256]); from gu_lds: preloaded gate/up weights
   extern __shared__ float red[];
@@ -824,9 +865,26 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     if (gu_tile) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's preloaded weights are in LDS
       if (tid < 256) {
-        gemm_tile<1, SG, EPI_SWIGLU, false, true>(gu, b, 0, 1, 4, red, &f, pre_lds, pre);
+        gemm_tile<1, SG, EPI_SWIGLU, false, 1>(gu, b, 0, 1, 4, red, &f, pre_lds, pre);
       } else {                                      // the tile's two barriers
         attn::fuse_wait_on<kFuseLanes>(f.counters + 2 * kFuseLanes * kFuseStride, f.n_odone, f.err);
+        __syncthreads();
+      }
+      if constexpr (SD > 0) {                       // h of this tile complete: count in
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        __syncthreads();
+        if (tid == 0)
+          __hip_atomic_fetch_add(f.counters + (3 * kFuseLanes + b % kFuseLanes) * kFuseStride, 1, __ATOMIC_RELAXED,
+                                 __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+  if constexpr (SD > 0) {
+    if (b < f.d_tiles) {                            // uniform
+      if (tid < 256) {
+        gemm_tile<1, 1, EPI_RESID, false, 2>(dn, b, 0, 1, 4, red, &f);
+      } else {                                      // the tile's two barriers
+        attn::fuse_wait_on<kFuseLanes>(f.counters + 3 * kFuseLanes * kFuseStride, f.gu_tiles, f.err);
         __syncthreads();
       }
     }
@@ -1832,16 +1890,17 @@ struct FuseQuery {
 };
 
 template <int MT, int S, int OKI, int SG>
-constexpr size_t fuse_red_bytes() {
+constexpr size_t fuse_red_bytes() {   // (a fused down tile's [4][256] fits below the O units')
   return std::max({(size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0,
                    SG > 0 ? (size_t)4 * SG * 256 : (size_t)0}) * sizeof(float);
 }
 
-template <int MT, int S, int HD, int OKI, int SG>
+template <int MT, int S, int HD, int OKI, int SG, int SD>
 hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseCtl& f, const GemmArgs& o,
-                               const GemmArgs& gu, hipStream_t st, LaunchEvents ev, FuseQuery& q) {
+                               const GemmArgs& gu, const GemmArgs& dn, hipStream_t st, LaunchEvents ev,
+                               FuseQuery& q) {
   constexpr size_t red = fuse_red_bytes<MT, S, OKI, SG>();
-  auto kern = k_qkv_attn<MT, S, HD, OKI, SG>;
+  auto kern = k_qkv_attn<MT, S, HD, OKI, SG, SD>;
   const int pre = q.what == FuseQuery::LAUNCH ? std::max(f.gu_pre, f.gu_pre_q) : q.pre;
   const size_t lds = red + (SG > 0 ? (size_t)4 * pre * SG * 1024 : 0);
   if (q.what != FuseQuery::LAUNCH) {
@@ -1870,51 +1929,56 @@ hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseC
   fl.gu_lds = (int)red;
   const int grid = g.n_tiles + f.n_cons + f.o_extra;
   if (ev.start) {
-    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, fl, o, gu);
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, fl, o, gu, dn);
   } else {
-    kern<<<grid, 512, lds, st>>>(g, a, fl, o, gu);
+    kern<<<grid, 512, lds, st>>>(g, a, fl, o, gu, dn);
   }
   return hipGetLastError();
 }
 
 template <int MT, int S, int HD>
-hipError_t launch_qkv_attn_oki(int oki, int sg, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                               const GemmArgs& o, const GemmArgs& gu, hipStream_t st, LaunchEvents ev,
-                               FuseQuery& q) {
-  if (oki == 0 && sg == 0) return launch_qkv_attn_one<MT, S, HD, 0, 0>(g, a, f, o, gu, st, ev, q);
+hipError_t launch_qkv_attn_oki(int oki, int sg, int sd, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
+                               const GemmArgs& o, const GemmArgs& gu, const GemmArgs& dn, hipStream_t st,
+                               LaunchEvents ev, FuseQuery& q) {
+  if (oki == 0 && sg == 0 && sd == 0) return launch_qkv_attn_one<MT, S, HD, 0, 0, 0>(g, a, f, o, gu, dn, st, ev, q);
   if constexpr (MT == 1) {
-    switch (oki * 100 + sg) {
-      case 800: return launch_qkv_attn_one<MT, S, HD, 8, 0>(g, a, f, o, gu, st, ev, q);
-      case 804: return launch_qkv_attn_one<MT, S, HD, 8, 4>(g, a, f, o, gu, st, ev, q);
-      case 807: return launch_qkv_attn_one<MT, S, HD, 8, 7>(g, a, f, o, gu, st, ev, q);
-      case 1600: return launch_qkv_attn_one<MT, S, HD, 16, 0>(g, a, f, o, gu, st, ev, q);
-      case 1604: return launch_qkv_attn_one<MT, S, HD, 16, 4>(g, a, f, o, gu, st, ev, q);
-      case 1607: return launch_qkv_attn_one<MT, S, HD, 16, 7>(g, a, f, o, gu, st, ev, q);
+    switch (oki * 1000 + sg * 10 + sd) {
+      case 8000: return launch_qkv_attn_one<MT, S, HD, 8, 0, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 8040: return launch_qkv_attn_one<MT, S, HD, 8, 4, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 8070: return launch_qkv_attn_one<MT, S, HD, 8, 7, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 8041: return launch_qkv_attn_one<MT, S, HD, 8, 4, 1>(g, a, f, o, gu, dn, st, ev, q);
+      case 8071: return launch_qkv_attn_one<MT, S, HD, 8, 7, 1>(g, a, f, o, gu, dn, st, ev, q);
+      case 16000: return launch_qkv_attn_one<MT, S, HD, 16, 0, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 16040: return launch_qkv_attn_one<MT, S, HD, 16, 4, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 16070: return launch_qkv_attn_one<MT, S, HD, 16, 7, 0>(g, a, f, o, gu, dn, st, ev, q);
+      case 16041: return launch_qkv_attn_one<MT, S, HD, 16, 4, 1>(g, a, f, o, gu, dn, st, ev, q);
+      case 16071: return launch_qkv_attn_one<MT, S, HD, 16, 7, 1>(g, a, f, o, gu, dn, st, ev, q);
     }
   }
   return hipErrorInvalidValue;
 }
 
 template <int MT, int S>
-hipError_t launch_qkv_attn_hd(int hd, int oki, int sg, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                              const GemmArgs& o, const GemmArgs& gu, hipStream_t st, LaunchEvents ev, FuseQuery& q) {
-  if (hd == 64) return launch_qkv_attn_oki<MT, S, 64>(oki, sg, g, a, f, o, gu, st, ev, q);
-  if (hd == 128) return launch_qkv_attn_oki<MT, S, 128>(oki, sg, g, a, f, o, gu, st, ev, q);
+hipError_t launch_qkv_attn_hd(int hd, int oki, int sg, int sd, const GemmArgs& g, const AttnArgs& a,
+                              const FuseCtl& f, const GemmArgs& o, const GemmArgs& gu, const GemmArgs& dn,
+                              hipStream_t st, LaunchEvents ev, FuseQuery& q) {
+  if (hd == 64) return launch_qkv_attn_oki<MT, S, 64>(oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+  if (hd == 128) return launch_qkv_attn_oki<MT, S, 128>(oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_qkv_attn_any(int mt, int S, int hd, int oki, int sg, const GemmArgs& g, const AttnArgs& a,
-                               const FuseCtl& f, const GemmArgs& o, const GemmArgs& gu, hipStream_t st,
-                               LaunchEvents ev, FuseQuery& q) {
+hipError_t launch_qkv_attn_any(int mt, int S, int hd, int oki, int sg, int sd, const GemmArgs& g, const AttnArgs& a,
+                               const FuseCtl& f, const GemmArgs& o, const GemmArgs& gu, const GemmArgs& dn,
+                               hipStream_t st, LaunchEvents ev, FuseQuery& q) {
   switch (mt * 4 + S) {
-    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
-    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, oki, sg, g, a, f, o, gu, st, ev, q);
+    case 1 * 4 + 1: return launch_qkv_attn_hd<1, 1>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 1 * 4 + 2: return launch_qkv_attn_hd<1, 2>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 2 * 4 + 1: return launch_qkv_attn_hd<2, 1>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 2 * 4 + 2: return launch_qkv_attn_hd<2, 2>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 3 * 4 + 1: return launch_qkv_attn_hd<3, 1>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 3 * 4 + 2: return launch_qkv_attn_hd<3, 2>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 4 * 4 + 1: return launch_qkv_attn_hd<4, 1>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
+    case 4 * 4 + 2: return launch_qkv_attn_hd<4, 2>(hd, oki, sg, sd, g, a, f, o, gu, dn, st, ev, q);
   }
   return hipErrorInvalidValue;
 }
@@ -1927,44 +1991,48 @@ int o_ki(int kb) { return kb == 0 ? 0 : kb <= 64 ? 8 : kb <= kFuseOMaxKb ? 16 : 
 
 // Shape key of the fused launch queries (cached: the answers do not change,
 // and nothing is asked during a graph capture once the engine has warmed up).
-static int64_t fuse_key(int kind, int mt, int S, int head_dim, int oki, int sg, int pre) {
-  return ((((((int64_t)kind * 8 + mt) * 4 + S) * 256 + head_dim) * 32 + oki) * 16 + sg) * 16 + pre;
+static int64_t fuse_key(int kind, int mt, int S, int head_dim, int oki, int sg, int sd, int pre) {
+  return (((((((int64_t)kind * 8 + mt) * 4 + S) * 256 + head_dim) * 32 + oki) * 16 + sg) * 4 + sd) * 16 + pre;
 }
 
-static int fuse_query(int kind, int mt, int S, int head_dim, int oki, int sg, int pre) {
+static int fuse_query(int kind, int mt, int S, int head_dim, int oki, int sg, int sd, int pre) {
   static std::map<int64_t, int> cache;   // 0 or more: the answer; -1: unsupported
-  const int64_t key = fuse_key(kind, mt, S, head_dim, oki, sg, pre);
+  const int64_t key = fuse_key(kind, mt, S, head_dim, oki, sg, sd, pre);
   auto it = cache.find(key);
   if (it != cache.end()) return it->second;
   FuseQuery q;
   q.what = kind == 0 ? FuseQuery::CAPACITY : FuseQuery::PRE_MAX;
   q.pre = pre;
   int r = -1;
-  if (launch_qkv_attn_any(mt, S, head_dim, oki, sg, GemmArgs{}, AttnArgs{}, FuseCtl{}, GemmArgs{}, GemmArgs{},
-                          nullptr, LaunchEvents{}, q) == hipSuccess)
+  if (launch_qkv_attn_any(mt, S, head_dim, oki, sg, sd, GemmArgs{}, AttnArgs{}, FuseCtl{}, GemmArgs{}, GemmArgs{},
+                          GemmArgs{}, nullptr, LaunchEvents{}, q) == hipSuccess)
     r = q.result;
   cache[key] = r;
   return r;
 }
 
-int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb, int gu_S, int gu_pre) {
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb, int gu_S, int gu_pre, int d_S) {
   const int oki = o_ki(o_kb);
   if (mt < 1 || mt > 4 || S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki < 0 || (oki > 0 && mt != 1) ||
-      (gu_S != 0 && gu_S != 4 && gu_S != 7) || (gu_S > 0 && (oki == 0 || gu_pre < 1 || gu_pre > kGuPreMax)))
+      (gu_S != 0 && gu_S != 4 && gu_S != 7) || (gu_S > 0 && (oki == 0 || gu_pre < 1 || gu_pre > kGuPreMax)) ||
+      (d_S != 0 && (d_S != 1 || gu_S == 0)))
     return 0;
-  const int r = fuse_query(0, mt, S, head_dim, oki, gu_S, gu_S > 0 ? gu_pre : 0);
+  const int r = fuse_query(0, mt, S, head_dim, oki, gu_S, d_S, gu_S > 0 ? gu_pre : 0);
   return r > 0 ? r : 0;
 }
 
-int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S) {
+int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S, int d_S) {
   const int oki = o_ki(o_kb);
-  if (S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki <= 0 || (gu_S != 4 && gu_S != 7)) return 0;
-  const int r = fuse_query(1, 1, S, head_dim, oki, gu_S, 0);
+  if (S < 1 || S > 2 || (head_dim != 64 && head_dim != 128) || oki <= 0 || (gu_S != 4 && gu_S != 7) ||
+      (d_S != 0 && d_S != 1))
+    return 0;
+  const int r = fuse_query(1, 1, S, head_dim, oki, gu_S, d_S, 0);
   return r > 0 ? r : 0;
 }
 
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           const GemmArgs* o, const GemmArgs* gu, int gu_S, hipStream_t st, LaunchEvents ev) {
+                           const GemmArgs* o, const GemmArgs* gu, int gu_S, const GemmArgs* dn, hipStream_t st,
+                           LaunchEvents ev) {
   // the GEMM tiles cover the strips exactly, one input range; the attention
   // part is the single-chunk plan with one query tile per workgroup
   if (g.n_tiles < 1 || g.ksplit != 1 || g.kb_split < g.kb_total || (size_t)g.n_tiles * S != (size_t)g.n_strips)
@@ -2000,11 +2068,23 @@ hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const
   } else if (f.gu_tiles != 0) {
     return hipErrorInvalidValue;
   }
-  const int cap = qkv_attn_capacity(mt, S, head_dim, o ? o->kb_total : 0, gu ? gu_S : 0, gu ? f.gu_pre : 0);
+  if (dn) {
+    // down: needs gate/up; one strip per tile, one per workgroup of the grid
+    // at most, one input range; its input is gate/up's output, its residual
+    // and outputs the O workers'
+    if (!gu || dn->n_tiles != f.d_tiles || f.d_tiles < 1 || f.d_tiles > grid || dn->n_tiles != dn->n_strips ||
+        dn->ksplit != 1 || dn->kb_split < dn->kb_total || dn->A != gu->out || dn->x != o->x || dn->xg != o->xg ||
+        dn->ss_out != o->ss_out || !dn->g_next || dn->act_rows != a.act_rows || dn->desc != a.desc)
+      return hipErrorInvalidValue;
+  } else if (f.d_tiles != 0) {
+    return hipErrorInvalidValue;
+  }
+  const int cap = qkv_attn_capacity(mt, S, head_dim, o ? o->kb_total : 0, gu ? gu_S : 0, gu ? f.gu_pre : 0,
+                                    dn ? 1 : 0);
   if (cap <= 0 || grid > cap) return hipErrorInvalidValue;
   FuseQuery q;
-  return launch_qkv_attn_any(mt, S, head_dim, oki, gu ? gu_S : 0, g, a, f, o ? *o : GemmArgs{}, gu ? *gu : GemmArgs{},
-                             st, ev, q);
+  return launch_qkv_attn_any(mt, S, head_dim, oki, gu ? gu_S : 0, dn ? 1 : 0, g, a, f, o ? *o : GemmArgs{},
+                             gu ? *gu : GemmArgs{}, dn ? *dn : GemmArgs{}, st, ev, q);
 }
 
 hipError_t launch_gemm(int epi, int mt, int S, int nw, const GemmArgs& a, hipStream_t st, LaunchEvents ev) {

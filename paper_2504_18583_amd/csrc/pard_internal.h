@@ -289,9 +289,13 @@ struct AttnArgs {
 // epilogue's device-scope stores are complete, and the gate/up tiles wait for
 // n_odone such arrivals before reading the O-projection's output (at device
 // scope).
+//
+// Down tiles (d_tiles > 0, with gate/up): workgroup b < d_tiles runs down
+// tile b once every gate/up tile has counted itself in on counter
+// 3 kFuseLanes + t % kFuseLanes (h stored at device scope).
 constexpr int kFuseLanes = 8;      // arrival counters per phase (spread over XCDs and memory channels)
 constexpr int kFuseStride = 64;    // ints between two counters
-constexpr int kFuseInts = 3 * kFuseLanes * kFuseStride;   // one layer's set: QKV, attention and O arrivals
+constexpr int kFuseInts = 4 * kFuseLanes * kFuseStride;   // one layer's set: QKV, attention, O, gate/up arrivals
 struct FuseCtl {
   int* counters = nullptr;         // this layer's kFuseInts ints, zero at the launch
   int n_prod = 0, n_cons = 0;      // QKV workgroups, attention workgroups
@@ -299,6 +303,7 @@ struct FuseCtl {
   int o_units = 0, o_extra = 0, o_two = 0;
   int gu_tiles = 0, gu_pre = 0, gu_pre_q = 0;
   int n_odone = 0;                 // O workers with units
+  int d_tiles = 0;
   int gu_lds = 0;                  // byte offset of the preloaded weights in the dynamic LDS (set by the launcher)
 };
 
@@ -330,13 +335,15 @@ hipError_t launch_gemm_rows(int epi, const GemmArgs& a, hipStream_t st, LaunchEv
 // tile, one input range of at most kFuseOMaxKb k-blocks; f's O fields set).
 // With gu as well (o required; f's gate/up fields set) it carries the
 // gate/up GEMM (EPI_SWIGLU, gu_S strips per tile, one input range, four
-// wavefronts), its first weight blocks preloaded into LDS.
+// wavefronts), its first weight blocks preloaded into LDS; with dn as well
+// (gu required) the down projection + residual (EPI_RESID, one strip per
+// tile, one input range, four wavefronts; d_S = 1 in the queries).
 constexpr int kFuseOMaxKb = 128;
-int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb = 0, int gu_S = 0, int gu_pre = 0);
+int qkv_attn_capacity(int mt, int S, int head_dim, int o_kb = 0, int gu_S = 0, int gu_pre = 0, int d_S = 0);
 // largest gu_pre the LDS holds for this launch shape (0: none)
-int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S);
+int qkv_attn_gu_pre_max(int S, int head_dim, int o_kb, int gu_S, int d_S = 0);
 hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const AttnArgs& a, const FuseCtl& f,
-                           const GemmArgs* o, const GemmArgs* gu, int gu_S, hipStream_t st,
+                           const GemmArgs* o, const GemmArgs* gu, int gu_S, const GemmArgs* dn, hipStream_t st,
                            LaunchEvents ev = LaunchEvents{});
 hipError_t launch_tail(const TailArgs& a, int n_seq, hipStream_t st);
 hipError_t launch_stage(const TailArgs& a, hipStream_t st);

@@ -557,8 +557,9 @@ GemmArgs gu_args(const ModelDev& M, const Layer& L, int act_rows, int ss_tiles, 
 
 // Down projection + residual of layer l: x += h W_down^T, then fp16(x * g)
 // for the next layer's (or the final) norm and the row sums of squares.
-// fused: the tile plan of a fused launch (one strip per tile, one input range).
-GemmArgs d_args(const ModelDev& M, int l, int act_rows, bool fused) {
+// fused: the tile plan of a fused launch (one strip per tile, the plan's
+// input ranges; part and counters for the partial-tile exchange).
+GemmArgs d_args(const ModelDev& M, int l, int act_rows, bool fused, float* part, int* counters) {
   GemmArgs a = gemm_base(M, M.layers[l].wd, act_rows);
   a.A = M.h;
   a.lda = M.f_pad;
@@ -571,8 +572,10 @@ GemmArgs d_args(const ModelDev& M, int l, int act_rows, bool fused) {
     a.kb_total = M.p_d.kb_total;
     a.n_strips = M.p_d.n_strips;
     a.n_tiles = M.p_d.n_strips;
-    a.ksplit = 1;
-    a.kb_split = M.p_d.kb_total;
+    a.ksplit = M.p_d.ksplit;
+    a.kb_split = ceil_div(M.p_d.kb_total, M.p_d.ksplit);
+    a.part = part;
+    a.counters = counters;
   }
   return a;
 }
@@ -707,14 +710,15 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
     const int gu_tiles = M.p_gu.n_strips / S_gu;
     // and the down projection (one strip per tile, one input range), whose
     // workgroups wait for every gate/up tile
-    const int d_S = c->use_fused_d && M.p_d.ksplit == 1 && pick_S(EPI_RESID, M.p_d.n_strips, 1) == 1 &&
+    const int d_S = c->use_fused_d && M.p_d.ksplit <= 2 && pick_S(EPI_RESID, M.p_d.n_strips, 1) == 1 &&
                     plan_nw(M.p_d, 1, 1) == 4 ? 1 : 0;
+    const int d_units = d_S ? M.p_d.n_strips * M.p_d.ksplit : 0;
     const int pre_max = std::min(qkv_attn_gu_pre_max(S_q, s.head_dim, M.p_o.kb_total, S_gu, d_S), M.p_gu.kb_total / 4);
     const int pre = c->gu_pre >= 0 ? std::min(c->gu_pre, pre_max) : pre_max;
     const int pre_q = c->gu_pre_q >= 0 ? std::min(c->gu_pre_q, pre) : pre;
     const int cap = pre >= 1 ? qkv_attn_capacity(1, S_q, s.head_dim, M.p_o.kb_total, S_gu, pre, d_S) : 0;
     FuseCtl t = fo;
-    t.o_extra = std::max({fo.o_extra, gu_tiles - n_qkv - n_attn_wg, d_S ? M.p_d.n_strips - n_qkv - n_attn_wg : 0});
+    t.o_extra = std::max({fo.o_extra, gu_tiles - n_qkv - n_attn_wg, d_units - n_qkv - n_attn_wg});
     t.o_two = std::max(0, t.o_units - n_qkv - t.o_extra);
     if (cap > 0 && gu_tiles <= cap && n_qkv + n_attn_wg + t.o_extra <= cap && t.o_two <= t.o_extra) {
       fused_gu = true;
@@ -723,7 +727,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
       t.gu_pre = pre;
       t.gu_pre_q = pre_q;
       t.n_odone = std::min(n_qkv + t.o_extra, t.o_units - t.o_two);
-      t.d_tiles = fused_d ? M.p_d.n_strips : 0;
+      t.d_tiles = d_units;
       fo = t;
     }
   }
@@ -782,7 +786,7 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
         GemmArgs o{}, gu{}, dn{};
         if (fused_o) o = o_args(M, L, act_rows);
         if (fused_gu) gu = gu_args(M, L, act_rows, ss_tiles, S_gu);
-        if (fused_d) dn = d_args(M, l, act_rows, true);
+        if (fused_d) dn = d_args(M, l, act_rows, true, c->rows_part, c->split_counters);
         // the kernel timer's QKV class covers the fused launch (attention included)
         LaunchEvents ev;
         if (c->timer_class == cls0 + 1 && c->timer_used < c->timer_max) {
@@ -807,7 +811,8 @@ pard_status forward(pard_ctx* c, int w, const PassSpec& ps) {
       HIP_TRY(c, run_gemm(c, cls0 + 4, EPI_SWIGLU, ps.max_rows, typ, gu_args(M, L, act_rows, ss_tiles, 0), M.p_gu));
     }
     if (!fused_d) {  // down + residual
-      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, ps.max_rows, typ, d_args(M, l, act_rows, false), M.p_d));
+      HIP_TRY(c, run_gemm(c, cls0 + 5, EPI_RESID, ps.max_rows, typ, d_args(M, l, act_rows, false, nullptr, nullptr),
+                          M.p_d));
     }
   }
   if (ps.max_lm_rows > 0) {

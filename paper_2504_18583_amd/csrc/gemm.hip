@@ -880,12 +880,17 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     }
   }
   if constexpr (SD > 0) {
-    if (b < f.d_tiles) {                            // uniform
+    if (b < f.d_tiles) {                            // uniform: unit b = (strip, input range)
+      const int P = dn.ksplit;
       if (tid < 256) {
-        gemm_tile<1, 1, EPI_RESID, false, 2>(dn, b, 0, 1, 4, red, &f);
-      } else {                                      // the tile's two barriers
+        gemm_tile<1, 1, EPI_RESID, false, 2>(dn, b / P, b % P, P, 4, red, &f);
+      } else {                                      // the tile's barriers
         attn::fuse_wait_on<kFuseLanes>(f.counters + 3 * kFuseLanes * kFuseStride, f.gu_tiles, f.err);
         __syncthreads();
+        if (P > 1) {                                // the partial-tile exchange's two
+          __syncthreads();
+          __syncthreads();
+        }
       }
     }
   }
@@ -2069,12 +2074,17 @@ hipError_t launch_qkv_attn(int mt, int S, int head_dim, const GemmArgs& g, const
     return hipErrorInvalidValue;
   }
   if (dn) {
-    // down: needs gate/up; one strip per tile, one per workgroup of the grid
-    // at most, one input range; its input is gate/up's output, its residual
-    // and outputs the O workers'
-    if (!gu || dn->n_tiles != f.d_tiles || f.d_tiles < 1 || f.d_tiles > grid || dn->n_tiles != dn->n_strips ||
-        dn->ksplit != 1 || dn->kb_split < dn->kb_total || dn->A != gu->out || dn->x != o->x || dn->xg != o->xg ||
-        dn->ss_out != o->ss_out || !dn->g_next || dn->act_rows != a.act_rows || dn->desc != a.desc)
+    // down: needs gate/up; one strip per tile, one or two input ranges (each
+    // unit, a tile's range, one workgroup of the grid at most); its input is
+    // gate/up's output, its residual and outputs the O workers'
+    if (!gu || dn->n_tiles * dn->ksplit != f.d_tiles || f.d_tiles < 1 || f.d_tiles > grid ||
+        dn->n_tiles != dn->n_strips || dn->ksplit < 1 || dn->ksplit > 2 || dn->kb_split < 1 ||
+        (dn->ksplit - 1) * dn->kb_split >= dn->kb_total || dn->ksplit * dn->kb_split < dn->kb_total ||
+        dn->A != gu->out || dn->x != o->x || dn->xg != o->xg || dn->ss_out != o->ss_out || !dn->g_next ||
+        dn->act_rows != a.act_rows || dn->desc != a.desc)
+      return hipErrorInvalidValue;
+    if (dn->ksplit > 1 && (!dn->part || !dn->counters || dn->n_tiles > kSplitCounters ||
+                           (size_t)dn->n_tiles * dn->ksplit * 256 > kSplitPartFloats))
       return hipErrorInvalidValue;
   } else if (f.d_tiles != 0) {
     return hipErrorInvalidValue;

@@ -35,35 +35,39 @@ METRIC = "tokens/sec batch-1 PARD decode, 1B draft/8B target K=8; step HBM GB/s 
 PEAK_HBM_GBPS = 8000.0
 SAMPLING_T, SAMPLING_SEED = 1.0, 2504   # speculative-sampling measurement beside the greedy headline
 # measured HBM traffic of the dominant kernel (rocprofv3 FETCH_SIZE / WRITE_SIZE,
-# scaled by a copy of known size); valid only while the kernel source is unchanged
+# scaled by a copy of known size); valid only while the kernel source is unchanged:
+# the 8B gate/up GEMM launched on its own, and the 8B decode layer's one launch
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gemm_swiglu_8b_gateup_traffic.txt")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f) for f in ("gemm.hip", "pard_internal.h")]
+LAYER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_qkv_attn_8b_layer_traffic.txt")
+LAYER_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f)
+                 for f in ("gemm.hip", "attn_tile.h", "pard_internal.h")]
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_source_sha256() -> str:
+def kernel_source_sha256(sources=KERNEL_SOURCES) -> str:
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
     """HBM bytes per launch of the dominant kernel from the committed counter
     summary, or None when it is missing or the kernel source changed since."""
     try:
         kv = {}
-        with open(TRAFFIC_FILE) as fh:
+        with open(path) as fh:
             for line in fh:
                 if ":" in line and not line.startswith("#"):
                     k, v = line.split(":", 1)
                     kv[k.strip()] = v.strip()
-        if kv.get("kernel_source_sha256") != kernel_source_sha256():
+        if kv.get("kernel_source_sha256") != kernel_source_sha256(sources):
             return None
         return int(float(kv["traffic_bytes_per_launch"]))
     except (OSError, KeyError, ValueError):
@@ -579,7 +583,9 @@ def main() -> int:
         kbytes = bm.layer_launch_bytes(t_spec, k + 1, int(round(l_mean)), with_down)
         kname = (f"k_qkv_attn (target decode layer: QKV GEMM, attention, O-projection, gate/up"
                  f"{' and down' if with_down else ''} GEMMs, {k + 1} rows)")
-        traffic = None                               # no counter summary of this launch
+        # the counter summary covers the 8B-shaped launch with the down projection, 9 rows
+        traffic = (measured_traffic(LAYER_TRAFFIC_FILE, LAYER_SOURCES)
+                   if (t_spec.d_model, t_spec.ffn_dim, k) == (4096, 14336, 8) and with_down else None)
     avg_s = total_ms / 1e3 / max(launches, 1)
     achieved = kbytes / avg_s / 1e9 if launches > 0 else 0.0
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",

@@ -3,8 +3,9 @@
 Usage: python -m paper_2504_18583_amd.csrc.build   (or call build()).
 Objects go to ``_build/`` beside the package; the shared library is written
 into the package directory, where the binding loads it from.  The same call
-links ``gemm_counters`` (a stand-alone launch of the gate/up GEMM for
-hardware-counter runs) from the GEMM object.
+links ``gemm_counters`` (a stand-alone launch of the gate/up GEMM) and
+``layer_counters`` (stand-alone launches of the one-launch decode layer), for
+hardware-counter runs, from the GEMM object.
 """
 from __future__ import annotations
 
@@ -20,8 +21,10 @@ ROOT = os.path.dirname(PKG)
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpard.so")
 COUNTERS_EXE = os.path.join(PKG, "gemm_counters")
+LAYER_EXE = os.path.join(PKG, "layer_counters")
 
-SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "cod.hip", "gemm_counters.hip"]
+SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "cod.hip", "gemm_counters.hip",
+           "layer_counters.hip"]
 LIB_SOURCES = SOURCES[:5]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -54,8 +57,9 @@ def build(verbose: bool = False) -> str:
     obj = dict(zip(SOURCES, objs))
     _link(LIB, ["-shared", "-fPIC"], [obj[s] for s in LIB_SOURCES])
     _link(COUNTERS_EXE, [], [obj["gemm_counters.hip"], obj["gemm.hip"]])
+    _link(LAYER_EXE, [], [obj["layer_counters.hip"], obj["gemm.hip"]])
     if verbose:
-        print(f"built {LIB} and {COUNTERS_EXE}")
+        print(f"built {LIB}, {COUNTERS_EXE} and {LAYER_EXE}")
     return LIB
 
 

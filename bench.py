@@ -42,6 +42,12 @@ KERNEL_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f) for f in
 LAYER_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_qkv_attn_8b_layer_traffic.txt")
 LAYER_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f)
                  for f in ("gemm.hip", "attn_tile.h", "pard_internal.h")]
+# measured HBM traffic of whole decode steps of the 8B/1B K = 8 workload (every
+# kernel of the step), valid while the decode path's sources are unchanged
+STEP_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "step_8b_1b_k8_counters.txt")
+STEP_SOURCES = [os.path.join(ROOT, "paper_2504_18583_amd", "csrc", f)
+                for f in ("attention.hip", "attn_tile.h", "device_init.h", "device_init.hip", "engine.hip",
+                          "gemm.hip", "pard_internal.h")]
 
 
 def log(msg: str) -> None:
@@ -57,9 +63,10 @@ def kernel_source_sha256(sources=KERNEL_SOURCES) -> str:
     return h.hexdigest()
 
 
-def measured_traffic(path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
-    """HBM bytes per launch of the dominant kernel from the committed counter
-    summary, or None when it is missing or the kernel source changed since."""
+def measured_traffic(path=TRAFFIC_FILE, sources=KERNEL_SOURCES, key="traffic_bytes_per_launch"):
+    """HBM bytes per launch of the dominant kernel (or, with key, another
+    figure) from the committed counter summary, or None when it is missing or
+    the kernel source changed since."""
     try:
         kv = {}
         with open(path) as fh:
@@ -69,7 +76,7 @@ def measured_traffic(path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
                     kv[k.strip()] = v.strip()
         if kv.get("kernel_source_sha256") != kernel_source_sha256(sources):
             return None
-        return int(float(kv["traffic_bytes_per_launch"]))
+        return int(float(kv[key]))
     except (OSError, KeyError, ValueError):
         return None
 
@@ -386,6 +393,7 @@ def bench_batched(args, wl) -> int:
         "step_gemm_tflops": round(step_tflops, 1),
         "step_mfma_frac": round(step_tflops / PEAK_F16_TFLOPS, 4),
         "bytes_per_step": round(tot_bytes / steps),
+        "step_traffic": step_traffic,
         "context": [min(l_t0), max(l_t1)],
         "prefill_ms": round(prefill_ms, 1),
         "device_ms_per_step": round(stats.elapsed_ms / steps, 4),
@@ -598,6 +606,17 @@ def main() -> int:
     del eng
     copy_gbps, read_gbps = copy_ceiling()
     log(f"device copy: {copy_gbps:.0f} GB/s (read + write); torch.sum read: {read_gbps:.0f} GB/s")
+    # HBM bytes per step counted by rocprofv3 over whole steps of this workload
+    # (FETCH_SIZE / WRITE_SIZE of every kernel, scaled by a copy of known size)
+    step_traffic = None
+    if wl.name == "llama8b_1b" and k == 8:
+        counted = measured_traffic(STEP_TRAFFIC_FILE, STEP_SOURCES, "traffic_bytes_per_step")
+        algo = measured_traffic(STEP_TRAFFIC_FILE, STEP_SOURCES, "algorithmic_bytes_per_step")
+        if counted and algo:
+            step_traffic = {"bytes_per_step": counted, "over_algorithmic": round(counted / algo, 4),
+                            "gbps": round(counted / step_s / 1e9, 1),
+                            "frac": round(counted / step_s / 1e9 / PEAK_HBM_GBPS, 4),
+                            "source": os.path.relpath(STEP_TRAFFIC_FILE, ROOT)}
 
     result = {
         "metric": METRIC,
@@ -624,6 +643,7 @@ def main() -> int:
         "read_gbps": round(read_gbps, 1),
         "step_frac_of_copy": round(step_gbps / copy_gbps, 4),
         "bytes_per_step": round(tot_bytes / steps),
+        "step_traffic": step_traffic,
         "context": [l_t0, l_t1],
         "ttft_ms": round(ttft_ms, 2),
         "device_ms_per_step": round(stats.elapsed_ms / steps, 4),

@@ -4,8 +4,9 @@ Usage: python -m paper_2504_18583_amd.csrc.build   (or call build()).
 Objects go to ``_build/`` beside the package; the shared library is written
 into the package directory, where the binding loads it from.  The same call
 links ``gemm_counters`` (a stand-alone launch of the gate/up GEMM) and
-``layer_counters`` (stand-alone launches of the one-launch decode layer), for
-hardware-counter runs, from the GEMM object.
+``layer_counters`` (stand-alone launches of the one-launch decode layer) from
+the GEMM object, and ``step_counters`` (whole decode steps through the C ABI)
+against the library, for hardware-counter runs.
 """
 from __future__ import annotations
 
@@ -22,9 +23,10 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libpard.so")
 COUNTERS_EXE = os.path.join(PKG, "gemm_counters")
 LAYER_EXE = os.path.join(PKG, "layer_counters")
+STEP_EXE = os.path.join(PKG, "step_counters")
 
 SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "cod.hip", "gemm_counters.hip",
-           "layer_counters.hip"]
+           "layer_counters.hip", "step_counters.hip"]
 LIB_SOURCES = SOURCES[:5]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -58,8 +60,9 @@ def build(verbose: bool = False) -> str:
     _link(LIB, ["-shared", "-fPIC"], [obj[s] for s in LIB_SOURCES])
     _link(COUNTERS_EXE, [], [obj["gemm_counters.hip"], obj["gemm.hip"]])
     _link(LAYER_EXE, [], [obj["layer_counters.hip"], obj["gemm.hip"]])
+    _link(STEP_EXE, [f"-L{PKG}", "-Wl,-rpath,$ORIGIN"], [obj["step_counters.hip"], "-lpard"])
     if verbose:
-        print(f"built {LIB}, {COUNTERS_EXE} and {LAYER_EXE}")
+        print(f"built {LIB}, {COUNTERS_EXE}, {LAYER_EXE} and {STEP_EXE}")
     return LIB
 
 

@@ -3,11 +3,15 @@
     python -m paper_2504_18583_amd.profile_summary trace <dir>/run_kernel_trace.csv [--last N]
     python -m paper_2504_18583_amd.profile_summary pmc <dir>/run_counter_collection.csv \
         --kernel NAME_SUBSTRING [--workgroups WG] [--skip N]
+    python -m paper_2504_18583_amd.profile_summary window <dir>/run_counter_collection.csv \
+        --after NAME_SUBSTRING
 
 ``trace`` groups dispatches by kernel (template arguments included) and
 workgroup count -- the same template runs for the target and the draft with
 different grids -- and prints calls and mean / min / max duration.  ``pmc``
 averages each counter over the dispatches of one kernel and grid.
+``window`` sums each counter over every dispatch after the last dispatch of a
+marker kernel, in total and per kernel (a program's measured region).
 """
 from __future__ import annotations
 
@@ -63,6 +67,38 @@ def pmc(path: str, kernel: str, workgroups: int, skip: int) -> str:
     return "\n".join(out)
 
 
+def window(path: str, after: str) -> str:
+    rows = list(csv.DictReader(open(path)))
+    if not rows:
+        return "no dispatches"
+    key = "Dispatch_Id" if "Dispatch_Id" in rows[0] else "Correlation_Id"
+    disp = {}
+    for r in rows:
+        d = disp.setdefault(int(r[key]), {"name": r["Kernel_Name"], "c": defaultdict(float)})
+        d["c"][r["Counter_Name"]] += float(r["Counter_Value"])
+    order = sorted(disp)
+    marks = [i for i, k in enumerate(order) if after in disp[k]["name"]]
+    if not marks:
+        return f"no dispatch of {after!r}"
+    sel = [disp[k] for k in order[marks[-1] + 1:]]
+    tot = defaultdict(float)
+    per = defaultdict(lambda: [0, defaultdict(float)])
+    for d in sel:
+        e = per[_short(d["name"])]
+        e[0] += 1
+        for c, v in d["c"].items():
+            tot[c] += v
+            e[1][c] += v
+    out = [f"dispatches after the last {after!r}: {len(sel)}"]
+    for c, v in sorted(tot.items()):
+        out.append(f"{c}: total {v:.1f}")
+    names = sorted(tot)
+    out.append(f"{'kernel':34s} {'calls':>6s} " + " ".join(f"{c:>16s}" for c in names))
+    for k, (n, cs) in sorted(per.items(), key=lambda kv: -sum(kv[1][1].values())):
+        out.append(f"{k:34s} {n:6d} " + " ".join(f"{cs[c]:16.1f}" for c in names))
+    return "\n".join(out)
+
+
 def main(argv=None) -> int:
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="mode", required=True)
@@ -74,8 +110,16 @@ def main(argv=None) -> int:
     p.add_argument("--kernel", required=True)
     p.add_argument("--workgroups", type=int, default=0)
     p.add_argument("--skip", type=int, default=0)
+    w = sub.add_parser("window")
+    w.add_argument("csv")
+    w.add_argument("--after", required=True)
     a = ap.parse_args(argv)
-    print(trace(a.csv, a.last) if a.mode == "trace" else pmc(a.csv, a.kernel, a.workgroups, a.skip))
+    if a.mode == "trace":
+        print(trace(a.csv, a.last))
+    elif a.mode == "pmc":
+        print(pmc(a.csv, a.kernel, a.workgroups, a.skip))
+    else:
+        print(window(a.csv, a.after))
     return 0
 
 

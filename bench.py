@@ -393,7 +393,6 @@ def bench_batched(args, wl) -> int:
         "step_gemm_tflops": round(step_tflops, 1),
         "step_mfma_frac": round(step_tflops / PEAK_F16_TFLOPS, 4),
         "bytes_per_step": round(tot_bytes / steps),
-        "step_traffic": step_traffic,
         "context": [min(l_t0), max(l_t1)],
         "prefill_ms": round(prefill_ms, 1),
         "device_ms_per_step": round(stats.elapsed_ms / steps, 4),

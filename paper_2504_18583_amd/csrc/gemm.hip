@@ -1439,9 +1439,10 @@ __global__ __launch_bounds__(256) void k_stage(const TailArgs p) {
 // through LDS one k-block (9 KiB) at a time and are shared by the wavefronts;
 // each wavefront streams its own 4 strips of W from HBM straight into the MFMA
 // B-operand registers and accumulates 9 x 4 tiles of 16x16 (per k-block:
-// 9 KiB of LDS reads and 4 KiB of weights for 36 MFMAs).  Both operands go
-// through a register ring kRowsDepth k-blocks deep, so that several k-blocks
-// of loads are in flight while one is multiplied.  Row tiles past the pass's
+// 9 KiB of LDS reads and 4 KiB of weights for 36 MFMAs).  The k-blocks are
+// software-pipelined (loads 4 k-blocks ahead, A through LDS 2 ahead and into
+// fragment registers 1 ahead), so the MFMAs of a k-block wait on nothing
+// requested in the same iteration.  Row tiles past the pass's
 // rows skip their MFMAs; row blocks past them leave at once.
 //
 // Blocks are numbered so that the row blocks of one column tile run on the
@@ -1470,26 +1471,41 @@ __device__ __forceinline__ void static_for(F&& f) {
 // (fixed order), 16 threads per row.
 template <bool LM>
 __device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s) {
+  // 16 threads per row, rows tid / 16 + 16 k: every row's loads are in flight
+  // together (one round of loads per 64 tiles, not one per row), each thread
+  // adding its tiles in increasing order
   const int tid = threadIdx.x;
-  for (int r = tid >> 4; r < kRowTiles * 16; r += blockDim.x >> 4) {
-    const int gr = row0 + r;
-    const int row = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
-    float t = 0.f;
-    for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 256) {
-      float part[16];
+  constexpr int R = kRowTiles;                     // rows per thread group
+  int src[R];
+  float t[R];
 #pragma unroll
-      for (int u = 0; u < 16; ++u) {
+  for (int k = 0; k < R; ++k) {
+    const int gr = row0 + (tid >> 4) + 16 * k;
+    src[k] = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
+    t[k] = 0.f;
+  }
+  for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 64) {
+    float part[R][4];
+#pragma unroll
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
         const int q = q0 + 16 * u;
-        part[u] = q < p.ss_tiles ? p.ss_in[(size_t)row * p.ss_stride + q] : 0.f;
+        part[k][u] = q < p.ss_tiles ? p.ss_in[(size_t)src[k] * p.ss_stride + q] : 0.f;
       }
 #pragma unroll
-      for (int u = 0; u < 16; ++u) t += part[u];
-    }
-    t += __shfl_xor(t, 8);
-    t += __shfl_xor(t, 4);
-    t += __shfl_xor(t, 2);
-    t += __shfl_xor(t, 1);
-    if ((tid & 15) == 0) rs_s[r] = 1.0f / sqrtf(t * p.inv_k + p.eps);
+    for (int k = 0; k < R; ++k)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) t[k] += part[k][u];
+  }
+#pragma unroll
+  for (int k = 0; k < R; ++k) {
+    float v = t[k];
+    v += __shfl_xor(v, 8);
+    v += __shfl_xor(v, 4);
+    v += __shfl_xor(v, 2);
+    v += __shfl_xor(v, 1);
+    if ((tid & 15) == 0) rs_s[(tid >> 4) + 16 * k] = 1.0f / sqrtf(v * p.inv_k + p.eps);
   }
 }
 
@@ -1499,7 +1515,7 @@ __device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp
 template <int EPI>
 __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* dp, RowsAcc& acc, int tile, int row0,
                                               int row_count, int mt_lo, int mt_live, int wave, int lane,
-                                              const float* rs_s) {
+                                              const float* rs_s, u32x4* o_lds = nullptr) {
   const int c16 = lane & 15, g4 = lane >> 4;
   const int strip0 = tile * kRowsTileStrips + wave * kRowsWaveStrips;
   [[maybe_unused]] bool bad = false;
@@ -1572,7 +1588,12 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
     });
     flag_range(bad, p.ovf);
   } else if constexpr (EPI == EPI_SWIGLU) {
-    // 8 gate columns then the 8 up columns of the same features per strip
+    // 8 gate columns then the 8 up columns of the same features per strip.
+    // The wavefront's 4 strips are the 32 features of one k-block of h
+    // (block tile * 4 + wave): with o_lds (this wavefront's 9 KiB) the block
+    // is assembled in LDS and written with 16-byte stores, one row's 64 bytes
+    // per 4 lanes (2-byte stores straight from the accumulator layout made the
+    // epilogue as long as the GEMM); without, each lane stores its values.
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
       constexpr int mt = decltype(mtc)::value;
       if (mt < mt_lo || mt >= mt_live) return;       // uniform
@@ -1584,12 +1605,40 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
         for (int i = 0; i < 4; ++i) {
           const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
           const float gt = acc[mt][s][i] * rs_s[rl];
-          const float up = __shfl_xor(gt, 8);
-          const float h = gt / (1.0f + expf(-gt)) * up;
-          if (c16 < 8 && r < row_count) p.out[act_index(r, f, p.act_rows)] = f16_flagged(h, bad);
+          // the up value of lane l < 8 is in lane l + 8 of its row of 16 (DPP row rotate by 8)
+          const float up = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, gt), 0x128,
+                                                                              0xF, 0xF, false));
+          // silu(g) = g / (1 + e^-g), with the hardware exp2 and reciprocal
+          const float h = gt * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-gt * attn::kLog2e)) * up;
+          bool bad_h = false;
+          const uint16_t hb = f16_flagged(h, bad_h);
+          bad |= bad_h && c16 < 8 && r < row_count;
+          if (o_lds) {
+            // rows rl, chunk s (features s*8 .. s*8+7): lane pairs pack two
+            // values into one dword (DPP quad swap); chunks are swizzled by
+            // (rl / 4) % 4 so the four rows of one store land in different banks
+            const uint32_t pair =
+                (uint32_t)hb | ((uint32_t)__builtin_amdgcn_mov_dpp((int)hb, 0xB1, 0xF, 0xF, false) << 16);
+            if (c16 < 8 && !(c16 & 1))
+              reinterpret_cast<uint32_t*>(o_lds)[(rl * 4 + (s ^ ((rl >> 2) & 3))) * 4 + (c16 >> 1)] = pair;
+          } else if (c16 < 8 && r < row_count) {
+            p.out[act_index(r, f, p.act_rows)] = hb;
+          }
         }
       }
     });
+    if (o_lds) {
+      // this wavefront's rows [row0 + 16 mt_lo, row0 + 16 mt_live) of block tile * 4 + wave
+      const int blk = tile * kRowsWaves + wave;
+      if (blk * 4 < p.n_strips) {                    // uniform: the block holds features of the weight
+        for (int e = mt_lo * 64 + lane; e < mt_live * 64; e += 64) {
+          const int rl = e >> 2, c = e & 3, r = row0 + rl;
+          const u32x4 v = o_lds[rl * 4 + (c ^ ((rl >> 2) & 3))];
+          if (r < row_count)
+            *reinterpret_cast<u32x4*>(p.out + act_index(r, blk * 32 + c * 8, p.act_rows)) = v;
+        }
+      }
+    }
     flag_range(bad, p.ovf);
   } else {  // EPI_LOGITS
     static_for<0, kRowTiles>([&](auto mtc) __attribute__((always_inline)) {
@@ -1648,11 +1697,15 @@ __device__ __forceinline__ void rows_block(const GemmArgs& p, int* tile, int* ks
 
 template <int EPI>
 __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
-  constexpr int MB = kRowTiles, NS = kRowsWaveStrips, D = kRowsDepth;
+  constexpr int MB = kRowTiles, NS = kRowsWaveStrips;
   constexpr int AE = MB * 64;                        // 16-byte A elements of one k-block
   constexpr int AJ = (AE + 255) / 256;               // per thread
   constexpr bool LM = EPI == EPI_LOGITS;             // rows are the pass's lm rows
-  __shared__ __attribute__((aligned(16))) u32x4 a_lds[2][AE];
+  // (padded to whole rounds of the workgroup's threads: every thread stores
+  // each of its AJ elements, those past AE are zeros never read)
+  __shared__ __attribute__((aligned(16))) u32x4 a_lds[2][AJ * 256];
+  // SwiGLU: each wavefront's block of h (MB * 16 rows x 64 bytes) for 16-byte stores
+  __shared__ __attribute__((aligned(16))) u32x4 o_lds[EPI == EPI_SWIGLU ? kRowsWaves * MB * 64 : 1];
   __shared__ float rs_s[MB * 16];
 
   int tile, ks, mb;
@@ -1690,25 +1743,43 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
     a_voff[j] = (e < AE && gr < row_count) ? src * 64 + (e & 3) * 16 : kOutOfRange;
   }
 
-  // Register ring of D k-blocks: the loads of k-block it + D go out as soon as
-  // k-block it has been used, so D - 1 k-blocks of W and A are in flight while
-  // one is multiplied.
-  u32x4 wr[D][NS], ar[D][AJ];
-  auto issue = [&](int slot, int it) {
+  // Software pipeline over the k-blocks.  k-block k's weights are loaded into
+  // a register ring D = 4 k-blocks ahead; its A rows are loaded into registers
+  // 6 k-blocks ahead, written to LDS (one of two buffers) 2 ahead and read
+  // into fragment registers 1 ahead, so each iteration's MFMAs wait on
+  // nothing issued in the last few iterations: iteration it reads A(it + 1)'s
+  // fragments and writes A(it + 2) to LDS, multiplies k-block it, then
+  // requests A(it + 6) and W(it + 4).  One barrier per k-block separates an
+  // LDS buffer's writes from its reads.  Indices past the range are clamped
+  // (cache hits, never multiplied), so every iteration issues the same loads
+  // on every path, in the same order (the compiler's waits then hold the
+  // intended depth).
+  constexpr int D = 4, DA = 4;   // weight ring, A register ring (A is requested 6 k-blocks ahead)
+  static_assert(D % DA == 0 && DA % 2 == 0, "one unrolled turn of the weight ring turns the others whole");
+  u32x4 wr[D][NS], ar[DA][AJ], av[2][MB];
+  auto issue_w = [&](int slot, int it) {
     const int kb = kb0 + min(it, n_kb - 1);
 #pragma unroll
     for (int s = 0; s < NS; ++s)
       wr[slot][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT);
+  };
+  auto issue_a = [&](int slot, int it) {
+    const int kb = kb0 + min(it, n_kb - 1);
 #pragma unroll
     for (int j = 0; j < AJ; ++j)
       ar[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(ars, a_voff[j], kb * (p.act_rows * 64), 0);
   };
+  // LDS holds row r's 16-byte chunk c at r * 4 + (c ^ ((r >> 1) & 3)): a
+  // fragment read (lanes 0-15 take rows 0-15 of one chunk) then touches
+  // eight different 16-byte bank groups per eight lanes instead of two
+  auto swz = [](int e) { return (e & ~3) | ((e & 3) ^ ((e >> 3) & 3)); };
   auto put_a = [&](int slot, int buf) {
 #pragma unroll
-    for (int j = 0; j < AJ; ++j) {
-      const int e = tid + 256 * j;
-      if (e < AE) a_lds[buf][e] = ar[slot][j];
-    }
+    for (int j = 0; j < AJ; ++j) a_lds[buf][swz(tid + 256 * j)] = ar[slot][j];
+  };
+  auto read_a = [&](int slot, int buf) {
+#pragma unroll
+    for (int mt = 0; mt < MB; ++mt) av[slot][mt] = a_lds[buf][swz((mt * 16 + (lane & 15)) * 4 + (lane >> 4))];
   };
 
   RowsAcc acc;
@@ -1717,44 +1788,52 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // all A fragments of the k-block are read from LDS first, so their
-  // latencies overlap; row tiles past the pass multiply zeros (no branches
-  // between the fragment reads and the MFMAs)
-  auto mma = [&](int slot, int buf) {
-    u32x4 av[MB];
-#pragma unroll
-    for (int mt = 0; mt < MB; ++mt) av[mt] = a_lds[buf][(mt * 16 + (lane & 15)) * 4 + (lane >> 4)];
+  // row tiles past the pass multiply zeros (no branches between the fragment
+  // reads and the MFMAs)
+  auto mma = [&](int wslot, int aslot) {
 #pragma unroll
     for (int mt = 0; mt < MB; ++mt) {
 #pragma unroll
       for (int s = 0; s < NS; ++s)
-        acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av[mt]),
-                                                            __builtin_bit_cast(f16x8, wr[slot][s]), acc[mt][s], 0, 0, 0);
+        acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av[aslot][mt]),
+                                                            __builtin_bit_cast(f16x8, wr[wslot][s]), acc[mt][s], 0, 0, 0);
     }
   };
 
   if (n_kb > 0) {
-    // Every iteration issues its loads and stages A whether or not its
-    // k-block exists (indices are clamped: past the end they re-read the last
-    // k-block, from cache), so the number of loads in flight is the same on
-    // every path and each wait covers exactly the k-block about to be used.
-    // The loop runs whole turns of the ring; only the MFMAs are skipped.
-#pragma unroll
-    for (int d = 0; d < D; ++d) issue(d, d);
+    // A(0) and A(1) into LDS, then the loads of the four turns before the
+    // first in the loop's order (A(k + 6), then W(k + 4), for k = -4 .. -1),
+    // so the waits the compiler places at the loop's top match every turn's
+    issue_a(0, 0);
+    issue_a(1, 1);
+    __builtin_amdgcn_sched_barrier(0);
     put_a(0, 0);
+    put_a(1, 1);
+#pragma unroll
+    for (int k = -D; k < 0; ++k) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (k >= -4) issue_a((k + 6) % DA, k + 6);    // A(2) .. A(5)
+      __builtin_amdgcn_sched_barrier(0);
+      issue_w(k + D, k + D);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
+    read_a(0, 0);
+    __syncthreads();                                 // buffer 0 is free again
     const int n_it = (n_kb + D - 1) / D * D;
     for (int it0 = 0; it0 < n_it; it0 += D) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int it = it0 + d;
-        // k-block it+1's A goes to the other LDS buffer (free since the last
-        // barrier), k-block it is multiplied, its ring slot is refilled
-        put_a((d + 1) % D, (it + 1) & 1);
+        read_a((d + 1) & 1, (d + 1) & 1);            // A(it + 1): written before the last barrier
+        put_a((d + 2) % DA, d & 1);                  // A(it + 2) into A(it)'s buffer
         __builtin_amdgcn_sched_barrier(0);
-        if (it < n_kb) mma(d, it & 1);               // uniform
+        if (it < n_kb) mma(d, d & 1);                // uniform
         __builtin_amdgcn_sched_barrier(0);
-        issue(d, it + D);
+        issue_a((d + 2) % DA, it + 6);
+        __builtin_amdgcn_sched_barrier(0);
+        issue_w(d, it + D);
+        __builtin_amdgcn_sched_barrier(0);
         __syncthreads();
       }
     }
@@ -1776,7 +1855,8 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
     rows_scales<LM>(p, dp, row0, row_count, rs_s);
     __syncthreads();
   }
-  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, 0, mt_live, wave, lane, rs_s);
+  rows_epilogue<EPI>(p, dp, acc, tile, row0, row_count, 0, mt_live, wave, lane, rs_s,
+                    EPI == EPI_SWIGLU ? o_lds + wave * MB * 64 : nullptr);
 }
 
 // Sum of the input splits of k_gemm_rows in split order, then the epilogue.

@@ -44,7 +44,6 @@ constexpr int kMaxLmRows = kMaxPassRows;
 // row-block GEMM: a workgroup of kRowsWaves wavefronts computes kRowTiles*16
 // rows x kRowsWaves*kRowsWaveStrips strips of 16 columns
 constexpr int kRowTiles = 9;
-constexpr int kRowsDepth = 6;         // k-blocks of loads in the register ring
 constexpr int kRowsWaves = 4;
 constexpr int kRowsWaveStrips = 4;
 constexpr int kRowsTileStrips = kRowsWaves * kRowsWaveStrips;

@@ -535,7 +535,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       const int row = mt * 16 + rsub;
       const int n = (tile * S + s) * 16 + csub;
       float y = v[j] * rs_s[row] + e0[j];            // + bias
-      const float partner = __shfl_xor(y, 1);
+      // rotary partner column (n ^ 1) is in lane l ^ 1 (DPP quad swap)
+      const float partner = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, y), 0xB1, 0xF,
+                                                                               0xF, false));
       if (row < row_count) {
         const int pos = e_pos[mt];
         const size_t cache = (size_t)e_slot[mt] * p.kv_seq_stride;
@@ -596,7 +598,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       for (int mt = 0; mt < MT; ++mt) {
         const int row = mt * 16 + rsub;
         const float gt = v[s * MT + mt] * rs_s[row];
-        const float up = __shfl_xor(gt, 8);
+        // lane l ^ 8 of the row of 16 (DPP row rotate by 8)
+        const float up = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, gt), 0x128, 0xF,
+                                                                            0xF, false));
         const float h = gt / (1.0f + expf(-gt)) * up;
         const int f = (tile * S + s) * 8 + csub;
         if (csub < 8 && row < row_count && s <= s_last) {
@@ -1470,20 +1474,23 @@ __device__ __forceinline__ void static_for(F&& f) {
 // 1/rms of the block's rows from the producer's per-tile sums of squares
 // (fixed order), 16 threads per row.
 template <bool LM>
-__device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s) {
+__device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp, int row0, int row_count, float* rs_s,
+                                            int mt_only = -1) {
   // 16 threads per row, rows tid / 16 + 16 k: every row's loads are in flight
   // together (one round of loads per 64 tiles, not one per row), each thread
-  // adding its tiles in increasing order
+  // adding its tiles in increasing order.  mt_only >= 0: the rows of that row
+  // tile only (rs_s entries of the others are not written).
   const int tid = threadIdx.x;
   constexpr int R = kRowTiles;                     // rows per thread group
   int src[R];
   float t[R];
 #pragma unroll
   for (int k = 0; k < R; ++k) {
-    const int gr = row0 + (tid >> 4) + 16 * k;
+    const int gr = row0 + (tid >> 4) + 16 * (mt_only >= 0 ? mt_only : k);
     src[k] = gr < row_count ? (LM ? dp->lm_src[gr] : gr) : 0;
     t[k] = 0.f;
   }
+  const int n_k = mt_only >= 0 ? 1 : R;            // uniform
   for (int q0 = tid & 15; q0 < p.ss_tiles; q0 += 64) {
     float part[R][4];
 #pragma unroll
@@ -1491,7 +1498,7 @@ __device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         const int q = q0 + 16 * u;
-        part[k][u] = q < p.ss_tiles ? p.ss_in[(size_t)src[k] * p.ss_stride + q] : 0.f;
+        part[k][u] = q < p.ss_tiles && k < n_k ? p.ss_in[(size_t)src[k] * p.ss_stride + q] : 0.f;
       }
 #pragma unroll
     for (int k = 0; k < R; ++k)
@@ -1505,7 +1512,7 @@ __device__ __forceinline__ void rows_scales(const GemmArgs& p, const FwdDesc* dp
     v += __shfl_xor(v, 4);
     v += __shfl_xor(v, 2);
     v += __shfl_xor(v, 1);
-    if ((tid & 15) == 0) rs_s[(tid >> 4) + 16 * k] = 1.0f / sqrtf(v * p.inv_k + p.eps);
+    if ((tid & 15) == 0 && k < n_k) rs_s[(tid >> 4) + 16 * (mt_only >= 0 ? mt_only : k)] = 1.0f / sqrtf(v * p.inv_k + p.eps);
   }
 }
 
@@ -1532,7 +1539,9 @@ __device__ __forceinline__ void rows_epilogue(const GemmArgs& p, const FwdDesc* 
         for (int i = 0; i < 4; ++i) {
           const int rl = mt * 16 + g4 * 4 + i, r = row0 + rl;
           float y = acc[mt][s][i] * rs_s[rl] + bias;
-          const float partner = __shfl_xor(y, 1);
+          // rotary partner column (n ^ 1) is in lane l ^ 1 (DPP quad swap)
+          const float partner = __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, y), 0xB1,
+                                                                                   0xF, 0xF, false));
           if (col_ok && r < row_count) {
             const int pos = dp->pos[r];
             const size_t cache = (size_t)dp->slot[r] * p.kv_seq_stride;
@@ -1877,7 +1886,7 @@ __global__ __launch_bounds__(256) void k_gemm_rows_red(const GemmArgs p) {
   const int mt_live = min(MB, (row_count - row0 + 15) / 16);
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  if constexpr (EPI != EPI_RESID) rows_scales<LM>(p, dp, row0, row_count, rs_s);
+  if constexpr (EPI != EPI_RESID) rows_scales<LM>(p, dp, row0, row_count, rs_s, mt_sel);
   const float* base = p.part + (size_t)(tile * p.m_blocks + mb) * p.ksplit * kRowsPartFloats +
                       (size_t)(((wave * MB + mt_sel) * NS) * 64 + lane) * 4;
   f32x4 sum[NS];

@@ -262,9 +262,14 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
   }
   const float scale2 = p.scale * kLog2e;   // scores in base 2
 
+  // Not fused (the standalone kernel): the next pair's K is requested once
+  // this pair's scores are computed and its V once this pair's V has been
+  // multiplied, so a pair's loads are in flight during the previous pair's
+  // work.  Fused (the decode launch) the loads stay at the top of each pair
+  // (the early requests measured slower there).
   for (int it0 = 0; it0 < n_my; it0 += 2) {
     const int nt = min(2, n_my - it0);     // tiles in this pair (uniform)
-    if (it0 > 0) {
+    if (FUSED && it0 > 0) {
       load(0, it0);
       if (nt > 1) load(1, it0 + 1);
     }
@@ -286,6 +291,14 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
                   s[t][tt][kb], 0, 0, 0);
           }
         }
+    if constexpr (!FUSED) {
+      if (it0 + 2 < n_my) {                // uniform: the next pair's keys
+        __builtin_amdgcn_sched_barrier(0);
+        load_k(0, it0 + 2);
+        load_k(1, it0 + 3);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
     // causal / range mask; only tiles that reach past the context end or the
     // first query's position need it
 #pragma unroll
@@ -355,6 +368,14 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
             o[t][db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, vf[tt][db]),
                                                                __builtin_bit_cast(f16x8, pf[t][tt]), o[t][db], 0, 0, 0);
         }
+    }
+    if constexpr (!FUSED) {
+      if (it0 + 2 < n_my) {                // uniform: the next pair's values
+        __builtin_amdgcn_sched_barrier(0);
+        load_v(0, it0 + 2);
+        load_v(1, it0 + 3);
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
 

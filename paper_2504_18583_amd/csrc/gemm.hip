@@ -1766,12 +1766,6 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
   constexpr int D = 4, DA = 4;   // weight ring, A register ring (A is requested 6 k-blocks ahead)
   static_assert(D % DA == 0 && DA % 2 == 0, "one unrolled turn of the weight ring turns the others whole");
   u32x4 wr[D][NS], ar[DA][AJ], av[2][MB];
-  auto issue_w = [&](int slot, int it) {
-    const int kb = kb0 + min(it, n_kb - 1);
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      wr[slot][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT);
-  };
   auto issue_a = [&](int slot, int it) {
     const int kb = kb0 + min(it, n_kb - 1);
 #pragma unroll
@@ -1797,22 +1791,29 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
 #pragma unroll
     for (int s = 0; s < NS; ++s) acc[mt][s] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // row tiles past the pass multiply zeros (no branches between the fragment
-  // reads and the MFMAs)
-  auto mma = [&](int wslot, int aslot) {
+  // one strip's MFMAs (row tiles past the pass multiply zeros: no branches
+  // between the fragment reads and the MFMAs)
+  auto mma_strip = [&](int wslot, int aslot, int s) {
 #pragma unroll
-    for (int mt = 0; mt < MB; ++mt) {
+    for (int mt = 0; mt < MB; ++mt)
+      acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av[aslot][mt]),
+                                                          __builtin_bit_cast(f16x8, wr[wslot][s]), acc[mt][s], 0, 0, 0);
+  };
+  auto issue_w_strip = [&](int slot, int it, int s) {
+    const int kb = kb0 + min(it, n_kb - 1);
+    wr[slot][s] = __builtin_amdgcn_raw_buffer_load_b128(wrs, w_voff, (kb * p.n_strips + s) * 1024, kCachePolicyNT);
+  };
+  // the A fragments of row tiles [m0, m1)
+  auto read_a_part = [&](int slot, int buf, int m0, int m1) {
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
-        acc[mt][s] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, av[aslot][mt]),
-                                                            __builtin_bit_cast(f16x8, wr[wslot][s]), acc[mt][s], 0, 0, 0);
-    }
+    for (int mt = m0; mt < m1; ++mt) av[slot][mt] = a_lds[buf][swz((mt * 16 + (lane & 15)) * 4 + (lane >> 4))];
   };
 
   if (n_kb > 0) {
     // A(0) and A(1) into LDS, then the loads of the four turns before the
-    // first in the loop's order (A(k + 6), then W(k + 4), for k = -4 .. -1),
-    // so the waits the compiler places at the loop's top match every turn's
+    // first in the loop's order (W(k + 4) strip 0, A(k + 6), W(k + 4) strips
+    // 1-3, for k = -4 .. -1), so the waits the compiler places at the loop's
+    // top match every turn's
     issue_a(0, 0);
     issue_a(1, 1);
     __builtin_amdgcn_sched_barrier(0);
@@ -1820,29 +1821,41 @@ __global__ __launch_bounds__(256) void k_gemm_rows(const GemmArgs p) {
     put_a(1, 1);
 #pragma unroll
     for (int k = -D; k < 0; ++k) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (k >= -4) issue_a((k + 6) % DA, k + 6);    // A(2) .. A(5)
-      __builtin_amdgcn_sched_barrier(0);
-      issue_w(k + D, k + D);
+#pragma unroll
+      for (int s2 = 0; s2 < NS; ++s2) {
+        __builtin_amdgcn_sched_barrier(0);
+        if (s2 == 1 && k >= -4) issue_a((k + 6) % DA, k + 6);   // A(2) .. A(5)
+        issue_w_strip(k + D, k + D, s2);
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
     read_a(0, 0);
     __syncthreads();                                 // buffer 0 is free again
+    // One wavefront issues its loads and LDS operations in order with its
+    // MFMAs, so they are interleaved: after each strip's MFMAs go that strip's
+    // next weight load (its registers are free then) and a share of the
+    // fragment reads of A(it + 1); A(it + 2) goes to LDS after the first strip
+    // and A(it + 6) is requested after the second.  The issue cost of the
+    // loads and LDS operations then hides under the MFMAs in flight (issued
+    // as blocks they measured ~650 cycles per k-block against ~650 of MFMA).
     const int n_it = (n_kb + D - 1) / D * D;
     for (int it0 = 0; it0 < n_it; it0 += D) {
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int it = it0 + d;
-        read_a((d + 1) & 1, (d + 1) & 1);            // A(it + 1): written before the last barrier
-        put_a((d + 2) % DA, d & 1);                  // A(it + 2) into A(it)'s buffer
-        __builtin_amdgcn_sched_barrier(0);
-        if (it < n_kb) mma(d, d & 1);                // uniform
-        __builtin_amdgcn_sched_barrier(0);
-        issue_a((d + 2) % DA, it + 6);
-        __builtin_amdgcn_sched_barrier(0);
-        issue_w(d, it + D);
-        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+          if (it < n_kb) mma_strip(d, d & 1, s);     // uniform
+          __builtin_amdgcn_sched_barrier(0);
+          if (s == 1) issue_a((d + 2) % DA, it + 6);
+          issue_w_strip(d, it + D, s);
+          __builtin_amdgcn_sched_barrier(0);
+          // A(it + 1): written before the last barrier; row tiles 3s .. 3s + 2
+          read_a_part((d + 1) & 1, (d + 1) & 1, min(3 * s, MB), min(3 * s + 3, MB));
+          if (s == 0) put_a((d + 2) % DA, d & 1);    // A(it + 2) into A(it)'s buffer
+          __builtin_amdgcn_sched_barrier(0);
+        }
         __syncthreads();
       }
     }

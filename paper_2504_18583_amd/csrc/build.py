@@ -6,7 +6,8 @@ into the package directory, where the binding loads it from.  The same call
 links ``gemm_counters`` (a stand-alone launch of the gate/up GEMM) and
 ``layer_counters`` (stand-alone launches of the one-launch decode layer) from
 the GEMM object, and ``step_counters`` (whole decode steps through the C ABI)
-against the library, for hardware-counter runs.
+against the library, for hardware-counter runs, and ``mfma_peak`` (the
+attainable rate of the GEMMs' MFMA instructions).
 """
 from __future__ import annotations
 
@@ -24,9 +25,10 @@ LIB = os.path.join(PKG, "libpard.so")
 COUNTERS_EXE = os.path.join(PKG, "gemm_counters")
 LAYER_EXE = os.path.join(PKG, "layer_counters")
 STEP_EXE = os.path.join(PKG, "step_counters")
+MFMA_EXE = os.path.join(PKG, "mfma_peak")
 
 SOURCES = ["engine.hip", "gemm.hip", "attention.hip", "device_init.hip", "cod.hip", "gemm_counters.hip",
-           "layer_counters.hip", "step_counters.hip"]
+           "layer_counters.hip", "step_counters.hip", "mfma_peak.hip"]
 LIB_SOURCES = SOURCES[:5]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
@@ -61,8 +63,9 @@ def build(verbose: bool = False) -> str:
     _link(COUNTERS_EXE, [], [obj["gemm_counters.hip"], obj["gemm.hip"]])
     _link(LAYER_EXE, [], [obj["layer_counters.hip"], obj["gemm.hip"]])
     _link(STEP_EXE, [f"-L{PKG}", "-Wl,-rpath,$ORIGIN"], [obj["step_counters.hip"], "-lpard"])
+    _link(MFMA_EXE, [], [obj["mfma_peak.hip"]])
     if verbose:
-        print(f"built {LIB}, {COUNTERS_EXE}, {LAYER_EXE} and {STEP_EXE}")
+        print(f"built {LIB}, {COUNTERS_EXE}, {LAYER_EXE}, {STEP_EXE} and {MFMA_EXE}")
     return LIB
 
 

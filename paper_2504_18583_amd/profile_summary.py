@@ -2,14 +2,17 @@
 
     python -m paper_2504_18583_amd.profile_summary trace <dir>/run_kernel_trace.csv [--last N]
     python -m paper_2504_18583_amd.profile_summary pmc <dir>/run_counter_collection.csv \
-        --kernel NAME_SUBSTRING [--workgroups WG] [--skip N]
+        --kernel NAME_SUBSTRING [--workgroups WG] [--skip N] [--at-max COUNTER]
     python -m paper_2504_18583_amd.profile_summary window <dir>/run_counter_collection.csv \
         --after NAME_SUBSTRING
 
 ``trace`` groups dispatches by kernel (template arguments included) and
 workgroup count -- the same template runs for the target and the draft with
 different grids -- and prints calls and mean / min / max duration.  ``pmc``
-averages each counter over the dispatches of one kernel and grid.
+averages each counter over the dispatches of one kernel and grid (with
+``--at-max``, only over the dispatches whose value of that counter is the
+largest seen: e.g. the full-size passes of a GEMM whose shorter prefill passes
+share its grid).
 ``window`` sums each counter over every dispatch after the last dispatch of a
 marker kernel, in total and per kernel (a program's measured region).
 """
@@ -49,19 +52,29 @@ def trace(path: str, last: int) -> str:
     return "\n".join(out)
 
 
-def pmc(path: str, kernel: str, workgroups: int, skip: int) -> str:
+def pmc(path: str, kernel: str, workgroups: int, skip: int, at_max: str = "") -> str:
     rows = list(csv.DictReader(open(path)))
-    vals = defaultdict(list)
+    key = "Dispatch_Id" if rows and "Dispatch_Id" in rows[0] else "Correlation_Id"
+    disp = {}
     for r in rows:
         if kernel not in r["Kernel_Name"]:
             continue
         wgs = int(r["Grid_Size"]) // int(r["Workgroup_Size"])
         if workgroups and wgs != workgroups:
             continue
-        vals[r["Counter_Name"]].append(float(r["Counter_Value"]))
-    out = [f"kernel ~ {kernel!r}, workgroups {workgroups or 'any'}"]
+        disp.setdefault(int(r[key]), {})[r["Counter_Name"]] = float(r["Counter_Value"])
+    order = [disp[k] for k in sorted(disp)]
+    order = order[skip:] if len(order) > skip else order
+    if at_max:
+        top = max((d.get(at_max, float("-inf")) for d in order), default=0.0)
+        order = [d for d in order if d.get(at_max) == top]
+    vals = defaultdict(list)
+    for d in order:
+        for name, v in d.items():
+            vals[name].append(v)
+    sel = f", dispatches at the largest {at_max}" if at_max else ""
+    out = [f"kernel ~ {kernel!r}, workgroups {workgroups or 'any'}{sel}"]
     for name, v in sorted(vals.items()):
-        v = v[skip:] if len(v) > skip else v
         out.append(f"{name}: dispatches {len(v)}, mean {statistics.mean(v):.1f}, "
                    f"min {min(v):.1f}, max {max(v):.1f}")
     return "\n".join(out)
@@ -110,6 +123,7 @@ def main(argv=None) -> int:
     p.add_argument("--kernel", required=True)
     p.add_argument("--workgroups", type=int, default=0)
     p.add_argument("--skip", type=int, default=0)
+    p.add_argument("--at-max", default="")
     w = sub.add_parser("window")
     w.add_argument("csv")
     w.add_argument("--after", required=True)
@@ -117,7 +131,7 @@ def main(argv=None) -> int:
     if a.mode == "trace":
         print(trace(a.csv, a.last))
     elif a.mode == "pmc":
-        print(pmc(a.csv, a.kernel, a.workgroups, a.skip))
+        print(pmc(a.csv, a.kernel, a.workgroups, a.skip, a.at_max))
     else:
         print(window(a.csv, a.after))
     return 0

@@ -46,7 +46,8 @@ using namespace attn;
 // One workgroup per (KV head, query group, sequence x key chunk).
 template <int HD, int NQ, int NW>
 __global__ __launch_bounds__(64 * NW) void k_attn(const AttnArgs p) {
-  attn_tile<HD, NQ, NW, false>(p, blockIdx.x, blockIdx.y, blockIdx.z, FuseCtl{});
+  __shared__ AttnLds<HD, NQ> sm;
+  attn_tile<HD, NQ, NW, false>(p, blockIdx.x, blockIdx.y, blockIdx.z, FuseCtl{}, sm);
 }
 
 // Combine a few key chunks of k_attn (passes with many sequences or query

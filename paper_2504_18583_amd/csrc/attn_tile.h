@@ -102,9 +102,20 @@ __device__ __forceinline__ void fuse_wait_on(const int* lanes, const int n, int*
 // Wait for every QKV workgroup of the launch.
 __device__ __forceinline__ void fuse_wait(const FuseCtl& f) { fuse_wait_on<kFuseLanes>(f.counters, f.n_prod, f.err); }
 
+// The attention tile's LDS arrays: Q fragments in B-operand lane order, and the
+// wavefronts' output tiles and softmax statistics for the final merge.  The
+// kernel declares them (static LDS, so the compiler keeps them apart from its
+// dynamic LDS), and a fused launch reuses them once the tile is done.
+template <int HD, int NQ>
+struct AttnLds {
+  u32x4 q[NQ * (HD / 32) * 64];
+  float o[kAttnWaves][16 * NQ][HD + 4];
+  float m[kAttnWaves][16 * NQ], l[kAttnWaves][16 * NQ], sc[kAttnWaves][16 * NQ], linv[16 * NQ];
+};
+
 template <int HD, int NQ, int NW, bool FUSED>
 __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, const int qg, const unsigned zz,
-                                          const FuseCtl& fc) {
+                                          const FuseCtl& fc, AttnLds<HD, NQ>& sm) {
   constexpr int NWA = NW;
   constexpr int MW = kAttnWaves;     // waves in the final LDS merge
   constexpr int QP = 16 * NQ;        // query pairs per workgroup
@@ -112,9 +123,13 @@ __device__ __forceinline__ void attn_tile(const AttnArgs& p, const int kvh, cons
   constexpr int DB = HD / 16;        // 16-dim blocks of the output
   constexpr int OS = HD + 4;         // row stride of the per-wave output tiles in LDS
   constexpr int REC = QP * HD + 2 * QP;   // floats of one chunk record: o [QP][HD], m [QP], l [QP]
-  __shared__ u32x4 q_lds[NQ * KS * 64];   // Q fragments in B-operand lane order
-  __shared__ __attribute__((aligned(16))) float o_lds[MW][QP][OS];
-  __shared__ float m_lds[MW][QP], l_lds[MW][QP], sc_lds[MW][QP], linv_lds[QP];
+  static_assert(MW == kAttnWaves && OS == HD + 4 && QP == 16 * NQ, "AttnLds holds the tile's arrays");
+  auto& q_lds = sm.q;
+  auto& o_lds = sm.o;
+  auto& m_lds = sm.m;
+  auto& l_lds = sm.l;
+  auto& sc_lds = sm.sc;
+  auto& linv_lds = sm.linv;
 
   const int sj = zz / p.n_splits, ch = zz % p.n_splits;
   const int tid = threadIdx.x, lane = tid & 63;

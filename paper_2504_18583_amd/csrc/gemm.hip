@@ -105,8 +105,9 @@ constexpr int kGuPreMax = 8;
 // output) the Q / K / V stores are device-scope, so that workgroups on other
 // XCDs of the same launch read them after the count-in.  With PM = 1 (the gate/up
 // tile of such a launch: one row tile, one input range, four wavefronts) the
-// first `pre` iterations of each wavefront take their weights from pre_lds
-// (gu_preload put them there; the caller has waited for its loads), the
+// first `pre` iterations of each wavefront take their weights from LDS, the
+// first pre_d of them from pre_lds and the rest from pre_stat (gu_preload put
+// them there; the caller has waited for its loads), the
 // first global weight stages are requested before the tile waits for the O
 // workers (fc), and the activations and row sums they wrote in this launch
 // are read at device scope (one acquire fence per workgroup measured 8B/1B
@@ -119,7 +120,8 @@ constexpr int kGuPreMax = 8;
 template <int MT, int S, int EPI, bool FUSED = false, int PM = 0>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, const unsigned split, const int n_split,
                                           const int nw, float* red, const FuseCtl* fc = nullptr,
-                                          const uint32_t* pre_lds = nullptr, const int pre = 0) {
+                                          const uint32_t* pre_lds = nullptr, const int pre = 0,
+                                          const uint32_t* pre_stat = nullptr, const int pre_d = 0) {
   static_assert(PM != 1 || (MT == 1 && EPI == EPI_SWIGLU && S < 8), "preloaded tiles: one row tile of gate/up, not ragged");
   static_assert(PM != 2 || (MT == 1 && EPI == EPI_RESID && S == 1), "fused down tiles: one row tile, one strip");
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
@@ -413,7 +415,9 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
       if (i < pre) {                                    // uniform
 #pragma unroll
         for (int s = 0; s < S; ++s) {
-          const u32x4 wl = *reinterpret_cast<const u32x4*>(pre_lds + ((wave * pre + i) * S + s) * 256 + lane * 4);
+          const uint32_t* wb = i < pre_d ? pre_lds + ((wave * pre_d + i) * S + s) * 256
+                                         : pre_stat + ((wave * (pre - pre_d) + i - pre_d) * S + s) * 256;
+          const u32x4 wl = *reinterpret_cast<const u32x4*>(wb + lane * 4);
           acc[s][0] = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, ap[i]),
                                                              __builtin_bit_cast(f16x8, wl), acc[s][0], 0, 0, 0);
         }
@@ -781,24 +785,38 @@ __device__ __forceinline__ void o_part(const GemmArgs& p, const FuseCtl& f, cons
   }
 }
 
-// Gate/up weights of tile `tile` for the first `pre` input iterations of
+// Gate/up weights of tile `tile` for input iterations [i0, i1) of
 // wavefronts 0-3 (k-blocks w + 4i, as gemm_tile streams them), loaded
-// straight into LDS at [w][i][strip] (1 KiB blocks, lane-ordered) with no
-// registers held; called by wavefronts 0-3, each for its own blocks.
-template <int S>
-__device__ __forceinline__ void gu_preload(const GemmArgs& p, const int tile, const int pre, uint32_t* lds) {
+// straight into LDS (1 KiB blocks, lane-ordered) with no registers held:
+// iterations below pre_d at dyn [w][i][strip], the others (STAT) at stat
+// [w][i - pre_d][strip] for a workgroup of `pre` iterations; called by
+// wavefronts 0-3, each for its own blocks.  Every load's LDS target derives
+// from one LDS object, so the compiler's LDS-DMA waits stay precise.
+template <int S, bool STAT>
+__device__ __forceinline__ void gu_preload(const GemmArgs& p, const int tile, const int i0, const int i1,
+                                           const int pre, const int pre_d, uint32_t* dyn, uint32_t* stat) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(p.W), 0, (int)min((size_t)p.n_strips * p.kb_total * 1024, (size_t)0x7fffffff), kRsrcWord3);
   const int voff = (tile * S * 64 + lane) * 16;
-  for (int i = 0; i < pre; ++i) {
+  for (int i = i0; i < min(i1, pre_d); ++i) {
     const int kb = wave + 4 * i;                     // < kb_total: pre <= kb_total / 4 (host)
 #pragma unroll
     for (int s = 0; s < S; ++s)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          wrs, (__attribute__((address_space(3))) void*)(lds + ((wave * pre + i) * S + s) * 256), 16, voff,
+          wrs, (__attribute__((address_space(3))) void*)(dyn + ((wave * pre_d + i) * S + s) * 256), 16, voff,
           (kb * p.n_strips + s) * 1024, 0, kCachePolicyNT);
+  }
+  if constexpr (STAT) {
+    for (int i = max(i0, pre_d); i < i1; ++i) {
+      const int kb = wave + 4 * i;
+#pragma unroll
+      for (int s = 0; s < S; ++s)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            wrs, (__attribute__((address_space(3))) void*)(stat + ((wave * (pre - pre_d) + i - pre_d) * S + s) * 256),
+            16, voff, (kb * p.n_strips + s) * 1024, 0, kCachePolicyNT);
+    }
   }
 }
 
@@ -827,14 +845,17 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
   // [0, gu_lds): reductions (GEMM tiles [4][S * MT * 256], O units [8][2][256],
   // gate/up [4][SG * 256]); from gu_lds: preloaded gate/up weights
   extern __shared__ float red[];
+  __shared__ attn::AttnLds<HD, 1> attn_sm;
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   uint32_t* pre_lds = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(red) + f.gu_lds);
+  uint32_t* stat_lds = reinterpret_cast<uint32_t*>(&attn_sm);
   const bool gu_tile = SG > 0 && b < f.gu_tiles;          // uniform
   const int pre = b < g.n_tiles ? f.gu_pre_q : f.gu_pre;
+  const int pre_d = pre - min(pre, f.gu_stat);            // the rest go into attn_sm
   auto preload = [&]() {
     if constexpr (SG > 0) {
-      if (gu_tile && tid < 256) gu_preload<SG>(gu, b, pre, pre_lds);
+      if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, 0, pre, pre, pre_d, pre_lds, stat_lds);
     }
   };
   if (b < g.n_tiles) {
@@ -853,14 +874,21 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     const int i = b - g.n_tiles;
     const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
     const unsigned z = i / (a.n_kv * a.n_qblocks);
-    preload();                                      // behind nothing: the attention waits long anyway
-    attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f);
+    // the iterations of the dynamic area behind nothing (the attention waits
+    // long anyway); those of attn_sm once the attention is done with it
+    if constexpr (SG > 0) {
+      if (gu_tile && tid < 256) gu_preload<SG, false>(gu, b, 0, pre_d, pre, pre_d, pre_lds, stat_lds);
+    }
+    attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f, attn_sm);
     if constexpr (OKI > 0) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's output stores are complete
       __syncthreads();
       if (tid < kFuseLanes)   // every counter: each poller reads the one of its XCD
         __hip_atomic_fetch_add(f.counters + (kFuseLanes + tid) * kFuseStride, 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if constexpr (SG > 0) {   // (SG > 0 implies OKI > 0: the barrier above ended the attention's use of attn_sm)
+      if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, pre_d, pre, pre, pre_d, pre_lds, stat_lds);
     }
   } else {
     if constexpr (OKI > 0) o_part<OKI, (SG > 0)>(o, f, b - g.n_tiles - f.n_cons, red, preload);
@@ -869,7 +897,7 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     if (gu_tile) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's preloaded weights are in LDS
       if (tid < 256) {
-        gemm_tile<1, SG, EPI_SWIGLU, false, 1>(gu, b, 0, 1, 4, red, &f, pre_lds, pre);
+        gemm_tile<1, SG, EPI_SWIGLU, false, 1>(gu, b, 0, 1, 4, red, &f, pre_lds, pre, stat_lds, pre_d);
       } else {                                      // the tile's two barriers
         attn::fuse_wait_on<kFuseLanes>(f.counters + 2 * kFuseLanes * kFuseStride, f.n_odone, f.err);
         __syncthreads();
@@ -2007,9 +2035,14 @@ hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseC
                                const GemmArgs& gu, const GemmArgs& dn, hipStream_t st, LaunchEvents ev,
                                FuseQuery& q) {
   constexpr size_t red = fuse_red_bytes<MT, S, OKI, SG>();
+  constexpr size_t iter = (size_t)4 * SG * 1024;            // one preloaded iteration
+  // preloaded iterations that the attention arrays' static LDS holds (the
+  // last ones of each workgroup; the attention workgroups load them there
+  // after their attention)
+  constexpr int stat_fit = SG > 0 ? (int)(sizeof(attn::AttnLds<HD, 1>) / std::max<size_t>(iter, 1)) : 0;
   auto kern = k_qkv_attn<MT, S, HD, OKI, SG, SD>;
   const int pre = q.what == FuseQuery::LAUNCH ? std::max(f.gu_pre, f.gu_pre_q) : q.pre;
-  const size_t lds = red + (SG > 0 ? (size_t)4 * pre * SG * 1024 : 0);
+  const size_t lds = red + (SG > 0 ? (size_t)(pre - std::min(pre, stat_fit)) * iter : 0);
   if (q.what != FuseQuery::LAUNCH) {
     int dev = 0;
     hipDeviceProp_t prop;
@@ -2020,7 +2053,7 @@ hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseC
     const size_t room = (size_t)prop.maxSharedMemoryPerMultiProcessor;
     if (q.what == FuseQuery::PRE_MAX) {
       const size_t used = attr.sharedSizeBytes + red;
-      q.result = SG > 0 && room > used ? (int)std::min<size_t>(kGuPreMax, (room - used) / ((size_t)4 * SG * 1024)) : 0;
+      q.result = SG > 0 && room > used ? (int)std::min<size_t>(kGuPreMax, (room - used) / iter + stat_fit) : 0;
       return hipSuccess;
     }
     if (attr.sharedSizeBytes + lds > room) return hipErrorInvalidValue;
@@ -2034,6 +2067,7 @@ hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseC
   }
   FuseCtl fl = f;
   fl.gu_lds = (int)red;
+  fl.gu_stat = stat_fit;
   const int grid = g.n_tiles + f.n_cons + f.o_extra;
   if (ev.start) {
     hipExtLaunchKernelGGL(kern, dim3(grid), dim3(512), (uint32_t)lds, st, ev.start, ev.stop, 0u, g, a, fl, o, gu, dn);

@@ -304,6 +304,8 @@ struct FuseCtl {
   int n_odone = 0;                 // O workers with units
   int d_tiles = 0;
   int gu_lds = 0;                  // byte offset of the preloaded weights in the dynamic LDS (set by the launcher)
+  int gu_stat = 0;                 // the last preloaded iterations of a workgroup that go into the attention
+                                   // arrays' LDS instead (at most this many; set by the launcher)
 };
 
 // Optional timing events of one launch (recorded at the kernel's start and end).

@@ -121,7 +121,8 @@ template <int MT, int S, int EPI, bool FUSED = false, int PM = 0>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, const unsigned split, const int n_split,
                                           const int nw, float* red, const FuseCtl* fc = nullptr,
                                           const uint32_t* pre_lds = nullptr, const int pre = 0,
-                                          const uint32_t* pre_stat = nullptr, const int pre_d = 0) {
+                                          const uint32_t* pre_stat = nullptr, const int pre_d = 0,
+                                          const int red_stride = 0) {
   static_assert(PM != 1 || (MT == 1 && EPI == EPI_SWIGLU && S < 8), "preloaded tiles: one row tile of gate/up, not ragged");
   static_assert(PM != 2 || (MT == 1 && EPI == EPI_RESID && S == 1), "fused down tiles: one row tile, one strip");
   constexpr int NE = S * MT * 256;   // elements of one workgroup tile
@@ -477,12 +478,13 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   }
 
   // ---- workgroup reduction over the NW input-dimension slices (wave order) ----
+  const int rs = red_stride > 0 ? red_stride : NE;    // floats between the wavefronts' partial tiles
 #pragma unroll
   for (int s = 0; s < S; ++s)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) red[wave * NE + ((s * MT + mt) * 4 + i) * 64 + lane] = acc[s][mt][i];
+      for (int i = 0; i < 4; ++i) red[wave * rs + ((s * MT + mt) * 4 + i) * 64 + lane] = acc[s][mt][i];
 
   __syncthreads();
 
@@ -493,7 +495,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& p, const int tile, con
   for (int j = 0; j < NJ; ++j) {
     const int e = j * 256 + (tid & 255);
     float t = red[e];
-    for (int w = 1; w < nw; ++w) t += red[w * NE + e];
+    for (int w = 1; w < nw; ++w) t += red[w * rs + e];
     v[j] = t;
   }
 
@@ -820,6 +822,15 @@ __device__ __forceinline__ void gu_preload(const GemmArgs& p, const int tile, co
   }
 }
 
+// Static LDS of the one-launch layer: the attention arrays of its attention
+// workgroups, and in the others (and in those after their attention) the last
+// preloaded gate/up iterations (two).
+template <int HD, int SG>
+union FusedStatLds {
+  attn::AttnLds<HD, 1> attn;
+  uint32_t pre[SG > 0 ? 2 * 4 * SG * 256 : 4];
+};
+
 // Decode passes over contexts of one attention chunk: the QKV GEMM, the
 // attention that reads its output and (OKI > 0) the O-projection of the
 // attention output in one launch.  Workgroups [0, n_tiles) are GEMM tiles
@@ -845,11 +856,12 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
   // [0, gu_lds): reductions (GEMM tiles [4][S * MT * 256], O units [8][2][256],
   // gate/up [4][SG * 256]); from gu_lds: preloaded gate/up weights
   extern __shared__ float red[];
-  __shared__ attn::AttnLds<HD, 1> attn_sm;
+  __shared__ FusedStatLds<HD, SG> stat_sm;
+  attn::AttnLds<HD, 1>& attn_sm = stat_sm.attn;
   const int tid = threadIdx.x;
   const int b = blockIdx.x;
   uint32_t* pre_lds = reinterpret_cast<uint32_t*>(reinterpret_cast<char*>(red) + f.gu_lds);
-  uint32_t* stat_lds = reinterpret_cast<uint32_t*>(&attn_sm);
+  uint32_t* stat_lds = stat_sm.pre;
   const bool gu_tile = SG > 0 && b < f.gu_tiles;          // uniform
   const int pre = b < g.n_tiles ? f.gu_pre_q : f.gu_pre;
   const int pre_d = pre - min(pre, f.gu_stat);            // the rest go into attn_sm
@@ -897,7 +909,10 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     if (gu_tile) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's preloaded weights are in LDS
       if (tid < 256) {
-        gemm_tile<1, SG, EPI_SWIGLU, false, 1>(gu, b, 0, 1, 4, red, &f, pre_lds, pre, stat_lds, pre_d);
+        // the tile's reduction in each wavefront's own first block of the
+        // dynamic preload area (read only by that wavefront, before it)
+        gemm_tile<1, SG, EPI_SWIGLU, false, 1>(gu, b, 0, 1, 4, reinterpret_cast<float*>(pre_lds), &f, pre_lds, pre,
+                                               stat_lds, pre_d, max(pre_d, 1) * SG * 256);
       } else {                                      // the tile's two barriers
         attn::fuse_wait_on<kFuseLanes>(f.counters + 2 * kFuseLanes * kFuseStride, f.n_odone, f.err);
         __syncthreads();
@@ -2025,9 +2040,9 @@ struct FuseQuery {
 };
 
 template <int MT, int S, int OKI, int SG>
-constexpr size_t fuse_red_bytes() {   // (a fused down tile's [4][256] fits below the O units')
-  return std::max({(size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0,
-                   SG > 0 ? (size_t)4 * SG * 256 : (size_t)0}) * sizeof(float);
+constexpr size_t fuse_red_bytes() {   // (a fused down tile's [4][256] fits below the O units'; the gate/up
+                                       // tile reduces in the preload area)
+  return std::max((size_t)4 * S * MT * 256, OKI > 0 ? (size_t)8 * 2 * 256 : (size_t)0) * sizeof(float);
 }
 
 template <int MT, int S, int HD, int OKI, int SG, int SD>
@@ -2039,10 +2054,11 @@ hipError_t launch_qkv_attn_one(const GemmArgs& g, const AttnArgs& a, const FuseC
   // preloaded iterations that the attention arrays' static LDS holds (the
   // last ones of each workgroup; the attention workgroups load them there
   // after their attention)
-  constexpr int stat_fit = SG > 0 ? (int)(sizeof(attn::AttnLds<HD, 1>) / std::max<size_t>(iter, 1)) : 0;
+  constexpr int stat_fit = SG > 0 ? (int)(sizeof(FusedStatLds<HD, SG>) / std::max<size_t>(iter, 1)) : 0;
   auto kern = k_qkv_attn<MT, S, HD, OKI, SG, SD>;
   const int pre = q.what == FuseQuery::LAUNCH ? std::max(f.gu_pre, f.gu_pre_q) : q.pre;
-  const size_t lds = red + (SG > 0 ? (size_t)(pre - std::min(pre, stat_fit)) * iter : 0);
+  // (at least one iteration's room: the gate/up tile's reduction)
+  const size_t lds = red + (SG > 0 ? (size_t)std::max(pre - std::min(pre, stat_fit), 1) * iter : 0);
   if (q.what != FuseQuery::LAUNCH) {
     int dev = 0;
     hipDeviceProp_t prop;

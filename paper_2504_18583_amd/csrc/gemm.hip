@@ -854,7 +854,8 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
   static_assert(SG == 0 || (MT == 1 && OKI > 0), "gate/up joins only launches with O units");
   static_assert(SD == 0 || (SD == 1 && SG > 0), "the down projection joins only launches with gate/up");
   // [0, gu_lds): reductions (GEMM tiles [4][S * MT * 256], O units [8][2][256],
-  // gate/up [4][SG * 256]); from gu_lds: preloaded gate/up weights
+  // down tiles [4][256]); from gu_lds: preloaded gate/up weights, whose first
+  // block of each wavefront later holds that wavefront's gate/up partial tile
   extern __shared__ float red[];
   __shared__ FusedStatLds<HD, SG> stat_sm;
   attn::AttnLds<HD, 1>& attn_sm = stat_sm.attn;
@@ -864,7 +865,7 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
   uint32_t* stat_lds = stat_sm.pre;
   const bool gu_tile = SG > 0 && b < f.gu_tiles;          // uniform
   const int pre = b < g.n_tiles ? f.gu_pre_q : f.gu_pre;
-  const int pre_d = pre - min(pre, f.gu_stat);            // the rest go into attn_sm
+  const int pre_d = pre - min(pre, f.gu_stat);            // the rest go into stat_sm
   auto preload = [&]() {
     if constexpr (SG > 0) {
       if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, 0, pre, pre, pre_d, pre_lds, stat_lds);
@@ -887,7 +888,7 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
     const unsigned z = i / (a.n_kv * a.n_qblocks);
     // the iterations of the dynamic area behind nothing (the attention waits
-    // long anyway); those of attn_sm once the attention is done with it
+    // long anyway); those of stat_sm once the attention is done with it
     if constexpr (SG > 0) {
       if (gu_tile && tid < 256) gu_preload<SG, false>(gu, b, 0, pre_d, pre, pre_d, pre_lds, stat_lds);
     }
@@ -899,7 +900,7 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
         __hip_atomic_fetch_add(f.counters + (kFuseLanes + tid) * kFuseStride, 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     }
-    if constexpr (SG > 0) {   // (SG > 0 implies OKI > 0: the barrier above ended the attention's use of attn_sm)
+    if constexpr (SG > 0) {   // (SG > 0 implies OKI > 0: the barrier above ended the attention's use of stat_sm)
       if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, pre_d, pre, pre, pre_d, pre_lds, stat_lds);
     }
   } else {

@@ -50,7 +50,7 @@ typedef enum {
   PARD_ERR_CAPACITY = -3,    /* would exceed max_ctx / max_k / max_batch */
   PARD_ERR_NOMEM = -4,       /* arena smaller than pard_arena_bytes() */
   PARD_ERR_DEVICE = -5,      /* a HIP runtime call failed */
-  PARD_ERR_UNSUPPORTED = -6, /* valid request this build does not implement */
+  PARD_ERR_UNSUPPORTED = -6, /* valid request the library does not implement */
   PARD_ERR_RANGE = -7        /* the call ran, but an activation exceeded fp16's range (see below) */
 } pard_status;
 

@@ -887,11 +887,6 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
     const int i = b - g.n_tiles;
     const int kvh = i % a.n_kv, qg = (i / a.n_kv) % a.n_qblocks;
     const unsigned z = i / (a.n_kv * a.n_qblocks);
-    // the iterations of the dynamic area behind nothing (the attention waits
-    // long anyway); those of stat_sm once the attention is done with it
-    if constexpr (SG > 0) {
-      if (gu_tile && tid < 256) gu_preload<SG, false>(gu, b, 0, pre_d, pre, pre_d, pre_lds, stat_lds);
-    }
     attn::attn_tile<HD, 1, 2 * kAttnWaves, true>(a, kvh, qg, z, f, attn_sm);
     if constexpr (OKI > 0) {
       __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);      // this wavefront's output stores are complete
@@ -900,8 +895,11 @@ __global__ __launch_bounds__(512) void k_qkv_attn(const GemmArgs g, const AttnAr
         __hip_atomic_fetch_add(f.counters + (kFuseLanes + tid) * kFuseStride, 1, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
     }
-    if constexpr (SG > 0) {   // (SG > 0 implies OKI > 0: the barrier above ended the attention's use of stat_sm)
-      if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, pre_d, pre, pre, pre_d, pre_lds, stat_lds);
+    // the gate/up preload only now: issued earlier it competes with the QKV
+    // weights that the attention waits for (SG > 0 implies OKI > 0: the
+    // barrier above ended the attention's use of stat_sm)
+    if constexpr (SG > 0) {
+      if (gu_tile && tid < 256) gu_preload<SG, true>(gu, b, 0, pre, pre, pre_d, pre_lds, stat_lds);
     }
   } else {
     if constexpr (OKI > 0) o_part<OKI, (SG > 0)>(o, f, b - g.n_tiles - f.n_cons, red, preload);

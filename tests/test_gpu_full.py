@@ -70,6 +70,50 @@ def test_llama_8b_1b_full_width_slice_lockstep(B):
         eng.close()
 
 
+def test_llama_8b_1b_gate_up_preload_depth_is_bitwise_neutral(B, monkeypatch):
+    """The one-launch layer's gate/up tiles take their first iterations from
+    LDS (the dynamic area, then the static area shared with the attention
+    arrays; QKV workgroups may preload fewer, down to none) and stream the
+    rest; where an iteration comes from never changes the arithmetic or its
+    order, and the tile's reduction (kept in the preload area) sums in wave
+    order.  So every preload split gives bitwise the logits of the default
+    plan, at the 8B/1B tile shapes."""
+    from paper_2504_18583_amd.binding import PARD_DRAFT, PARD_TARGET
+    wl = pi.WORKLOADS["llama8b_1b"]
+    t_spec, d_spec = _slice(wl.target, 2), _slice(wl.draft, 1)
+    prompt = [int(x) for x in pi.workload_prompts(wl)[0]]
+    ref = None
+    # (iterations per workgroup, of the QKV workgroups); None: the default plan
+    for pre, pre_q in [(None, None), (1, 0), (2, 1), (3, 3), (5, 1), (5, 4)]:
+        for name, v in (("PARD_GU_PRE", pre), ("PARD_GU_PRE_Q", pre_q)):
+            if v is None:
+                monkeypatch.delenv(name, raising=False)
+            else:
+                monkeypatch.setenv(name, str(v))
+        say(f"[gpu] 8B/1B slice: gate/up preload {pre}, QKV workgroups {pre_q}")
+        eng = B.Engine(t_spec, d_spec, wl.mask_id, max_ctx=len(prompt) + 64, max_k=wl.k)
+        try:
+            first = eng.prefill(prompt)
+            hist = prompt + [first]
+            got = []
+            for _ in range(2):
+                cands = eng.draft(hist, wl.k)
+                dl = eng.read_logits(PARD_DRAFT, wl.k)
+                a, bonus = eng.verify(cands)
+                vl = eng.read_logits(PARD_TARGET, wl.k + 1)
+                got.append((cands, a, bonus, dl, vl))
+                hist += cands[:a] + [bonus]
+        finally:
+            eng.close()
+        if ref is None:
+            ref = got
+            continue
+        for (c0, a0, b0, d0, v0), (c1, a1, b1, d1, v1) in zip(ref, got):
+            assert (c1, a1, b1) == (c0, a0, b0)
+            assert np.array_equal(d1.view(np.uint32), d0.view(np.uint32))
+            assert np.array_equal(v1.view(np.uint32), v0.view(np.uint32))
+
+
 QWEN = pi.WORKLOADS["qwen7b_05b"]
 QWEN_T, QWEN_D = _slice(QWEN.target, 2), _slice(QWEN.draft, 2)
 
